@@ -1,0 +1,207 @@
+/*
+ * ent.h -- C ABI of the entropic-time decode step on MI355X (gfx950).
+ *
+ * One batched decode step of entropic-time inference (arXiv 2603.03310):
+ * per sequence, the exact Shannon entropy of the next-token distribution,
+ * entropic time and the temperature control law, entropy-driven pruning of
+ * the paged KV cache, decode attention over the kept blocks, and sampling at
+ * the controlled temperature.
+ *
+ * Conventions for every entry point:
+ *  - Pointers are DEVICE pointers owned by the caller, unless a parameter says
+ *    "host".  The context owns only its workspace, allocated once by ent_init.
+ *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL is
+ *    the default stream).  They allocate nothing and never synchronise, except
+ *    ent_init, ent_destroy and ent_device_status.
+ *  - Arguments are validated on the host before anything is launched.  A bad
+ *    argument returns ENT_E_INVAL (or ENT_E_UNSUPPORTED) with nothing launched,
+ *    and a message for ent_last_error.  A HIP failure returns ENT_E_HIP.
+ *    Outputs are undefined after an error.
+ *  - Device-side checks: a block table entry outside [0, num_pool_blocks) or a
+ *    context length outside [0, max_blocks_per_seq * 16] is never
+ *    dereferenced; the kernel skips it and raises a flag that
+ *    ent_device_status reports.
+ *  - A context is not thread-safe; calls that share a context must be ordered
+ *    on one stream (the workspace is reused by every call).
+ *  - Batch sizes: 0 <= B <= max_batch.  B == 0 launches nothing.
+ *
+ * Paged KV cache layout (block size 16 tokens, P = num_pool_blocks):
+ *    k_cache [P, H_kv, 16, d]   token-major tile per (physical block, KV head)
+ *    v_cache [P, H_kv, d, 16]   dim-major tile per (physical block, KV head)
+ *  element type kv_dtype (bf16 or fp32); queries have the same type.  Logical
+ *  token i of sequence b is slot i % 16 of physical block
+ *  block_tables[b * max_blocks_per_seq + i / 16].  A sequence of N tokens
+ *  occupies nb = ceil(N / 16) logical blocks; the last holds N - 16 (nb - 1).
+ */
+#ifndef ENT_H
+#define ENT_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ent_ctx ent_ctx;
+
+enum {
+  ENT_OK = 0,
+  ENT_E_INVAL = -1,        /* bad argument: nothing launched */
+  ENT_E_NOMEM = -2,        /* workspace allocation failed (ent_init) */
+  ENT_E_HIP = -3,          /* a HIP runtime call or launch failed */
+  ENT_E_UNSUPPORTED = -4   /* shape outside what the kernels implement */
+};
+
+enum { ENT_F32 = 0, ENT_BF16 = 1 };
+
+/* Tokens per logical row chunk of the entropy reduction; row statistics hold
+ * one (max, sum) pair per chunk: ent_row_stats_chunks(vocab) chunks per row. */
+#define ENT_ROW_CHUNK 4096
+#define ENT_BLOCK_SIZE 16
+
+/* Device-status flags (ent_device_status). */
+#define ENT_DEV_BAD_TABLE 1u     /* a block table entry was out of range */
+#define ENT_DEV_BAD_CTXLEN 2u    /* a context length was out of range */
+#define ENT_DEV_CACHE_FULL 4u    /* append found no room in the block table */
+
+/* Shapes and control parameters; host values, copied by ent_init.
+ * The paper names the control symbols but gives no values (Section 3.3, the
+ * temperature law and the estimator error bound; Section 3.3 "Conservative
+ * pruning under uncertainty bounds" and Section 5 for H_min and B_min). */
+typedef struct {
+  int max_batch;           /* largest B any call will pass, >= 1 */
+  int num_q_heads;         /* H_q */
+  int num_kv_heads;        /* H_kv; H_q % H_kv == 0, G = H_q / H_kv <= 16 */
+  int head_dim;            /* d: 64 or 128 */
+  int block_size;          /* tokens per KV block: must be 16 */
+  int max_blocks_per_seq;  /* MAXB: row length of block_tables, <= 16384 */
+  int num_pool_blocks;     /* P: physical blocks in k_cache / v_cache */
+  int vocab;               /* |V|: logits per row */
+  int kv_dtype;            /* ENT_BF16 or ENT_F32 (K, V and queries) */
+  float scale;             /* softmax scale of scoring and attention, e.g. 1/sqrt(d) */
+  float eta;               /* SIGNED gain of the temperature law; < 0 stabilises */
+  float h_target;          /* target entropy H* (nats) */
+  float t_min, t_max;      /* temperature clip bounds, 0 < t_min <= t_max */
+  float eps_h;             /* entropy estimator error bound (0 for exact entropy) */
+  float h_min;             /* entropy floor for pruning decisions */
+  float kappa_min;         /* smallest kept fraction of blocks, in [0, 1] */
+  int b_min;               /* smallest number of kept blocks, >= 0 */
+  float log_v;             /* log |V| as float32; must exceed h_min */
+} ent_config;
+
+/* Per-sequence controller state, device arrays of B floats each, read and
+ * updated in place by ent_entropy_temperature: the previous step's entropy
+ * H_{t-1} (NaN = no previous step), entropic time tau, and temperature T_t. */
+typedef struct {
+  float* h_prev;
+  float* tau;
+  float* temp;
+} ent_state;
+
+/* Defaults: Llama-3-8B decode shapes (32/8 heads, d = 128, bf16, |V| = 128256),
+ * eta = -0.05, H* = 2.5, T in [0.05, 5], eps_H = 0, H_min = H*, kappa_min = 0.05,
+ * B_min = 4.  max_batch, max_blocks_per_seq and num_pool_blocks must be set. */
+void ent_default_config(ent_config* out);
+
+/* Host-only check of a configuration (no HIP call).  Returns ENT_OK, or
+ * ENT_E_INVAL / ENT_E_UNSUPPORTED and writes a message into msg (host buffer
+ * of msg_len bytes; may be NULL). */
+int ent_check_config(const ent_config* cfg, char* msg, int msg_len);
+
+/* Number of row-statistics chunks per logit row: ceil(vocab / ENT_ROW_CHUNK). */
+int ent_row_stats_chunks(int vocab);
+
+/* Create a context on the current HIP device: validates cfg, allocates and
+ * zeroes the workspace (size grows with max_batch, H_q, MAXB).  *out receives
+ * the context (host pointer) or NULL on error. */
+int ent_init(const ent_config* cfg, ent_ctx** out);
+
+/* Free the workspace and the context.  Synchronises the device first. */
+int ent_destroy(ent_ctx* c);
+
+/* Message of the last error on this context ("" if none).  The string is
+ * owned by the context and valid until its next call.  ent_last_error(NULL)
+ * returns the message of the last failed ent_init. */
+const char* ent_last_error(const ent_ctx* c);
+
+/* Synchronise `stream`, then return in *flags (host) the ENT_DEV_* flags
+ * raised by kernels since the last call, and clear them. */
+int ent_device_status(ent_ctx* c, void* stream, unsigned* flags);
+
+/* Entropy and controller (Section 2: H_t, Delta H_t, entropic time tau;
+ * Section 2.1: exact entropy of the tempered softmax; Section 3.3: the
+ * temperature law T_{t+1} = clip(T_t exp(eta (H_t - H*)), T_min, T_max)).
+ *
+ * For each row b < B of logits (fp32, row stride ld >= vocab elements):
+ *   H_t      = -sum_x p(x) ln p(x),  p = softmax(z / T_t),  T_t = st.temp[b]
+ *   h_out[b] = H_t;  temp_used[b] = T_t
+ *   st.tau[b]   += max(0, st.h_prev[b] - H_t)   (unchanged if h_prev is NaN)
+ *   st.h_prev[b] = H_t;  st.temp[b] = T_{t+1}
+ * row_stats (nullable): float [B, ent_row_stats_chunks(vocab), 2] chunk
+ * statistics of the same pass at T_t, reused by ent_sample.
+ * Preconditions: >= 1 finite logit per row, temp > 0.  h_out must not alias
+ * st.h_prev; temp_used must not alias st.temp. */
+int ent_entropy_temperature(ent_ctx* c, int B, const float* logits, long long ld,
+                            ent_state st, float* h_out, float* temp_used, float* row_stats,
+                            void* stream);
+
+/* Per-block mean keys (the summaries block scoring reads).  For each
+ * sequence b < B and logical block j < nb_b, with p = block_tables[b][j]:
+ *   ksum[p, g, :] = (1/n_j) sum over the n_j valid slots of k_cache[p, g, slot, :]
+ * ksum: float [P, H_kv, d], indexed by physical block.  Entries of blocks not
+ * listed are left untouched.  ctx_lens: int [B]. */
+int ent_block_summary(ent_ctx* c, int B, const void* k_cache, const int* block_tables,
+                      const int* ctx_lens, float* ksum, void* stream);
+
+/* Block scores and kept-block selection (Section 3.2: block entropic
+ * contribution I_b and the kept set B_t = {b : I_b >= theta_t}; Section 3.3
+ * and Section 5: the safety floor and the minimum block budget).
+ *   z_bh  = scale <q_h, ksum[p_b, h / G]>,  weights a_bh = e^{z_bh} / sum_b' n_b' e^{z_b'h}
+ *   I_b   = (1/H_q) sum_h n_b a_bh (-ln a_bh)
+ *   H_g   = max(h[b] + eps_H, H_min);  u = clip((H_g - H_min)/(log_v - H_min), 0, 1)
+ *   k     = min(nb, max(min(B_min, nb), ceil((kappa_min + (1 - kappa_min) u) nb)))
+ *           (float32, in exactly this order, no fused multiply-add)
+ *   theta = k-th largest I_b;  kept = {b : I_b >= theta} in ascending order
+ * q: [B, H_q, d] (kv_dtype); ksum from ent_block_summary; h: float [B] (the
+ * entropy from ent_entropy_temperature).  Outputs: kept int [B, MAXB] (first
+ * n_kept[b] entries valid, logical block ids), n_kept int [B]; scores
+ * (nullable) float [B, MAXB] (I_b for b < nb); theta (nullable) float [B]
+ * (+inf when nothing is kept). */
+int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum,
+                     const int* block_tables, const int* ctx_lens, const float* h, int* kept,
+                     int* n_kept, float* scores, float* theta, void* stream);
+
+/* Decode attention over the kept blocks only (Section 3.2: attention is
+ * restricted to B_t).  For query head h (KV head g = h / G), over the valid
+ * tokens i of the kept blocks of sequence b:
+ *   s_i = scale <q_h, k_i>;  out[b, h, :] = sum_i softmax(s)_i v_i;
+ *   lse[b, h] = ln sum_i e^{s_i}
+ * The softmax is renormalised over the kept tokens.  An empty kept set gives
+ * out = 0 and lse = -inf.  out: float [B, H_q, d]; lse (nullable) float [B, H_q]. */
+int ent_sparse_paged_decode(ent_ctx* c, int B, const void* q, const void* k_cache,
+                            const void* v_cache, const int* block_tables, const int* ctx_lens,
+                            const int* kept, const int* n_kept, float* out, float* lse,
+                            void* stream);
+
+/* Sampling at the controlled temperature (Sections 2.1 and 3.3).  Token of
+ * row b = inverse CDF of softmax(z / temp_used[b]) in index order at the
+ * uniform uniforms[b] in [0, 1): the smallest x with C_x > u S (C the running
+ * sum of e^{z/T - max}, S its total), or the last token of positive mass if
+ * rounding leaves none.  row_stats (nullable) must come from
+ * ent_entropy_temperature on the same logits and temperatures; when NULL the
+ * statistics are recomputed (one more pass over the logits).  tokens: int [B]. */
+int ent_sample(ent_ctx* c, int B, const float* logits, long long ld, const float* row_stats,
+               const float* temp_used, const float* uniforms, int* tokens, void* stream);
+
+/* Append one token per sequence to the paged cache (the memory part of the
+ * step's state, Section 3).  With N = ctx_lens[b] and p = block_tables[b][N/16]:
+ * write k_new[b, g, :] to k_cache[p, g, N%16, :] and v_new[b, g, :] to
+ * v_cache[p, g, :, N%16], recompute ksum[p, g, :] over the block's N%16 + 1
+ * valid slots (bit-identical to ent_block_summary), and set ctx_lens[b] = N+1.
+ * k_new, v_new: [B, H_kv, d] (kv_dtype). */
+int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new,
+                  const int* block_tables, int* ctx_lens, void* k_cache, void* v_cache,
+                  float* ksum, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ENT_H */

@@ -1,0 +1,322 @@
+// Host side of the C ABI: configuration checks, the workspace, argument
+// validation and launch sequencing.  No entry point allocates except
+// ent_init; none synchronises except ent_init, ent_destroy and
+// ent_device_status.
+
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+
+#include "ent_internal.h"
+
+namespace {
+
+thread_local std::string g_init_error;
+
+constexpr int kMaxBatch = 4096;
+constexpr int kMaxQHeads = 128;
+constexpr int kMaxVocab = 256 * ENT_ROW_CHUNK;
+
+bool is_pow2_group(int g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
+
+std::string check_config(const ent_config* c, int* code) {
+  *code = ENT_E_INVAL;
+  if (!c) return "config is NULL";
+  if (c->max_batch < 1 || c->max_batch > kMaxBatch) return "max_batch must be in [1, 4096]";
+  if (c->num_kv_heads < 1 || c->num_q_heads < 1) return "head counts must be >= 1";
+  if (c->num_q_heads % c->num_kv_heads != 0) return "num_q_heads must be a multiple of num_kv_heads";
+  if (c->block_size != ENT_BLOCK_SIZE) return "block_size must be 16";
+  if (c->max_blocks_per_seq < 1) return "max_blocks_per_seq must be >= 1";
+  if (c->num_pool_blocks < 1) return "num_pool_blocks must be >= 1";
+  if (c->vocab < 1) return "vocab must be >= 1";
+  if (c->kv_dtype != ENT_F32 && c->kv_dtype != ENT_BF16) return "kv_dtype must be ENT_F32 or ENT_BF16";
+  if (!isfinite(c->scale)) return "scale must be finite";
+  if (!isfinite(c->eta) || !isfinite(c->h_target)) return "eta and h_target must be finite";
+  if (!(c->t_min > 0.f) || !(c->t_max >= c->t_min) || !isfinite(c->t_max))
+    return "need 0 < t_min <= t_max < inf";
+  if (!(c->eps_h >= 0.f) || !isfinite(c->eps_h)) return "eps_h must be finite and >= 0";
+  if (!isfinite(c->h_min) || !isfinite(c->log_v) || !(c->log_v > c->h_min))
+    return "need finite h_min < log_v";
+  if (!(c->kappa_min >= 0.f && c->kappa_min <= 1.f)) return "kappa_min must be in [0, 1]";
+  if (c->b_min < 0) return "b_min must be >= 0";
+  *code = ENT_E_UNSUPPORTED;
+  if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
+  if (!is_pow2_group(c->num_q_heads / c->num_kv_heads))
+    return "num_q_heads / num_kv_heads must be 1, 2, 4, 8 or 16";
+  if (c->num_q_heads > kMaxQHeads) return "num_q_heads must be <= 128";
+  if (c->max_blocks_per_seq > ent::kMaxBlocksPerSeq) return "max_blocks_per_seq must be <= 16384";
+  if (c->vocab > kMaxVocab) return "vocab must be <= 1048576";
+  *code = ENT_OK;
+  return "";
+}
+
+int fail(ent_ctx* c, int code, const std::string& msg) {
+  c->err = msg;
+  return code;
+}
+
+int hip_fail(ent_ctx* c, hipError_t e, const char* what) {
+  c->err = std::string(what) + ": " + hipGetErrorString(e);
+  return ENT_E_HIP;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int check_batch(ent_ctx* c, int B) {
+  if (B < 0 || B > c->cfg.max_batch)
+    return fail(c, ENT_E_INVAL, "B must be in [0, max_batch]");
+  return ENT_OK;
+}
+
+size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+}  // namespace
+
+extern "C" {
+
+void ent_default_config(ent_config* out) {
+  if (!out) return;
+  memset(out, 0, sizeof(*out));
+  out->max_batch = 64;
+  out->num_q_heads = 32;
+  out->num_kv_heads = 8;
+  out->head_dim = 128;
+  out->block_size = ENT_BLOCK_SIZE;
+  out->max_blocks_per_seq = 512;
+  out->num_pool_blocks = 1;
+  out->vocab = 128256;
+  out->kv_dtype = ENT_BF16;
+  out->scale = static_cast<float>(1.0 / sqrt(128.0));
+  out->eta = -0.05f;
+  out->h_target = 2.5f;
+  out->t_min = 0.05f;
+  out->t_max = 5.0f;
+  out->eps_h = 0.0f;
+  out->h_min = 2.5f;
+  out->kappa_min = 0.05f;
+  out->b_min = 4;
+  out->log_v = static_cast<float>(log(128256.0));
+}
+
+int ent_check_config(const ent_config* cfg, char* msg, int msg_len) {
+  int code;
+  const std::string m = check_config(cfg, &code);
+  if (msg && msg_len > 0) snprintf(msg, static_cast<size_t>(msg_len), "%s", m.c_str());
+  return code;
+}
+
+int ent_row_stats_chunks(int vocab) { return vocab <= 0 ? 0 : (vocab + ENT_ROW_CHUNK - 1) / ENT_ROW_CHUNK; }
+
+int ent_init(const ent_config* cfg, ent_ctx** out) {
+  if (!out) {
+    g_init_error = "out is NULL";
+    return ENT_E_INVAL;
+  }
+  *out = nullptr;
+  int code;
+  const std::string m = check_config(cfg, &code);
+  if (code != ENT_OK) {
+    g_init_error = m;
+    return code;
+  }
+  ent_ctx* c = new (std::nothrow) ent_ctx();
+  if (!c) {
+    g_init_error = "host allocation failed";
+    return ENT_E_NOMEM;
+  }
+  c->cfg = *cfg;
+  hipError_t e = hipGetDevice(&c->device);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&c->num_cu, hipDeviceAttributeMultiprocessorCount, c->device);
+  if (e != hipSuccess) {
+    g_init_error = std::string("no usable HIP device: ") + hipGetErrorString(e);
+    delete c;
+    return ENT_E_HIP;
+  }
+  const ent_config& f = c->cfg;
+  c->group = f.num_q_heads / f.num_kv_heads;
+  c->chunks = ent_row_stats_chunks(f.vocab);
+  c->score_chunks = (f.max_blocks_per_seq + ent::kScoreChunk - 1) / ent::kScoreChunk;
+  c->splits_max = (f.max_blocks_per_seq + ent::kSplitBlocks - 1) / ent::kSplitBlocks;
+
+  const size_t Bm = static_cast<size_t>(f.max_batch);
+  const size_t sz_ent_part = align_up(Bm * c->chunks * 3 * sizeof(float));
+  const size_t sz_ent_ticket = align_up(Bm * sizeof(unsigned));
+  const size_t sz_stats = align_up(Bm * c->chunks * 2 * sizeof(float));
+  const size_t sz_z = align_up(Bm * f.max_blocks_per_seq * f.num_q_heads * sizeof(float));
+  const size_t sz_lse = align_up(Bm * c->score_chunks * f.num_q_heads * 2 * sizeof(float));
+  const size_t sz_score = align_up(Bm * f.max_blocks_per_seq * sizeof(float));
+  const size_t sz_sel_ticket = align_up(Bm * sizeof(unsigned));
+  const size_t nslots = Bm * f.num_kv_heads * c->splits_max;
+  const size_t sz_acc = align_up(nslots * c->group * f.head_dim * sizeof(float));
+  const size_t sz_ml = align_up(nslots * c->group * 2 * sizeof(float));
+  const size_t sz_dec_ticket = align_up(Bm * f.num_kv_heads * sizeof(unsigned));
+  const size_t sz_flags = align_up(sizeof(unsigned));
+  c->ws_bytes = sz_ent_part + sz_ent_ticket + sz_stats + sz_z + sz_lse + sz_score +
+                sz_sel_ticket + sz_acc + sz_ml + sz_dec_ticket + sz_flags;
+  e = hipMalloc(&c->ws, c->ws_bytes);
+  if (e != hipSuccess) {
+    g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
+    delete c;
+    return ENT_E_NOMEM;
+  }
+  e = hipMemset(c->ws, 0, c->ws_bytes);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    g_init_error = std::string("workspace clear failed: ") + hipGetErrorString(e);
+    (void)hipFree(c->ws);
+    delete c;
+    return ENT_E_HIP;
+  }
+  char* p = static_cast<char*>(c->ws);
+  auto take = [&p](size_t n) { char* r = p; p += n; return r; };
+  c->ent_part = reinterpret_cast<float*>(take(sz_ent_part));
+  c->ent_ticket = reinterpret_cast<unsigned*>(take(sz_ent_ticket));
+  c->stats_tmp = reinterpret_cast<float*>(take(sz_stats));
+  c->zbuf = reinterpret_cast<float*>(take(sz_z));
+  c->lse_part = reinterpret_cast<float*>(take(sz_lse));
+  c->score_ws = reinterpret_cast<float*>(take(sz_score));
+  c->sel_ticket = reinterpret_cast<unsigned*>(take(sz_sel_ticket));
+  c->dec_acc = reinterpret_cast<float*>(take(sz_acc));
+  c->dec_ml = reinterpret_cast<float*>(take(sz_ml));
+  c->dec_ticket = reinterpret_cast<unsigned*>(take(sz_dec_ticket));
+  c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));
+  c->decode_grid = ent::decode_grid_size(c);
+  *out = c;
+  return ENT_OK;
+}
+
+int ent_destroy(ent_ctx* c) {
+  if (!c) return ENT_E_INVAL;
+  hipError_t e = hipDeviceSynchronize();
+  const hipError_t e2 = hipFree(c->ws);
+  delete c;
+  return (e == hipSuccess && e2 == hipSuccess) ? ENT_OK : ENT_E_HIP;
+}
+
+const char* ent_last_error(const ent_ctx* c) {
+  return c ? c->err.c_str() : g_init_error.c_str();
+}
+
+int ent_device_status(ent_ctx* c, void* stream, unsigned* flags) {
+  if (!c || !flags) return c ? fail(c, ENT_E_INVAL, "flags is NULL") : ENT_E_INVAL;
+  hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "stream synchronise");
+  unsigned v = 0;
+  e = hipMemcpy(&v, c->dev_flags, sizeof(unsigned), hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemset(c->dev_flags, 0, sizeof(unsigned));
+  if (e != hipSuccess) return hip_fail(c, e, "device status read");
+  *flags = v;
+  c->err.clear();
+  return ENT_OK;
+}
+
+int ent_entropy_temperature(ent_ctx* c, int B, const float* logits, long long ld, ent_state st,
+                            float* h_out, float* temp_used, float* row_stats, void* stream) {
+  if (!c) return ENT_E_INVAL;
+  if (int r = check_batch(c, B)) return r;
+  if (B == 0) return ENT_OK;
+  if (!logits || !st.h_prev || !st.tau || !st.temp || !h_out || !temp_used)
+    return fail(c, ENT_E_INVAL, "ent_entropy_temperature: NULL required pointer");
+  if (ld < c->cfg.vocab) return fail(c, ENT_E_INVAL, "ent_entropy_temperature: ld < vocab");
+  if (h_out == st.h_prev) return fail(c, ENT_E_INVAL, "ent_entropy_temperature: h_out aliases h_prev");
+  if (temp_used == st.temp) return fail(c, ENT_E_INVAL, "ent_entropy_temperature: temp_used aliases temp");
+  const hipError_t e = ent::launch_entropy(c, B, logits, ld, st, h_out, temp_used, row_stats, true,
+                                           static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "ent_entropy_temperature launch");
+  c->err.clear();
+  return ENT_OK;
+}
+
+int ent_block_summary(ent_ctx* c, int B, const void* k_cache, const int* block_tables,
+                      const int* ctx_lens, float* ksum, void* stream) {
+  if (!c) return ENT_E_INVAL;
+  if (int r = check_batch(c, B)) return r;
+  if (B == 0) return ENT_OK;
+  if (!k_cache || !block_tables || !ctx_lens || !ksum)
+    return fail(c, ENT_E_INVAL, "ent_block_summary: NULL required pointer");
+  const hipError_t e = ent::launch_block_summary(c, B, k_cache, block_tables, ctx_lens, ksum,
+                                                 static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "ent_block_summary launch");
+  c->err.clear();
+  return ENT_OK;
+}
+
+int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum, const int* block_tables,
+                     const int* ctx_lens, const float* h, int* kept, int* n_kept, float* scores,
+                     float* theta, void* stream) {
+  if (!c) return ENT_E_INVAL;
+  if (int r = check_batch(c, B)) return r;
+  if (B == 0) return ENT_OK;
+  if (!q || !ksum || !block_tables || !ctx_lens || !h || !kept || !n_kept)
+    return fail(c, ENT_E_INVAL, "ent_block_select: NULL required pointer");
+  const size_t qa = c->cfg.kv_dtype == ENT_BF16 ? 8 : 16;
+  if (!aligned(q, qa) || !aligned(ksum, 16))
+    return fail(c, ENT_E_INVAL, "ent_block_select: q or ksum misaligned");
+  const hipError_t e = ent::launch_block_select(c, B, q, ksum, block_tables, ctx_lens, h, kept,
+                                                n_kept, scores, theta,
+                                                static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "ent_block_select launch");
+  c->err.clear();
+  return ENT_OK;
+}
+
+int ent_sparse_paged_decode(ent_ctx* c, int B, const void* q, const void* k_cache,
+                            const void* v_cache, const int* block_tables, const int* ctx_lens,
+                            const int* kept, const int* n_kept, float* out, float* lse,
+                            void* stream) {
+  if (!c) return ENT_E_INVAL;
+  if (int r = check_batch(c, B)) return r;
+  if (B == 0) return ENT_OK;
+  if (!q || !k_cache || !v_cache || !block_tables || !ctx_lens || !kept || !n_kept || !out)
+    return fail(c, ENT_E_INVAL, "ent_sparse_paged_decode: NULL required pointer");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16))
+    return fail(c, ENT_E_INVAL, "ent_sparse_paged_decode: q, caches and out need 16-byte alignment");
+  const hipError_t e = ent::launch_decode(c, B, q, k_cache, v_cache, block_tables, ctx_lens, kept,
+                                          n_kept, out, lse, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "ent_sparse_paged_decode launch");
+  c->err.clear();
+  return ENT_OK;
+}
+
+int ent_sample(ent_ctx* c, int B, const float* logits, long long ld, const float* row_stats,
+               const float* temp_used, const float* uniforms, int* tokens, void* stream) {
+  if (!c) return ENT_E_INVAL;
+  if (int r = check_batch(c, B)) return r;
+  if (B == 0) return ENT_OK;
+  if (!logits || !temp_used || !uniforms || !tokens)
+    return fail(c, ENT_E_INVAL, "ent_sample: NULL required pointer");
+  if (ld < c->cfg.vocab) return fail(c, ENT_E_INVAL, "ent_sample: ld < vocab");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float* stats = row_stats;
+  if (!stats) {
+    ent_state none{nullptr, nullptr, nullptr};
+    const hipError_t e = ent::launch_entropy(c, B, logits, ld, none, nullptr, const_cast<float*>(temp_used),
+                                             c->stats_tmp, false, s);
+    if (e != hipSuccess) return hip_fail(c, e, "ent_sample statistics launch");
+    stats = c->stats_tmp;
+  }
+  const hipError_t e = ent::launch_sample(c, B, logits, ld, stats, temp_used, uniforms, tokens, s);
+  if (e != hipSuccess) return hip_fail(c, e, "ent_sample launch");
+  c->err.clear();
+  return ENT_OK;
+}
+
+int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new, const int* block_tables,
+                  int* ctx_lens, void* k_cache, void* v_cache, float* ksum, void* stream) {
+  if (!c) return ENT_E_INVAL;
+  if (int r = check_batch(c, B)) return r;
+  if (B == 0) return ENT_OK;
+  if (!k_new || !v_new || !block_tables || !ctx_lens || !k_cache || !v_cache || !ksum)
+    return fail(c, ENT_E_INVAL, "ent_kv_append: NULL required pointer");
+  const hipError_t e = ent::launch_kv_append(c, B, k_new, v_new, block_tables, ctx_lens, k_cache,
+                                             v_cache, ksum, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "ent_kv_append launch");
+  c->err.clear();
+  return ENT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,121 @@
+// Internal declarations shared by the HIP translation units of libent.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "ent.h"
+
+namespace ent {
+
+constexpr int kBlock = ENT_BLOCK_SIZE;      // tokens per KV block
+constexpr int kRowChunk = ENT_ROW_CHUNK;    // logits per entropy chunk
+constexpr int kScoreChunk = 64;             // blocks per scoring workgroup
+constexpr int kSplitBlocks = 16;            // kept blocks per decode work item
+constexpr int kMaxGroup = 16;               // query heads per KV head
+constexpr int kMaxBlocksPerSeq = 16384;     // selection keeps all scores in LDS
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+}  // namespace ent
+
+struct ent_ctx {
+  ent_config cfg;
+  int device = 0;
+  int num_cu = 0;
+  int group = 1;            // G = H_q / H_kv
+  int chunks = 0;           // entropy chunks per logit row
+  int score_chunks = 0;     // scoring workgroups per sequence
+  int splits_max = 0;       // decode work items per (sequence, KV head)
+  int decode_grid = 0;      // persistent decode workgroups
+
+  void* ws = nullptr;       // one workspace allocation
+  size_t ws_bytes = 0;
+  float* ent_part = nullptr;      // [max_batch, chunks, 3]  (max, sum, weighted sum)
+  unsigned* ent_ticket = nullptr; // [max_batch]
+  float* stats_tmp = nullptr;     // [max_batch, chunks, 2]  row statistics scratch
+  float* zbuf = nullptr;          // [max_batch, MAXB, H_q]  block logits
+  float* lse_part = nullptr;      // [max_batch, score_chunks, H_q, 2]
+  float* score_ws = nullptr;      // [max_batch, MAXB]       block scores
+  unsigned* sel_ticket = nullptr; // [max_batch]
+  float* dec_acc = nullptr;       // [max_batch * H_kv * splits_max, G, d]
+  float* dec_ml = nullptr;        // [max_batch * H_kv * splits_max, G, 2]
+  unsigned* dec_ticket = nullptr; // [max_batch * H_kv]
+  unsigned* dev_flags = nullptr;  // [1]
+
+  std::string err;
+};
+
+namespace ent {
+
+// Launchers (one per kernel family); each returns the launch status.
+hipError_t launch_entropy(const ent_ctx* c, int B, const float* logits, long long ld,
+                          ent_state st, float* h_out, float* temp_used, float* row_stats,
+                          bool controller, hipStream_t s);
+hipError_t launch_sample(const ent_ctx* c, int B, const float* logits, long long ld,
+                         const float* row_stats, const float* temp_used, const float* uniforms,
+                         int* tokens, hipStream_t s);
+hipError_t launch_block_summary(const ent_ctx* c, int B, const void* k_cache,
+                                const int* tables, const int* ctx_lens, float* ksum,
+                                hipStream_t s);
+hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const float* ksum,
+                               const int* tables, const int* ctx_lens, const float* h,
+                               int* kept, int* n_kept, float* scores, float* theta,
+                               hipStream_t s);
+hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
+                         const void* v_cache, const int* tables, const int* ctx_lens,
+                         const int* kept, const int* n_kept, float* out, float* lse,
+                         hipStream_t s);
+hipError_t launch_kv_append(const ent_ctx* c, int B, const void* k_new, const void* v_new,
+                            const int* tables, int* ctx_lens, void* k_cache, void* v_cache,
+                            float* ksum, hipStream_t s);
+
+// Occupancy-derived persistent grid of the decode kernel.
+int decode_grid_size(const ent_ctx* c);
+
+}  // namespace ent
+
+// ---------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------
+#if defined(__HIPCC__)
+namespace ent {
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Round-to-nearest-even float -> bf16 bits (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_max(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ void raise_flag(unsigned* flags, unsigned f) {
+  atomicOr(flags, f);
+}
+
+}  // namespace ent
+#endif

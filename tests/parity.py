@@ -1,0 +1,188 @@
+"""GPU-vs-oracle comparison of one decode step (used by the GPU tests and smoke()).
+
+Per stage, the oracle is fed the GPU's own upstream values (teacher forcing):
+its entropy for the block budget, its block summaries for the scores, its
+kept list for attention, its temperature for sampling.  Bands:
+
+* entropy, entropic time, temperature: |delta| <= 1e-4 (nats / absolute);
+* kept list: bit-exact, except blocks whose oracle score lies within 1e-6
+  of the oracle threshold; the GPU's list must also be exactly the blocks
+  whose GPU score reaches the k-th largest GPU score, with k the budget the
+  oracle computes (in float32) from the GPU's entropy;
+* attention output and log-sum-exp: |delta| <= 2e-3 + 2e-3 |ref|;
+* token: equal, or, when the oracle's margin to a CDF edge is below 1e-6,
+  a token whose CDF interval contains u within that margin.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import Iterable, List, Optional
+
+import numpy as np
+
+from oracle import attention as OA
+from oracle import blocks as OB
+from oracle import entropy as OE
+from oracle import layout as OL
+from oracle import sample as OS
+
+H_TOL = 1e-4
+THETA_BAND = 1e-6
+ATT_ABS = 2e-3
+ATT_REL = 2e-3
+TOKEN_BAND = 1e-6
+
+
+@dataclass
+class StepResult:
+    """GPU outputs of one step, copied to host (numpy)."""
+    h: np.ndarray
+    tau: np.ndarray
+    temp_next: np.ndarray
+    temp_used: np.ndarray
+    ksum: np.ndarray
+    kept: np.ndarray
+    n_kept: np.ndarray
+    scores: np.ndarray
+    theta: np.ndarray
+    out: np.ndarray
+    lse: np.ndarray
+    tokens: np.ndarray
+
+
+@dataclass
+class Report:
+    failures: List[str] = field(default_factory=list)
+    notes: List[str] = field(default_factory=list)
+    band_exempt: int = 0
+    max_att_err: float = 0.0
+    max_h_err: float = 0.0
+
+    def fail(self, msg):
+        self.failures.append(msg)
+
+    def ok(self):
+        return not self.failures
+
+
+def collect(dev) -> StepResult:
+    c = lambda t: t.detach().cpu().numpy().copy()  # noqa: E731
+    return StepResult(h=c(dev.h), tau=c(dev.tau), temp_next=c(dev.temp), temp_used=c(dev.temp_used),
+                      ksum=c(dev.ksum), kept=c(dev.kept), n_kept=c(dev.n_kept), scores=c(dev.scores),
+                      theta=c(dev.theta), out=c(dev.out), lse=c(dev.lse), tokens=c(dev.tokens))
+
+
+def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev, tau, temp,
+               params, gpu: StepResult, block_size: int = 16, seqs: Optional[Iterable[int]] = None,
+               check_ksum: bool = True, report: Optional[Report] = None) -> Report:
+    """Compare the GPU step `gpu` with the oracle on sequences `seqs` (default all).
+
+    The input arrays are the host copies of what the GPU step consumed
+    (state before the step)."""
+    rep = report or Report()
+    B = len(ctx_lens)
+    for s in (range(B) if seqs is None else seqs):
+        N = int(ctx_lens[s])
+        z = np.asarray(logits[s], dtype=np.float64)
+        T = float(temp[s])
+        # Stage 1: entropy and controller.
+        h_o = OE.entropy(z, T)
+        dh = abs(float(gpu.h[s]) - h_o)
+        rep.max_h_err = max(rep.max_h_err, dh)
+        if dh > H_TOL:
+            rep.fail(f"seq {s}: entropy {gpu.h[s]} vs oracle {h_o}")
+        tau_o = OE.entropic_time(float(tau[s]), float(h_prev[s]), h_o)
+        if abs(float(gpu.tau[s]) - tau_o) > H_TOL:
+            rep.fail(f"seq {s}: tau {gpu.tau[s]} vs oracle {tau_o}")
+        tn_o = OE.temperature_next(T, h_o, params.h_target, params.eta, params.t_min, params.t_max)
+        if abs(float(gpu.temp_next[s]) - tn_o) > H_TOL:
+            rep.fail(f"seq {s}: next temperature {gpu.temp_next[s]} vs oracle {tn_o}")
+        if float(gpu.temp_used[s]) != np.float32(T):
+            rep.fail(f"seq {s}: temp_used {gpu.temp_used[s]} != input temperature {T}")
+
+        # Stage 2: summaries, scores, budget and kept set.
+        K, V = OL.gather_sequence(k_pool, v_pool, tables[s], N, block_size)
+        counts = OB.block_token_counts(N, block_size)
+        nb = len(counts)
+        phys = np.asarray(tables[s][:nb], dtype=np.int64)
+        kbar_g = gpu.ksum[phys].astype(np.float64) if nb else np.zeros((0,) + gpu.ksum.shape[1:])
+        if check_ksum and nb:
+            kbar_o = OB.block_means(K, block_size)
+            err = np.abs(kbar_g - kbar_o)
+            if np.any(err > 1e-5 + 1e-5 * np.abs(kbar_o)):
+                rep.fail(f"seq {s}: block summaries differ by {err.max():.3g}")
+        qs = OL.to_f64(q[s])
+        k_o = OB.keep_budget(float(gpu.h[s]), nb, params)
+        nk = int(gpu.n_kept[s])
+        kept_g = gpu.kept[s][:nk].astype(np.int64)
+        if nb == 0:
+            if nk != 0:
+                rep.fail(f"seq {s}: empty sequence kept {nk} blocks")
+        else:
+            I_o, _, _ = OB.block_scores(qs, kbar_g, counts, params.scale)
+            I_g = gpu.scores[s][:nb].astype(np.float32)
+            serr = np.abs(I_g.astype(np.float64) - I_o)
+            if np.any(serr > 1e-6 + 1e-4 * np.abs(I_o)):
+                rep.fail(f"seq {s}: block scores differ by {serr.max():.3g}")
+            _, theta_o = OB.select_blocks(I_o, k_o)
+            # GPU self-consistency, bit-exact on its own scores.
+            if k_o > 0:
+                theta_g_expect = np.sort(I_g)[::-1][k_o - 1]
+                if np.float32(gpu.theta[s]) != theta_g_expect:
+                    rep.fail(f"seq {s}: GPU threshold {gpu.theta[s]} is not the k={k_o}-th "
+                             f"largest GPU score {theta_g_expect}")
+                expect = np.nonzero(I_g >= np.float32(gpu.theta[s]))[0]
+                if not np.array_equal(expect, kept_g):
+                    rep.fail(f"seq {s}: GPU kept list is not its scores >= its threshold")
+            elif nk != 0:
+                rep.fail(f"seq {s}: budget 0 but {nk} blocks kept")
+            # Oracle band.
+            must = set(np.nonzero(I_o > theta_o + THETA_BAND)[0].tolist())
+            never = set(np.nonzero(I_o < theta_o - THETA_BAND)[0].tolist())
+            kg = set(kept_g.tolist())
+            if not must <= kg:
+                rep.fail(f"seq {s}: {len(must - kg)} blocks above the threshold band not kept")
+            if kg & never:
+                rep.fail(f"seq {s}: {len(kg & never)} blocks below the threshold band kept")
+            rep.band_exempt += int(np.sum(np.abs(I_o - theta_o) <= THETA_BAND))
+
+        # Stage 3: attention over the GPU's kept blocks.
+        o_ref, lse_ref = OA.sparse_decode(qs, K, V, kept_g, block_size, params.scale)
+        o_g = gpu.out[s].astype(np.float64)
+        err = np.abs(o_g - o_ref)
+        rep.max_att_err = max(rep.max_att_err, float(err.max(initial=0.0)))
+        if np.any(err > ATT_ABS + ATT_REL * np.abs(o_ref)):
+            rep.fail(f"seq {s}: attention output differs by {err.max():.3g}")
+        lg = gpu.lse[s].astype(np.float64)
+        fin = np.isfinite(lse_ref)
+        if not np.array_equal(fin, np.isfinite(lg)) or \
+                np.any(np.abs(lg[fin] - lse_ref[fin]) > ATT_ABS + ATT_REL * np.abs(lse_ref[fin])):
+            rep.fail(f"seq {s}: attention log-sum-exp differs")
+
+        # Stage 4: sampling at the GPU's temperature.
+        Tu = float(gpu.temp_used[s])
+        u = float(uniforms[s])
+        x_o, margin = OS.sample(z, Tu, u)
+        x_g = int(gpu.tokens[s])
+        if x_g != x_o:
+            ok = False
+            if margin < TOKEN_BAND and 0 <= x_g < len(z):
+                lo, hi = OS.cdf_interval(z, Tu, x_g)
+                ok = (lo - TOKEN_BAND <= u < hi + TOKEN_BAND) and hi > lo
+            if not ok:
+                rep.fail(f"seq {s}: token {x_g} vs oracle {x_o} (margin {margin:.3g})")
+            else:
+                rep.notes.append(f"seq {s}: token {x_g} accepted in the tie band (oracle {x_o})")
+    return rep
+
+
+def run_step(dec, dev, step: int = 0, stream=None):
+    """Issue one decode step of the uploaded inputs on the library (no sync)."""
+    B = dev.ctx_lens.shape[0]
+    dec.step(B, logits=dev.logits[step], h_prev=dev.h_prev, tau=dev.tau, temp=dev.temp,
+             q=dev.q[step], k_cache=dev.k_pool, v_cache=dev.v_pool, block_tables=dev.block_tables,
+             ctx_lens=dev.ctx_lens, ksum=dev.ksum, uniforms=dev.uniforms[step], h=dev.h,
+             temp_used=dev.temp_used, row_stats=dev.row_stats, kept=dev.kept, n_kept=dev.n_kept,
+             out=dev.out, tokens=dev.tokens, lse=dev.lse, scores=dev.scores, theta=dev.theta,
+             stream=stream)
