@@ -29,6 +29,7 @@ class Workload:
     kv_dtype: str                 # "f32" or "bf16" (queries use the same dtype)
     vocab: int
     ctx: Tuple                    # ("uniform", lo, hi) | ("lognormal", median, sigma, lo, hi)
+                                  # | ("fixed", [lengths])
     logits: str                   # "normal" | "zipf_flat"
     logit_scale: Tuple[float, float]   # U[lo, hi] of the per-sequence logit std
     h_target: float
@@ -44,7 +45,11 @@ class Workload:
 
     @property
     def ctx_max(self) -> int:
-        return int(self.ctx[2] if self.ctx[0] == "uniform" else self.ctx[4])
+        if self.ctx[0] == "uniform":
+            return int(self.ctx[2])
+        if self.ctx[0] == "fixed":
+            return int(max(self.ctx[1]))
+        return int(self.ctx[4])
 
     @property
     def max_blocks_per_seq(self) -> int:
