@@ -1,0 +1,235 @@
+"""Benchmark of one entropic-time decode step on one MI355X.
+
+A step is the whole hot path over one batch: entropy and controller
+(ent_entropy_temperature), block scoring and selection (ent_block_select),
+kept-block decode attention (ent_sparse_paged_decode) and sampling
+(ent_sample).  Inputs are seeded synthetic data of the named workload,
+resident in HBM before timing; two copies of every input rotate between
+steps so the 256 MB Infinity Cache cannot serve a step from the previous
+one, and every step starts from a fresh copy of the controller state, so all
+timed steps do identical work.
+
+Prints one JSON line: decode steps/s, the achieved HBM rate on kept KV +
+logit bytes, the roofline of the dominant kernel (decode attention, timed
+with HIP events on its own stream), and the float64 oracle timed on the
+host's cores on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "decode steps/sec and achieved HBM GB/s (kept KV + logits) vs peak, 1 MI355X"
+COUNTERS = os.path.join(ROOT, "profiles", "decode_counters.json")
+DECODE_SRC = os.path.join(ROOT, "paper_2603_03310_amd", "csrc", "decode.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama3_8b_decode")
+    ap.add_argument("--copies", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    return ap.parse_args()
+
+
+def kv_bytes_kept(x, n_kept, kept, elem):
+    """Bytes of K and V in the kept blocks (valid tokens only)."""
+    w = x.workload
+    per_tok = w.num_kv_heads * w.head_dim * 2 * elem
+    tot = 0
+    for s in range(w.batch):
+        N = int(x.ctx_lens[s])
+        nb = -(-N // 16)
+        ks = kept[s][: int(n_kept[s])]
+        toks = 16 * len(ks)
+        if nb and (nb - 1) in set(ks.tolist()):
+            toks -= 16 - (N - 16 * (nb - 1))
+        tot += toks * per_tok
+    return tot
+
+
+def cpu_baseline(x, p, seconds):
+    """The float64 oracle on the host, single thread, on the first sequences of
+    the step until `seconds` of work; scaled to whole steps per second."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import step as St
+    B = x.workload.batch
+    done = 0
+    t0 = time.perf_counter()
+    with threadpool_limits(limits=1):
+        while done < B and time.perf_counter() - t0 < seconds:
+            St.sequence_step(done, k_pool=x.k_pool, v_pool=x.v_pool, tables=x.block_tables,
+                             ctx_lens=x.ctx_lens, q=x.q[0], logits=x.logits[0], h_prev=x.h_prev,
+                             tau=x.tau, temp=x.temp, uniforms=x.uniforms[0], params=p,
+                             block_size=16)
+            done += 1
+    el = time.perf_counter() - t0
+    return {"value": (done / B) / el, "unit": "steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"float64 oracle, all stages, sequences 0..{done - 1} of {B} of one "
+                      f"{x.workload.name} step ({el:.1f} s, one thread); scaled to a whole step"}
+
+
+def traffic_from_counters():
+    """HBM bytes per decode launch from committed rocprofv3 counters, if they
+    were taken on the current decode kernel source (else None)."""
+    if not os.path.exists(COUNTERS):
+        return None
+    with open(COUNTERS) as f:
+        c = json.load(f)
+    src = hashlib.sha256(open(DECODE_SRC, "rb").read()).hexdigest()
+    if c.get("decode_src_sha256") != src:
+        return None
+    return c.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2603_03310_amd import ent
+    from synth import WORKLOADS, default_params, generate
+    from synth.device import config_fields, upload
+
+    ent.load()
+    w = WORKLOADS[args.workload]
+    if w.steps != 1:
+        raise SystemExit("bench.py times single decode steps; closed loops are parity cases")
+    p = default_params(w)
+    t0 = time.perf_counter()
+    x = generate(w)
+    print(f"[bench] generated {w.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
+          flush=True)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    copies = [upload(x, dev) for _ in range(max(1, args.copies))]
+    B = w.batch
+    K, W = args.steps, args.warmup
+    nslots = K + W
+    init = torch.stack([torch.from_numpy(x.h_prev), torch.from_numpy(x.tau),
+                        torch.from_numpy(x.temp)]).to(dev)
+    states = [init.unsqueeze(0).repeat(nslots, 1, 1).contiguous() for _ in range(2)]
+    cfg = ent.ent_config()
+    for k, v in config_fields(w, p, x.num_pool_blocks).items():
+        setattr(cfg, k, v)
+    ctx = ent.ent_init(cfg)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    for c in copies:
+        ent.ent_block_summary(ctx, B, c.k_pool, c.block_tables, c.ctx_lens, c.ksum, sp)
+    o = copies[0]          # outputs shared by all copies
+    ld = x.logits.shape[2]
+
+    def issue(i, st, ev=None):
+        c = copies[i % len(copies)]
+        hp, ta, te = st[i, 0], st[i, 1], st[i, 2]
+        if ev: ev[0].record(stream)
+        ent.ent_entropy_temperature(ctx, B, c.logits[0], ld, hp, ta, te, o.h, o.temp_used,
+                                    o.row_stats, sp)
+        if ev: ev[1].record(stream)
+        ent.ent_block_select(ctx, B, c.q[0], c.ksum, c.block_tables, c.ctx_lens, o.h, o.kept,
+                             o.n_kept, None, None, sp)
+        if ev: ev[2].record(stream)
+        ent.ent_sparse_paged_decode(ctx, B, c.q[0], c.k_pool, c.v_pool, c.block_tables,
+                                    c.ctx_lens, o.kept, o.n_kept, o.out, o.lse, sp)
+        if ev: ev[3].record(stream)
+        ent.ent_sample(ctx, B, c.logits[0], ld, o.row_stats, o.temp_used, c.uniforms[0],
+                       o.tokens, sp)
+        if ev: ev[4].record(stream)
+
+    # Pass A: the timed steps, nothing between the launches.
+    for i in range(W):
+        issue(i, states[0])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for i in range(W, W + K):
+        issue(i, states[0])
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    ms_step = e0.elapsed_time(e1) / K
+
+    # Pass B: the same steps with an event around every entry point (per-kernel times).
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
+    for i in range(W):
+        issue(i, states[1])
+    for i in range(K):
+        issue(W + i, states[1], evs[i])
+    torch.cuda.synchronize()
+    names = ["entropy_temperature", "block_select", "sparse_paged_decode", "sample"]
+    per_k = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(K)])) * 1e3
+             for j, n in enumerate(names)}
+    flags = ent.ent_device_status(ctx, sp)
+    if flags:
+        raise SystemExit(f"device flags raised: {flags}")
+
+    n_kept = o.n_kept.cpu().numpy()
+    kept = o.kept.cpu().numpy()
+    elem = 2 if w.kv_dtype == "bf16" else 4
+    kv_kept = kv_bytes_kept(x, n_kept, kept, elem)
+    logit_bytes = 4 * B * w.vocab
+    metric_bytes = kv_kept + logit_bytes
+    nb_tot = int(sum(-(-int(n) // 16) for n in x.ctx_lens))
+    kept_frac = float(n_kept.sum()) / max(1, nb_tot)
+    steps_per_s = 1e3 / ms_step
+    gbps = metric_bytes / (ms_step * 1e-3) / 1e9
+
+    # Decode kernel roofline: algorithmic bytes of one launch / its average duration.
+    Hq, d = w.num_q_heads, w.head_dim
+    dec_bytes = (kv_kept + B * Hq * d * elem + B * Hq * d * 4 + B * Hq * 4
+                 + 2 * 4 * int(n_kept.sum()) + 4 * B)
+    dec_us = per_k["sparse_paged_decode"]
+    achieved = dec_bytes / (dec_us * 1e-6) / 1e9
+    ent.ent_destroy(ctx)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(x, p, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC, "value": round(steps_per_s, 3), "unit": "steps/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; shapes and value recipes of the workload)",
+        "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": w.num_kv_heads,
+                   "head_dim": d, "block_size": 16, "ctx": list(w.ctx), "vocab": w.vocab,
+                   "kv_dtype": w.kv_dtype},
+        "hbm_gbps_kept_kv_plus_logits": round(gbps, 1),
+        "hbm_frac_kept_kv_plus_logits": round(gbps / HBM_PEAK_GBPS, 4),
+        "metric_bytes_per_step": int(metric_bytes),
+        "kept_block_fraction": round(kept_frac, 4),
+        "per_kernel_us": {k: round(v, 2) for k, v in per_k.items()},
+        "wall_ms_per_step": round(wall_ms / K, 5),
+        "roofline": {"kernel": "sparse_paged_decode", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic_from_counters(),
+                     "bytes_per_launch": int(dec_bytes), "avg_launch_us": round(dec_us, 2)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
