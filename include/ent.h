@@ -69,7 +69,8 @@ enum { ENT_F32 = 0, ENT_BF16 = 1 };
 typedef struct {
   int max_batch;           /* largest B any call will pass, >= 1 */
   int num_q_heads;         /* H_q */
-  int num_kv_heads;        /* H_kv; H_q % H_kv == 0, G = H_q / H_kv <= 16 */
+  int num_kv_heads;        /* H_kv; H_q % H_kv == 0, G = H_q / H_kv in {1,2,4,8,16},
+                              H_q <= 128, H_kv * head_dim <= 2048 */
   int head_dim;            /* d: 64 or 128 */
   int block_size;          /* tokens per KV block: must be 16 */
   int max_blocks_per_seq;  /* MAXB: row length of block_tables, <= 16384 */

@@ -49,6 +49,7 @@ std::string check_config(const ent_config* c, int* code) {
     return "num_q_heads / num_kv_heads must be 1, 2, 4, 8 or 16";
   if (c->num_q_heads > kMaxQHeads) return "num_q_heads must be <= 128";
   if (c->max_blocks_per_seq > ent::kMaxBlocksPerSeq) return "max_blocks_per_seq must be <= 16384";
+  if (c->num_kv_heads * c->head_dim > 2048) return "num_kv_heads * head_dim must be <= 2048";
   if (c->vocab > kMaxVocab) return "vocab must be <= 1048576";
   *code = ENT_OK;
   return "";
@@ -144,19 +145,15 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
 
   const size_t Bm = static_cast<size_t>(f.max_batch);
   const size_t sz_ent_part = align_up(Bm * c->chunks * 3 * sizeof(float));
-  const size_t sz_ent_ticket = align_up(Bm * sizeof(unsigned));
   const size_t sz_stats = align_up(Bm * c->chunks * 2 * sizeof(float));
   const size_t sz_z = align_up(Bm * f.max_blocks_per_seq * f.num_q_heads * sizeof(float));
   const size_t sz_lse = align_up(Bm * c->score_chunks * f.num_q_heads * 2 * sizeof(float));
   const size_t sz_score = align_up(Bm * f.max_blocks_per_seq * sizeof(float));
-  const size_t sz_sel_ticket = align_up(Bm * sizeof(unsigned));
   const size_t nslots = Bm * f.num_kv_heads * c->splits_max;
   const size_t sz_acc = align_up(nslots * c->group * f.head_dim * sizeof(float));
   const size_t sz_ml = align_up(nslots * c->group * 2 * sizeof(float));
-  const size_t sz_dec_ticket = align_up(Bm * f.num_kv_heads * sizeof(unsigned));
   const size_t sz_flags = align_up(sizeof(unsigned));
-  c->ws_bytes = sz_ent_part + sz_ent_ticket + sz_stats + sz_z + sz_lse + sz_score +
-                sz_sel_ticket + sz_acc + sz_ml + sz_dec_ticket + sz_flags;
+  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_score + sz_acc + sz_ml + sz_flags;
   e = hipMalloc(&c->ws, c->ws_bytes);
   if (e != hipSuccess) {
     g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
@@ -174,15 +171,12 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   char* p = static_cast<char*>(c->ws);
   auto take = [&p](size_t n) { char* r = p; p += n; return r; };
   c->ent_part = reinterpret_cast<float*>(take(sz_ent_part));
-  c->ent_ticket = reinterpret_cast<unsigned*>(take(sz_ent_ticket));
   c->stats_tmp = reinterpret_cast<float*>(take(sz_stats));
   c->zbuf = reinterpret_cast<float*>(take(sz_z));
   c->lse_part = reinterpret_cast<float*>(take(sz_lse));
   c->score_ws = reinterpret_cast<float*>(take(sz_score));
-  c->sel_ticket = reinterpret_cast<unsigned*>(take(sz_sel_ticket));
   c->dec_acc = reinterpret_cast<float*>(take(sz_acc));
   c->dec_ml = reinterpret_cast<float*>(take(sz_ml));
-  c->dec_ticket = reinterpret_cast<unsigned*>(take(sz_dec_ticket));
   c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));
   c->decode_grid = ent::decode_grid_size(c);
   *out = c;

@@ -12,12 +12,11 @@
 //
 // Kernels:
 //   summary_kernel   per-block mean keys (setup)
-//   score_kernel     z for 64 blocks x all heads per workgroup; per-chunk
-//                    log-sum-exp partials per head
-//   select_kernel    merges the partials, computes I_b for its 64 blocks; the
-//                    last workgroup of a sequence (atomic ticket) runs a 4-pass
-//                    8-bit radix select for the k-th largest score and compacts
-//                    the kept blocks in ascending order with wave ballots
+//   score_kernel        z for 64 blocks x all heads per workgroup; per-chunk
+//                       log-sum-exp partials per head
+//   block_score_kernel  merges the partials into L_h and computes I_b
+//   select_kernel       per sequence: budget, 4-pass 8-bit radix select of the
+//                       k-th largest score, ascending compaction with ballots
 //   append_kernel    writes one token and refreshes its block's mean key
 
 #include "ent_internal.h"
@@ -106,12 +105,17 @@ __global__ __launch_bounds__(kThreads) void append_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Scoring.  Lane layout: a group of L = D/4 lanes covers one (block, KV head)
-// summary, 4 dims per lane (float4 loads, fully coalesced); a wave covers
-// U = 64/L KV heads per instruction.  Each lane forms G partial dot products
-// (one per query head of its KV head); a halving butterfly reduces them over
-// the L lanes, leaving head r = li * G / L in lane li.
+// Scoring.  A workgroup takes 64 blocks of one sequence (16 per wave).  The
+// query heads are staged once in LDS as fp32.  A block's summary
+// (H_kv x d floats) is read as NP passes of 256 floats, one float4 per lane
+// per pass, fully coalesced; the next block's passes are prefetched while the
+// current one is reduced.  In a pass, a group of L = d/4 lanes covers one KV
+// head: each lane forms G partial dot products (one per query head of that KV
+// head) and a halving butterfly reduces them over the L lanes, leaving head
+// r = li * G / L in lane li.
 // ---------------------------------------------------------------------------
+constexpr int kMaxPasses = 8;               // H_kv * d <= 2048
+
 template <int G, int L>
 __device__ __forceinline__ float reduce_heads(float (&a)[G], int li) {
 #pragma unroll
@@ -130,20 +134,14 @@ __device__ __forceinline__ float reduce_heads(float (&a)[G], int li) {
   return v;
 }
 
-template <typename T>
-__device__ __forceinline__ void load_q4(const T* p, float (&o)[4]);
-template <>
-__device__ __forceinline__ void load_q4<float>(const float* p, float (&o)[4]) {
-  const float4 x = *reinterpret_cast<const float4*>(p);
-  o[0] = x.x; o[1] = x.y; o[2] = x.z; o[3] = x.w;
-}
-template <>
-__device__ __forceinline__ void load_q4<uint16_t>(const uint16_t* p, float (&o)[4]) {
-  const uint2 x = *reinterpret_cast<const uint2*>(p);
-  o[0] = bf16_to_f32(static_cast<uint16_t>(x.x & 0xffffu));
-  o[1] = bf16_to_f32(static_cast<uint16_t>(x.x >> 16));
-  o[2] = bf16_to_f32(static_cast<uint16_t>(x.y & 0xffffu));
-  o[3] = bf16_to_f32(static_cast<uint16_t>(x.y >> 16));
+__device__ __forceinline__ void load_summary(const float* __restrict__ base, int n_floats, int np,
+                                             int lane, float4 (&kv)[kMaxPasses]) {
+#pragma unroll
+  for (int k = 0; k < kMaxPasses; ++k) {
+    const int f = 256 * k + 4 * lane;
+    if (k < np && f < n_floats) kv[k] = *reinterpret_cast<const float4*>(base + f);
+    else kv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
 }
 
 template <typename T, int D, int G>
@@ -152,57 +150,72 @@ __global__ __launch_bounds__(kThreads) void score_kernel(
     const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
     int Hkv, int MAXB, int P, int nch, float scale, unsigned* flags) {
   constexpr int L = D / 4;
-  constexpr int U = 64 / L;
   static_assert(G <= L, "heads per KV head exceed the lane group");
-  extern __shared__ float zt[];              // [kScoreChunk][Hq]
+  extern __shared__ float smem[];            // q [Hq][D] fp32, then z tile [kScoreChunk][Hq]
   const int Hq = Hkv * G;
+  float* qs = smem;
+  float* zt = smem + Hq * D;
   const int ch = blockIdx.x, b = blockIdx.y;
   const int N = ctx_lens[b];
-  if (N < 0 || N > MAXB * kBlock) return;    // flagged by the select kernel
+  if (N < 0 || N > MAXB * kBlock) return;    // flagged by the selection kernel
   const int nb = (N + kBlock - 1) / kBlock;
   const int j_lo = ch * kScoreChunk;
   if (j_lo >= nb) return;
   const int nblk = min(kScoreChunk, nb - j_lo);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int u = lane / L, li = lane % L;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int li = lane % L;
   const int* trow = tables + static_cast<long long>(b) * MAXB;
 
-  for (int gp = 0; gp * U < Hkv; ++gp) {
-    const int g = gp * U + u;
-    const bool gv = g < Hkv;
-    float qv[G][4];
-#pragma unroll
-    for (int r = 0; r < G; ++r) {
-      if (gv) {
-        load_q4<T>(q + (static_cast<long long>(b) * Hq + g * G + r) * D + 4 * li, qv[r]);
-      } else {
-        qv[r][0] = qv[r][1] = qv[r][2] = qv[r][3] = 0.f;
-      }
-    }
-    for (int i = wave; i < nblk; i += 4) {
-      int p = trow[j_lo + i];
-      if (p < 0 || p >= P) {
-        if (lane == 0) raise_flag(flags, ENT_DEV_BAD_TABLE);
-        p = 0;
-      }
-      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (gv) kv = *reinterpret_cast<const float4*>(ksum + (static_cast<long long>(p) * Hkv + g) * D + 4 * li);
-      float a[G];
-#pragma unroll
-      for (int r = 0; r < G; ++r)
-        a[r] = qv[r][0] * kv.x + qv[r][1] * kv.y + qv[r][2] * kv.z + qv[r][3] * kv.w;
-      const float z = reduce_heads<G, L>(a, li) * scale;
-      const int r = li / (L / G);
-      if (gv && (li % (L / G)) == 0) zt[i * Hq + g * G + r] = z;
+  for (int e = t; e < Hq * D; e += kThreads)
+    qs[e] = load_elem<T>(q + static_cast<long long>(b) * Hq * D + e);
+  // Physical blocks of this wave's 16 blocks, one per lane.
+  const int jw = wave * 16;
+  int my_p = 0;
+  if (lane < 16 && jw + lane < nblk) {
+    my_p = trow[j_lo + jw + lane];
+    if (my_p < 0 || my_p >= P) {
+      raise_flag(flags, ENT_DEV_BAD_TABLE);
+      my_p = 0;
     }
   }
   __syncthreads();
+
+  const int nfl = Hkv * D;
+  const int np = (nfl + 255) / 256;
+  const int nmine = max(0, min(16, nblk - jw));
+  float4 cur[kMaxPasses], nxt[kMaxPasses];
+  if (nmine > 0)
+    load_summary(ksum + static_cast<long long>(__shfl(my_p, 0)) * nfl, nfl, np, lane, cur);
+  for (int i = 0; i < nmine; ++i) {
+    if (i + 1 < nmine)
+      load_summary(ksum + static_cast<long long>(__shfl(my_p, i + 1)) * nfl, nfl, np, lane, nxt);
+    const int jl = jw + i;
+#pragma unroll
+    for (int k = 0; k < kMaxPasses; ++k) {
+      if (k >= np) continue;
+      const int f = 256 * k + 4 * lane;
+      const bool gv = f < nfl;
+      const int g = f / D, dd = f % D;
+      float a[G];
+#pragma unroll
+      for (int r = 0; r < G; ++r) {
+        float4 qq = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (gv) qq = *reinterpret_cast<const float4*>(qs + (g * G + r) * D + dd);
+        a[r] = qq.x * cur[k].x + qq.y * cur[k].y + qq.z * cur[k].z + qq.w * cur[k].w;
+      }
+      const float z = reduce_heads<G, L>(a, li) * scale;
+      if (gv && (li % (L / G)) == 0) zt[jl * Hq + g * G + li / (L / G)] = z;
+    }
+#pragma unroll
+    for (int k = 0; k < kMaxPasses; ++k) cur[k] = nxt[k];
+  }
+  __syncthreads();
   float* zrow = zbuf + (static_cast<long long>(b) * MAXB + j_lo) * Hq;
-  for (int e = threadIdx.x; e < nblk * Hq; e += kThreads) zrow[e] = zt[e];
+  for (int e = t; e < nblk * Hq; e += kThreads) zrow[e] = zt[e];
   // Per-head log-sum-exp of l = z + ln n_b over this chunk's blocks.
   const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
   const float ln_full = logf(static_cast<float>(kBlock));
-  for (int h = threadIdx.x; h < Hq; h += kThreads) {
+  for (int h = t; h < Hq; h += kThreads) {
     float m = -INFINITY;
     for (int i = 0; i < nblk; ++i) {
       const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
@@ -216,6 +229,53 @@ __global__ __launch_bounds__(kThreads) void score_kernel(
     float* lp = lse_part + ((static_cast<long long>(b) * nch + ch) * Hq + h) * 2;
     lp[0] = m;
     lp[1] = s;
+  }
+}
+
+// Block scores I_b of one chunk of 64 blocks: merges the per-chunk
+// log-sum-exp partials into L_h, then 4 threads per block sum over heads.
+__global__ __launch_bounds__(kThreads) void block_score_kernel(
+    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, float* __restrict__ score_ws, float* __restrict__ scores_out,
+    int Hq, int MAXB, int nch_max) {
+  __shared__ float sL[128];
+  const int ch = blockIdx.x, b = blockIdx.y;
+  const int t = threadIdx.x;
+  const int N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) return;
+  const int nb = (N + kBlock - 1) / kBlock;
+  const int j_lo = ch * kScoreChunk;
+  if (j_lo >= nb) return;
+  const int nblk = min(kScoreChunk, nb - j_lo);
+  const int nch = (nb + kScoreChunk - 1) / kScoreChunk;
+  for (int h = t; h < Hq; h += kThreads) {
+    const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
+    float m = -INFINITY;
+    for (int c = 0; c < nch; ++c) m = fmaxf(m, lp[c * Hq * 2]);
+    float s = 0.f;
+    for (int c = 0; c < nch; ++c) s += lp[c * Hq * 2 + 1] * expf(lp[c * Hq * 2] - m);
+    sL[h] = m + logf(s);
+  }
+  __syncthreads();
+  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
+  const float ln_full = logf(static_cast<float>(kBlock));
+  const int i = t >> 2, q4 = t & 3;
+  float acc = 0.f;
+  if (i < nblk) {
+    const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
+    const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j_lo + i) * Hq;
+    for (int h = q4; h < Hq; h += 4) {
+      const float z = zr[h];
+      const float Lh = sL[h];
+      acc += expf(z + lnn - Lh) * (Lh - z);
+    }
+  }
+  acc += __shfl_xor(acc, 1);
+  acc += __shfl_xor(acc, 2);
+  if (i < nblk && q4 == 0) {
+    const float I = __fdiv_rn(acc, static_cast<float>(Hq));
+    score_ws[static_cast<long long>(b) * MAXB + j_lo + i] = I;
+    if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j_lo + i] = I;
   }
 }
 
@@ -240,22 +300,22 @@ __device__ __forceinline__ int keep_budget(float h, int nb, float eps_h, float h
   return min(nb, max(min(b_min, nb), k));
 }
 
+// Kept set of one sequence (one workgroup): budget k from the entropy, the
+// k-th largest score by a 4-pass 8-bit radix select over the scores held in
+// LDS, then ascending compaction of {b : I_b >= theta} with wave ballots.
 __global__ __launch_bounds__(kThreads) void select_kernel(
-    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, const float* __restrict__ hvec,
-    float* __restrict__ score_ws, float* __restrict__ scores_out, float* __restrict__ theta_out,
-    int* __restrict__ kept, int* __restrict__ n_kept, unsigned* __restrict__ ticket,
-    int Hq, int MAXB, int nch_max, float eps_h, float h_min, float log_v, float kappa_min,
+    const float* __restrict__ score_ws, const int* __restrict__ ctx_lens,
+    const float* __restrict__ hvec, float* __restrict__ theta_out, int* __restrict__ kept,
+    int* __restrict__ n_kept, int MAXB, float eps_h, float h_min, float log_v, float kappa_min,
     int b_min, unsigned* flags) {
-  extern __shared__ unsigned keys[];        // [MAXB] (also holds L_h before selection)
+  extern __shared__ unsigned keys[];        // [MAXB]
   __shared__ unsigned hist[256];
-  __shared__ int s_last, s_digit, s_krem, s_wcnt[4];
-  __shared__ float sL[128];
-  const int ch = blockIdx.x, b = blockIdx.y;
+  __shared__ int s_digit, s_krem, s_wcnt[4];
+  const int b = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int N = ctx_lens[b];
   if (N < 0 || N > MAXB * kBlock) {
-    if (ch == 0 && t == 0) {
+    if (t == 0) {
       raise_flag(flags, ENT_DEV_BAD_CTXLEN);
       n_kept[b] = 0;
       if (theta_out) theta_out[b] = INFINITY;
@@ -263,141 +323,84 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     return;
   }
   const int nb = (N + kBlock - 1) / kBlock;
-  if (nb == 0) {
-    if (ch == 0 && t == 0) {
+  const int k = keep_budget(hvec[b], nb, eps_h, h_min, log_v, kappa_min, b_min);
+  if (k <= 0) {
+    if (t == 0) {
       n_kept[b] = 0;
       if (theta_out) theta_out[b] = INFINITY;
     }
     return;
   }
-  const int j_lo = ch * kScoreChunk;
-  if (j_lo >= nb) return;
-  const int nblk = min(kScoreChunk, nb - j_lo);
-  const int nch = (nb + kScoreChunk - 1) / kScoreChunk;
-
-  // L_h = ln sum_b n_b e^{z_bh}, merged from the per-chunk partials.
-  for (int h = t; h < Hq; h += kThreads) {
-    const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
-    float m = -INFINITY;
-    for (int c = 0; c < nch; ++c) m = fmaxf(m, lp[c * Hq * 2]);
-    float s = 0.f;
-    for (int c = 0; c < nch; ++c) s += lp[c * Hq * 2 + 1] * expf(lp[c * Hq * 2] - m);
-    sL[h] = m + logf(s);
-  }
-  __syncthreads();
-
-  // Scores of this chunk's blocks: 4 threads per block, heads strided by 4.
-  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
-  const float ln_full = logf(static_cast<float>(kBlock));
-  {
-    const int i = t >> 2, q4 = t & 3;
-    float acc = 0.f;
-    if (i < nblk) {
-      const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
-      const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j_lo + i) * Hq;
-      for (int h = q4; h < Hq; h += 4) {
-        const float z = zr[h];
-        const float Lh = sL[h];
-        acc += expf(z + lnn - Lh) * (Lh - z);
-      }
-    }
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
-    if (i < nblk && q4 == 0) {
-      const float I = __fdiv_rn(acc, static_cast<float>(Hq));
-      score_ws[static_cast<long long>(b) * MAXB + j_lo + i] = I;
-      if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j_lo + i] = I;
-    }
-  }
-
-  // The last workgroup of this sequence selects.
-  __syncthreads();
-  if (t == 0) {
-    __threadfence();
-    const unsigned prev = atomicAdd(&ticket[b], 1u);
-    s_last = (prev == static_cast<unsigned>(nch - 1));
-    if (s_last) __threadfence();
-  }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-
-  const int k = keep_budget(hvec[b], nb, eps_h, h_min, log_v, kappa_min, b_min);
   for (int i = t; i < nb; i += kThreads)
     keys[i] = float_key(score_ws[static_cast<long long>(b) * MAXB + i]);
   if (t == 0) s_krem = k;
   __syncthreads();
 
   unsigned prefix = 0u, mask = 0u;
-  if (k > 0) {
-    for (int pass = 0; pass < 4; ++pass) {
-      const int shift = 24 - 8 * pass;
-      hist[t] = 0u;
-      __syncthreads();
-      for (int i = t; i < nb; i += kThreads) {
-        const unsigned key = keys[i];
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-      }
-      __syncthreads();
-      if (wave == 0) {
-        // Bins 4*lane .. 4*lane+3; suffix sums over lanes locate the digit
-        // holding the k_rem-th largest remaining key.
-        const unsigned c0 = hist[4 * lane], c1 = hist[4 * lane + 1], c2 = hist[4 * lane + 2],
-                       c3 = hist[4 * lane + 3];
-        const unsigned cl = c0 + c1 + c2 + c3;
-        unsigned suf = cl;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const unsigned n = __shfl_down(suf, o);
-          if (lane + o < 64) suf += n;
-        }
-        const unsigned krem = static_cast<unsigned>(s_krem);
-        const unsigned above = suf - cl;     // keys in higher lanes' bins
-        if (above < krem && suf >= krem) {
-          unsigned run = above;
-          const unsigned cs[4] = {c0, c1, c2, c3};
-          int d = 4 * lane;
-          for (int x = 3; x >= 0; --x) {
-            if (run + cs[x] >= krem) {
-              d = 4 * lane + x;
-              break;
-            }
-            run += cs[x];
-          }
-          s_digit = d;
-          s_krem = static_cast<int>(krem - run);
-        }
-      }
-      __syncthreads();
-      prefix |= static_cast<unsigned>(s_digit) << shift;
-      mask |= 255u << shift;
-      __syncthreads();
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    hist[t] = 0u;
+    __syncthreads();
+    for (int i = t; i < nb; i += kThreads) {
+      const unsigned key = keys[i];
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
     }
+    __syncthreads();
+    if (wave == 0) {
+      // Bins 4*lane .. 4*lane+3; suffix sums over lanes locate the digit
+      // holding the k_rem-th largest remaining key.
+      const unsigned c0 = hist[4 * lane], c1 = hist[4 * lane + 1], c2 = hist[4 * lane + 2],
+                     c3 = hist[4 * lane + 3];
+      const unsigned cl = c0 + c1 + c2 + c3;
+      unsigned suf = cl;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const unsigned n = __shfl_down(suf, o);
+        if (lane + o < 64) suf += n;
+      }
+      const unsigned krem = static_cast<unsigned>(s_krem);
+      const unsigned above = suf - cl;       // keys in higher lanes' bins
+      if (above < krem && suf >= krem) {
+        unsigned run = above;
+        const unsigned cs[4] = {c0, c1, c2, c3};
+        int d = 4 * lane;
+        for (int x = 3; x >= 0; --x) {
+          if (run + cs[x] >= krem) {
+            d = 4 * lane + x;
+            break;
+          }
+          run += cs[x];
+        }
+        s_digit = d;
+        s_krem = static_cast<int>(krem - run);
+      }
+    }
+    __syncthreads();
+    prefix |= static_cast<unsigned>(s_digit) << shift;
+    mask |= 255u << shift;
+    __syncthreads();
   }
   const unsigned tkey = prefix;
 
   // Compaction in ascending block order.
   int total = 0;
   int* krow = kept + static_cast<long long>(b) * MAXB;
-  if (k > 0) {
-    for (int base = 0; base < nb; base += kThreads) {
-      const int i = base + t;
-      const bool f = i < nb && keys[i] >= tkey;
-      const unsigned long long bal = __ballot(f);
-      const int rank = __popcll(bal & ((1ull << lane) - 1ull));
-      if (lane == 0) s_wcnt[wave] = __popcll(bal);
-      __syncthreads();
-      int off = total;
-      for (int w = 0; w < wave; ++w) off += s_wcnt[w];
-      if (f) krow[off + rank] = i;
-      total += s_wcnt[0] + s_wcnt[1] + s_wcnt[2] + s_wcnt[3];
-      __syncthreads();
-    }
+  for (int base = 0; base < nb; base += kThreads) {
+    const int i = base + t;
+    const bool f = i < nb && keys[i] >= tkey;
+    const unsigned long long bal = __ballot(f);
+    const int rank = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) s_wcnt[wave] = __popcll(bal);
+    __syncthreads();
+    int off = total;
+    for (int w = 0; w < wave; ++w) off += s_wcnt[w];
+    if (f) krow[off + rank] = i;
+    total += s_wcnt[0] + s_wcnt[1] + s_wcnt[2] + s_wcnt[3];
+    __syncthreads();
   }
   if (t == 0) {
     n_kept[b] = total;
-    if (theta_out) theta_out[b] = (k > 0) ? key_float(tkey) : INFINITY;
-    ticket[b] = 0u;
+    if (theta_out) theta_out[b] = key_float(tkey);
   }
 }
 
@@ -406,7 +409,8 @@ hipError_t launch_score_d(const ent_ctx* c, int B, const void* q, const float* k
                           const int* tables, const int* ctx_lens, hipStream_t s) {
   const ent_config& cf = c->cfg;
   const dim3 grid(c->score_chunks, B);
-  const size_t lds = static_cast<size_t>(kScoreChunk) * cf.num_q_heads * sizeof(float);
+  const size_t lds = (static_cast<size_t>(cf.num_q_heads) * D +
+                      static_cast<size_t>(kScoreChunk) * cf.num_q_heads) * sizeof(float);
   const T* qq = static_cast<const T*>(q);
 #define ENT_SCORE_CASE(GG)                                                                     \
   case GG:                                                                                     \
@@ -458,11 +462,15 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
     e = cf.head_dim == 128 ? launch_score_d<float, 128>(c, B, q, ksum, tables, ctx_lens, s)
                            : launch_score_d<float, 64>(c, B, q, ksum, tables, ctx_lens, s);
   if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(block_score_kernel, dim3(c->score_chunks, B), dim3(kThreads), 0, s, c->zbuf,
+                     c->lse_part, ctx_lens, c->score_ws, scores, cf.num_q_heads,
+                     cf.max_blocks_per_seq, c->score_chunks);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-  hipLaunchKernelGGL(select_kernel, dim3(c->score_chunks, B), dim3(kThreads), lds, s, c->zbuf,
-                     c->lse_part, ctx_lens, h, c->score_ws, scores, theta, kept, n_kept,
-                     c->sel_ticket, cf.num_q_heads, cf.max_blocks_per_seq, c->score_chunks,
-                     cf.eps_h, cf.h_min, cf.log_v, cf.kappa_min, cf.b_min, c->dev_flags);
+  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kThreads), lds, s, c->score_ws, ctx_lens, h,
+                     theta, kept, n_kept, cf.max_blocks_per_seq, cf.eps_h, cf.h_min, cf.log_v,
+                     cf.kappa_min, cf.b_min, c->dev_flags);
   return hipGetLastError();
 }
 

@@ -6,9 +6,9 @@
 // that share KV head g.  Items are enumerated from the device-resident kept
 // counts (sequences with nothing kept still get one item, which writes zeros),
 // so the host never learns how much was pruned.  The grid is persistent: each
-// wave walks items with a grid stride.  A sequence split over several items
-// writes (max, sum, unnormalised output) partials; the last item of the
-// (b, g) pair to finish (atomic ticket) merges them.
+// wave walks items with a grid stride.  A (b, g) pair split over several items
+// writes (max, sum, unnormalised output) partials, which a second kernel
+// merges; a pair with one item writes its output directly.
 //
 // bf16 path (MFMA, gfx950).  Per kept block of 16 tokens:
 //   S^T[16 tok x 16 heads] = K[16 x d] . Q^T[d x 16]   v_mfma_f32_16x16x32_bf16,
@@ -49,7 +49,6 @@ struct DecodeArgs {
   float* lse;
   float* part_acc;
   float* part_ml;
-  unsigned* ticket;
   unsigned* flags;
   int B, Hkv, G, MAXB, P, splits_max;
   float scale_log2;   // softmax scale times log2(e)
@@ -137,21 +136,28 @@ __device__ __forceinline__ Item locate_item(const DecodeArgs& a, int item, const
   return it;
 }
 
-// Merge of the ns split partials of (b, g) by one wave (the last to finish).
+// Merge of the split partials of each (b, g) pair that was split: one wave
+// per pair; pairs with a single split were finalised by the decode kernel.
 template <int D>
-__device__ void merge_splits(const DecodeArgs& a, const Item& it) {
+__global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
+  const int pair = blockIdx.x * kWaves + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
+  if (pair >= a.B * a.Hkv) return;
+  const int b = pair / a.Hkv, g = pair % a.Hkv;
+  const int nk = min(max(a.n_kept[b], 0), a.MAXB);
+  const int ns = max(1, (nk + CB - 1) / CB);
+  if (ns == 1) return;
   const int Hq = a.Hkv * a.G;
-  const long long base = (static_cast<long long>(it.b) * a.Hkv + it.g) * a.splits_max;
+  const long long base = static_cast<long long>(pair) * a.splits_max;
   for (int idx = lane; idx < a.G * D; idx += 64) {
     const int r = idx / D, d = idx % D;
     float M = -INFINITY;
-    for (int s = 0; s < it.ns; ++s) {
+    for (int s = 0; s < ns; ++s) {
       const float* ml = a.part_ml + ((base + s) * a.G + r) * 2;
       if (ml[1] > 0.f) M = fmaxf(M, ml[0]);
     }
     float Ls = 0.f, O = 0.f;
-    for (int s = 0; s < it.ns; ++s) {
+    for (int s = 0; s < ns; ++s) {
       const float* ml = a.part_ml + ((base + s) * a.G + r) * 2;
       const float ls = ml[1];
       if (ls > 0.f) {
@@ -160,25 +166,9 @@ __device__ void merge_splits(const DecodeArgs& a, const Item& it) {
         O += a.part_acc[((base + s) * a.G + r) * D + d] * f;
       }
     }
-    const long long oh = static_cast<long long>(it.b) * Hq + it.g * a.G + r;
+    const long long oh = static_cast<long long>(b) * Hq + g * a.G + r;
     a.out[oh * D + d] = Ls > 0.f ? O / Ls : 0.f;
     if (d == 0 && a.lse) a.lse[oh] = Ls > 0.f ? (M + log2f(Ls)) * kLn2 : -INFINITY;
-  }
-}
-
-// After a wave has written its partial: take the ticket; merge if last.
-template <int D>
-__device__ __forceinline__ void finish_split(const DecodeArgs& a, const Item& it) {
-  const int lane = threadIdx.x & 63;
-  __threadfence();
-  unsigned prev = 0;
-  unsigned* tk = a.ticket + static_cast<long long>(it.b) * a.Hkv + it.g;
-  if (lane == 0) prev = atomicAdd(tk, 1u);
-  prev = __shfl(prev, 0);
-  if (prev == static_cast<unsigned>(it.ns - 1)) {
-    __threadfence();
-    merge_splits<D>(a, it);
-    if (lane == 0) *tk = 0u;
   }
 }
 
@@ -301,7 +291,6 @@ __global__ __launch_bounds__(kThreads) void decode_bf16_kernel(DecodeArgs a) {
           a.part_ml[(slot * a.G + r16) * 2 + 1] = l_tot;
         }
       }
-      finish_split<D>(a, it);
     }
   }
 }
@@ -410,7 +399,6 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
           a.part_ml[(slot * a.G + h) * 2 + 1] = l_run[h];
         }
       }
-      finish_split<D>(a, it);
     }
   }
 }
@@ -455,7 +443,6 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   a.lse = lse;
   a.part_acc = c->dec_acc;
   a.part_ml = c->dec_ml;
-  a.ticket = c->dec_ticket;
   a.flags = c->dev_flags;
   a.B = B;
   a.Hkv = cf.num_kv_heads;
@@ -477,6 +464,13 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
     else
       hipLaunchKernelGGL(decode_f32_kernel<64>, grid, dim3(kThreads), lds, s, a);
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 cgrid((B * cf.num_kv_heads + kWaves - 1) / kWaves);
+  if (cf.head_dim == 128)
+    hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(combine_kernel<64>, cgrid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

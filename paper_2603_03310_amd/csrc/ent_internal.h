@@ -34,15 +34,12 @@ struct ent_ctx {
   void* ws = nullptr;       // one workspace allocation
   size_t ws_bytes = 0;
   float* ent_part = nullptr;      // [max_batch, chunks, 3]  (max, sum, weighted sum)
-  unsigned* ent_ticket = nullptr; // [max_batch]
   float* stats_tmp = nullptr;     // [max_batch, chunks, 2]  row statistics scratch
   float* zbuf = nullptr;          // [max_batch, MAXB, H_q]  block logits
   float* lse_part = nullptr;      // [max_batch, score_chunks, H_q, 2]
   float* score_ws = nullptr;      // [max_batch, MAXB]       block scores
-  unsigned* sel_ticket = nullptr; // [max_batch]
   float* dec_acc = nullptr;       // [max_batch * H_kv * splits_max, G, d]
   float* dec_ml = nullptr;        // [max_batch * H_kv * splits_max, G, 2]
-  unsigned* dec_ticket = nullptr; // [max_batch * H_kv]
   unsigned* dev_flags = nullptr;  // [1]
 
   std::string err;

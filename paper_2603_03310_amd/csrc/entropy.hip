@@ -6,8 +6,8 @@
 // chunks of ENT_ROW_CHUNK logits, one 256-thread workgroup per (chunk, row);
 // each thread holds 16 logits in registers, so the chunk's maximum and the
 // sums   S = sum 2^(t - M),  W = sum 2^(t - M) (t - M)   (t = z log2(e) / T)
-// come from one read of HBM.  The last workgroup of a row to finish (atomic
-// ticket) merges the chunk triples and runs the controller:
+// come from one read of HBM.  A second kernel (one wave per row) merges the
+// chunk triples and runs the controller:
 //   H = ln 2 (log2 S - W / S)
 //   tau += max(0, H_prev - H)                    (Section 2, entropic time)
 //   T'  = clip(T exp(eta (H - H*)), T_min, T_max)  (Section 3.3, signed eta)
@@ -75,17 +75,16 @@ __device__ __forceinline__ void load_chunk(const float* __restrict__ row, int V,
   }
 }
 
-template <bool VEC, bool CTRL>
-__global__ __launch_bounds__(kThreads) void entropy_kernel(
+// Chunk pass: per (chunk, row) the maximum M, S = sum 2^(t - M) and
+// W = sum 2^(t - M) (t - M).  Writes the triple to `part` (when non-null) and
+// (M, S) to `row_stats` (when non-null).
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void entropy_chunk_kernel(
     const float* __restrict__ logits, long long ld, int V, int C,
-    float* __restrict__ temp,          // state T_t [B]; overwritten with T_{t+1} when CTRL
-    float* __restrict__ part,          // [B, C, 3]
-    float* __restrict__ row_stats,     // nullable [B, C, 2]
-    unsigned* __restrict__ ticket,     // [B]
-    float* __restrict__ h_prev, float* __restrict__ tau, float* __restrict__ h_out,
-    float* __restrict__ temp_used, float eta, float h_target, float t_min, float t_max) {
+    const float* __restrict__ temp,    // T_t [B]
+    float* __restrict__ part,          // nullable [B, C, 3]
+    float* __restrict__ row_stats) {   // nullable [B, C, 2]
   __shared__ float red[4];
-  __shared__ int s_last;
   const int c = blockIdx.x;
   const int b = blockIdx.y;
   const float T = temp[b];
@@ -118,28 +117,28 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(
       row_stats[2 * o + 0] = M;
       row_stats[2 * o + 1] = S;
     }
-    if (CTRL) {
+    if (part) {
       part[3 * o + 0] = M;
       part[3 * o + 1] = S;
       part[3 * o + 2] = W;
-      __threadfence();
-      const unsigned prev = atomicAdd(&ticket[b], 1u);
-      s_last = (prev == static_cast<unsigned>(C - 1));
-      if (s_last) __threadfence();
     }
   }
-  if (!CTRL) return;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
+}
 
-  // Merge the C chunk triples of row b (this workgroup finished last).
+// Merge of a row's C chunk triples (one wave per row) and the controller.
+__global__ __launch_bounds__(kThreads) void entropy_finalize_kernel(
+    int B, int C, const float* __restrict__ part, float* __restrict__ temp,
+    float* __restrict__ h_prev, float* __restrict__ tau, float* __restrict__ h_out,
+    float* __restrict__ temp_used, float eta, float h_target, float t_min, float t_max) {
+  const int b = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (b >= B) return;
   const float* pr = part + static_cast<long long>(b) * C * 3;
   float mloc = -INFINITY;
-  for (int i = threadIdx.x; i < C; i += kThreads) mloc = fmaxf(mloc, pr[3 * i]);
-  const float MG = block_max_256(mloc, red);
+  for (int i = lane; i < C; i += 64) mloc = fmaxf(mloc, pr[3 * i]);
+  const float MG = wave_max(mloc);
   float s = 0.f, w = 0.f;
-  for (int i = threadIdx.x; i < C; i += kThreads) {
+  for (int i = lane; i < C; i += 64) {
     const float mc = pr[3 * i];
     const float sc = pr[3 * i + 1];
     const float wc = pr[3 * i + 2];
@@ -150,9 +149,10 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(
       w += f * (wc + sc * dm);
     }
   }
-  s = block_sum_256(s, red);
-  w = block_sum_256(w, red);
-  if (threadIdx.x == 0) {
+  s = wave_sum(s);
+  w = wave_sum(w);
+  if (lane == 0) {
+    const float T = temp[b];
     const float H = (log2f(s) - w / s) * kLn2;
     h_out[b] = H;
     temp_used[b] = T;
@@ -164,7 +164,6 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(
     tau[b] = ta;
     h_prev[b] = H;
     temp[b] = tn;
-    ticket[b] = 0u;
   }
 }
 
@@ -298,18 +297,18 @@ hipError_t launch_entropy(const ent_ctx* c, int B, const float* logits, long lon
   const ent_config& cf = c->cfg;
   const dim3 grid(c->chunks, B);
   const bool vec = row_vec_ok(logits, ld);
-  if (controller) {
-    auto k = vec ? entropy_kernel<true, true> : entropy_kernel<false, true>;
-    hipLaunchKernelGGL(k, grid, dim3(kThreads), 0, s, logits, ld, cf.vocab, c->chunks, st.temp,
-                       c->ent_part, row_stats, c->ent_ticket, st.h_prev, st.tau, h_out, temp_used,
-                       cf.eta, cf.h_target, cf.t_min, cf.t_max);
-  } else {
-    auto k = vec ? entropy_kernel<true, false> : entropy_kernel<false, false>;
-    hipLaunchKernelGGL(k, grid, dim3(kThreads), 0, s, logits, ld, cf.vocab, c->chunks,
-                       const_cast<float*>(temp_used), c->ent_part, row_stats, c->ent_ticket,
-                       nullptr, nullptr, nullptr, nullptr, cf.eta, cf.h_target, cf.t_min,
-                       cf.t_max);
-  }
+  auto k = vec ? entropy_chunk_kernel<true> : entropy_chunk_kernel<false>;
+  // Without the controller (statistics for the sampler) the temperatures are
+  // the ones passed in temp_used.
+  const float* T = controller ? st.temp : temp_used;
+  hipLaunchKernelGGL(k, grid, dim3(kThreads), 0, s, logits, ld, cf.vocab, c->chunks, T,
+                     controller ? c->ent_part : nullptr, row_stats);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !controller) return e;
+  const int rows_per_wg = kThreads / 64;
+  hipLaunchKernelGGL(entropy_finalize_kernel, dim3((B + rows_per_wg - 1) / rows_per_wg),
+                     dim3(kThreads), 0, s, B, c->chunks, c->ent_part, st.temp, st.h_prev, st.tau,
+                     h_out, temp_used, cf.eta, cf.h_target, cf.t_min, cf.t_max);
   return hipGetLastError();
 }
 
