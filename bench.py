@@ -42,7 +42,9 @@ def parse():
     ap.add_argument("--workload", default="llama3_8b_decode")
     ap.add_argument("--copies", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
 
 
@@ -63,8 +65,8 @@ def kv_bytes_kept(x, n_kept, kept, elem):
 
 
 def cpu_baseline(x, p, seconds):
-    """The float64 oracle on the host, single thread, on the first sequences of
-    the step until `seconds` of work; scaled to whole steps per second."""
+    """The float64 oracle on the host, single thread, over the step's sequences
+    in order (cycling) for about `seconds`; scaled to whole steps per second."""
     from threadpoolctl import threadpool_limits
 
     from oracle import step as St
@@ -72,16 +74,17 @@ def cpu_baseline(x, p, seconds):
     done = 0
     t0 = time.perf_counter()
     with threadpool_limits(limits=1):
-        while done < B and time.perf_counter() - t0 < seconds:
-            St.sequence_step(done, k_pool=x.k_pool, v_pool=x.v_pool, tables=x.block_tables,
+        while done == 0 or time.perf_counter() - t0 < seconds:
+            St.sequence_step(done % B, k_pool=x.k_pool, v_pool=x.v_pool, tables=x.block_tables,
                              ctx_lens=x.ctx_lens, q=x.q[0], logits=x.logits[0], h_prev=x.h_prev,
                              tau=x.tau, temp=x.temp, uniforms=x.uniforms[0], params=p,
                              block_size=16)
             done += 1
     el = time.perf_counter() - t0
     return {"value": (done / B) / el, "unit": "steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"float64 oracle, all stages, sequences 0..{done - 1} of {B} of one "
-                      f"{x.workload.name} step ({el:.1f} s, one thread); scaled to a whole step"}
+            "sample": f"float64 oracle, all stages, {done} sequence-steps cycling over the {B} "
+                      f"sequences of one {x.workload.name} step ({el:.1f} s, one thread); "
+                      f"scaled to whole steps"}
 
 
 def traffic_from_counters():
@@ -155,6 +158,16 @@ def main():
         ent.ent_sample(ctx, B, c.logits[0], ld, o.row_stats, o.temp_used, c.uniforms[0],
                        o.tokens, sp)
         if ev: ev[4].record(stream)
+
+    if args.calibrate_copy:
+        # A plain copy kernel of known size: profilers' byte counters for this
+        # kernel calibrate those taken on the step's kernels.
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # Pass A: the timed steps, nothing between the launches.
     for i in range(W):

@@ -141,19 +141,18 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->group = f.num_q_heads / f.num_kv_heads;
   c->chunks = ent_row_stats_chunks(f.vocab);
   c->score_chunks = (f.max_blocks_per_seq + ent::kScoreChunk - 1) / ent::kScoreChunk;
-  c->splits_max = (f.max_blocks_per_seq + ent::kSplitBlocks - 1) / ent::kSplitBlocks;
+  c->decode_grid = ent::decode_grid_size(c);
 
   const size_t Bm = static_cast<size_t>(f.max_batch);
   const size_t sz_ent_part = align_up(Bm * c->chunks * 3 * sizeof(float));
   const size_t sz_stats = align_up(Bm * c->chunks * 2 * sizeof(float));
   const size_t sz_z = align_up(Bm * f.max_blocks_per_seq * f.num_q_heads * sizeof(float));
-  const size_t sz_lse = align_up(Bm * c->score_chunks * f.num_q_heads * 2 * sizeof(float));
-  const size_t sz_score = align_up(Bm * f.max_blocks_per_seq * sizeof(float));
-  const size_t nslots = Bm * f.num_kv_heads * c->splits_max;
+  const size_t nslots = static_cast<size_t>(
+      ent::decode_partial_slots(c->decode_grid, f.max_batch, f.num_kv_heads));
   const size_t sz_acc = align_up(nslots * c->group * f.head_dim * sizeof(float));
   const size_t sz_ml = align_up(nslots * c->group * 2 * sizeof(float));
   const size_t sz_flags = align_up(sizeof(unsigned));
-  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_score + sz_acc + sz_ml + sz_flags;
+  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_acc + sz_ml + sz_flags;
   e = hipMalloc(&c->ws, c->ws_bytes);
   if (e != hipSuccess) {
     g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
@@ -173,12 +172,9 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->ent_part = reinterpret_cast<float*>(take(sz_ent_part));
   c->stats_tmp = reinterpret_cast<float*>(take(sz_stats));
   c->zbuf = reinterpret_cast<float*>(take(sz_z));
-  c->lse_part = reinterpret_cast<float*>(take(sz_lse));
-  c->score_ws = reinterpret_cast<float*>(take(sz_score));
   c->dec_acc = reinterpret_cast<float*>(take(sz_acc));
   c->dec_ml = reinterpret_cast<float*>(take(sz_ml));
   c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));
-  c->decode_grid = ent::decode_grid_size(c);
   *out = c;
   return ENT_OK;
 }

@@ -12,10 +12,9 @@
 //
 // Kernels:
 //   summary_kernel   per-block mean keys (setup)
-//   score_kernel        z for 64 blocks x all heads per workgroup; per-chunk
-//                       log-sum-exp partials per head
-//   block_score_kernel  merges the partials into L_h and computes I_b
-//   select_kernel       per sequence: budget, 4-pass 8-bit radix select of the
+//   score_kernel        z for 16 blocks x all heads per workgroup
+//   select_kernel       per sequence: the per-head log-sum-exp L_h, computes
+//                       I_b, the budget, a 4-pass 8-bit radix select of the
 //                       k-th largest score, ascending compaction with ballots
 //   append_kernel    writes one token and refreshes its block's mean key
 
@@ -105,16 +104,20 @@ __global__ __launch_bounds__(kThreads) void append_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Scoring.  A workgroup takes 64 blocks of one sequence (16 per wave).  The
-// query heads are staged once in LDS as fp32.  A block's summary
-// (H_kv x d floats) is read as NP passes of 256 floats, one float4 per lane
-// per pass, fully coalesced; the next block's passes are prefetched while the
-// current one is reduced.  In a pass, a group of L = d/4 lanes covers one KV
-// head: each lane forms G partial dot products (one per query head of that KV
-// head) and a halving butterfly reduces them over the L lanes, leaving head
-// r = li * G / L in lane li.
+// Scoring.  A workgroup of 4 waves takes 16 blocks of one sequence, 4 per
+// wave, and writes z_bh = scale <q_h, kbar_b,g(h)> for all of them.  The
+// critical path is two memory round trips: the wave's table entries and the
+// query heads (staged once in LDS as fp32) are loaded together, then all
+// summary loads of the wave's 4 blocks are in flight at once.  A block's
+// summary (H_kv x d floats) is read as NP passes of 256 floats, one float4
+// per lane per pass, fully coalesced.  In a pass, a group of L = d/4 lanes
+// covers one KV head: each lane forms G partial dot products (one per query
+// head of that KV head) and a halving butterfly reduces them over the L
+// lanes, leaving head r = li * G / L in lane li.
 // ---------------------------------------------------------------------------
-constexpr int kMaxPasses = 8;               // H_kv * d <= 2048
+constexpr int kScoreThreads = 256;
+constexpr int kScoreWaves = kScoreThreads / 64;
+constexpr int kScorePerWave = kScoreChunk / kScoreWaves;   // 4 blocks per wave
 
 template <int G, int L>
 __device__ __forceinline__ float reduce_heads(float (&a)[G], int li) {
@@ -134,21 +137,11 @@ __device__ __forceinline__ float reduce_heads(float (&a)[G], int li) {
   return v;
 }
 
-__device__ __forceinline__ void load_summary(const float* __restrict__ base, int n_floats, int np,
-                                             int lane, float4 (&kv)[kMaxPasses]) {
-#pragma unroll
-  for (int k = 0; k < kMaxPasses; ++k) {
-    const int f = 256 * k + 4 * lane;
-    if (k < np && f < n_floats) kv[k] = *reinterpret_cast<const float4*>(base + f);
-    else kv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-}
-
-template <typename T, int D, int G>
-__global__ __launch_bounds__(kThreads) void score_kernel(
+template <typename T, int D, int G, int kMaxPasses>   // np <= kMaxPasses
+__global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const T* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
-    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
-    int Hkv, int MAXB, int P, int nch, float scale, unsigned* flags) {
+    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, int Hkv, int MAXB, int P,
+    float scale, unsigned* flags) {
   constexpr int L = D / 4;
   static_assert(G <= L, "heads per KV head exceed the lane group");
   extern __shared__ float smem[];            // q [Hq][D] fp32, then z tile [kScoreChunk][Hq]
@@ -156,40 +149,48 @@ __global__ __launch_bounds__(kThreads) void score_kernel(
   float* qs = smem;
   float* zt = smem + Hq * D;
   const int ch = blockIdx.x, b = blockIdx.y;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int li = lane % L;
+  const int j_lo = ch * kScoreChunk;
+  const int jw = j_lo + wave * kScorePerWave;
+  // Table entries are read before the context length is known (the row has
+  // MAXB entries, so the read is in bounds); invalid ones are masked below.
+  int my_p = 0;
+  if (lane < kScorePerWave && jw + lane < MAXB) my_p = tables[static_cast<long long>(b) * MAXB + jw + lane];
   const int N = ctx_lens[b];
   if (N < 0 || N > MAXB * kBlock) return;    // flagged by the selection kernel
   const int nb = (N + kBlock - 1) / kBlock;
-  const int j_lo = ch * kScoreChunk;
   if (j_lo >= nb) return;
   const int nblk = min(kScoreChunk, nb - j_lo);
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  const int li = lane % L;
-  const int* trow = tables + static_cast<long long>(b) * MAXB;
+  const int nmine = max(0, min(kScorePerWave, nb - jw));
+  if (lane < nmine && (my_p < 0 || my_p >= P)) {
+    raise_flag(flags, ENT_DEV_BAD_TABLE);
+    my_p = 0;
+  }
+  if (lane >= nmine) my_p = 0;
+  const int nfl = Hkv * D;
+  const int np = (nfl + 255) >> 8;
 
-  for (int e = t; e < Hq * D; e += kThreads)
-    qs[e] = load_elem<T>(q + static_cast<long long>(b) * Hq * D + e);
-  // Physical blocks of this wave's 16 blocks, one per lane.
-  const int jw = wave * 16;
-  int my_p = 0;
-  if (lane < 16 && jw + lane < nblk) {
-    my_p = trow[j_lo + jw + lane];
-    if (my_p < 0 || my_p >= P) {
-      raise_flag(flags, ENT_DEV_BAD_TABLE);
-      my_p = 0;
+  float4 kv[kScorePerWave][kMaxPasses];
+#pragma unroll
+  for (int blk = 0; blk < kScorePerWave; ++blk) {
+    const int p = __shfl(my_p, blk);
+#pragma unroll
+    for (int k = 0; k < kMaxPasses; ++k) {
+      const int f = 256 * k + 4 * lane;
+      if (blk < nmine && k < np && f < nfl)
+        kv[blk][k] = *reinterpret_cast<const float4*>(ksum + static_cast<long long>(p) * nfl + f);
+      else
+        kv[blk][k] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
   }
+  for (int e = t; e < Hq * D; e += kScoreThreads)
+    qs[e] = load_elem<T>(q + static_cast<long long>(b) * Hq * D + e);
   __syncthreads();
 
-  const int nfl = Hkv * D;
-  const int np = (nfl + 255) / 256;
-  const int nmine = max(0, min(16, nblk - jw));
-  float4 cur[kMaxPasses], nxt[kMaxPasses];
-  if (nmine > 0)
-    load_summary(ksum + static_cast<long long>(__shfl(my_p, 0)) * nfl, nfl, np, lane, cur);
-  for (int i = 0; i < nmine; ++i) {
-    if (i + 1 < nmine)
-      load_summary(ksum + static_cast<long long>(__shfl(my_p, i + 1)) * nfl, nfl, np, lane, nxt);
-    const int jl = jw + i;
+#pragma unroll
+  for (int blk = 0; blk < kScorePerWave; ++blk) {
+    if (blk >= nmine) continue;
 #pragma unroll
     for (int k = 0; k < kMaxPasses; ++k) {
       if (k >= np) continue;
@@ -201,82 +202,19 @@ __global__ __launch_bounds__(kThreads) void score_kernel(
       for (int r = 0; r < G; ++r) {
         float4 qq = make_float4(0.f, 0.f, 0.f, 0.f);
         if (gv) qq = *reinterpret_cast<const float4*>(qs + (g * G + r) * D + dd);
-        a[r] = qq.x * cur[k].x + qq.y * cur[k].y + qq.z * cur[k].z + qq.w * cur[k].w;
+        a[r] = qq.x * kv[blk][k].x + qq.y * kv[blk][k].y + qq.z * kv[blk][k].z +
+               qq.w * kv[blk][k].w;
       }
       const float z = reduce_heads<G, L>(a, li) * scale;
-      if (gv && (li % (L / G)) == 0) zt[jl * Hq + g * G + li / (L / G)] = z;
+      if (gv && (li % (L / G)) == 0)
+        zt[(wave * kScorePerWave + blk) * Hq + g * G + li / (L / G)] = z;
     }
-#pragma unroll
-    for (int k = 0; k < kMaxPasses; ++k) cur[k] = nxt[k];
+    // Keep the next block's LDS reads from being hoisted above this point.
+    asm volatile("" ::: "memory");
   }
   __syncthreads();
   float* zrow = zbuf + (static_cast<long long>(b) * MAXB + j_lo) * Hq;
-  for (int e = t; e < nblk * Hq; e += kThreads) zrow[e] = zt[e];
-  // Per-head log-sum-exp of l = z + ln n_b over this chunk's blocks.
-  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
-  const float ln_full = logf(static_cast<float>(kBlock));
-  for (int h = t; h < Hq; h += kThreads) {
-    float m = -INFINITY;
-    for (int i = 0; i < nblk; ++i) {
-      const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
-      m = fmaxf(m, zt[i * Hq + h] + lnn);
-    }
-    float s = 0.f;
-    for (int i = 0; i < nblk; ++i) {
-      const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
-      s += expf(zt[i * Hq + h] + lnn - m);
-    }
-    float* lp = lse_part + ((static_cast<long long>(b) * nch + ch) * Hq + h) * 2;
-    lp[0] = m;
-    lp[1] = s;
-  }
-}
-
-// Block scores I_b of one chunk of 64 blocks: merges the per-chunk
-// log-sum-exp partials into L_h, then 4 threads per block sum over heads.
-__global__ __launch_bounds__(kThreads) void block_score_kernel(
-    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, float* __restrict__ score_ws, float* __restrict__ scores_out,
-    int Hq, int MAXB, int nch_max) {
-  __shared__ float sL[128];
-  const int ch = blockIdx.x, b = blockIdx.y;
-  const int t = threadIdx.x;
-  const int N = ctx_lens[b];
-  if (N < 0 || N > MAXB * kBlock) return;
-  const int nb = (N + kBlock - 1) / kBlock;
-  const int j_lo = ch * kScoreChunk;
-  if (j_lo >= nb) return;
-  const int nblk = min(kScoreChunk, nb - j_lo);
-  const int nch = (nb + kScoreChunk - 1) / kScoreChunk;
-  for (int h = t; h < Hq; h += kThreads) {
-    const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
-    float m = -INFINITY;
-    for (int c = 0; c < nch; ++c) m = fmaxf(m, lp[c * Hq * 2]);
-    float s = 0.f;
-    for (int c = 0; c < nch; ++c) s += lp[c * Hq * 2 + 1] * expf(lp[c * Hq * 2] - m);
-    sL[h] = m + logf(s);
-  }
-  __syncthreads();
-  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
-  const float ln_full = logf(static_cast<float>(kBlock));
-  const int i = t >> 2, q4 = t & 3;
-  float acc = 0.f;
-  if (i < nblk) {
-    const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
-    const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j_lo + i) * Hq;
-    for (int h = q4; h < Hq; h += 4) {
-      const float z = zr[h];
-      const float Lh = sL[h];
-      acc += expf(z + lnn - Lh) * (Lh - z);
-    }
-  }
-  acc += __shfl_xor(acc, 1);
-  acc += __shfl_xor(acc, 2);
-  if (i < nblk && q4 == 0) {
-    const float I = __fdiv_rn(acc, static_cast<float>(Hq));
-    score_ws[static_cast<long long>(b) * MAXB + j_lo + i] = I;
-    if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j_lo + i] = I;
-  }
+  for (int e = t; e < nblk * Hq; e += kScoreThreads) zrow[e] = zt[e];
 }
 
 __device__ __forceinline__ unsigned float_key(float f) {
@@ -300,17 +238,25 @@ __device__ __forceinline__ int keep_budget(float h, int nb, float eps_h, float h
   return min(nb, max(min(b_min, nb), k));
 }
 
-// Kept set of one sequence (one workgroup): budget k from the entropy, the
-// k-th largest score by a 4-pass 8-bit radix select over the scores held in
-// LDS, then ascending compaction of {b : I_b >= theta} with wave ballots.
-__global__ __launch_bounds__(kThreads) void select_kernel(
-    const float* __restrict__ score_ws, const int* __restrict__ ctx_lens,
-    const float* __restrict__ hvec, float* __restrict__ theta_out, int* __restrict__ kept,
-    int* __restrict__ n_kept, int MAXB, float eps_h, float h_min, float log_v, float kappa_min,
-    int b_min, unsigned* flags) {
+// Kept set of one sequence (one workgroup of 512 threads):
+//  1. L_h = ln sum_b n_b e^{z_bh}, from the block logits z;
+//  2. I_b = (1/H_q) sum_h e^{z_bh + ln n_b - L_h} (L_h - z_bh) for every block,
+//     held in LDS as order-preserving integer keys;
+//  3. budget k from the entropy, the k-th largest key by a 4-pass 8-bit radix
+//     select, and ascending compaction of {b : I_b >= theta} with wave ballots.
+constexpr int kSelThreads = 512;
+constexpr int kSelWaves = kSelThreads / 64;
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(
+    const float* __restrict__ zbuf, const int* __restrict__ ctx_lens,
+    const float* __restrict__ hvec, float* __restrict__ scores_out,
+    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int Hq,
+    int MAXB, float eps_h, float h_min,
+    float log_v, float kappa_min, int b_min, unsigned* flags) {
   extern __shared__ unsigned keys[];        // [MAXB]
   __shared__ unsigned hist[256];
-  __shared__ int s_digit, s_krem, s_wcnt[4];
+  __shared__ float s_pm[kSelThreads], s_ps[kSelThreads], sL[128];
+  __shared__ int s_digit, s_krem, s_wcnt[kSelWaves];
   const int b = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int N = ctx_lens[b];
@@ -324,6 +270,65 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
   }
   const int nb = (N + kBlock - 1) / kBlock;
   const int k = keep_budget(hvec[b], nb, eps_h, h_min, log_v, kappa_min, b_min);
+  if (nb == 0) {
+    if (t == 0) {
+      n_kept[b] = 0;
+      if (theta_out) theta_out[b] = INFINITY;
+    }
+    return;
+  }
+  // 1. L_h = ln sum_b n_b e^{z_bh}: each thread folds, online, a strided
+  //    subset of the blocks for head t % Hq; one thread per head folds the
+  //    subsets.
+  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
+  const float ln_full = logf(static_cast<float>(kBlock));
+  const float* zb = zbuf + static_cast<long long>(b) * MAXB * Hq;
+  const int per_head = kSelThreads / Hq;     // threads per head (Hq <= 128)
+  {
+    float m = -INFINITY, sum = 0.f;
+    if (t < per_head * Hq) {
+      const int h = t % Hq;
+      for (int j = t / Hq; j < nb; j += per_head) {
+        const float l = zb[static_cast<long long>(j) * Hq + h] + ((j == nb - 1) ? ln_last : ln_full);
+        if (l > m) {
+          sum = sum * expf(m - l) + 1.f;
+          m = l;
+        } else {
+          sum += expf(l - m);
+        }
+      }
+    }
+    s_pm[t] = m;
+    s_ps[t] = sum;
+  }
+  __syncthreads();
+  if (t < Hq) {
+    float m = -INFINITY, sum = 0.f;
+    for (int i = 0; i < per_head; ++i) {
+      const float mc = s_pm[i * Hq + t], sc = s_ps[i * Hq + t];
+      if (mc == -INFINITY) continue;
+      const float mn = fmaxf(m, mc);
+      sum = sum * expf(m - mn) + sc * expf(mc - mn);
+      m = mn;
+    }
+    sL[t] = m + logf(sum);
+  }
+  __syncthreads();
+
+  // 2. Block scores.
+  for (int j = t; j < nb; j += kSelThreads) {
+    const float lnn = (j == nb - 1) ? ln_last : ln_full;
+    const float* zr = zb + static_cast<long long>(j) * Hq;
+    float acc = 0.f;
+    for (int h = 0; h < Hq; ++h) {
+      const float z = zr[h];
+      const float Lh = sL[h];
+      acc += expf(z + lnn - Lh) * (Lh - z);
+    }
+    const float I = __fdiv_rn(acc, static_cast<float>(Hq));
+    keys[j] = float_key(I);
+    if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j] = I;
+  }
   if (k <= 0) {
     if (t == 0) {
       n_kept[b] = 0;
@@ -331,17 +336,16 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     }
     return;
   }
-  for (int i = t; i < nb; i += kThreads)
-    keys[i] = float_key(score_ws[static_cast<long long>(b) * MAXB + i]);
   if (t == 0) s_krem = k;
   __syncthreads();
 
+  // 3. Radix select of the k-th largest key.
   unsigned prefix = 0u, mask = 0u;
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    hist[t] = 0u;
+    if (t < 256) hist[t] = 0u;
     __syncthreads();
-    for (int i = t; i < nb; i += kThreads) {
+    for (int i = t; i < nb; i += kSelThreads) {
       const unsigned key = keys[i];
       if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
     }
@@ -385,7 +389,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
   // Compaction in ascending block order.
   int total = 0;
   int* krow = kept + static_cast<long long>(b) * MAXB;
-  for (int base = 0; base < nb; base += kThreads) {
+  for (int base = 0; base < nb; base += kSelThreads) {
     const int i = base + t;
     const bool f = i < nb && keys[i] >= tkey;
     const unsigned long long bal = __ballot(f);
@@ -395,7 +399,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     int off = total;
     for (int w = 0; w < wave; ++w) off += s_wcnt[w];
     if (f) krow[off + rank] = i;
-    total += s_wcnt[0] + s_wcnt[1] + s_wcnt[2] + s_wcnt[3];
+    for (int w = 0; w < kSelWaves; ++w) total += s_wcnt[w];
     __syncthreads();
   }
   if (t == 0) {
@@ -412,11 +416,17 @@ hipError_t launch_score_d(const ent_ctx* c, int B, const void* q, const float* k
   const size_t lds = (static_cast<size_t>(cf.num_q_heads) * D +
                       static_cast<size_t>(kScoreChunk) * cf.num_q_heads) * sizeof(float);
   const T* qq = static_cast<const T*>(q);
-#define ENT_SCORE_CASE(GG)                                                                     \
-  case GG:                                                                                     \
-    hipLaunchKernelGGL((score_kernel<T, D, GG>), grid, dim3(kThreads), lds, s, qq, ksum, tables, \
-                       ctx_lens, c->zbuf, c->lse_part, cf.num_kv_heads, cf.max_blocks_per_seq,   \
-                       cf.num_pool_blocks, c->score_chunks, cf.scale, c->dev_flags);           \
+  const int np = (cf.num_kv_heads * D + 255) / 256;
+#define ENT_SCORE_CASE(GG)                                                                      \
+  case GG:                                                                                      \
+    if (np <= 4)                                                                                \
+      hipLaunchKernelGGL((score_kernel<T, D, GG, 4>), grid, dim3(kScoreThreads), lds, s, qq,    \
+                         ksum, tables, ctx_lens, c->zbuf, cf.num_kv_heads,                      \
+                         cf.max_blocks_per_seq, cf.num_pool_blocks, cf.scale, c->dev_flags);    \
+    else                                                                                        \
+      hipLaunchKernelGGL((score_kernel<T, D, GG, 8>), grid, dim3(kScoreThreads), lds, s, qq,    \
+                         ksum, tables, ctx_lens, c->zbuf, cf.num_kv_heads,                      \
+                         cf.max_blocks_per_seq, cf.num_pool_blocks, cf.scale, c->dev_flags);    \
     break;
   switch (c->group) {
     ENT_SCORE_CASE(1)
@@ -462,15 +472,10 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
     e = cf.head_dim == 128 ? launch_score_d<float, 128>(c, B, q, ksum, tables, ctx_lens, s)
                            : launch_score_d<float, 64>(c, B, q, ksum, tables, ctx_lens, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(block_score_kernel, dim3(c->score_chunks, B), dim3(kThreads), 0, s, c->zbuf,
-                     c->lse_part, ctx_lens, c->score_ws, scores, cf.num_q_heads,
-                     cf.max_blocks_per_seq, c->score_chunks);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kThreads), lds, s, c->score_ws, ctx_lens, h,
-                     theta, kept, n_kept, cf.max_blocks_per_seq, cf.eps_h, cf.h_min, cf.log_v,
-                     cf.kappa_min, cf.b_min, c->dev_flags);
+  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelThreads), lds, s, c->zbuf, ctx_lens, h,
+                     scores, theta, kept, n_kept, cf.num_q_heads, cf.max_blocks_per_seq, cf.eps_h, cf.h_min, cf.log_v, cf.kappa_min, cf.b_min,
+                     c->dev_flags);
   return hipGetLastError();
 }
 

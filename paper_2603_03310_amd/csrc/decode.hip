@@ -1,26 +1,32 @@
 // Decode attention over the kept blocks only (Section 3.2 of the paper:
 // attention computation is restricted to the kept block set).
 //
-// Work decomposition.  A work item is (sequence b, KV head g, split s): up to
-// kSplitBlocks consecutive entries of b's kept list, for the G query heads
-// that share KV head g.  Items are enumerated from the device-resident kept
-// counts (sequences with nothing kept still get one item, which writes zeros),
-// so the host never learns how much was pruned.  The grid is persistent: each
-// wave walks items with a grid stride.  A (b, g) pair split over several items
-// writes (max, sum, unnormalised output) partials, which a second kernel
-// merges; a pair with one item writes its output directly.
+// Work decomposition (stream-K).  A unit is one kept block of one sequence
+// for one KV head (its G query heads together).  Units are laid end to end,
+// sequence-major, then KV head, then kept-list order; the (sequence, KV head)
+// runs are "segments".  Every wave of the persistent grid takes an equal
+// contiguous range of units, so all waves do the same amount of work and the
+// pipeline never drains between work items.  A wave walks its range with a
+// 64-unit metadata window (kept id and physical block per lane, gathered in
+// parallel) and a one-block-ahead register prefetch of the K and V tiles.
+// Where its range covers a whole segment it writes the output directly;
+// where it covers part of one it writes an unnormalised partial
+// (max, sum, output) to slot (wave + segment), which is unique because both
+// partitions are ordered intervals.  A second kernel merges the partials of
+// every segment that was cut.  The kept counts stay on the device.
 //
 // bf16 path (MFMA, gfx950).  Per kept block of 16 tokens:
 //   S^T[16 tok x 16 heads] = K[16 x d] . Q^T[d x 16]   v_mfma_f32_16x16x32_bf16,
-//     A = K rows straight from the token-major K tile (16 B per lane per step),
+//     A = K rows from the token-major K tile (16 B per lane per step),
 //     B = the G query heads (zero-padded to 16 columns), held in registers;
-//   online softmax per head column (log2 domain, fp32);
+//   online softmax per head column (log2 domain, fp32); the cross-lane max is
+//   taken only when some score exceeds a head's running max;
 //   O^T[d x 16] += V^T[d x 16 tok] . P^T[16 tok x 16]   v_mfma_f32_16x16x16_bf16,
 //     A = rows of the dim-major V tile (8 B per lane per 16-dim tile),
 //     B = P^T taken straight from the S^T accumulator registers, split into
 //         a bf16 high part and a bf16 remainder (two MFMAs), so P keeps
 //         about 16 bits.
-// fp32 path (VALU): the same items and merge, scalar dot products.
+// fp32 path (VALU): the same decomposition with scalar dot products.
 
 #include "ent_internal.h"
 
@@ -31,7 +37,8 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int CB = kSplitBlocks;
+constexpr int kWindow = 64;                  // units of metadata per window
+constexpr int kCombineMaxSplits = 64;        // partials staged in LDS per pass
 
 typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef short s16x4_t __attribute__((__vector_size__(4 * sizeof(short))));
@@ -47,26 +54,30 @@ struct DecodeArgs {
   const int* n_kept;
   float* out;
   float* lse;
-  float* part_acc;
-  float* part_ml;
+  float* part_acc;    // [W + S, G, D]
+  float* part_ml;     // [W + S, G, 2]
   unsigned* flags;
-  int B, Hkv, G, MAXB, P, splits_max;
+  int B, Hkv, G, MAXB, P;
+  int W;              // waves of the decode grid
   float scale_log2;   // softmax scale times log2(e)
 };
 
-// Builds, in LDS, the first work item of each sequence (s_pref[0..B]) and its
-// number of splits (s_ns[0..B-1]).
-__device__ void build_items(const DecodeArgs& a, int* s_pref, int* s_ns, int* s_red) {
+// Plan in LDS: s_pref[b] = first unit of sequence b (s_pref[B] = total),
+// s_nk[b] = kept blocks of b (0 when its context length is invalid),
+// s_N[b] = context length.
+__device__ void build_plan(const DecodeArgs& a, int* s_pref, int* s_nk, int* s_N, int* s_red) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int per = (a.B + kThreads - 1) / kThreads;
   int loc = 0;
   for (int i = 0; i < per; ++i) {
     const int b = t * per + i;
     if (b < a.B) {
-      const int nk = min(max(a.n_kept[b], 0), a.MAXB);
-      const int ns = max(1, (nk + CB - 1) / CB);
-      s_ns[b] = ns;
-      loc += ns * a.Hkv;
+      const int N = a.ctx_lens[b];
+      const bool ok = N >= 0 && N <= a.MAXB * kBlock;
+      const int nk = ok ? min(max(a.n_kept[b], 0), a.MAXB) : 0;
+      s_nk[b] = nk;
+      s_N[b] = ok ? N : 0;
+      loc += nk * a.Hkv;
     }
   }
   int incl = loc;
@@ -83,93 +94,63 @@ __device__ void build_items(const DecodeArgs& a, int* s_pref, int* s_ns, int* s_
     const int b = t * per + i;
     if (b < a.B) {
       s_pref[b] = run;
-      run += s_ns[b] * a.Hkv;
+      run += s_nk[b] * a.Hkv;
     }
   }
   if (t == kThreads - 1) s_pref[a.B] = run;
   __syncthreads();
 }
 
-struct Item {
-  int b, g, sp, ns, N, nb, cnt;
-  int my_j, my_p;   // lane i < cnt: kept block id and its physical block (-1 = skip)
-};
-
-__device__ __forceinline__ Item locate_item(const DecodeArgs& a, int item, const int* s_pref,
-                                            const int* s_ns) {
-  Item it;
-  int lo = 0, hi = a.B;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (s_pref[mid] <= item) lo = mid; else hi = mid;
-  }
-  it.b = lo;
-  it.ns = s_ns[lo];
-  const int rr = item - s_pref[lo];
-  it.g = rr / it.ns;
-  it.sp = rr % it.ns;
-  const int lane = threadIdx.x & 63;
-  const int N = a.ctx_lens[it.b];
-  const bool ok = N >= 0 && N <= a.MAXB * kBlock;
-  it.N = ok ? N : 0;
-  it.nb = (it.N + kBlock - 1) / kBlock;
-  const int nk = min(max(a.n_kept[it.b], 0), a.MAXB);
-  const int j0 = it.sp * CB;
-  it.cnt = max(0, min(nk, j0 + CB) - j0);
-  it.my_j = -1;
-  it.my_p = -1;
-  if (lane < it.cnt) {
-    const long long row = static_cast<long long>(it.b) * a.MAXB;
-    const int j = a.kept[row + j0 + lane];
-    if (j >= 0 && j < it.nb) {
-      const int p = a.tables[row + j];
-      if (p >= 0 && p < a.P) {
-        it.my_j = j;
-        it.my_p = p;
-      } else if (it.g == 0) {
-        raise_flag(a.flags, ENT_DEV_BAD_TABLE);
-      }
-    } else if (it.g == 0) {
-      raise_flag(a.flags, ENT_DEV_BAD_TABLE);
-    }
-  }
-  return it;
+__device__ __forceinline__ long long range_begin(int w, long long U, int W) {
+  return static_cast<long long>(w) * U / W;
+}
+// The wave whose range holds unit x (U > 0).
+__device__ __forceinline__ int wave_of(long long x, long long U, int W) {
+  return static_cast<int>(((x + 1) * W - 1) / U);
 }
 
-// Merge of the split partials of each (b, g) pair that was split: one wave
-// per pair; pairs with a single split were finalised by the decode kernel.
-template <int D>
-__global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
-  const int pair = blockIdx.x * kWaves + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (pair >= a.B * a.Hkv) return;
-  const int b = pair / a.Hkv, g = pair % a.Hkv;
-  const int nk = min(max(a.n_kept[b], 0), a.MAXB);
-  const int ns = max(1, (nk + CB - 1) / CB);
-  if (ns == 1) return;
-  const int Hq = a.Hkv * a.G;
-  const long long base = static_cast<long long>(pair) * a.splits_max;
-  for (int idx = lane; idx < a.G * D; idx += 64) {
-    const int r = idx / D, d = idx % D;
-    float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) {
-      const float* ml = a.part_ml + ((base + s) * a.G + r) * 2;
-      if (ml[1] > 0.f) M = fmaxf(M, ml[0]);
-    }
-    float Ls = 0.f, O = 0.f;
-    for (int s = 0; s < ns; ++s) {
-      const float* ml = a.part_ml + ((base + s) * a.G + r) * 2;
-      const float ls = ml[1];
-      if (ls > 0.f) {
-        const float f = exp2f(ml[0] - M);
-        Ls += ls * f;
-        O += a.part_acc[((base + s) * a.G + r) * D + d] * f;
-      }
-    }
-    const long long oh = static_cast<long long>(b) * Hq + g * a.G + r;
-    a.out[oh * D + d] = Ls > 0.f ? O / Ls : 0.f;
-    if (d == 0 && a.lse) a.lse[oh] = Ls > 0.f ? (M + log2f(Ls)) * kLn2 : -INFINITY;
+// Sequence holding unit x: the largest b with s_pref[b] <= x.
+__device__ __forceinline__ int seq_of(long long x, const int* s_pref, int B) {
+  int lo = 0, hi = B;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (s_pref[mid] <= x) lo = mid; else hi = mid;
   }
+  return lo;
+}
+
+// Metadata of one unit, gathered by one lane.
+struct UnitMeta {
+  int seg;   // b * H_kv + g, or -1 past the end of the range
+  int p;     // physical block, -1 to skip
+  int nv;    // valid tokens of the block
+};
+
+__device__ __forceinline__ UnitMeta unit_meta(const DecodeArgs& a, long long x, long long u1,
+                                              const int* s_pref, const int* s_nk, const int* s_N) {
+  UnitMeta m{-1, -1, 0};
+  if (x >= u1) return m;
+  const int b = seq_of(x, s_pref, a.B);
+  const int nk = s_nk[b];
+  const int r = static_cast<int>(x - s_pref[b]);
+  const int g = r / nk, j = r % nk;
+  m.seg = b * a.Hkv + g;
+  const int N = s_N[b];
+  const int nb = (N + kBlock - 1) / kBlock;
+  const long long row = static_cast<long long>(b) * a.MAXB;
+  const int kid = a.kept[row + j];
+  if (kid >= 0 && kid < nb) {
+    const int p = a.tables[row + kid];
+    if (p >= 0 && p < a.P) {
+      m.p = p;
+      m.nv = (kid == nb - 1) ? N - kBlock * (nb - 1) : kBlock;
+    } else if (g == 0) {
+      raise_flag(a.flags, ENT_DEV_BAD_TABLE);
+    }
+  } else if (g == 0) {
+    raise_flag(a.flags, ENT_DEV_BAD_TABLE);
+  }
+  return m;
 }
 
 __device__ __forceinline__ bf16x8_t load_bf16x8(const uint16_t* p) {
@@ -182,67 +163,137 @@ __device__ __forceinline__ s16x4_t load_s16x4(const uint16_t* p) {
 }
 
 template <int D>
-__global__ __launch_bounds__(kThreads) void decode_bf16_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) {
   constexpr int KS = D / 32;      // QK k-steps (32 dims each)
   constexpr int MT = D / 16;      // PV output tiles (16 dims each)
-  constexpr int DL = D / 4;       // dims per lane group in QK
   extern __shared__ int s_mem[];
   __shared__ int s_red[kWaves];
   int* s_pref = s_mem;
-  int* s_ns = s_mem + a.B + 1;
-  build_items(a, s_pref, s_ns, s_red);
-  const int total = s_pref[a.B];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int* s_nk = s_mem + a.B + 1;
+  int* s_N = s_nk + a.B;
+  build_plan(a, s_pref, s_nk, s_N, s_red);
+  const long long U = s_pref[a.B];
+  const int lane = threadIdx.x & 63;
+  const int w = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (U == 0) return;
+  const long long u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
+  if (u0 >= u1) return;
   const int r16 = lane & 15, gq = lane >> 4;
-  const int Hq = a.Hkv * a.G;
+  const int G = a.G;
+  const int Hq = a.Hkv * G;
+  const bool head_ok = r16 < G;
   const uint16_t* q = static_cast<const uint16_t*>(a.q);
   const uint16_t* kc = static_cast<const uint16_t*>(a.kc);
   const uint16_t* vc = static_cast<const uint16_t*>(a.vc);
 
-  for (int item = blockIdx.x * kWaves + wave; item < total; item += gridDim.x * kWaves) {
-    const Item it = locate_item(a, item, s_pref, s_ns);
-    const bool head_ok = r16 < a.G;
-    const long long qh = static_cast<long long>(it.b) * Hq + it.g * a.G + r16;
-    bf16x8_t qreg[KS];
+  long long ubase = u0;
+  UnitMeta win = unit_meta(a, ubase + lane, u1, s_pref, s_nk, s_N);
+
+  bf16x8_t kcur[KS], knxt[KS];
+  s16x4_t vcur[MT], vnxt[MT];
+  auto load_tiles = [&](int i, bf16x8_t (&kr)[KS], s16x4_t (&vr)[MT]) {
+    const int seg = __shfl(win.seg, i);
+    const int p = max(__shfl(win.p, i), 0);
+    const int g = max(seg, 0) % a.Hkv;
+    const long long tile = (static_cast<long long>(p) * a.Hkv + g) * kBlock * D;
+    // MFMA k-slot (gq, element e) of QK step ks holds dim ks*32 + gq*8 + e,
+    // for both operands.
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (head_ok) qreg[ks] = load_bf16x8(q + qh * D + gq * DL + ks * 8);
-      else qreg[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+    for (int ks = 0; ks < KS; ++ks) kr[ks] = load_bf16x8(kc + tile + r16 * D + ks * 32 + gq * 8);
+#pragma unroll
+    for (int m = 0; m < MT; ++m) vr[m] = load_s16x4(vc + tile + (16 * m + r16) * kBlock + 4 * gq);
+  };
+  load_tiles(0, kcur, vcur);
+
+  int cur_seg = -1;
+  bf16x8_t qreg[KS];
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4_t oacc[MT];
+
+  auto flush = [&]() {
+    float l_tot = l_run + __shfl_xor(l_run, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    const int b = cur_seg / a.Hkv, g = cur_seg % a.Hkv;
+    const long long seg_start = s_pref[b] + static_cast<long long>(g) * s_nk[b];
+    const long long seg_end = seg_start + s_nk[b];
+    if (!head_ok) return;
+    if (seg_start >= u0 && seg_end <= u1) {
+      const long long oh = static_cast<long long>(b) * Hq + g * G + r16;
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const f32x4_t o = oacc[m] * inv;
+        *reinterpret_cast<float4*>(a.out + oh * D + 16 * m + 4 * gq) = make_float4(o[0], o[1], o[2], o[3]);
+      }
+      if (gq == 0 && a.lse) a.lse[oh] = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
+    } else {
+      const long long slot = static_cast<long long>(w) + cur_seg;
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+        *reinterpret_cast<float4*>(a.part_acc + (slot * G + r16) * D + 16 * m + 4 * gq) =
+            make_float4(oacc[m][0], oacc[m][1], oacc[m][2], oacc[m][3]);
+      if (gq == 0) {
+        a.part_ml[(slot * G + r16) * 2 + 0] = m_run;
+        a.part_ml[(slot * G + r16) * 2 + 1] = l_tot;
+      }
     }
-    float m_run = -INFINITY, l_run = 0.f;
-    f32x4_t oacc[MT];
-#pragma unroll
-    for (int m = 0; m < MT; ++m) oacc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  };
 
-    for (int i = 0; i < it.cnt; ++i) {
-      const int j = __shfl(it.my_j, i);
-      const int p = __shfl(it.my_p, i);
-      if (p < 0) continue;
-      const int nv = (j == it.nb - 1) ? it.N - kBlock * (it.nb - 1) : kBlock;
-      const long long tile = (static_cast<long long>(p) * a.Hkv + it.g) * kBlock * D;
-      bf16x8_t kreg[KS];
+  for (long long u = u0; u < u1; ++u) {
+    int i = static_cast<int>(u - ubase);
+    if (i == kWindow) {
+      ubase = u;
+      i = 0;
+      win = unit_meta(a, ubase + lane, u1, s_pref, s_nk, s_N);
+      load_tiles(0, kcur, vcur);
+    }
+    const int seg = __shfl(win.seg, i);
+    if (seg != cur_seg) {
+      if (cur_seg >= 0) flush();
+      cur_seg = seg;
+      const int b = seg / a.Hkv, g = seg % a.Hkv;
+      const long long qh = static_cast<long long>(b) * Hq + g * G + r16;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kreg[ks] = load_bf16x8(kc + tile + r16 * D + gq * DL + ks * 8);
-      s16x4_t vreg[MT];
+      for (int ks = 0; ks < KS; ++ks) {
+        if (head_ok) qreg[ks] = load_bf16x8(q + qh * D + ks * 32 + gq * 8);
+        else qreg[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+      }
+      m_run = -INFINITY;
+      l_run = 0.f;
 #pragma unroll
-      for (int m = 0; m < MT; ++m) vreg[m] = load_s16x4(vc + tile + (16 * m + r16) * kBlock + 4 * gq);
-
+      for (int m = 0; m < MT; ++m) oacc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+    if (i + 1 < kWindow && u + 1 < u1) load_tiles(i + 1, knxt, vnxt);
+    const int p = __shfl(win.p, i);
+    const int nv = __shfl(win.nv, i);
+    if (p >= 0) {
       f32x4_t sacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kreg[ks], qreg[ks], sacc, 0, 0, 0);
-      float s[4];
+        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kcur[ks], qreg[ks], sacc, 0, 0, 0);
+      float sc[4];
+      bool up = false;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) s[e] = (4 * gq + e < nv) ? sacc[e] * a.scale_log2 : -INFINITY;
-      float mloc = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-      const float m_new = fmaxf(m_run, mloc);
-      const float alpha = exp2f(m_run - m_new);
+      for (int e = 0; e < 4; ++e) {
+        sc[e] = (4 * gq + e < nv) ? sacc[e] * a.scale_log2 : -INFINITY;
+        up |= sc[e] > m_run;
+      }
+      // The running max moves only when some score exceeds it.
+      if (__any(up)) {
+        float mloc = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        const float m_new = fmaxf(m_run, mloc);
+        const float alpha = exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int m = 0; m < MT; ++m) oacc[m] *= alpha;
+        m_run = m_new;
+      }
       float pe[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pe[e] = exp2f(s[e] - m_new);
-      l_run = l_run * alpha + ((pe[0] + pe[1]) + (pe[2] + pe[3]));
+      for (int e = 0; e < 4; ++e) pe[e] = exp2f(sc[e] - m_run);
+      l_run += (pe[0] + pe[1]) + (pe[2] + pe[3]);
       s16x4_t phi, plo;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -255,44 +306,20 @@ __global__ __launch_bounds__(kThreads) void decode_bf16_kernel(DecodeArgs a) {
         for (int m = 0; m < MT; ++m)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (4 * gq + e >= nv) vreg[m][e] = 0;
+            if (4 * gq + e >= nv) vcur[m][e] = 0;
       }
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
-        oacc[m] *= alpha;
-        oacc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vreg[m], phi, oacc[m], 0, 0, 0);
-        oacc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vreg[m], plo, oacc[m], 0, 0, 0);
-      }
-      m_run = m_new;
-    }
-
-    float l_tot = l_run + __shfl_xor(l_run, 16);
-    l_tot += __shfl_xor(l_tot, 32);
-    if (it.ns == 1) {
-      if (head_ok) {
-        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-#pragma unroll
-        for (int m = 0; m < MT; ++m) {
-          const f32x4_t o = oacc[m] * inv;
-          *reinterpret_cast<float4*>(a.out + qh * D + 16 * m + 4 * gq) =
-              make_float4(o[0], o[1], o[2], o[3]);
-        }
-        if (gq == 0 && a.lse) a.lse[qh] = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
-      }
-    } else {
-      const long long slot = (static_cast<long long>(it.b) * a.Hkv + it.g) * a.splits_max + it.sp;
-      if (head_ok) {
-#pragma unroll
-        for (int m = 0; m < MT; ++m)
-          *reinterpret_cast<float4*>(a.part_acc + (slot * a.G + r16) * D + 16 * m + 4 * gq) =
-              make_float4(oacc[m][0], oacc[m][1], oacc[m][2], oacc[m][3]);
-        if (gq == 0) {
-          a.part_ml[(slot * a.G + r16) * 2 + 0] = m_run;
-          a.part_ml[(slot * a.G + r16) * 2 + 1] = l_tot;
-        }
+        oacc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vcur[m], phi, oacc[m], 0, 0, 0);
+        oacc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vcur[m], plo, oacc[m], 0, 0, 0);
       }
     }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kcur[ks] = knxt[ks];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) vcur[m] = vnxt[m];
   }
+  flush();
 }
 
 template <int D>
@@ -301,104 +328,245 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
   extern __shared__ int s_mem[];
   __shared__ int s_red[kWaves];
   int* s_pref = s_mem;
-  int* s_ns = s_mem + a.B + 1;
-  build_items(a, s_pref, s_ns, s_red);
-  const int total = s_pref[a.B];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int* s_nk = s_mem + a.B + 1;
+  int* s_N = s_nk + a.B;
+  build_plan(a, s_pref, s_nk, s_N, s_red);
+  const long long U = s_pref[a.B];
+  const int lane = threadIdx.x & 63;
+  const int w = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (U == 0) return;
+  const long long u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
+  if (u0 >= u1) return;
   const int t16 = lane & 15, hs = lane >> 4;
-  const int Hq = a.Hkv * a.G;
+  const int G = a.G;
+  const int Hq = a.Hkv * G;
   const float* q = static_cast<const float*>(a.q);
   const float* kc = static_cast<const float*>(a.kc);
   const float* vc = static_cast<const float*>(a.vc);
 
-  for (int item = blockIdx.x * kWaves + wave; item < total; item += gridDim.x * kWaves) {
-    const Item it = locate_item(a, item, s_pref, s_ns);
-    const long long qbase = (static_cast<long long>(it.b) * Hq + it.g * a.G) * D;
-    float m_run[kMaxGroup], l_run[kMaxGroup], o[kMaxGroup][DPL];
+  long long ubase = u0;
+  UnitMeta win = unit_meta(a, ubase + lane, u1, s_pref, s_nk, s_N);
+  int cur_seg = -1;
+  long long qbase = 0;
+  float m_run[kMaxGroup], l_run[kMaxGroup], o[kMaxGroup][DPL];
+
+  auto flush = [&]() {
+    const int b = cur_seg / a.Hkv, g = cur_seg % a.Hkv;
+    const long long seg_start = s_pref[b] + static_cast<long long>(g) * s_nk[b];
+    const long long seg_end = seg_start + s_nk[b];
+    const bool whole = seg_start >= u0 && seg_end <= u1;
+    const long long slot = static_cast<long long>(w) + cur_seg;
 #pragma unroll
     for (int h = 0; h < kMaxGroup; ++h) {
-      m_run[h] = -INFINITY;
-      l_run[h] = 0.f;
-#pragma unroll
-      for (int y = 0; y < DPL; ++y) o[h][y] = 0.f;
-    }
-    for (int i = 0; i < it.cnt; ++i) {
-      const int j = __shfl(it.my_j, i);
-      const int p = __shfl(it.my_p, i);
-      if (p < 0) continue;
-      const int nv = (j == it.nb - 1) ? it.N - kBlock * (it.nb - 1) : kBlock;
-      const long long tile = (static_cast<long long>(p) * a.Hkv + it.g) * kBlock * D;
-      // Scores: lane (t16, hs) takes token t16 for heads hs, hs+4, hs+8, hs+12.
-      float sc[4];
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const int h = hs + 4 * x;
-        float dot = 0.f;
-        if (h < a.G && t16 < nv) {
-          for (int d = 0; d < D; ++d) dot += q[qbase + h * D + d] * kc[tile + t16 * D + d];
-          sc[x] = dot * a.scale_log2;
-        } else {
-          sc[x] = -INFINITY;
-        }
-      }
-      float vv[DPL][kBlock];
-#pragma unroll
-      for (int y = 0; y < DPL; ++y)
-#pragma unroll
-        for (int tt = 0; tt < kBlock; ++tt)
-          vv[y][tt] = (tt < nv) ? vc[tile + (lane + 64 * y) * kBlock + tt] : 0.f;
-#pragma unroll
-      for (int h = 0; h < kMaxGroup; ++h) {
-        if (h >= a.G) continue;
-        float st[kBlock];
-        float mb = -INFINITY;
-#pragma unroll
-        for (int tt = 0; tt < kBlock; ++tt) {
-          st[tt] = __shfl(sc[h >> 2], 16 * (h & 3) + tt);
-          mb = fmaxf(mb, st[tt]);
-        }
-        const float m_new = fmaxf(m_run[h], mb);
-        const float alpha = exp2f(m_run[h] - m_new);
-        float lsum = 0.f;
-        float acc[DPL];
-#pragma unroll
-        for (int y = 0; y < DPL; ++y) acc[y] = 0.f;
-#pragma unroll
-        for (int tt = 0; tt < kBlock; ++tt) {
-          const float pt = exp2f(st[tt] - m_new);
-          lsum += pt;
-#pragma unroll
-          for (int y = 0; y < DPL; ++y) acc[y] += pt * vv[y][tt];
-        }
-        l_run[h] = l_run[h] * alpha + lsum;
-#pragma unroll
-        for (int y = 0; y < DPL; ++y) o[h][y] = o[h][y] * alpha + acc[y];
-        m_run[h] = m_new;
-      }
-    }
-    if (it.ns == 1) {
-#pragma unroll
-      for (int h = 0; h < kMaxGroup; ++h) {
-        if (h >= a.G) continue;
-        const long long oh = static_cast<long long>(it.b) * Hq + it.g * a.G + h;
+      if (h >= G) continue;
+      if (whole) {
+        const long long oh = static_cast<long long>(b) * Hq + g * G + h;
         const float inv = l_run[h] > 0.f ? 1.f / l_run[h] : 0.f;
 #pragma unroll
         for (int y = 0; y < DPL; ++y) a.out[oh * D + lane + 64 * y] = o[h][y] * inv;
         if (lane == 0 && a.lse)
           a.lse[oh] = l_run[h] > 0.f ? (m_run[h] + log2f(l_run[h])) * kLn2 : -INFINITY;
-      }
-    } else {
-      const long long slot = (static_cast<long long>(it.b) * a.Hkv + it.g) * a.splits_max + it.sp;
+      } else {
 #pragma unroll
-      for (int h = 0; h < kMaxGroup; ++h) {
-        if (h >= a.G) continue;
-#pragma unroll
-        for (int y = 0; y < DPL; ++y) a.part_acc[(slot * a.G + h) * D + lane + 64 * y] = o[h][y];
+        for (int y = 0; y < DPL; ++y) a.part_acc[(slot * G + h) * D + lane + 64 * y] = o[h][y];
         if (lane == 0) {
-          a.part_ml[(slot * a.G + h) * 2 + 0] = m_run[h];
-          a.part_ml[(slot * a.G + h) * 2 + 1] = l_run[h];
+          a.part_ml[(slot * G + h) * 2 + 0] = m_run[h];
+          a.part_ml[(slot * G + h) * 2 + 1] = l_run[h];
         }
       }
+    }
+  };
+
+  for (long long u = u0; u < u1; ++u) {
+    int i = static_cast<int>(u - ubase);
+    if (i == kWindow) {
+      ubase = u;
+      i = 0;
+      win = unit_meta(a, ubase + lane, u1, s_pref, s_nk, s_N);
+    }
+    const int seg = __shfl(win.seg, i);
+    if (seg != cur_seg) {
+      if (cur_seg >= 0) flush();
+      cur_seg = seg;
+      const int b = seg / a.Hkv, g = seg % a.Hkv;
+      qbase = (static_cast<long long>(b) * Hq + g * G) * D;
+#pragma unroll
+      for (int h = 0; h < kMaxGroup; ++h) {
+        m_run[h] = -INFINITY;
+        l_run[h] = 0.f;
+#pragma unroll
+        for (int y = 0; y < DPL; ++y) o[h][y] = 0.f;
+      }
+    }
+    const int p = __shfl(win.p, i);
+    const int nv = __shfl(win.nv, i);
+    if (p < 0) continue;
+    const long long tile = (static_cast<long long>(p) * a.Hkv + (seg % a.Hkv)) * kBlock * D;
+    // Scores: lane (t16, hs) takes token t16 for heads hs, hs+4, hs+8, hs+12.
+    float sc[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int h = hs + 4 * x;
+      float dot = 0.f;
+      if (h < G && t16 < nv) {
+        for (int d = 0; d < D; ++d) dot += q[qbase + h * D + d] * kc[tile + t16 * D + d];
+        sc[x] = dot * a.scale_log2;
+      } else {
+        sc[x] = -INFINITY;
+      }
+    }
+    float vv[DPL][kBlock];
+#pragma unroll
+    for (int y = 0; y < DPL; ++y)
+#pragma unroll
+      for (int tt = 0; tt < kBlock; ++tt)
+        vv[y][tt] = (tt < nv) ? vc[tile + (lane + 64 * y) * kBlock + tt] : 0.f;
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h) {
+      if (h >= G) continue;
+      float st[kBlock];
+      float mb = -INFINITY;
+#pragma unroll
+      for (int tt = 0; tt < kBlock; ++tt) {
+        st[tt] = __shfl(sc[h >> 2], 16 * (h & 3) + tt);
+        mb = fmaxf(mb, st[tt]);
+      }
+      const float m_new = fmaxf(m_run[h], mb);
+      const float alpha = exp2f(m_run[h] - m_new);
+      float lsum = 0.f;
+      float acc[DPL];
+#pragma unroll
+      for (int y = 0; y < DPL; ++y) acc[y] = 0.f;
+#pragma unroll
+      for (int tt = 0; tt < kBlock; ++tt) {
+        const float pt = exp2f(st[tt] - m_new);
+        lsum += pt;
+#pragma unroll
+        for (int y = 0; y < DPL; ++y) acc[y] += pt * vv[y][tt];
+      }
+      l_run[h] = l_run[h] * alpha + lsum;
+#pragma unroll
+      for (int y = 0; y < DPL; ++y) o[h][y] = o[h][y] * alpha + acc[y];
+      m_run[h] = m_new;
+    }
+  }
+  flush();
+}
+
+// Merge of the partials of every segment that the decode ranges cut (one
+// workgroup per segment).  Segments with nothing kept get zeros and -inf.
+// The (max, sum) pairs of all contributing waves are read at once; per head
+// M = max m, L = sum l 2^(m - M), then out = sum acc 2^(m - M) / L with every
+// thread streaming its outputs' partial accumulators as independent loads.
+template <int D>
+__global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
+  extern __shared__ int s_mem[];
+  __shared__ int s_red[kWaves];
+  __shared__ float s_m[kCombineMaxSplits * kMaxGroup], s_l[kCombineMaxSplits * kMaxGroup];
+  __shared__ float s_M[kMaxGroup], s_L[kMaxGroup];
+  int* s_pref = s_mem;
+  int* s_nk = s_mem + a.B + 1;
+  int* s_N = s_nk + a.B;
+  build_plan(a, s_pref, s_nk, s_N, s_red);
+  const long long U = s_pref[a.B];
+  const int t = threadIdx.x;
+  const int seg = blockIdx.x;
+  const int b = seg / a.Hkv, g = seg % a.Hkv;
+  const int G = a.G;
+  const int Hq = a.Hkv * G;
+  const int nk = s_nk[b];
+  if (nk == 0) {
+    for (int idx = t; idx < G * D; idx += kThreads) {
+      const int r = idx / D, d = idx % D;
+      const long long oh = static_cast<long long>(b) * Hq + g * G + r;
+      a.out[oh * D + d] = 0.f;
+      if (d == 0 && a.lse) a.lse[oh] = -INFINITY;
+    }
+    return;
+  }
+  const long long seg_start = s_pref[b] + static_cast<long long>(g) * nk;
+  const int w0 = wave_of(seg_start, U, a.W);
+  const int w1 = wave_of(seg_start + nk - 1, U, a.W);
+  if (w0 == w1) return;                      // written whole by the decode kernel
+  const int ns = w1 - w0 + 1;
+
+  // Pass 1: M and L per head.
+  float M = -INFINITY, L = 0.f;              // meaningful in threads t < G
+  for (int c0 = 0; c0 < ns; c0 += kCombineMaxSplits) {
+    const int n = min(kCombineMaxSplits, ns - c0);
+    for (int e = t; e < n * G; e += kThreads) {
+      const int k = e / G, r = e % G;
+      const int wi = w0 + c0 + k;
+      // A wave with an empty range (fewer units than waves) wrote no partial.
+      const bool live = range_begin(wi + 1, U, a.W) > range_begin(wi, U, a.W);
+      const long long slot = static_cast<long long>(wi) + seg;
+      s_m[e] = live ? a.part_ml[(slot * G + r) * 2 + 0] : 0.f;
+      s_l[e] = live ? a.part_ml[(slot * G + r) * 2 + 1] : 0.f;
+    }
+    __syncthreads();
+    if (t < G) {
+      float Mc = M;
+      for (int k = 0; k < n; ++k)
+        if (s_l[k * G + t] > 0.f) Mc = fmaxf(Mc, s_m[k * G + t]);
+      float Lc = (L > 0.f) ? L * exp2f(M - Mc) : 0.f;
+      for (int k = 0; k < n; ++k) {
+        const float l = s_l[k * G + t];
+        if (l > 0.f) Lc += l * exp2f(s_m[k * G + t] - Mc);
+      }
+      M = Mc;
+      L = Lc;
+    }
+    __syncthreads();
+  }
+  if (t < G) {
+    s_M[t] = M;
+    s_L[t] = L;
+  }
+  __syncthreads();
+
+  // Pass 2: weighted sum of the partial outputs.
+  constexpr int kPer = (kMaxGroup * D + kThreads - 1) / kThreads;
+  float acc[kPer];
+#pragma unroll
+  for (int x = 0; x < kPer; ++x) acc[x] = 0.f;
+  for (int c0 = 0; c0 < ns; c0 += kCombineMaxSplits) {
+    const int n = min(kCombineMaxSplits, ns - c0);
+    for (int e = t; e < n * G; e += kThreads) {
+      const int k = e / G, r = e % G;
+      const int wi = w0 + c0 + k;
+      const bool live = range_begin(wi + 1, U, a.W) > range_begin(wi, U, a.W);
+      const long long slot = static_cast<long long>(wi) + seg;
+      const float m = live ? a.part_ml[(slot * G + r) * 2 + 0] : 0.f;
+      const float l = live ? a.part_ml[(slot * G + r) * 2 + 1] : 0.f;
+      s_m[e] = (l > 0.f && s_L[r] > 0.f) ? exp2f(m - s_M[r]) / s_L[r] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int x = 0; x < kPer; ++x) {
+      const int idx = t + x * kThreads;
+      if (idx < G * D) {
+        const int r = idx / D, d = idx % D;
+        const float* pa = a.part_acc + ((static_cast<long long>(w0 + c0) + seg) * G + r) * D + d;
+        float o = 0.f;
+#pragma unroll 8
+        for (int k = 0; k < n; ++k) {
+          const float wk = s_m[k * G + r];
+          const float v = pa[static_cast<long long>(k) * G * D];
+          o += wk > 0.f ? wk * v : 0.f;
+        }
+        acc[x] += o;
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int x = 0; x < kPer; ++x) {
+    const int idx = t + x * kThreads;
+    if (idx < G * D) {
+      const int r = idx / D, d = idx % D;
+      const long long oh = static_cast<long long>(b) * Hq + g * G + r;
+      a.out[oh * D + d] = acc[x];
+      if (d == 0 && a.lse) a.lse[oh] = s_L[r] > 0.f ? (s_M[r] + log2f(s_L[r])) * kLn2 : -INFINITY;
     }
   }
 }
@@ -411,11 +579,13 @@ int occupancy_blocks(K kernel, size_t lds) {
   return n;
 }
 
+size_t plan_lds_bytes(int B) { return static_cast<size_t>(3 * B + 1) * sizeof(int); }
+
 }  // namespace
 
 int decode_grid_size(const ent_ctx* c) {
   const ent_config& cf = c->cfg;
-  const size_t lds = static_cast<size_t>(2 * cf.max_batch + 1) * sizeof(int);
+  const size_t lds = plan_lds_bytes(cf.max_batch);
   int per_cu = 1;
   if (cf.kv_dtype == ENT_BF16)
     per_cu = cf.head_dim == 128 ? occupancy_blocks(decode_bf16_kernel<128>, lds)
@@ -424,6 +594,11 @@ int decode_grid_size(const ent_ctx* c) {
     per_cu = cf.head_dim == 128 ? occupancy_blocks(decode_f32_kernel<128>, lds)
                                 : occupancy_blocks(decode_f32_kernel<64>, lds);
   return c->num_cu * per_cu;
+}
+
+long long decode_partial_slots(int decode_grid, int max_batch, int num_kv_heads) {
+  return static_cast<long long>(decode_grid) * kWaves +
+         static_cast<long long>(max_batch) * num_kv_heads;
 }
 
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
@@ -449,9 +624,9 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   a.G = c->group;
   a.MAXB = cf.max_blocks_per_seq;
   a.P = cf.num_pool_blocks;
-  a.splits_max = c->splits_max;
+  a.W = c->decode_grid * kWaves;
   a.scale_log2 = cf.scale * kLog2e;
-  const size_t lds = static_cast<size_t>(2 * B + 1) * sizeof(int);
+  const size_t lds = plan_lds_bytes(B);
   const dim3 grid(c->decode_grid);
   if (cf.kv_dtype == ENT_BF16) {
     if (cf.head_dim == 128)
@@ -466,11 +641,11 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const dim3 cgrid((B * cf.num_kv_heads + kWaves - 1) / kWaves);
+  const dim3 cgrid(B * cf.num_kv_heads);
   if (cf.head_dim == 128)
-    hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), lds, s, a);
   else
-    hipLaunchKernelGGL(combine_kernel<64>, cgrid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(combine_kernel<64>, cgrid, dim3(kThreads), lds, s, a);
   return hipGetLastError();
 }
 

@@ -12,8 +12,7 @@ namespace ent {
 
 constexpr int kBlock = ENT_BLOCK_SIZE;      // tokens per KV block
 constexpr int kRowChunk = ENT_ROW_CHUNK;    // logits per entropy chunk
-constexpr int kScoreChunk = 64;             // blocks per scoring workgroup
-constexpr int kSplitBlocks = 16;            // kept blocks per decode work item
+constexpr int kScoreChunk = 16;             // blocks per scoring workgroup
 constexpr int kMaxGroup = 16;               // query heads per KV head
 constexpr int kMaxBlocksPerSeq = 16384;     // selection keeps all scores in LDS
 constexpr float kLog2e = 1.4426950408889634f;
@@ -28,7 +27,6 @@ struct ent_ctx {
   int group = 1;            // G = H_q / H_kv
   int chunks = 0;           // entropy chunks per logit row
   int score_chunks = 0;     // scoring workgroups per sequence
-  int splits_max = 0;       // decode work items per (sequence, KV head)
   int decode_grid = 0;      // persistent decode workgroups
 
   void* ws = nullptr;       // one workspace allocation
@@ -36,10 +34,8 @@ struct ent_ctx {
   float* ent_part = nullptr;      // [max_batch, chunks, 3]  (max, sum, weighted sum)
   float* stats_tmp = nullptr;     // [max_batch, chunks, 2]  row statistics scratch
   float* zbuf = nullptr;          // [max_batch, MAXB, H_q]  block logits
-  float* lse_part = nullptr;      // [max_batch, score_chunks, H_q, 2]
-  float* score_ws = nullptr;      // [max_batch, MAXB]       block scores
-  float* dec_acc = nullptr;       // [max_batch * H_kv * splits_max, G, d]
-  float* dec_ml = nullptr;        // [max_batch * H_kv * splits_max, G, 2]
+  float* dec_acc = nullptr;       // [decode partial slots, G, d]
+  float* dec_ml = nullptr;        // [decode partial slots, G, 2]
   unsigned* dev_flags = nullptr;  // [1]
 
   std::string err;
@@ -69,8 +65,10 @@ hipError_t launch_kv_append(const ent_ctx* c, int B, const void* k_new, const vo
                             const int* tables, int* ctx_lens, void* k_cache, void* v_cache,
                             float* ksum, hipStream_t s);
 
-// Occupancy-derived persistent grid of the decode kernel.
+// Occupancy-derived persistent grid of the decode kernel, and the number of
+// partial slots its split segments may use (waves + segments).
 int decode_grid_size(const ent_ctx* c);
+long long decode_partial_slots(int decode_grid, int max_batch, int num_kv_heads);
 
 }  // namespace ent
 
