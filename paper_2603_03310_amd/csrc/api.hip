@@ -140,19 +140,20 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   const ent_config& f = c->cfg;
   c->group = f.num_q_heads / f.num_kv_heads;
   c->chunks = ent_row_stats_chunks(f.vocab);
-  c->score_chunks = (f.max_blocks_per_seq + ent::kScoreChunk - 1) / ent::kScoreChunk;
+  c->lse_chunks = (f.max_blocks_per_seq + ent::kMinScoreChunk - 1) / ent::kMinScoreChunk;
   c->decode_grid = ent::decode_grid_size(c);
 
   const size_t Bm = static_cast<size_t>(f.max_batch);
   const size_t sz_ent_part = align_up(Bm * c->chunks * 3 * sizeof(float));
   const size_t sz_stats = align_up(Bm * c->chunks * 2 * sizeof(float));
   const size_t sz_z = align_up(Bm * f.max_blocks_per_seq * f.num_q_heads * sizeof(float));
+  const size_t sz_lse = align_up(Bm * c->lse_chunks * f.num_q_heads * 2 * sizeof(float));
   const size_t nslots = static_cast<size_t>(
       ent::decode_partial_slots(c->decode_grid, f.max_batch, f.num_kv_heads));
   const size_t sz_acc = align_up(nslots * c->group * f.head_dim * sizeof(float));
   const size_t sz_ml = align_up(nslots * c->group * 2 * sizeof(float));
   const size_t sz_flags = align_up(sizeof(unsigned));
-  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_acc + sz_ml + sz_flags;
+  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_acc + sz_ml + sz_flags;
   e = hipMalloc(&c->ws, c->ws_bytes);
   if (e != hipSuccess) {
     g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
@@ -172,6 +173,7 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->ent_part = reinterpret_cast<float*>(take(sz_ent_part));
   c->stats_tmp = reinterpret_cast<float*>(take(sz_stats));
   c->zbuf = reinterpret_cast<float*>(take(sz_z));
+  c->lse_part = reinterpret_cast<float*>(take(sz_lse));
   c->dec_acc = reinterpret_cast<float*>(take(sz_acc));
   c->dec_ml = reinterpret_cast<float*>(take(sz_ml));
   c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));
@@ -243,8 +245,7 @@ int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum, const 
   if (B == 0) return ENT_OK;
   if (!q || !ksum || !block_tables || !ctx_lens || !h || !kept || !n_kept)
     return fail(c, ENT_E_INVAL, "ent_block_select: NULL required pointer");
-  const size_t qa = c->cfg.kv_dtype == ENT_BF16 ? 8 : 16;
-  if (!aligned(q, qa) || !aligned(ksum, 16))
+  if (!aligned(q, 16) || !aligned(ksum, 16))
     return fail(c, ENT_E_INVAL, "ent_block_select: q or ksum misaligned");
   const hipError_t e = ent::launch_block_select(c, B, q, ksum, block_tables, ctx_lens, h, kept,
                                                 n_kept, scores, theta,

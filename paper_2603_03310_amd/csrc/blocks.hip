@@ -12,8 +12,10 @@
 //
 // Kernels:
 //   summary_kernel   per-block mean keys (setup)
-//   score_kernel        z for 16 blocks x all heads per workgroup
-//   select_kernel       per sequence: the per-head log-sum-exp L_h, computes
+//   score_mfma_kernel   z for 64 blocks x all heads per workgroup (bf16, MFMA)
+//   score_valu_kernel   z for 16 blocks x all heads per workgroup (fp32, VALU)
+//   select_kernel       per sequence: merges the per-chunk log-sum-exp
+//                       partials into L_h, computes
 //                       I_b, the budget, a 4-pass 8-bit radix select of the
 //                       k-th largest score, ascending compaction with ballots
 //   append_kernel    writes one token and refreshes its block's mean key
@@ -104,20 +106,165 @@ __global__ __launch_bounds__(kThreads) void append_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Scoring.  A workgroup of 4 waves takes 16 blocks of one sequence, 4 per
-// wave, and writes z_bh = scale <q_h, kbar_b,g(h)> for all of them.  The
-// critical path is two memory round trips: the wave's table entries and the
-// query heads (staged once in LDS as fp32) are loaded together, then all
-// summary loads of the wave's 4 blocks are in flight at once.  A block's
-// summary (H_kv x d floats) is read as NP passes of 256 floats, one float4
-// per lane per pass, fully coalesced.  In a pass, a group of L = d/4 lanes
-// covers one KV head: each lane forms G partial dot products (one per query
-// head of that KV head) and a halving butterfly reduces them over the L
-// lanes, leaving head r = li * G / L in lane li.
+// Scoring.  Both scoring kernels write the block logits
+//   z_bh = scale <q_h, kbar_b,g(h)>     zbuf [B, MAXB, H_q]
+// and, per chunk of blocks and head, the log-sum-exp partial (max, sum) of
+// l_bh = z_bh + ln n_b over the chunk's blocks.
+//
+// bf16 queries (MFMA).  A workgroup of 4 waves takes 64 blocks, a tile of 16
+// per wave.  For each KV head g the tile's logits are one small contraction
+//   Z[16 blocks x 16] = Kbar_g[16 x d] . Q_g^T[d x 16]   (columns: the G query
+// heads of g, zero-padded), on v_mfma_f32_16x16x32_bf16.  The fp32 summaries
+// are split exactly into three bf16 parts (hi + mid + lo: x - hi and the
+// remainder after mid are exact in fp32 and fit bf16), so three MFMAs per
+// k-step give the fp32 dot product of exact bf16 products.  A operands come
+// straight from global memory (8 dims per lane), the queries are staged in
+// LDS as bf16, and the next KV head's summaries are prefetched.
+//
+// fp32 queries (VALU).  A workgroup of 4 waves takes 16 blocks, 4 per wave;
+// a block's summary is read as NP passes of 256 floats, one float4 per lane
+// per pass; each lane forms G partial dot products over its 4 dims and a
+// halving butterfly reduces them over the d/4 lanes of its KV head.
 // ---------------------------------------------------------------------------
 constexpr int kScoreThreads = 256;
 constexpr int kScoreWaves = kScoreThreads / 64;
-constexpr int kScorePerWave = kScoreChunk / kScoreWaves;   // 4 blocks per wave
+constexpr int kMfmaChunk = 64;                 // blocks per MFMA scoring workgroup
+constexpr int kValuChunk = 16;                 // blocks per VALU scoring workgroup
+constexpr int kValuPerWave = kValuChunk / kScoreWaves;
+
+typedef __bf16 sbf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef float sf32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
+
+// Per-head log-sum-exp partial of l = z + ln n over the chunk's nblk blocks
+// (z tile in LDS, row stride Hq).
+__device__ __forceinline__ void chunk_lse(const float* zt, int nblk, int Hq, int j_lo, int nb,
+                                          int N, float* lp_chunk) {
+  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
+  const float ln_full = logf(static_cast<float>(kBlock));
+  for (int h = threadIdx.x; h < Hq; h += blockDim.x) {
+    float m = -INFINITY;
+    for (int i = 0; i < nblk; ++i) {
+      const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
+      m = fmaxf(m, zt[i * Hq + h] + lnn);
+    }
+    float s = 0.f;
+    for (int i = 0; i < nblk; ++i) {
+      const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
+      s += expf(zt[i * Hq + h] + lnn - m);
+    }
+    lp_chunk[h * 2 + 0] = m;
+    lp_chunk[h * 2 + 1] = s;
+  }
+}
+
+// Exact three-way bf16 split of 8 floats (two float4) into packed bf16x8.
+__device__ __forceinline__ void split3(const float4& x0, const float4& x1, sbf16x8_t& hi,
+                                       sbf16x8_t& mid, sbf16x8_t& lo) {
+  const float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+  uint32_t h[4], m[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t hb[2], mb[2], lb[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const uint32_t ux = __float_as_uint(v[2 * i + k]);
+      const uint32_t uh = ux & 0xFFFF0000u;
+      const float r = v[2 * i + k] - __uint_as_float(uh);
+      const uint32_t um = __float_as_uint(r) & 0xFFFF0000u;
+      const uint32_t ul = __float_as_uint(r - __uint_as_float(um));
+      hb[k] = uh;
+      mb[k] = um;
+      lb[k] = ul;
+    }
+    h[i] = (hb[0] >> 16) | hb[1];
+    m[i] = (mb[0] >> 16) | mb[1];
+    l[i] = (lb[0] >> 16) | (lb[1] & 0xFFFF0000u);
+  }
+  hi = __builtin_bit_cast(sbf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
+  mid = __builtin_bit_cast(sbf16x8_t, make_uint4(m[0], m[1], m[2], m[3]));
+  lo = __builtin_bit_cast(sbf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
+}
+
+template <int D>
+__global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
+    const uint16_t* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
+    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
+    int Hkv, int G, int MAXB, int P, int nch_max, float scale, unsigned* flags) {
+  constexpr int KS = D / 32;
+  extern __shared__ float smem[];            // z tile [kMfmaChunk][Hq] fp32, then q [Hq][D] bf16
+  const int Hq = Hkv * G;
+  float* zt = smem;
+  uint16_t* qs = reinterpret_cast<uint16_t*>(smem + kMfmaChunk * Hq);
+  const int ch = blockIdx.x, b = blockIdx.y;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int r16 = lane & 15, gq = lane >> 4;
+  const int j_lo = ch * kMfmaChunk;
+  const int jt = j_lo + wave * 16;           // first block of this wave's tile
+  // Table entry of block jt + r16, read before the context length is known
+  // (in bounds of the MAXB-entry row); masked below.
+  int p = 0;
+  if (jt + r16 < MAXB) p = tables[static_cast<long long>(b) * MAXB + jt + r16];
+  const int N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) return;    // flagged by the selection kernel
+  const int nb = (N + kBlock - 1) / kBlock;
+  if (j_lo >= nb) return;
+  const int nblk = min(kMfmaChunk, nb - j_lo);
+  const bool row_ok = jt + r16 < nb;
+  if (row_ok && (p < 0 || p >= P)) {
+    raise_flag(flags, ENT_DEV_BAD_TABLE);
+    p = 0;
+  }
+  if (!row_ok) p = 0;
+  const bool any_rows = jt < nb;
+  const int nfl = Hkv * D;
+
+  float4 cur[2 * KS], nxt[2 * KS];
+  auto load_g = [&](int g, float4 (&buf)[2 * KS]) {
+    const float* src = ksum + static_cast<long long>(p) * nfl + g * D + gq * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      buf[2 * ks] = *reinterpret_cast<const float4*>(src + ks * 32);
+      buf[2 * ks + 1] = *reinterpret_cast<const float4*>(src + ks * 32 + 4);
+    }
+  };
+  if (any_rows) load_g(0, cur);
+  // Stage the queries (bf16) in LDS, 16 bytes per thread per step.
+  const uint4* qsrc = reinterpret_cast<const uint4*>(q + static_cast<long long>(b) * Hq * D);
+  for (int e = t; e < Hq * D / 8; e += kScoreThreads) reinterpret_cast<uint4*>(qs)[e] = qsrc[e];
+  __syncthreads();
+
+  if (any_rows) {
+    for (int g = 0; g < Hkv; ++g) {
+      if (g + 1 < Hkv) load_g(g + 1, nxt);
+      sf32x4_t acc = sf32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        sbf16x8_t hi, mid, lo;
+        split3(cur[2 * ks], cur[2 * ks + 1], hi, mid, lo);
+        uint4 qb = make_uint4(0u, 0u, 0u, 0u);
+        if (r16 < G) qb = *reinterpret_cast<const uint4*>(qs + (g * G + r16) * D + ks * 32 + gq * 8);
+        const sbf16x8_t bq = __builtin_bit_cast(sbf16x8_t, qb);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mid, bq, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, bq, acc, 0, 0, 0);
+      }
+      // acc[e]: block 4*gq + e of the tile, query head g*G + r16.
+      if (r16 < G) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int blk = 4 * gq + e;
+          if (jt + blk < nb) zt[(wave * 16 + blk) * Hq + g * G + r16] = acc[e] * scale;
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 2 * KS; ++k) cur[k] = nxt[k];
+    }
+  }
+  __syncthreads();
+  float* zrow = zbuf + (static_cast<long long>(b) * MAXB + j_lo) * Hq;
+  for (int e = t; e < nblk * Hq; e += kScoreThreads) zrow[e] = zt[e];
+  chunk_lse(zt, nblk, Hq, j_lo, nb, N, lse_part + (static_cast<long long>(b) * nch_max + ch) * Hq * 2);
+}
 
 template <int G, int L>
 __device__ __forceinline__ float reduce_heads(float (&a)[G], int li) {
@@ -137,84 +284,64 @@ __device__ __forceinline__ float reduce_heads(float (&a)[G], int li) {
   return v;
 }
 
-template <typename T, int D, int G, int kMaxPasses>   // np <= kMaxPasses
-__global__ __launch_bounds__(kScoreThreads) void score_kernel(
-    const T* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
-    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, int Hkv, int MAXB, int P,
-    float scale, unsigned* flags) {
+template <int D, int G>
+__global__ __launch_bounds__(kScoreThreads) void score_valu_kernel(
+    const float* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
+    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
+    int Hkv, int MAXB, int P, int nch_max, float scale, unsigned* flags) {
   constexpr int L = D / 4;
+  constexpr int kMaxPasses = 8;              // H_kv * d <= 2048
   static_assert(G <= L, "heads per KV head exceed the lane group");
-  extern __shared__ float smem[];            // q [Hq][D] fp32, then z tile [kScoreChunk][Hq]
+  extern __shared__ float smem[];            // q [Hq][D] fp32, then z tile [kValuChunk][Hq]
   const int Hq = Hkv * G;
   float* qs = smem;
   float* zt = smem + Hq * D;
   const int ch = blockIdx.x, b = blockIdx.y;
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int li = lane % L;
-  const int j_lo = ch * kScoreChunk;
-  const int jw = j_lo + wave * kScorePerWave;
-  // Table entries are read before the context length is known (the row has
-  // MAXB entries, so the read is in bounds); invalid ones are masked below.
-  int my_p = 0;
-  if (lane < kScorePerWave && jw + lane < MAXB) my_p = tables[static_cast<long long>(b) * MAXB + jw + lane];
   const int N = ctx_lens[b];
   if (N < 0 || N > MAXB * kBlock) return;    // flagged by the selection kernel
   const int nb = (N + kBlock - 1) / kBlock;
+  const int j_lo = ch * kValuChunk;
   if (j_lo >= nb) return;
-  const int nblk = min(kScoreChunk, nb - j_lo);
-  const int nmine = max(0, min(kScorePerWave, nb - jw));
-  if (lane < nmine && (my_p < 0 || my_p >= P)) {
-    raise_flag(flags, ENT_DEV_BAD_TABLE);
-    my_p = 0;
-  }
-  if (lane >= nmine) my_p = 0;
-  const int nfl = Hkv * D;
-  const int np = (nfl + 255) >> 8;
-
-  float4 kv[kScorePerWave][kMaxPasses];
-#pragma unroll
-  for (int blk = 0; blk < kScorePerWave; ++blk) {
-    const int p = __shfl(my_p, blk);
-#pragma unroll
-    for (int k = 0; k < kMaxPasses; ++k) {
-      const int f = 256 * k + 4 * lane;
-      if (blk < nmine && k < np && f < nfl)
-        kv[blk][k] = *reinterpret_cast<const float4*>(ksum + static_cast<long long>(p) * nfl + f);
-      else
-        kv[blk][k] = make_float4(0.f, 0.f, 0.f, 0.f);
+  const int nblk = min(kValuChunk, nb - j_lo);
+  const int jw = j_lo + wave * kValuPerWave;
+  const int nmine = max(0, min(kValuPerWave, nb - jw));
+  int my_p = 0;
+  if (lane < nmine) {
+    my_p = tables[static_cast<long long>(b) * MAXB + jw + lane];
+    if (my_p < 0 || my_p >= P) {
+      raise_flag(flags, ENT_DEV_BAD_TABLE);
+      my_p = 0;
     }
   }
-  for (int e = t; e < Hq * D; e += kScoreThreads)
-    qs[e] = load_elem<T>(q + static_cast<long long>(b) * Hq * D + e);
+  for (int e = t; e < Hq * D; e += kScoreThreads) qs[e] = q[static_cast<long long>(b) * Hq * D + e];
   __syncthreads();
-
-#pragma unroll
-  for (int blk = 0; blk < kScorePerWave; ++blk) {
-    if (blk >= nmine) continue;
-#pragma unroll
-    for (int k = 0; k < kMaxPasses; ++k) {
-      if (k >= np) continue;
+  const int nfl = Hkv * D;
+  const int np = (nfl + 255) >> 8;
+  for (int blk = 0; blk < nmine; ++blk) {
+    const int p = __shfl(my_p, blk);
+    for (int k = 0; k < np; ++k) {
       const int f = 256 * k + 4 * lane;
       const bool gv = f < nfl;
+      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (gv) kv = *reinterpret_cast<const float4*>(ksum + static_cast<long long>(p) * nfl + f);
       const int g = f / D, dd = f % D;
       float a[G];
 #pragma unroll
       for (int r = 0; r < G; ++r) {
         float4 qq = make_float4(0.f, 0.f, 0.f, 0.f);
         if (gv) qq = *reinterpret_cast<const float4*>(qs + (g * G + r) * D + dd);
-        a[r] = qq.x * kv[blk][k].x + qq.y * kv[blk][k].y + qq.z * kv[blk][k].z +
-               qq.w * kv[blk][k].w;
+        a[r] = qq.x * kv.x + qq.y * kv.y + qq.z * kv.z + qq.w * kv.w;
       }
       const float z = reduce_heads<G, L>(a, li) * scale;
-      if (gv && (li % (L / G)) == 0)
-        zt[(wave * kScorePerWave + blk) * Hq + g * G + li / (L / G)] = z;
+      if (gv && (li % (L / G)) == 0) zt[(wave * kValuPerWave + blk) * Hq + g * G + li / (L / G)] = z;
     }
-    // Keep the next block's LDS reads from being hoisted above this point.
-    asm volatile("" ::: "memory");
   }
   __syncthreads();
   float* zrow = zbuf + (static_cast<long long>(b) * MAXB + j_lo) * Hq;
   for (int e = t; e < nblk * Hq; e += kScoreThreads) zrow[e] = zt[e];
+  chunk_lse(zt, nblk, Hq, j_lo, nb, N, lse_part + (static_cast<long long>(b) * nch_max + ch) * Hq * 2);
 }
 
 __device__ __forceinline__ unsigned float_key(float f) {
@@ -239,7 +366,7 @@ __device__ __forceinline__ int keep_budget(float h, int nb, float eps_h, float h
 }
 
 // Kept set of one sequence (one workgroup of 512 threads):
-//  1. L_h = ln sum_b n_b e^{z_bh}, from the block logits z;
+//  1. L_h = ln sum_b n_b e^{z_bh}, merged from the scoring kernel's partials;
 //  2. I_b = (1/H_q) sum_h e^{z_bh + ln n_b - L_h} (L_h - z_bh) for every block,
 //     held in LDS as order-preserving integer keys;
 //  3. budget k from the entropy, the k-th largest key by a 4-pass 8-bit radix
@@ -248,10 +375,10 @@ constexpr int kSelThreads = 512;
 constexpr int kSelWaves = kSelThreads / 64;
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
-    const float* __restrict__ zbuf, const int* __restrict__ ctx_lens,
-    const float* __restrict__ hvec, float* __restrict__ scores_out,
-    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int Hq,
-    int MAXB, float eps_h, float h_min,
+    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, const float* __restrict__ hvec,
+    float* __restrict__ scores_out, float* __restrict__ theta_out, int* __restrict__ kept,
+    int* __restrict__ n_kept, int Hq, int MAXB, int chunk, int nch_max, float eps_h, float h_min,
     float log_v, float kappa_min, int b_min, unsigned* flags) {
   extern __shared__ unsigned keys[];        // [MAXB]
   __shared__ unsigned hist[256];
@@ -277,25 +404,21 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     }
     return;
   }
-  // 1. L_h = ln sum_b n_b e^{z_bh}: each thread folds, online, a strided
-  //    subset of the blocks for head t % Hq; one thread per head folds the
-  //    subsets.
-  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
-  const float ln_full = logf(static_cast<float>(kBlock));
-  const float* zb = zbuf + static_cast<long long>(b) * MAXB * Hq;
+  // 1. L_h = ln sum_b n_b e^{z_bh}, merged from the per-chunk partials: each
+  //    thread folds a strided subset of the chunks of head t % Hq, then one
+  //    thread per head folds the subsets.
+  const int nch = (nb + chunk - 1) / chunk;
   const int per_head = kSelThreads / Hq;     // threads per head (Hq <= 128)
   {
     float m = -INFINITY, sum = 0.f;
     if (t < per_head * Hq) {
       const int h = t % Hq;
-      for (int j = t / Hq; j < nb; j += per_head) {
-        const float l = zb[static_cast<long long>(j) * Hq + h] + ((j == nb - 1) ? ln_last : ln_full);
-        if (l > m) {
-          sum = sum * expf(m - l) + 1.f;
-          m = l;
-        } else {
-          sum += expf(l - m);
-        }
+      const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
+      for (int c = t / Hq; c < nch; c += per_head) {
+        const float mc = lp[static_cast<long long>(c) * Hq * 2], sc = lp[static_cast<long long>(c) * Hq * 2 + 1];
+        const float mn = fmaxf(m, mc);
+        sum = sum * expf(m - mn) + sc * expf(mc - mn);
+        m = mn;
       }
     }
     s_pm[t] = m;
@@ -315,15 +438,24 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   }
   __syncthreads();
 
-  // 2. Block scores.
+  // 2. Block scores; a thread reads its block's logit row as float4s.
+  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
+  const float ln_full = logf(static_cast<float>(kBlock));
+  const float* zb = zbuf + static_cast<long long>(b) * MAXB * Hq;
   for (int j = t; j < nb; j += kSelThreads) {
     const float lnn = (j == nb - 1) ? ln_last : ln_full;
     const float* zr = zb + static_cast<long long>(j) * Hq;
     float acc = 0.f;
-    for (int h = 0; h < Hq; ++h) {
-      const float z = zr[h];
-      const float Lh = sL[h];
-      acc += expf(z + lnn - Lh) * (Lh - z);
+    if ((Hq & 3) == 0) {
+      for (int h = 0; h < Hq; h += 4) {
+        const float4 z4 = *reinterpret_cast<const float4*>(zr + h);
+        acc += expf(z4.x + lnn - sL[h]) * (sL[h] - z4.x);
+        acc += expf(z4.y + lnn - sL[h + 1]) * (sL[h + 1] - z4.y);
+        acc += expf(z4.z + lnn - sL[h + 2]) * (sL[h + 2] - z4.z);
+        acc += expf(z4.w + lnn - sL[h + 3]) * (sL[h + 3] - z4.w);
+      }
+    } else {
+      for (int h = 0; h < Hq; ++h) acc += expf(zr[h] + lnn - sL[h]) * (sL[h] - zr[h]);
     }
     const float I = __fdiv_rn(acc, static_cast<float>(Hq));
     keys[j] = float_key(I);
@@ -408,25 +540,30 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   }
 }
 
-template <typename T, int D>
+template <int D>
 hipError_t launch_score_d(const ent_ctx* c, int B, const void* q, const float* ksum,
                           const int* tables, const int* ctx_lens, hipStream_t s) {
   const ent_config& cf = c->cfg;
-  const dim3 grid(c->score_chunks, B);
-  const size_t lds = (static_cast<size_t>(cf.num_q_heads) * D +
-                      static_cast<size_t>(kScoreChunk) * cf.num_q_heads) * sizeof(float);
-  const T* qq = static_cast<const T*>(q);
-  const int np = (cf.num_kv_heads * D + 255) / 256;
-#define ENT_SCORE_CASE(GG)                                                                      \
-  case GG:                                                                                      \
-    if (np <= 4)                                                                                \
-      hipLaunchKernelGGL((score_kernel<T, D, GG, 4>), grid, dim3(kScoreThreads), lds, s, qq,    \
-                         ksum, tables, ctx_lens, c->zbuf, cf.num_kv_heads,                      \
-                         cf.max_blocks_per_seq, cf.num_pool_blocks, cf.scale, c->dev_flags);    \
-    else                                                                                        \
-      hipLaunchKernelGGL((score_kernel<T, D, GG, 8>), grid, dim3(kScoreThreads), lds, s, qq,    \
-                         ksum, tables, ctx_lens, c->zbuf, cf.num_kv_heads,                      \
-                         cf.max_blocks_per_seq, cf.num_pool_blocks, cf.scale, c->dev_flags);    \
+  const int Hq = cf.num_q_heads;
+  if (cf.kv_dtype == ENT_BF16) {
+    const dim3 grid((cf.max_blocks_per_seq + kMfmaChunk - 1) / kMfmaChunk, B);
+    const size_t lds = static_cast<size_t>(kMfmaChunk) * Hq * sizeof(float) +
+                       static_cast<size_t>(Hq) * D * sizeof(uint16_t);
+    hipLaunchKernelGGL(score_mfma_kernel<D>, grid, dim3(kScoreThreads), lds, s,
+                       static_cast<const uint16_t*>(q), ksum, tables, ctx_lens, c->zbuf,
+                       c->lse_part, cf.num_kv_heads, c->group, cf.max_blocks_per_seq,
+                       cf.num_pool_blocks, c->lse_chunks, cf.scale, c->dev_flags);
+    return hipGetLastError();
+  }
+  const dim3 grid((cf.max_blocks_per_seq + kValuChunk - 1) / kValuChunk, B);
+  const size_t lds = (static_cast<size_t>(Hq) * D + static_cast<size_t>(kValuChunk) * Hq) * sizeof(float);
+  const float* qq = static_cast<const float*>(q);
+#define ENT_SCORE_CASE(GG)                                                                    \
+  case GG:                                                                                    \
+    hipLaunchKernelGGL((score_valu_kernel<D, GG>), grid, dim3(kScoreThreads), lds, s, qq,     \
+                       ksum, tables, ctx_lens, c->zbuf, c->lse_part, cf.num_kv_heads,         \
+                       cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, cf.scale,    \
+                       c->dev_flags);                                                         \
     break;
   switch (c->group) {
     ENT_SCORE_CASE(1)
@@ -464,18 +601,15 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
                                const int* tables, const int* ctx_lens, const float* h, int* kept,
                                int* n_kept, float* scores, float* theta, hipStream_t s) {
   const ent_config& cf = c->cfg;
-  hipError_t e;
-  if (cf.kv_dtype == ENT_BF16)
-    e = cf.head_dim == 128 ? launch_score_d<uint16_t, 128>(c, B, q, ksum, tables, ctx_lens, s)
-                           : launch_score_d<uint16_t, 64>(c, B, q, ksum, tables, ctx_lens, s);
-  else
-    e = cf.head_dim == 128 ? launch_score_d<float, 128>(c, B, q, ksum, tables, ctx_lens, s)
-                           : launch_score_d<float, 64>(c, B, q, ksum, tables, ctx_lens, s);
+  const hipError_t e = cf.head_dim == 128 ? launch_score_d<128>(c, B, q, ksum, tables, ctx_lens, s)
+                                          : launch_score_d<64>(c, B, q, ksum, tables, ctx_lens, s);
   if (e != hipSuccess) return e;
+  const int chunk = cf.kv_dtype == ENT_BF16 ? kMfmaChunk : kValuChunk;
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelThreads), lds, s, c->zbuf, ctx_lens, h,
-                     scores, theta, kept, n_kept, cf.num_q_heads, cf.max_blocks_per_seq, cf.eps_h, cf.h_min, cf.log_v, cf.kappa_min, cf.b_min,
-                     c->dev_flags);
+  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelThreads), lds, s, c->zbuf, c->lse_part,
+                     ctx_lens, h, scores, theta, kept, n_kept, cf.num_q_heads,
+                     cf.max_blocks_per_seq, chunk, c->lse_chunks, cf.eps_h, cf.h_min, cf.log_v,
+                     cf.kappa_min, cf.b_min, c->dev_flags);
   return hipGetLastError();
 }
 

@@ -12,7 +12,7 @@ namespace ent {
 
 constexpr int kBlock = ENT_BLOCK_SIZE;      // tokens per KV block
 constexpr int kRowChunk = ENT_ROW_CHUNK;    // logits per entropy chunk
-constexpr int kScoreChunk = 16;             // blocks per scoring workgroup
+constexpr int kMinScoreChunk = 16;          // smallest scoring chunk (blocks)
 constexpr int kMaxGroup = 16;               // query heads per KV head
 constexpr int kMaxBlocksPerSeq = 16384;     // selection keeps all scores in LDS
 constexpr float kLog2e = 1.4426950408889634f;
@@ -26,7 +26,7 @@ struct ent_ctx {
   int num_cu = 0;
   int group = 1;            // G = H_q / H_kv
   int chunks = 0;           // entropy chunks per logit row
-  int score_chunks = 0;     // scoring workgroups per sequence
+  int lse_chunks = 0;       // log-sum-exp partials per sequence (finest chunking)
   int decode_grid = 0;      // persistent decode workgroups
 
   void* ws = nullptr;       // one workspace allocation
@@ -34,6 +34,7 @@ struct ent_ctx {
   float* ent_part = nullptr;      // [max_batch, chunks, 3]  (max, sum, weighted sum)
   float* stats_tmp = nullptr;     // [max_batch, chunks, 2]  row statistics scratch
   float* zbuf = nullptr;          // [max_batch, MAXB, H_q]  block logits
+  float* lse_part = nullptr;      // [max_batch, lse_chunks, H_q, 2]
   float* dec_acc = nullptr;       // [decode partial slots, G, d]
   float* dec_ml = nullptr;        // [decode partial slots, G, 2]
   unsigned* dev_flags = nullptr;  // [1]
