@@ -1,9 +1,11 @@
 """Benchmark of one entropic-time decode step on one MI355X.
 
-A step is the whole hot path over one batch: entropy and controller
-(ent_entropy_temperature), block scoring and selection (ent_block_select),
-kept-block decode attention (ent_sparse_paged_decode) and sampling
-(ent_sample).  Inputs are seeded synthetic data of the named workload,
+A step is the whole hot path over one batch, issued as one ent_decode_step
+call: entropy and controller, block scoring and selection, kept-block decode
+attention and sampling.  A second pass issues the same steps through the
+per-stage entry points (ent_entropy_temperature, ent_block_select,
+ent_sparse_paged_decode, ent_sample) with events between them for the
+per-stage times.  Inputs are seeded synthetic data of the named workload,
 resident in HBM before timing; two copies of every input rotate between
 steps so the 256 MB Infinity Cache cannot serve a step from the previous
 one, and every step starts from a fresh copy of the controller state, so all
@@ -142,22 +144,29 @@ def main():
     o = copies[0]          # outputs shared by all copies
     ld = x.logits.shape[2]
 
-    def issue(i, st, ev=None):
+    def issue_fused(i, st):
+        c = copies[i % len(copies)]
+        ent.ent_decode_step(ctx, B, c.logits[0], ld, st[i, 0], st[i, 1], st[i, 2], c.q[0],
+                            c.k_pool, c.v_pool, c.ksum, c.block_tables, c.ctx_lens,
+                            c.uniforms[0], o.h, o.temp_used, o.kept, o.n_kept, o.out, o.tokens,
+                            o.row_stats, o.lse, None, None, sp)
+
+    def issue_staged(i, st, ev):
         c = copies[i % len(copies)]
         hp, ta, te = st[i, 0], st[i, 1], st[i, 2]
-        if ev: ev[0].record(stream)
+        ev[0].record(stream)
         ent.ent_entropy_temperature(ctx, B, c.logits[0], ld, hp, ta, te, o.h, o.temp_used,
                                     o.row_stats, sp)
-        if ev: ev[1].record(stream)
+        ev[1].record(stream)
         ent.ent_block_select(ctx, B, c.q[0], c.ksum, c.block_tables, c.ctx_lens, o.h, o.kept,
                              o.n_kept, None, None, sp)
-        if ev: ev[2].record(stream)
+        ev[2].record(stream)
         ent.ent_sparse_paged_decode(ctx, B, c.q[0], c.k_pool, c.v_pool, c.block_tables,
                                     c.ctx_lens, o.kept, o.n_kept, o.out, o.lse, sp)
-        if ev: ev[3].record(stream)
+        ev[3].record(stream)
         ent.ent_sample(ctx, B, c.logits[0], ld, o.row_stats, o.temp_used, c.uniforms[0],
                        o.tokens, sp)
-        if ev: ev[4].record(stream)
+        ev[4].record(stream)
 
     if args.calibrate_copy:
         # A plain copy kernel of known size: profilers' byte counters for this
@@ -169,26 +178,28 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # Pass A: the timed steps, nothing between the launches.
+    # Pass A: the timed steps (ent_decode_step), nothing between the launches.
     for i in range(W):
-        issue(i, states[0])
+        issue_fused(i, states[0])
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_wall = time.perf_counter()
     e0.record(stream)
     for i in range(W, W + K):
-        issue(i, states[0])
+        issue_fused(i, states[0])
     e1.record(stream)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_wall) * 1e3
     ms_step = e0.elapsed_time(e1) / K
 
-    # Pass B: the same steps with an event around every entry point (per-kernel times).
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
+    # Pass B: the same steps through the four per-stage entry points, with an
+    # event around each (per-stage times; the decode entry point is the
+    # roofline kernel's launch: attention plus the merge of split segments).
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K + W)]
     for i in range(W):
-        issue(i, states[1])
+        issue_staged(i, states[1], evs[K + i])
     for i in range(K):
-        issue(W + i, states[1], evs[i])
+        issue_staged(W + i, states[1], evs[i])
     torch.cuda.synchronize()
     names = ["entropy_temperature", "block_select", "sparse_paged_decode", "sample"]
     per_k = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(K)])) * 1e3
@@ -232,7 +243,8 @@ def main():
         "hbm_frac_kept_kv_plus_logits": round(gbps / HBM_PEAK_GBPS, 4),
         "metric_bytes_per_step": int(metric_bytes),
         "kept_block_fraction": round(kept_frac, 4),
-        "per_kernel_us": {k: round(v, 2) for k, v in per_k.items()},
+        "per_stage_us": {k: round(v, 2) for k, v in per_k.items()},
+        "staged_ms_per_step": round(sum(per_k.values()) * 1e-3, 5),
         "wall_ms_per_step": round(wall_ms / K, 5),
         "roofline": {"kernel": "sparse_paged_decode", "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",

@@ -192,6 +192,23 @@ int ent_sparse_paged_decode(ent_ctx* c, int B, const void* q, const void* k_cach
 int ent_sample(ent_ctx* c, int B, const float* logits, long long ld, const float* row_stats,
                const float* temp_used, const float* uniforms, int* tokens, void* stream);
 
+/* The whole decode step of Sections 2 to 3.3 in one call, bit-identical to
+ * ent_entropy_temperature, ent_block_select, ent_sparse_paged_decode and
+ * ent_sample called in that order on the same arguments (row_stats and
+ * temp_used passed from the first to the last).  The entropy passes and the
+ * block scoring share one launch; the per-sequence entropy, controller,
+ * sampling and selection share a second; decode attention follows.
+ * Arguments as in those calls: st is updated in place (tau, h_prev, temp
+ * for the next step); h_out, temp_used, tokens: [B]; kept, n_kept, out as
+ * in ent_sparse_paged_decode; row_stats, lse, scores, theta nullable.
+ * Alignment: q and ksum 16 bytes (and the caches and out, as for decode). */
+int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_state st,
+                    const void* q, const void* k_cache, const void* v_cache, const float* ksum,
+                    const int* block_tables, const int* ctx_lens, const float* uniforms,
+                    float* h_out, float* temp_used, float* row_stats, int* kept, int* n_kept,
+                    float* out, float* lse, int* tokens, float* scores, float* theta,
+                    void* stream);
+
 /* Append one token per sequence to the paged cache (the memory part of the
  * step's state, Section 3).  With N = ctx_lens[b] and p = block_tables[b][N/16]:
  * write k_new[b, g, :] to k_cache[p, g, N%16, :] and v_new[b, g, :] to

@@ -296,6 +296,35 @@ int ent_sample(ent_ctx* c, int B, const float* logits, long long ld, const float
   return ENT_OK;
 }
 
+int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_state st,
+                    const void* q, const void* k_cache, const void* v_cache, const float* ksum,
+                    const int* block_tables, const int* ctx_lens, const float* uniforms,
+                    float* h_out, float* temp_used, float* row_stats, int* kept, int* n_kept,
+                    float* out, float* lse, int* tokens, float* scores, float* theta,
+                    void* stream) {
+  if (!c) return ENT_E_INVAL;
+  if (int r = check_batch(c, B)) return r;
+  if (B == 0) return ENT_OK;
+  if (!logits || !st.h_prev || !st.tau || !st.temp || !q || !k_cache || !v_cache || !ksum ||
+      !block_tables || !ctx_lens || !uniforms || !h_out || !temp_used || !kept || !n_kept ||
+      !out || !tokens)
+    return fail(c, ENT_E_INVAL, "ent_decode_step: NULL required pointer");
+  if (ld < c->cfg.vocab) return fail(c, ENT_E_INVAL, "ent_decode_step: ld < vocab");
+  if (h_out == st.h_prev) return fail(c, ENT_E_INVAL, "ent_decode_step: h_out aliases h_prev");
+  if (temp_used == st.temp) return fail(c, ENT_E_INVAL, "ent_decode_step: temp_used aliases temp");
+  if (!aligned(q, 16) || !aligned(ksum, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
+      !aligned(out, 16))
+    return fail(c, ENT_E_INVAL, "ent_decode_step: q, ksum, caches and out need 16-byte alignment");
+  const hipError_t e = ent::launch_decode_step(c, B, logits, ld, st, q, k_cache, v_cache, ksum,
+                                               block_tables, ctx_lens, uniforms, h_out,
+                                               temp_used, row_stats, kept, n_kept, out, lse,
+                                               tokens, scores, theta,
+                                               static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "ent_decode_step launch");
+  c->err.clear();
+  return ENT_OK;
+}
+
 int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new, const int* block_tables,
                   int* ctx_lens, void* k_cache, void* v_cache, float* ksum, void* stream) {
   if (!c) return ENT_E_INVAL;

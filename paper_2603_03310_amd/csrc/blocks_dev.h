@@ -1,0 +1,475 @@
+// Device bodies of the block scoring and selection stages, shared by the
+// per-stage kernels (blocks.hip) and the fused step kernels (step.hip).
+//
+// Block entropic contribution (Section 3.2 of the paper): I_b is the
+// attention-weighted surprisal of block b's tokens.  Weights come from the
+// current query against each block's mean key (one summary per block and KV
+// head), surprisal is -ln of the same weight, and scores are averaged over
+// query heads:
+//   z_bh = scale <q_h, kbar_b,g>,   L_h = ln sum_b n_b e^{z_bh}
+//   I_b  = (1/H_q) sum_h e^{z_bh + ln n_b - L_h} (L_h - z_bh)
+// The kept set is {b : I_b >= theta} with theta the k-th largest score and k
+// the entropy-driven budget with its floor and minimum (Sections 3.2, 3.3, 5).
+#pragma once
+
+#include "ent_internal.h"
+
+#include <math.h>
+
+namespace ent {
+namespace {
+
+template <typename T>
+__device__ __forceinline__ float load_elem(const T* p);
+template <>
+__device__ __forceinline__ float load_elem<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+
+// ---------------------------------------------------------------------------
+// Scoring.  Both scoring kernels write the block logits
+//   z_bh = scale <q_h, kbar_b,g(h)>     zbuf [B, MAXB, H_q]
+// and, per chunk of blocks and head, the log-sum-exp partial (max, sum) of
+// l_bh = z_bh + ln n_b over the chunk's blocks.
+//
+// bf16 queries (MFMA).  A workgroup of 4 waves takes 64 blocks, a tile of 16
+// per wave.  For each KV head g the tile's logits are one small contraction
+//   Z[16 blocks x 16] = Kbar_g[16 x d] . Q_g^T[d x 16]   (columns: the G query
+// heads of g, zero-padded), on v_mfma_f32_16x16x32_bf16.  The fp32 summaries
+// are split exactly into three bf16 parts (hi + mid + lo: x - hi and the
+// remainder after mid are exact in fp32 and fit bf16), so three MFMAs per
+// k-step give the fp32 dot product of exact bf16 products.  A operands come
+// straight from global memory (8 dims per lane), the queries are staged in
+// LDS as bf16, and the next KV head's summaries are prefetched.
+//
+// fp32 queries (VALU).  A workgroup of 4 waves takes 16 blocks, 4 per wave;
+// a block's summary is read as NP passes of 256 floats, one float4 per lane
+// per pass; each lane forms G partial dot products over its 4 dims and a
+// halving butterfly reduces them over the d/4 lanes of its KV head.
+// ---------------------------------------------------------------------------
+constexpr int kScoreThreads = 256;
+constexpr int kScoreWaves = kScoreThreads / 64;
+constexpr int kMfmaChunk = 64;                 // blocks per MFMA scoring workgroup
+constexpr int kValuChunk = 16;                 // blocks per VALU scoring workgroup
+constexpr int kValuPerWave = kValuChunk / kScoreWaves;
+
+typedef __bf16 sbf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef float sf32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
+
+// Per-head log-sum-exp partial of l = z + ln n over the chunk's nblk blocks
+// (z tile in LDS, row stride Hq).
+__device__ __forceinline__ void chunk_lse(const float* zt, int nblk, int Hq, int j_lo, int nb,
+                                          int N, float* lp_chunk) {
+  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
+  const float ln_full = logf(static_cast<float>(kBlock));
+  for (int h = threadIdx.x; h < Hq; h += blockDim.x) {
+    float m = -INFINITY;
+    for (int i = 0; i < nblk; ++i) {
+      const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
+      m = fmaxf(m, zt[i * Hq + h] + lnn);
+    }
+    float s = 0.f;
+    for (int i = 0; i < nblk; ++i) {
+      const float lnn = (j_lo + i == nb - 1) ? ln_last : ln_full;
+      s += expf(zt[i * Hq + h] + lnn - m);
+    }
+    lp_chunk[h * 2 + 0] = m;
+    lp_chunk[h * 2 + 1] = s;
+  }
+}
+
+// Exact three-way bf16 split of 8 floats (two float4) into packed bf16x8.
+__device__ __forceinline__ void split3(const float4& x0, const float4& x1, sbf16x8_t& hi,
+                                       sbf16x8_t& mid, sbf16x8_t& lo) {
+  const float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+  uint32_t h[4], m[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t hb[2], mb[2], lb[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const uint32_t ux = __float_as_uint(v[2 * i + k]);
+      const uint32_t uh = ux & 0xFFFF0000u;
+      const float r = v[2 * i + k] - __uint_as_float(uh);
+      const uint32_t um = __float_as_uint(r) & 0xFFFF0000u;
+      const uint32_t ul = __float_as_uint(r - __uint_as_float(um));
+      hb[k] = uh;
+      mb[k] = um;
+      lb[k] = ul;
+    }
+    h[i] = (hb[0] >> 16) | hb[1];
+    m[i] = (mb[0] >> 16) | mb[1];
+    l[i] = (lb[0] >> 16) | (lb[1] & 0xFFFF0000u);
+  }
+  hi = __builtin_bit_cast(sbf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
+  mid = __builtin_bit_cast(sbf16x8_t, make_uint4(m[0], m[1], m[2], m[3]));
+  lo = __builtin_bit_cast(sbf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
+}
+
+// smem: z tile [kMfmaChunk][Hq] fp32, then q [Hq][D] bf16.
+template <int D>
+__device__ __forceinline__ void score_mfma_body(
+    const uint16_t* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
+    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
+    int Hkv, int G, int MAXB, int P, int nch_max, float scale, unsigned* flags, int ch, int b,
+    float* smem) {
+  constexpr int KS = D / 32;
+  const int Hq = Hkv * G;
+  float* zt = smem;
+  uint16_t* qs = reinterpret_cast<uint16_t*>(smem + kMfmaChunk * Hq);
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int r16 = lane & 15, gq = lane >> 4;
+  const int j_lo = ch * kMfmaChunk;
+  const int jt = j_lo + wave * 16;           // first block of this wave's tile
+  // Table entry of block jt + r16, read before the context length is known
+  // (in bounds of the MAXB-entry row); masked below.
+  int p = 0;
+  if (jt + r16 < MAXB) p = tables[static_cast<long long>(b) * MAXB + jt + r16];
+  const int N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) return;    // flagged by the selection kernel
+  const int nb = (N + kBlock - 1) / kBlock;
+  if (j_lo >= nb) return;
+  const int nblk = min(kMfmaChunk, nb - j_lo);
+  const bool row_ok = jt + r16 < nb;
+  if (row_ok && (p < 0 || p >= P)) {
+    raise_flag(flags, ENT_DEV_BAD_TABLE);
+    p = 0;
+  }
+  if (!row_ok) p = 0;
+  const bool any_rows = jt < nb;
+  const int nfl = Hkv * D;
+
+  float4 cur[2 * KS], nxt[2 * KS];
+  auto load_g = [&](int g, float4 (&buf)[2 * KS]) {
+    const float* src = ksum + static_cast<long long>(p) * nfl + g * D + gq * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      buf[2 * ks] = *reinterpret_cast<const float4*>(src + ks * 32);
+      buf[2 * ks + 1] = *reinterpret_cast<const float4*>(src + ks * 32 + 4);
+    }
+  };
+  if (any_rows) load_g(0, cur);
+  // Stage the queries (bf16) in LDS, 16 bytes per thread per step.
+  const uint4* qsrc = reinterpret_cast<const uint4*>(q + static_cast<long long>(b) * Hq * D);
+  for (int e = t; e < Hq * D / 8; e += kScoreThreads) reinterpret_cast<uint4*>(qs)[e] = qsrc[e];
+  __syncthreads();
+
+  if (any_rows) {
+    for (int g = 0; g < Hkv; ++g) {
+      if (g + 1 < Hkv) load_g(g + 1, nxt);
+      sf32x4_t acc = sf32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        sbf16x8_t hi, mid, lo;
+        split3(cur[2 * ks], cur[2 * ks + 1], hi, mid, lo);
+        uint4 qb = make_uint4(0u, 0u, 0u, 0u);
+        if (r16 < G) qb = *reinterpret_cast<const uint4*>(qs + (g * G + r16) * D + ks * 32 + gq * 8);
+        const sbf16x8_t bq = __builtin_bit_cast(sbf16x8_t, qb);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mid, bq, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, bq, acc, 0, 0, 0);
+      }
+      // acc[e]: block 4*gq + e of the tile, query head g*G + r16.
+      if (r16 < G) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int blk = 4 * gq + e;
+          if (jt + blk < nb) zt[(wave * 16 + blk) * Hq + g * G + r16] = acc[e] * scale;
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 2 * KS; ++k) cur[k] = nxt[k];
+    }
+  }
+  __syncthreads();
+  float* zrow = zbuf + (static_cast<long long>(b) * MAXB + j_lo) * Hq;
+  for (int e = t; e < nblk * Hq; e += kScoreThreads) zrow[e] = zt[e];
+  chunk_lse(zt, nblk, Hq, j_lo, nb, N, lse_part + (static_cast<long long>(b) * nch_max + ch) * Hq * 2);
+}
+
+template <int G, int L>
+__device__ __forceinline__ float reduce_heads(float (&a)[G], int li) {
+#pragma unroll
+  for (int n = G, s = L / 2; n > 1; n >>= 1, s >>= 1) {
+    const bool up = (li & s) != 0;
+#pragma unroll
+    for (int i = 0; i < n / 2; ++i) {
+      const float keep = up ? a[i + n / 2] : a[i];
+      const float send = up ? a[i] : a[i + n / 2];
+      a[i] = keep + __shfl_xor(send, s);
+    }
+  }
+  float v = a[0];
+#pragma unroll
+  for (int s = L / (2 * G); s >= 1; s >>= 1) v += __shfl_xor(v, s);
+  return v;
+}
+
+// smem: q [Hq][D] fp32, then z tile [kValuChunk][Hq].
+template <int D, int G>
+__device__ __forceinline__ void score_valu_body(
+    const float* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
+    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
+    int Hkv, int MAXB, int P, int nch_max, float scale, unsigned* flags, int ch, int b,
+    float* smem) {
+  constexpr int L = D / 4;
+  static_assert(G <= L, "heads per KV head exceed the lane group");
+  const int Hq = Hkv * G;
+  float* qs = smem;
+  float* zt = smem + Hq * D;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int li = lane % L;
+  const int N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) return;    // flagged by the selection kernel
+  const int nb = (N + kBlock - 1) / kBlock;
+  const int j_lo = ch * kValuChunk;
+  if (j_lo >= nb) return;
+  const int nblk = min(kValuChunk, nb - j_lo);
+  const int jw = j_lo + wave * kValuPerWave;
+  const int nmine = max(0, min(kValuPerWave, nb - jw));
+  int my_p = 0;
+  if (lane < nmine) {
+    my_p = tables[static_cast<long long>(b) * MAXB + jw + lane];
+    if (my_p < 0 || my_p >= P) {
+      raise_flag(flags, ENT_DEV_BAD_TABLE);
+      my_p = 0;
+    }
+  }
+  for (int e = t; e < Hq * D; e += kScoreThreads) qs[e] = q[static_cast<long long>(b) * Hq * D + e];
+  __syncthreads();
+  const int nfl = Hkv * D;
+  const int np = (nfl + 255) >> 8;
+  for (int blk = 0; blk < nmine; ++blk) {
+    const int p = __shfl(my_p, blk);
+    for (int k = 0; k < np; ++k) {
+      const int f = 256 * k + 4 * lane;
+      const bool gv = f < nfl;
+      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (gv) kv = *reinterpret_cast<const float4*>(ksum + static_cast<long long>(p) * nfl + f);
+      const int g = f / D, dd = f % D;
+      float a[G];
+#pragma unroll
+      for (int r = 0; r < G; ++r) {
+        float4 qq = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (gv) qq = *reinterpret_cast<const float4*>(qs + (g * G + r) * D + dd);
+        a[r] = qq.x * kv.x + qq.y * kv.y + qq.z * kv.z + qq.w * kv.w;
+      }
+      const float z = reduce_heads<G, L>(a, li) * scale;
+      if (gv && (li % (L / G)) == 0) zt[(wave * kValuPerWave + blk) * Hq + g * G + li / (L / G)] = z;
+    }
+  }
+  __syncthreads();
+  float* zrow = zbuf + (static_cast<long long>(b) * MAXB + j_lo) * Hq;
+  for (int e = t; e < nblk * Hq; e += kScoreThreads) zrow[e] = zt[e];
+  chunk_lse(zt, nblk, Hq, j_lo, nb, N, lse_part + (static_cast<long long>(b) * nch_max + ch) * Hq * 2);
+}
+
+__device__ __forceinline__ unsigned float_key(float f) {
+  const unsigned u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_float(unsigned k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// Budget k in float32, operation by operation (no contraction), so that the
+// integer matches a float32 evaluation of the same formula elsewhere.
+__device__ __forceinline__ int keep_budget(float h, int nb, float eps_h, float h_min,
+                                           float log_v, float kappa_min, int b_min) {
+  if (nb <= 0) return 0;
+  const float hg = fmaxf(__fadd_rn(h, eps_h), h_min);
+  float u = __fdiv_rn(__fsub_rn(hg, h_min), __fsub_rn(log_v, h_min));
+  u = fminf(fmaxf(u, 0.f), 1.f);
+  const float kappa = __fadd_rn(kappa_min, __fmul_rn(__fsub_rn(1.f, kappa_min), u));
+  const int k = static_cast<int>(ceilf(__fmul_rn(kappa, static_cast<float>(nb))));
+  return min(nb, max(min(b_min, nb), k));
+}
+
+// Kept set of one sequence (one workgroup of 512 threads):
+//  1. L_h = ln sum_b n_b e^{z_bh}, merged from the scoring kernel's partials;
+//  2. I_b = (1/H_q) sum_h e^{z_bh + ln n_b - L_h} (L_h - z_bh) for every block,
+//     held in LDS as order-preserving integer keys;
+//  3. budget k from the entropy, the k-th largest key by a 4-pass 8-bit radix
+//     select, and ascending compaction of {b : I_b >= theta} with wave ballots.
+constexpr int kSelThreads = 512;
+constexpr int kSelWaves = kSelThreads / 64;
+
+struct SelectShared {
+  unsigned hist[256];
+  float pm[kSelThreads], ps[kSelThreads], L[128];
+  int digit, krem, wcnt[kSelWaves];
+};
+
+// keys: LDS [MAXB]; h: the sequence's entropy.  Called by all kSelThreads
+// threads of the workgroup.
+__device__ __forceinline__ void select_body(
+    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, float hval,
+    float* __restrict__ scores_out, float* __restrict__ theta_out, int* __restrict__ kept,
+    int* __restrict__ n_kept, int Hq, int MAXB, int chunk, int nch_max, float eps_h, float h_min,
+    float log_v, float kappa_min, int b_min, unsigned* flags, int b, unsigned* keys,
+    SelectShared& sh) {
+  unsigned* hist = sh.hist;
+  float* s_pm = sh.pm;
+  float* s_ps = sh.ps;
+  float* sL = sh.L;
+  int& s_digit = sh.digit;
+  int& s_krem = sh.krem;
+  int* s_wcnt = sh.wcnt;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) {
+    if (t == 0) {
+      raise_flag(flags, ENT_DEV_BAD_CTXLEN);
+      n_kept[b] = 0;
+      if (theta_out) theta_out[b] = INFINITY;
+    }
+    return;
+  }
+  const int nb = (N + kBlock - 1) / kBlock;
+  const int k = keep_budget(hval, nb, eps_h, h_min, log_v, kappa_min, b_min);
+  if (nb == 0) {
+    if (t == 0) {
+      n_kept[b] = 0;
+      if (theta_out) theta_out[b] = INFINITY;
+    }
+    return;
+  }
+  // 1. L_h = ln sum_b n_b e^{z_bh}, merged from the per-chunk partials: each
+  //    thread folds a strided subset of the chunks of head t % Hq, then one
+  //    thread per head folds the subsets.
+  const int nch = (nb + chunk - 1) / chunk;
+  const int per_head = kSelThreads / Hq;     // threads per head (Hq <= 128)
+  {
+    float m = -INFINITY, sum = 0.f;
+    if (t < per_head * Hq) {
+      const int h = t % Hq;
+      const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
+      for (int c = t / Hq; c < nch; c += per_head) {
+        const float mc = lp[static_cast<long long>(c) * Hq * 2], sc = lp[static_cast<long long>(c) * Hq * 2 + 1];
+        const float mn = fmaxf(m, mc);
+        sum = sum * expf(m - mn) + sc * expf(mc - mn);
+        m = mn;
+      }
+    }
+    s_pm[t] = m;
+    s_ps[t] = sum;
+  }
+  __syncthreads();
+  if (t < Hq) {
+    float m = -INFINITY, sum = 0.f;
+    for (int i = 0; i < per_head; ++i) {
+      const float mc = s_pm[i * Hq + t], sc = s_ps[i * Hq + t];
+      if (mc == -INFINITY) continue;
+      const float mn = fmaxf(m, mc);
+      sum = sum * expf(m - mn) + sc * expf(mc - mn);
+      m = mn;
+    }
+    sL[t] = m + logf(sum);
+  }
+  __syncthreads();
+
+  // 2. Block scores; a thread reads its block's logit row as float4s.
+  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
+  const float ln_full = logf(static_cast<float>(kBlock));
+  const float* zb = zbuf + static_cast<long long>(b) * MAXB * Hq;
+  for (int j = t; j < nb; j += kSelThreads) {
+    const float lnn = (j == nb - 1) ? ln_last : ln_full;
+    const float* zr = zb + static_cast<long long>(j) * Hq;
+    float acc = 0.f;
+    if ((Hq & 3) == 0) {
+      for (int h = 0; h < Hq; h += 4) {
+        const float4 z4 = *reinterpret_cast<const float4*>(zr + h);
+        acc += expf(z4.x + lnn - sL[h]) * (sL[h] - z4.x);
+        acc += expf(z4.y + lnn - sL[h + 1]) * (sL[h + 1] - z4.y);
+        acc += expf(z4.z + lnn - sL[h + 2]) * (sL[h + 2] - z4.z);
+        acc += expf(z4.w + lnn - sL[h + 3]) * (sL[h + 3] - z4.w);
+      }
+    } else {
+      for (int h = 0; h < Hq; ++h) acc += expf(zr[h] + lnn - sL[h]) * (sL[h] - zr[h]);
+    }
+    const float I = __fdiv_rn(acc, static_cast<float>(Hq));
+    keys[j] = float_key(I);
+    if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j] = I;
+  }
+  if (k <= 0) {
+    if (t == 0) {
+      n_kept[b] = 0;
+      if (theta_out) theta_out[b] = INFINITY;
+    }
+    return;
+  }
+  if (t == 0) s_krem = k;
+  __syncthreads();
+
+  // 3. Radix select of the k-th largest key.
+  unsigned prefix = 0u, mask = 0u;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    if (t < 256) hist[t] = 0u;
+    __syncthreads();
+    for (int i = t; i < nb; i += kSelThreads) {
+      const unsigned key = keys[i];
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      // Bins 4*lane .. 4*lane+3; suffix sums over lanes locate the digit
+      // holding the k_rem-th largest remaining key.
+      const unsigned c0 = hist[4 * lane], c1 = hist[4 * lane + 1], c2 = hist[4 * lane + 2],
+                     c3 = hist[4 * lane + 3];
+      const unsigned cl = c0 + c1 + c2 + c3;
+      unsigned suf = cl;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const unsigned n = __shfl_down(suf, o);
+        if (lane + o < 64) suf += n;
+      }
+      const unsigned krem = static_cast<unsigned>(s_krem);
+      const unsigned above = suf - cl;       // keys in higher lanes' bins
+      if (above < krem && suf >= krem) {
+        unsigned run = above;
+        const unsigned cs[4] = {c0, c1, c2, c3};
+        int d = 4 * lane;
+        for (int x = 3; x >= 0; --x) {
+          if (run + cs[x] >= krem) {
+            d = 4 * lane + x;
+            break;
+          }
+          run += cs[x];
+        }
+        s_digit = d;
+        s_krem = static_cast<int>(krem - run);
+      }
+    }
+    __syncthreads();
+    prefix |= static_cast<unsigned>(s_digit) << shift;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  const unsigned tkey = prefix;
+
+  // Compaction in ascending block order.
+  int total = 0;
+  int* krow = kept + static_cast<long long>(b) * MAXB;
+  for (int base = 0; base < nb; base += kSelThreads) {
+    const int i = base + t;
+    const bool f = i < nb && keys[i] >= tkey;
+    const unsigned long long bal = __ballot(f);
+    const int rank = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) s_wcnt[wave] = __popcll(bal);
+    __syncthreads();
+    int off = total;
+    for (int w = 0; w < wave; ++w) off += s_wcnt[w];
+    if (f) krow[off + rank] = i;
+    for (int w = 0; w < kSelWaves; ++w) total += s_wcnt[w];
+    __syncthreads();
+  }
+  if (t == 0) {
+    n_kept[b] = total;
+    if (theta_out) theta_out[b] = key_float(tkey);
+  }
+}
+
+}  // namespace
+}  // namespace ent

@@ -62,6 +62,13 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
                          hipStream_t s);
+hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
+                              ent_state st, const void* q, const void* k_cache,
+                              const void* v_cache, const float* ksum, const int* tables,
+                              const int* ctx_lens, const float* uniforms, float* h_out,
+                              float* temp_used, float* row_stats, int* kept, int* n_kept,
+                              float* out, float* lse, int* tokens, float* scores, float* theta,
+                              hipStream_t s);
 hipError_t launch_kv_append(const ent_ctx* c, int B, const void* k_new, const void* v_new,
                             const int* tables, int* ctx_lens, void* k_cache, void* v_cache,
                             float* ksum, hipStream_t s);

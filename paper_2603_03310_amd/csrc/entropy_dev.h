@@ -1,0 +1,308 @@
+// Device bodies of the entropy, controller and sampling stages, shared by
+// the per-stage kernels (entropy.hip) and the fused step kernels (step.hip).
+//
+// Entropy (Section 2 and Section 2.1 of the paper): H = -sum_x p(x) ln p(x)
+// with p = softmax(z / T).  One pass over each logit row: the row is cut into
+// chunks of ENT_ROW_CHUNK logits, one 256-thread workgroup per (chunk, row);
+// each thread holds 16 logits in registers, so the chunk's maximum and the
+// sums   S = sum 2^(t - M),  W = sum 2^(t - M) (t - M)   (t = z log2(e) / T)
+// come from one read of HBM.  One wave per row then merges the chunk triples:
+//   H = ln 2 (log2 S - W / S)
+// and the controller updates the sequence's state:
+//   tau += max(0, H_prev - H)                      (Section 2, entropic time)
+//   T'  = clip(T exp(eta (H - H*)), T_min, T_max)    (Section 3.3, signed eta)
+// Chunk (max, sum) pairs double as the row statistics the sampler reuses.
+//
+// Sampling: the chunk masses S_c 2^(M_c - M) locate the chunk holding the
+// target u S; that chunk is re-read and scanned in index order with float64
+// running sums.
+#pragma once
+
+#include "ent_internal.h"
+
+#include <math.h>
+
+namespace ent {
+namespace {
+
+constexpr int kChunkThreads = 256;
+constexpr int kPerThread = kRowChunk / kChunkThreads;   // 16 logits per thread
+static_assert(kPerThread == 16, "chunk layout");
+constexpr int kSampleThreads = 256;                     // threads that scan a chunk
+constexpr int kMaxChunks = 256;                         // vocab <= 256 * 4096
+
+// Reductions over the first NT threads of the workgroup (NT a multiple of
+// 64); every thread of the workgroup must call them.
+template <int NT>
+__device__ __forceinline__ float block_max(float v, float* red) {
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0 && w < NT / 64) red[w] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < NT / 64; ++i) r = fmaxf(r, red[i]);
+  __syncthreads();
+  return r;
+}
+
+template <int NT>
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0 && w < NT / 64) red[w] = v;
+  __syncthreads();
+  float r = 0.f;
+#pragma unroll
+  for (int i = 0; i < NT / 64; i += 2) r += (i + 1 < NT / 64) ? (red[i] + red[i + 1]) : red[i];
+  __syncthreads();
+  return r;
+}
+
+// The thread's 16 logits of chunk c, scaled to log2 units: t = z * c2.
+// Positions past the vocabulary read as -inf (zero probability).
+template <bool VEC>
+__device__ __forceinline__ void load_chunk(const float* __restrict__ row, int V, int c,
+                                           float c2, float (&v)[kPerThread]) {
+  const int base = c * kRowChunk;
+  if (VEC) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = base + (i * kChunkThreads + threadIdx.x) * 4;
+      if (idx + 3 < V) {
+        const float4 x = *reinterpret_cast<const float4*>(row + idx);
+        v[4 * i + 0] = x.x * c2;
+        v[4 * i + 1] = x.y * c2;
+        v[4 * i + 2] = x.z * c2;
+        v[4 * i + 3] = x.w * c2;
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          v[4 * i + k] = (idx + k < V) ? row[idx + k] * c2 : -INFINITY;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+      const int idx = base + i * kChunkThreads + threadIdx.x;
+      v[i] = idx < V ? row[idx] * c2 : -INFINITY;
+    }
+  }
+}
+
+// Chunk pass of (chunk c, row b) by a 256-thread workgroup: writes the triple
+// (M, S, W) to part (when non-null) and (M, S) to row_stats (when non-null).
+template <bool VEC>
+__device__ __forceinline__ void entropy_chunk_body(const float* __restrict__ logits, long long ld,
+                                                   int V, int C, const float* __restrict__ temp,
+                                                   float* __restrict__ part,
+                                                   float* __restrict__ row_stats, int c, int b,
+                                                   float* red) {
+  const float T = temp[b];
+  const float c2 = __fdiv_rn(kLog2e, T);
+  const float* row = logits + static_cast<long long>(b) * ld;
+  float v[kPerThread];
+  load_chunk<VEC>(row, V, c, c2, v);
+  float m = v[0];
+#pragma unroll
+  for (int i = 1; i < kPerThread; ++i) m = fmaxf(m, v[i]);
+  const float M = block_max<kChunkThreads>(m, red);
+  float S = 0.f, W = 0.f;
+  if (M != -INFINITY) {
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+      const float d = v[i] - M;
+      const float e = exp2f(d);
+      S += e;
+      W += (e > 0.f) ? e * d : 0.f;
+    }
+  }
+  S = block_sum<kChunkThreads>(S, red);
+  W = block_sum<kChunkThreads>(W, red);
+  if (threadIdx.x == 0) {
+    const long long o = static_cast<long long>(b) * C + c;
+    if (row_stats) {
+      row_stats[2 * o + 0] = M;
+      row_stats[2 * o + 1] = S;
+    }
+    if (part) {
+      part[3 * o + 0] = M;
+      part[3 * o + 1] = S;
+      part[3 * o + 2] = W;
+    }
+  }
+}
+
+// Entropy of row b from its C chunk triples, by one wave (result in every lane).
+__device__ __forceinline__ float row_entropy(const float* __restrict__ part, int C, int b) {
+  const int lane = threadIdx.x & 63;
+  const float* pr = part + static_cast<long long>(b) * C * 3;
+  float mloc = -INFINITY;
+  for (int i = lane; i < C; i += 64) mloc = fmaxf(mloc, pr[3 * i]);
+  const float MG = wave_max(mloc);
+  float s = 0.f, w = 0.f;
+  for (int i = lane; i < C; i += 64) {
+    const float mc = pr[3 * i];
+    const float sc = pr[3 * i + 1];
+    const float wc = pr[3 * i + 2];
+    if (sc > 0.f) {
+      const float dm = mc - MG;
+      const float f = exp2f(dm);
+      s += sc * f;
+      w += f * (wc + sc * dm);
+    }
+  }
+  s = wave_sum(s);
+  w = wave_sum(w);
+  {
+    // No contraction here or in the controller: the entropy must be the same
+    // rounded float whether a caller keeps it in a register or reloads it.
+#pragma clang fp contract(off)
+    return (log2f(s) - w / s) * kLn2;
+  }
+}
+
+// Controller update of sequence b given its entropy H at temperature T.
+__device__ __forceinline__ void controller_update(int b, float H, float T, float* h_prev,
+                                                  float* tau, float* temp, float* h_out,
+                                                  float* temp_used, float eta, float h_target,
+                                                  float t_min, float t_max) {
+#pragma clang fp contract(off)
+  h_out[b] = H;
+  temp_used[b] = T;
+  const float hp = h_prev[b];
+  float ta = tau[b];
+  if (!isnan(hp)) ta += fmaxf(0.f, hp - H);
+  float tn = T * expf(eta * (H - h_target));
+  tn = fminf(fmaxf(tn, t_min), t_max);
+  tau[b] = ta;
+  h_prev[b] = H;
+  temp[b] = tn;
+}
+
+// Exclusive prefix sum (float64) over the first kSampleThreads threads.
+__device__ __forceinline__ double block_excl_scan_d(double v, double* wsum) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  double incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double n = __shfl_up(incl, o);
+    if (lane >= o) incl += n;
+  }
+  if (lane == 63 && w < kSampleThreads / 64) wsum[w] = incl;
+  __syncthreads();
+  double before = 0.0;
+  for (int i = 0; i < w && i < kSampleThreads / 64; ++i) before += wsum[i];
+  __syncthreads();
+  const double excl = __shfl_up(incl, 1);
+  return before + (lane == 0 ? 0.0 : excl);
+}
+
+struct SampleShared {
+  double w[kMaxChunks];
+  double wsum[kSampleThreads / 64];
+  float red[16];
+  int chunk, idx, lastpos;
+  double before, target;
+};
+
+// Inverse-CDF sample of row b at temperature T and uniform u.  Every thread
+// of the workgroup calls it; the first kSampleThreads threads do the work.
+// Returns the token (meaningful in thread 0).
+template <bool VEC>
+__device__ __forceinline__ int sample_body(const float* __restrict__ logits, long long ld, int V,
+                                           int C, const float* __restrict__ stats, float T,
+                                           float u, int b, SampleShared& sh) {
+  const int t = threadIdx.x;
+  const bool worker = t < kSampleThreads;
+  const float c2 = __fdiv_rn(kLog2e, T);
+  const float* row = logits + static_cast<long long>(b) * ld;
+  const float* st = stats + static_cast<long long>(b) * C * 2;
+  const float mc = (worker && t < C) ? st[2 * t] : -INFINITY;
+  const float sc = (worker && t < C) ? st[2 * t + 1] : 0.f;
+  const float M = block_max<kSampleThreads>(mc, sh.red);
+  if (worker)
+    sh.w[t] = (t < C && sc > 0.f)
+                  ? static_cast<double>(sc) * exp2(static_cast<double>(mc) - static_cast<double>(M))
+                  : 0.0;
+  if (t == 0) {
+    sh.idx = 0x7fffffff;
+    sh.lastpos = -1;
+  }
+  __syncthreads();
+  if (t == 0) {
+    double tot = 0.0;
+    for (int i = 0; i < C; ++i) tot += sh.w[i];
+    const double target = static_cast<double>(u) * tot;
+    double cum = 0.0;
+    int chunk = -1, lastpos = 0;
+    double before = 0.0;
+    for (int i = 0; i < C; ++i) {
+      if (sh.w[i] > 0.0) lastpos = i;
+      if (chunk < 0 && cum + sh.w[i] > target) {
+        chunk = i;
+        before = cum;
+      }
+      cum += sh.w[i];
+    }
+    double tgt = target;
+    if (chunk < 0) {            // rounding put the target at the very top:
+      chunk = lastpos;          // take the last token of positive mass
+      before = 0.0;
+      tgt = HUGE_VAL;
+    }
+    sh.chunk = chunk;
+    sh.before = before;
+    sh.target = tgt;
+  }
+  __syncthreads();
+  const int base = sh.chunk * kRowChunk + t * kPerThread;
+  float e[kPerThread];
+  if (!worker) {
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) e[i] = 0.f;
+  } else if (VEC && base + kPerThread <= V) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float4 x = *reinterpret_cast<const float4*>(row + base + 4 * i);
+      e[4 * i + 0] = exp2f(x.x * c2 - M);
+      e[4 * i + 1] = exp2f(x.y * c2 - M);
+      e[4 * i + 2] = exp2f(x.z * c2 - M);
+      e[4 * i + 3] = exp2f(x.w * c2 - M);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i)
+      e[i] = (base + i < V) ? exp2f(row[base + i] * c2 - M) : 0.f;
+  }
+  double local = 0.0;
+  int lastpos = -1;
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    local += static_cast<double>(e[i]);
+    if (e[i] > 0.f) lastpos = base + i;
+  }
+  double pos = sh.before + block_excl_scan_d(local, sh.wsum);
+  const double target = sh.target;
+  int found = 0x7fffffff;
+  if (worker) {
+    for (int i = 0; i < kPerThread; ++i) {
+      pos += static_cast<double>(e[i]);
+      if (pos > target) {
+        found = base + i;
+        break;
+      }
+    }
+    if (found != 0x7fffffff) atomicMin(&sh.idx, found);
+    if (lastpos >= 0) atomicMax(&sh.lastpos, lastpos);
+  }
+  __syncthreads();
+  return (sh.idx != 0x7fffffff) ? sh.idx : sh.lastpos;
+}
+
+inline bool row_vec_ok(const float* p, long long ld) {
+  return (reinterpret_cast<uintptr_t>(p) % 16 == 0) && (ld % 4 == 0);
+}
+
+}  // namespace
+}  // namespace ent

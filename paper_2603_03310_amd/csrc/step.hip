@@ -1,0 +1,220 @@
+// One whole decode step in four launches (ent_decode_step).  Each launch runs
+// the same device bodies as the per-stage entry points, so the results are
+// bit-identical to calling ent_entropy_temperature, ent_block_select,
+// ent_sparse_paged_decode and ent_sample in sequence:
+//
+//   A  entropy chunk passes and block scoring, as disjoint workgroup ranges
+//      of one grid: both stream from HBM (logits, block summaries) and do not
+//      depend on each other, so one launch overlaps them;
+//   B  one workgroup per sequence: the row's entropy from the chunk triples,
+//      sampling at the current temperature, the controller update, and the
+//      kept-block selection under the entropy-driven budget;
+//   C  kept-block decode attention and the merge of split segments.
+
+#include "blocks_dev.h"
+#include "entropy_dev.h"
+
+namespace ent {
+namespace {
+
+template <bool VEC, int D>
+__global__ __launch_bounds__(kChunkThreads) void step_a_mfma_kernel(
+    const float* __restrict__ logits, long long ld, int V, int C, const float* __restrict__ temp,
+    float* __restrict__ part, float* __restrict__ row_stats, const uint16_t* __restrict__ q,
+    const float* __restrict__ ksum, const int* __restrict__ tables,
+    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
+    int B, int Hkv, int G, int MAXB, int P, int nch_max, int nsc, float scale, unsigned* flags) {
+  extern __shared__ float smem[];
+  const int id = blockIdx.x;
+  if (id < C * B) {
+    entropy_chunk_body<VEC>(logits, ld, V, C, temp, part, row_stats, id % C, id / C, smem);
+    return;
+  }
+  const int sid = id - C * B;
+  score_mfma_body<D>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, G, MAXB, P, nch_max, scale,
+                     flags, sid % nsc, sid / nsc, smem);
+}
+
+template <bool VEC, int D, int G>
+__global__ __launch_bounds__(kChunkThreads) void step_a_valu_kernel(
+    const float* __restrict__ logits, long long ld, int V, int C, const float* __restrict__ temp,
+    float* __restrict__ part, float* __restrict__ row_stats, const float* __restrict__ q,
+    const float* __restrict__ ksum, const int* __restrict__ tables,
+    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
+    int B, int Hkv, int MAXB, int P, int nch_max, int nsc, float scale, unsigned* flags) {
+  extern __shared__ float smem[];
+  const int id = blockIdx.x;
+  if (id < C * B) {
+    entropy_chunk_body<VEC>(logits, ld, V, C, temp, part, row_stats, id % C, id / C, smem);
+    return;
+  }
+  const int sid = id - C * B;
+  score_valu_body<D, G>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, MAXB, P, nch_max, scale,
+                        flags, sid % nsc, sid / nsc, smem);
+}
+
+struct StepBArgs {
+  const float* part;
+  int C;
+  float* temp;
+  float* h_prev;
+  float* tau;
+  float* h_out;
+  float* temp_used;
+  float eta, h_target, t_min, t_max;
+  const float* logits;
+  long long ld;
+  int V;
+  const float* stats;
+  const float* uniforms;
+  int* tokens;
+  const float* zbuf;
+  const float* lse_part;
+  const int* ctx_lens;
+  float* scores;
+  float* theta;
+  int* kept;
+  int* n_kept;
+  int Hq, MAXB, chunk, nch_max;
+  float eps_h, h_min, log_v, kappa_min;
+  int b_min;
+  unsigned* flags;
+};
+
+template <bool VEC>
+__global__ __launch_bounds__(kSelThreads) void step_b_kernel(StepBArgs a) {
+  extern __shared__ unsigned keys[];        // [MAXB]
+  __shared__ SelectShared ssh;
+  __shared__ SampleShared smp;
+  __shared__ float s_H, s_T;
+  const int b = blockIdx.x;
+  const int t = threadIdx.x;
+  if (t < 64) {
+    const float H = row_entropy(a.part, a.C, b);
+    if (t == 0) {
+      s_H = H;
+      s_T = a.temp[b];
+    }
+  }
+  __syncthreads();
+  const float H = s_H, T = s_T;
+  const int tok = sample_body<VEC>(a.logits, a.ld, a.V, a.C, a.stats, T, a.uniforms[b], b, smp);
+  if (t == 0) {
+    a.tokens[b] = tok;
+    controller_update(b, H, T, a.h_prev, a.tau, a.temp, a.h_out, a.temp_used, a.eta, a.h_target,
+                      a.t_min, a.t_max);
+  }
+  select_body(a.zbuf, a.lse_part, a.ctx_lens, H, a.scores, a.theta, a.kept, a.n_kept, a.Hq,
+              a.MAXB, a.chunk, a.nch_max, a.eps_h, a.h_min, a.log_v, a.kappa_min, a.b_min,
+              a.flags, b, keys, ssh);
+}
+
+template <bool VEC, int D>
+hipError_t launch_step_a(const ent_ctx* c, int B, const float* logits, long long ld,
+                         const float* temp, float* row_stats, const void* q, const float* ksum,
+                         const int* tables, const int* ctx_lens, hipStream_t s) {
+  const ent_config& cf = c->cfg;
+  const int Hq = cf.num_q_heads;
+  if (cf.kv_dtype == ENT_BF16) {
+    const int nsc = (cf.max_blocks_per_seq + kMfmaChunk - 1) / kMfmaChunk;
+    const size_t lds = static_cast<size_t>(kMfmaChunk) * Hq * sizeof(float) +
+                       static_cast<size_t>(Hq) * D * sizeof(uint16_t);
+    hipLaunchKernelGGL((step_a_mfma_kernel<VEC, D>), dim3(c->chunks * B + nsc * B),
+                       dim3(kChunkThreads), lds, s, logits, ld, cf.vocab, c->chunks, temp,
+                       c->ent_part, row_stats, static_cast<const uint16_t*>(q), ksum, tables,
+                       ctx_lens, c->zbuf, c->lse_part, B, cf.num_kv_heads, c->group,
+                       cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, nsc, cf.scale,
+                       c->dev_flags);
+    return hipGetLastError();
+  }
+  const int nsc = (cf.max_blocks_per_seq + kValuChunk - 1) / kValuChunk;
+  const size_t lds = (static_cast<size_t>(Hq) * D + static_cast<size_t>(kValuChunk) * Hq) * sizeof(float);
+  const float* qq = static_cast<const float*>(q);
+#define ENT_STEPA_CASE(GG)                                                                     \
+  case GG:                                                                                     \
+    hipLaunchKernelGGL((step_a_valu_kernel<VEC, D, GG>), dim3(c->chunks * B + nsc * B),        \
+                       dim3(kChunkThreads), lds, s, logits, ld, cf.vocab, c->chunks, temp,     \
+                       c->ent_part, row_stats, qq, ksum, tables, ctx_lens, c->zbuf,            \
+                       c->lse_part, B, cf.num_kv_heads, cf.max_blocks_per_seq,                 \
+                       cf.num_pool_blocks, c->lse_chunks, nsc, cf.scale, c->dev_flags);        \
+    break;
+  switch (c->group) {
+    ENT_STEPA_CASE(1)
+    ENT_STEPA_CASE(2)
+    ENT_STEPA_CASE(4)
+    ENT_STEPA_CASE(8)
+    ENT_STEPA_CASE(16)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef ENT_STEPA_CASE
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
+                              ent_state st, const void* q, const void* k_cache,
+                              const void* v_cache, const float* ksum, const int* tables,
+                              const int* ctx_lens, const float* uniforms, float* h_out,
+                              float* temp_used, float* row_stats, int* kept, int* n_kept,
+                              float* out, float* lse, int* tokens, float* scores, float* theta,
+                              hipStream_t s) {
+  const ent_config& cf = c->cfg;
+  float* stats = row_stats ? row_stats : c->stats_tmp;
+  const bool vec = row_vec_ok(logits, ld);
+  hipError_t e;
+  if (cf.head_dim == 128)
+    e = vec ? launch_step_a<true, 128>(c, B, logits, ld, st.temp, stats, q, ksum, tables, ctx_lens, s)
+            : launch_step_a<false, 128>(c, B, logits, ld, st.temp, stats, q, ksum, tables, ctx_lens, s);
+  else
+    e = vec ? launch_step_a<true, 64>(c, B, logits, ld, st.temp, stats, q, ksum, tables, ctx_lens, s)
+            : launch_step_a<false, 64>(c, B, logits, ld, st.temp, stats, q, ksum, tables, ctx_lens, s);
+  if (e != hipSuccess) return e;
+
+  StepBArgs a;
+  a.part = c->ent_part;
+  a.C = c->chunks;
+  a.temp = st.temp;
+  a.h_prev = st.h_prev;
+  a.tau = st.tau;
+  a.h_out = h_out;
+  a.temp_used = temp_used;
+  a.eta = cf.eta;
+  a.h_target = cf.h_target;
+  a.t_min = cf.t_min;
+  a.t_max = cf.t_max;
+  a.logits = logits;
+  a.ld = ld;
+  a.V = cf.vocab;
+  a.stats = stats;
+  a.uniforms = uniforms;
+  a.tokens = tokens;
+  a.zbuf = c->zbuf;
+  a.lse_part = c->lse_part;
+  a.ctx_lens = ctx_lens;
+  a.scores = scores;
+  a.theta = theta;
+  a.kept = kept;
+  a.n_kept = n_kept;
+  a.Hq = cf.num_q_heads;
+  a.MAXB = cf.max_blocks_per_seq;
+  a.chunk = cf.kv_dtype == ENT_BF16 ? kMfmaChunk : kValuChunk;
+  a.nch_max = c->lse_chunks;
+  a.eps_h = cf.eps_h;
+  a.h_min = cf.h_min;
+  a.log_v = cf.log_v;
+  a.kappa_min = cf.kappa_min;
+  a.b_min = cf.b_min;
+  a.flags = c->dev_flags;
+  const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
+  if (vec)
+    hipLaunchKernelGGL(step_b_kernel<true>, dim3(B), dim3(kSelThreads), lds, s, a);
+  else
+    hipLaunchKernelGGL(step_b_kernel<false>, dim3(B), dim3(kSelThreads), lds, s, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s);
+}
+
+}  // namespace ent

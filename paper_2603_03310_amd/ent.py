@@ -24,7 +24,7 @@ ENT_DEV_BAD_TABLE, ENT_DEV_BAD_CTXLEN, ENT_DEV_CACHE_FULL = 1, 2, 4
 EXPORTED = ("ent_default_config", "ent_check_config", "ent_row_stats_chunks", "ent_init",
             "ent_destroy", "ent_last_error", "ent_device_status", "ent_entropy_temperature",
             "ent_block_summary", "ent_block_select", "ent_sparse_paged_decode", "ent_sample",
-            "ent_kv_append")
+            "ent_kv_append", "ent_decode_step")
 
 
 class ent_config(ctypes.Structure):
@@ -77,6 +77,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "ent_sparse_paged_decode": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "ent_sample": (i, [vp, i, vp, ll, vp, vp, vp, vp, vp]),
         "ent_kv_append": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "ent_decode_step": (i, [vp, i, vp, ll, ent_state] + [vp] * 18),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -183,3 +184,14 @@ def ent_kv_append(ctx, B, k_new, v_new, block_tables, ctx_lens, k_cache, v_cache
     _check(ctx, load().ent_kv_append(ctx, B, ptr(k_new), ptr(v_new), ptr(block_tables),
                                      ptr(ctx_lens), ptr(k_cache), ptr(v_cache), ptr(ksum),
                                      _stream(stream)))
+
+
+def ent_decode_step(ctx, B, logits, ld, h_prev, tau, temp, q, k_cache, v_cache, ksum,
+                    block_tables, ctx_lens, uniforms, h_out, temp_used, kept, n_kept, out,
+                    tokens, row_stats=None, lse=None, scores=None, theta=None, stream=None):
+    st = ent_state(ptr(h_prev), ptr(tau), ptr(temp))
+    _check(ctx, load().ent_decode_step(ctx, B, ptr(logits), ld, st, ptr(q), ptr(k_cache),
+                                       ptr(v_cache), ptr(ksum), ptr(block_tables), ptr(ctx_lens),
+                                       ptr(uniforms), ptr(h_out), ptr(temp_used), ptr(row_stats),
+                                       ptr(kept), ptr(n_kept), ptr(out), ptr(lse), ptr(tokens),
+                                       ptr(scores), ptr(theta), _stream(stream)))

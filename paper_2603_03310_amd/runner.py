@@ -16,8 +16,10 @@ def make_config(**fields) -> ent.ent_config:
 
 
 class Decoder:
-    """Owns one library context; `step` runs the whole decode step:
-    ent_entropy_temperature -> ent_block_select -> ent_sparse_paged_decode -> ent_sample."""
+    """Owns one library context; `step` runs the whole decode step, either as
+    ent_entropy_temperature -> ent_block_select -> ent_sparse_paged_decode ->
+    ent_sample (fused=False) or as the single call ent_decode_step (fused=True,
+    the default); the two give bit-identical results."""
 
     def __init__(self, **fields):
         self.cfg = make_config(**fields)
@@ -39,8 +41,13 @@ class Decoder:
 
     def step(self, B, *, logits, h_prev, tau, temp, q, k_cache, v_cache, block_tables, ctx_lens,
              ksum, uniforms, h, temp_used, row_stats, kept, n_kept, out, tokens, lse=None,
-             scores=None, theta=None, stream=None):
+             scores=None, theta=None, stream=None, fused=True):
         ld = logits.stride(0)
+        if fused:
+            ent.ent_decode_step(self.ctx, B, logits, ld, h_prev, tau, temp, q, k_cache, v_cache,
+                                ksum, block_tables, ctx_lens, uniforms, h, temp_used, kept,
+                                n_kept, out, tokens, row_stats, lse, scores, theta, stream)
+            return
         ent.ent_entropy_temperature(self.ctx, B, logits, ld, h_prev, tau, temp, h, temp_used,
                                     row_stats, stream)
         ent.ent_block_select(self.ctx, B, q, ksum, block_tables, ctx_lens, h, kept, n_kept,

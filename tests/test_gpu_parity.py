@@ -30,7 +30,7 @@ def torch_cuda():
     return torch
 
 
-def _run(torch, x, p, steps=1, seqs=None, max_blocks=None, check_ksum=True):
+def _run(torch, x, p, steps=1, seqs=None, max_blocks=None, check_ksum=True, fused=True):
     from paper_2603_03310_amd.runner import Decoder
     w = x.workload
     dev = upload(x)
@@ -43,7 +43,7 @@ def _run(torch, x, p, steps=1, seqs=None, max_blocks=None, check_ksum=True):
         for t in range(steps):
             state = (dev.h_prev.cpu().numpy().copy(), dev.tau.cpu().numpy().copy(),
                      dev.temp.cpu().numpy().copy())
-            run_step(dec, dev, t)
+            run_step(dec, dev, t, fused=fused)
             torch.cuda.synchronize()
             gpu = collect(dev)
             print(f"[parity] {w.name} step {t}: kept fraction "
@@ -141,12 +141,35 @@ def test_temperature_unchanged_at_target(torch_cuda):
         assert dev1.temp.cpu().numpy()[s] == np.float32(x1.temp[s])
 
 
-def test_closed_loop_with_appends(torch_cuda):
+@pytest.mark.parametrize("fused", [True, False], ids=["fused", "staged"])
+def test_closed_loop_with_appends(torch_cuda, fused):
     w = small(LLAMA70B_LOOP, 4, ctx=("uniform", 100, 600), steps=6)
     x = generate(w)
-    reps, dev = _run(torch_cuda, x, default_params(w), steps=6)
+    reps, dev = _run(torch_cuda, x, default_params(w), steps=6, fused=fused)
     _assert_ok(reps)
     assert list(dev.ctx_lens.cpu().numpy()) == list(x.ctx_lens + 6)
+
+
+FUSED_CASES = [
+    TINY,
+    small(LLAMA3_8B, 5, ctx=("uniform", 100, 2500), suffix="fused"),
+    small(SKEWED, 10, ctx=("fixed", [0, 1, 15, 16, 17, 33, 64, 65, 100, 1000]), vocab=5000,
+          suffix="fused_edge"),
+]
+
+
+@pytest.mark.parametrize("w", FUSED_CASES, ids=lambda w: w.name)
+def test_fused_step_matches_staged(torch_cuda, w):
+    """ent_decode_step gives exactly the outputs of the four per-stage calls."""
+    x = generate(w)
+    p = default_params(w)
+    reps_f, df = _run(torch_cuda, x, p, fused=True)
+    _assert_ok(reps_f)
+    _, ds = _run(torch_cuda, generate(w), p, fused=False)
+    for name in ("h", "tau", "temp", "temp_used", "row_stats", "kept", "n_kept", "scores",
+                 "theta", "out", "lse", "tokens"):
+        a, b = getattr(df, name).cpu().numpy(), getattr(ds, name).cpu().numpy()
+        assert np.array_equal(a, b, equal_nan=True), name
 
 
 def test_deterministic(torch_cuda):
