@@ -196,8 +196,9 @@ int ent_sample(ent_ctx* c, int B, const float* logits, long long ld, const float
  * ent_entropy_temperature, ent_block_select, ent_sparse_paged_decode and
  * ent_sample called in that order on the same arguments (row_stats and
  * temp_used passed from the first to the last).  The entropy passes and the
- * block scoring share one launch; the per-sequence entropy, controller,
- * sampling and selection share a second; decode attention follows.
+ * block scoring share one launch; the per-sequence entropy, controller and
+ * selection share a second; decode attention follows, and sampling shares
+ * the launch that merges the split attention segments.
  * Arguments as in those calls: st is updated in place (tau, h_prev, temp
  * for the next step); h_out, temp_used, tokens: [B]; kept, n_kept, out as
  * in ent_sparse_paged_decode; row_stats, lse, scores, theta nullable.

@@ -102,9 +102,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
     const uint16_t* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
     const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
     int Hkv, int G, int MAXB, int P, int nch_max, float scale, unsigned* flags) {
-  extern __shared__ float smem[];
   score_mfma_body<D>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, G, MAXB, P, nch_max, scale,
-                     flags, blockIdx.x, blockIdx.y, smem);
+                     flags, blockIdx.x, blockIdx.y);
 }
 
 template <int D, int G>
@@ -137,9 +136,7 @@ hipError_t launch_score_d(const ent_ctx* c, int B, const void* q, const float* k
   const int Hq = cf.num_q_heads;
   if (cf.kv_dtype == ENT_BF16) {
     const dim3 grid((cf.max_blocks_per_seq + kMfmaChunk - 1) / kMfmaChunk, B);
-    const size_t lds = static_cast<size_t>(kMfmaChunk) * Hq * sizeof(float) +
-                       static_cast<size_t>(Hq) * D * sizeof(uint16_t);
-    hipLaunchKernelGGL(score_mfma_kernel<D>, grid, dim3(kScoreThreads), lds, s,
+    hipLaunchKernelGGL(score_mfma_kernel<D>, grid, dim3(kScoreThreads), 0, s,
                        static_cast<const uint16_t*>(q), ksum, tables, ctx_lens, c->zbuf,
                        c->lse_part, cf.num_kv_heads, c->group, cf.max_blocks_per_seq,
                        cf.num_pool_blocks, c->lse_chunks, cf.scale, c->dev_flags);

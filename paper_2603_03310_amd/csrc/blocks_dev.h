@@ -32,15 +32,16 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p) { return
 // and, per chunk of blocks and head, the log-sum-exp partial (max, sum) of
 // l_bh = z_bh + ln n_b over the chunk's blocks.
 //
-// bf16 queries (MFMA).  A workgroup of 4 waves takes 64 blocks, a tile of 16
-// per wave.  For each KV head g the tile's logits are one small contraction
+// bf16 queries (MFMA).  A workgroup of 4 waves takes a tile of 16 blocks and
+// splits the KV heads among its waves.  For each KV head g the tile's logits
+// are one small contraction
 //   Z[16 blocks x 16] = Kbar_g[16 x d] . Q_g^T[d x 16]   (columns: the G query
 // heads of g, zero-padded), on v_mfma_f32_16x16x32_bf16.  The fp32 summaries
 // are split exactly into three bf16 parts (hi + mid + lo: x - hi and the
 // remainder after mid are exact in fp32 and fit bf16), so three MFMAs per
 // k-step give the fp32 dot product of exact bf16 products.  A operands come
-// straight from global memory (8 dims per lane), the queries are staged in
-// LDS as bf16, and the next KV head's summaries are prefetched.
+// straight from global memory (8 dims per lane), as do the B operands (the
+// queries, 16 bytes per lane per k-step, cache-resident).
 //
 // fp32 queries (VALU).  A workgroup of 4 waves takes 16 blocks, 4 per wave;
 // a block's summary is read as NP passes of 256 floats, one float4 per lane
@@ -49,7 +50,7 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p) { return
 // ---------------------------------------------------------------------------
 constexpr int kScoreThreads = 256;
 constexpr int kScoreWaves = kScoreThreads / 64;
-constexpr int kMfmaChunk = 64;                 // blocks per MFMA scoring workgroup
+constexpr int kMfmaChunk = 16;                 // blocks per MFMA scoring workgroup
 constexpr int kValuChunk = 16;                 // blocks per VALU scoring workgroup
 constexpr int kValuPerWave = kValuChunk / kScoreWaves;
 
@@ -106,21 +107,20 @@ __device__ __forceinline__ void split3(const float4& x0, const float4& x1, sbf16
   lo = __builtin_bit_cast(sbf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
 }
 
-// smem: z tile [kMfmaChunk][Hq] fp32, then q [Hq][D] bf16.
+// One tile of kMfmaChunk = 16 blocks of sequence b, by one workgroup of 4
+// waves; wave w takes the KV heads w, w + 4, ... two at a time (both heads'
+// summaries in flight at once).  No LDS and no barrier: each wave reduces the
+// log-sum-exp partial of its own query heads over the tile with shuffles.
 template <int D>
 __device__ __forceinline__ void score_mfma_body(
     const uint16_t* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
     const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
-    int Hkv, int G, int MAXB, int P, int nch_max, float scale, unsigned* flags, int ch, int b,
-    float* smem) {
+    int Hkv, int G, int MAXB, int P, int nch_max, float scale, unsigned* flags, int ch, int b) {
   constexpr int KS = D / 32;
   const int Hq = Hkv * G;
-  float* zt = smem;
-  uint16_t* qs = reinterpret_cast<uint16_t*>(smem + kMfmaChunk * Hq);
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, gq = lane >> 4;
-  const int j_lo = ch * kMfmaChunk;
-  const int jt = j_lo + wave * 16;           // first block of this wave's tile
+  const int jt = ch * kMfmaChunk;
   // Table entry of block jt + r16, read before the context length is known
   // (in bounds of the MAXB-entry row); masked below.
   int p = 0;
@@ -128,63 +128,73 @@ __device__ __forceinline__ void score_mfma_body(
   const int N = ctx_lens[b];
   if (N < 0 || N > MAXB * kBlock) return;    // flagged by the selection kernel
   const int nb = (N + kBlock - 1) / kBlock;
-  if (j_lo >= nb) return;
-  const int nblk = min(kMfmaChunk, nb - j_lo);
+  if (jt >= nb || wave >= Hkv) return;
   const bool row_ok = jt + r16 < nb;
   if (row_ok && (p < 0 || p >= P)) {
     raise_flag(flags, ENT_DEV_BAD_TABLE);
     p = 0;
   }
   if (!row_ok) p = 0;
-  const bool any_rows = jt < nb;
-  const int nfl = Hkv * D;
+  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
+  const float ln_full = logf(static_cast<float>(kBlock));
+  const float* src = ksum + static_cast<long long>(p) * Hkv * D + gq * 8;
+  const uint16_t* qrow = q + static_cast<long long>(b) * Hq * D + gq * 8;
+  float* zrow = zbuf + (static_cast<long long>(b) * MAXB + jt) * Hq;
+  float* lp = lse_part + (static_cast<long long>(b) * nch_max + ch) * Hq * 2;
 
-  float4 cur[2 * KS], nxt[2 * KS];
   auto load_g = [&](int g, float4 (&buf)[2 * KS]) {
-    const float* src = ksum + static_cast<long long>(p) * nfl + g * D + gq * 8;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      buf[2 * ks] = *reinterpret_cast<const float4*>(src + ks * 32);
-      buf[2 * ks + 1] = *reinterpret_cast<const float4*>(src + ks * 32 + 4);
+      buf[2 * ks] = *reinterpret_cast<const float4*>(src + g * D + ks * 32);
+      buf[2 * ks + 1] = *reinterpret_cast<const float4*>(src + g * D + ks * 32 + 4);
     }
   };
-  if (any_rows) load_g(0, cur);
-  // Stage the queries (bf16) in LDS, 16 bytes per thread per step.
-  const uint4* qsrc = reinterpret_cast<const uint4*>(q + static_cast<long long>(b) * Hq * D);
-  for (int e = t; e < Hq * D / 8; e += kScoreThreads) reinterpret_cast<uint4*>(qs)[e] = qsrc[e];
-  __syncthreads();
-
-  if (any_rows) {
-    for (int g = 0; g < Hkv; ++g) {
-      if (g + 1 < Hkv) load_g(g + 1, nxt);
-      sf32x4_t acc = sf32x4_t{0.f, 0.f, 0.f, 0.f};
+  auto score_g = [&](int g, const float4 (&buf)[2 * KS]) {
+    sf32x4_t acc = sf32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        sbf16x8_t hi, mid, lo;
-        split3(cur[2 * ks], cur[2 * ks + 1], hi, mid, lo);
-        uint4 qb = make_uint4(0u, 0u, 0u, 0u);
-        if (r16 < G) qb = *reinterpret_cast<const uint4*>(qs + (g * G + r16) * D + ks * 32 + gq * 8);
-        const sbf16x8_t bq = __builtin_bit_cast(sbf16x8_t, qb);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mid, bq, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, bq, acc, 0, 0, 0);
-      }
-      // acc[e]: block 4*gq + e of the tile, query head g*G + r16.
-      if (r16 < G) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int blk = 4 * gq + e;
-          if (jt + blk < nb) zt[(wave * 16 + blk) * Hq + g * G + r16] = acc[e] * scale;
-        }
-      }
-#pragma unroll
-      for (int k = 0; k < 2 * KS; ++k) cur[k] = nxt[k];
+    for (int ks = 0; ks < KS; ++ks) {
+      sbf16x8_t hi, mid, lo;
+      split3(buf[2 * ks], buf[2 * ks + 1], hi, mid, lo);
+      uint4 qb = make_uint4(0u, 0u, 0u, 0u);
+      if (r16 < G) qb = *reinterpret_cast<const uint4*>(qrow + (g * G + r16) * D + ks * 32);
+      const sbf16x8_t bq = __builtin_bit_cast(sbf16x8_t, qb);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mid, bq, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, bq, acc, 0, 0, 0);
     }
+    // acc[e]: block jt + 4 gq + e, query head g G + r16 (columns r16 >= G are padding).
+    float l[4];
+    float m = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int j = jt + 4 * gq + e;
+      const float z = acc[e] * scale;
+      const bool ok = j < nb;
+      if (ok && r16 < G) zrow[(4 * gq + e) * Hq + g * G + r16] = z;
+      l[e] = ok ? z + ((j == nb - 1) ? ln_last : ln_full) : -INFINITY;
+      m = fmaxf(m, l[e]);
+    }
+    m = fmaxf(m, __shfl_xor(m, 16));
+    m = fmaxf(m, __shfl_xor(m, 32));
+    float sum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sum += (l[e] == -INFINITY) ? 0.f : expf(l[e] - m);
+    sum += __shfl_xor(sum, 16);
+    sum += __shfl_xor(sum, 32);
+    if (gq == 0 && r16 < G) {
+      lp[(g * G + r16) * 2 + 0] = m;
+      lp[(g * G + r16) * 2 + 1] = sum;
+    }
+  };
+
+  float4 k0[2 * KS], k1[2 * KS];
+  for (int g0 = wave; g0 < Hkv; g0 += 2 * kScoreWaves) {
+    const int g1 = g0 + kScoreWaves;
+    load_g(g0, k0);
+    if (g1 < Hkv) load_g(g1, k1);
+    score_g(g0, k0);
+    if (g1 < Hkv) score_g(g1, k1);
   }
-  __syncthreads();
-  float* zrow = zbuf + (static_cast<long long>(b) * MAXB + j_lo) * Hq;
-  for (int e = t; e < nblk * Hq; e += kScoreThreads) zrow[e] = zt[e];
-  chunk_lse(zt, nblk, Hq, j_lo, nb, N, lse_part + (static_cast<long long>(b) * nch_max + ch) * Hq * 2);
 }
 
 template <int G, int L>

@@ -29,6 +29,7 @@
 // fp32 path (VALU): the same decomposition with scalar dot products.
 
 #include "ent_internal.h"
+#include "entropy_dev.h"
 
 #include <math.h>
 
@@ -459,7 +460,7 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
 // M = max m, L = sum l 2^(m - M), then out = sum acc 2^(m - M) / L with every
 // thread streaming its outputs' partial accumulators as independent loads.
 template <int D>
-__global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
+__device__ __forceinline__ void combine_body(const DecodeArgs& a, int seg) {
   extern __shared__ int s_mem[];
   __shared__ int s_red[kWaves];
   __shared__ float s_m[kCombineMaxSplits * kMaxGroup], s_l[kCombineMaxSplits * kMaxGroup];
@@ -470,7 +471,6 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
   build_plan(a, s_pref, s_nk, s_N, s_red);
   const long long U = s_pref[a.B];
   const int t = threadIdx.x;
-  const int seg = blockIdx.x;
   const int b = seg / a.Hkv, g = seg % a.Hkv;
   const int G = a.G;
   const int Hq = a.Hkv * G;
@@ -571,6 +571,28 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
+  combine_body<D>(a, blockIdx.x);
+}
+
+// The merge above, and in the same launch (workgroups 0 .. B-1, first) the
+// sampling of every row: the two are independent, and the sampling
+// workgroups run in the merge's shadow.
+template <int D, bool VEC>
+__global__ __launch_bounds__(kThreads) void combine_sample_kernel(DecodeArgs a, SampleArgs sa) {
+  static_assert(kThreads == kSampleThreads, "sampling workgroup size");
+  __shared__ SampleShared sh;
+  if (static_cast<int>(blockIdx.x) < a.B) {
+    const int b = blockIdx.x;
+    const int tok = sample_body<VEC>(sa.logits, sa.ld, sa.V, sa.C, sa.stats, sa.temp_used[b],
+                                     sa.uniforms[b], b, sh);
+    if (threadIdx.x == 0) sa.tokens[b] = tok;
+    return;
+  }
+  combine_body<D>(a, blockIdx.x - a.B);
+}
+
 template <typename K>
 int occupancy_blocks(K kernel, size_t lds) {
   int n = 0;
@@ -604,7 +626,7 @@ long long decode_partial_slots(int decode_grid, int max_batch, int num_kv_heads)
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
-                         hipStream_t s) {
+                         hipStream_t s, const SampleArgs* sample) {
   const ent_config& cf = c->cfg;
   DecodeArgs a;
   a.q = q;
@@ -641,6 +663,22 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (sample) {
+    const dim3 cgrid(B * cf.num_kv_heads + B);
+    const bool vec = row_vec_ok(sample->logits, sample->ld);
+    if (cf.head_dim == 128) {
+      if (vec)
+        hipLaunchKernelGGL((combine_sample_kernel<128, true>), cgrid, dim3(kThreads), lds, s, a, *sample);
+      else
+        hipLaunchKernelGGL((combine_sample_kernel<128, false>), cgrid, dim3(kThreads), lds, s, a, *sample);
+    } else {
+      if (vec)
+        hipLaunchKernelGGL((combine_sample_kernel<64, true>), cgrid, dim3(kThreads), lds, s, a, *sample);
+      else
+        hipLaunchKernelGGL((combine_sample_kernel<64, false>), cgrid, dim3(kThreads), lds, s, a, *sample);
+    }
+    return hipGetLastError();
+  }
   const dim3 cgrid(B * cf.num_kv_heads);
   if (cf.head_dim == 128)
     hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), lds, s, a);

@@ -58,10 +58,23 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
                                const int* tables, const int* ctx_lens, const float* h,
                                int* kept, int* n_kept, float* scores, float* theta,
                                hipStream_t s);
+// Sampling issued in the launch that merges the decode partials (the fused
+// step); the arguments of ent_sample.
+struct SampleArgs {
+  const float* logits;
+  long long ld;
+  int V, C;
+  const float* stats;
+  const float* temp_used;
+  const float* uniforms;
+  int* tokens;
+};
+
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
-                         hipStream_t s);
+                         hipStream_t s,
+                         const SampleArgs* sample = nullptr);
 hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
                               ent_state st, const void* q, const void* k_cache,
                               const void* v_cache, const float* ksum, const int* tables,

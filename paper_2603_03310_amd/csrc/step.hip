@@ -3,13 +3,16 @@
 // bit-identical to calling ent_entropy_temperature, ent_block_select,
 // ent_sparse_paged_decode and ent_sample in sequence:
 //
-//   A  entropy chunk passes and block scoring, as disjoint workgroup ranges
-//      of one grid: both stream from HBM (logits, block summaries) and do not
-//      depend on each other, so one launch overlaps them;
+//   A  block scoring and the entropy chunk passes, as disjoint workgroup
+//      ranges of one grid (scoring first: its workgroups run longer): both
+//      stream from HBM (block summaries, logits) and do not depend on each
+//      other, so one launch overlaps them;
 //   B  one workgroup per sequence: the row's entropy from the chunk triples,
-//      sampling at the current temperature, the controller update, and the
-//      kept-block selection under the entropy-driven budget;
-//   C  kept-block decode attention and the merge of split segments.
+//      the controller update, and the kept-block selection under the
+//      entropy-driven budget;
+//   C  kept-block decode attention;
+//   D  the merge of split decode segments and, in the same launch, sampling
+//      at the temperature the step used (independent of the merge).
 
 #include "blocks_dev.h"
 #include "entropy_dev.h"
@@ -24,15 +27,15 @@ __global__ __launch_bounds__(kChunkThreads) void step_a_mfma_kernel(
     const float* __restrict__ ksum, const int* __restrict__ tables,
     const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
     int B, int Hkv, int G, int MAXB, int P, int nch_max, int nsc, float scale, unsigned* flags) {
-  extern __shared__ float smem[];
+  __shared__ float red[16];
   const int id = blockIdx.x;
-  if (id < C * B) {
-    entropy_chunk_body<VEC>(logits, ld, V, C, temp, part, row_stats, id % C, id / C, smem);
+  if (id < nsc * B) {
+    score_mfma_body<D>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, G, MAXB, P, nch_max,
+                       scale, flags, id % nsc, id / nsc);
     return;
   }
-  const int sid = id - C * B;
-  score_mfma_body<D>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, G, MAXB, P, nch_max, scale,
-                     flags, sid % nsc, sid / nsc, smem);
+  const int eid = id - nsc * B;
+  entropy_chunk_body<VEC>(logits, ld, V, C, temp, part, row_stats, eid % C, eid / C, red);
 }
 
 template <bool VEC, int D, int G>
@@ -44,13 +47,13 @@ __global__ __launch_bounds__(kChunkThreads) void step_a_valu_kernel(
     int B, int Hkv, int MAXB, int P, int nch_max, int nsc, float scale, unsigned* flags) {
   extern __shared__ float smem[];
   const int id = blockIdx.x;
-  if (id < C * B) {
-    entropy_chunk_body<VEC>(logits, ld, V, C, temp, part, row_stats, id % C, id / C, smem);
+  if (id < nsc * B) {
+    score_valu_body<D, G>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, MAXB, P, nch_max,
+                          scale, flags, id % nsc, id / nsc, smem);
     return;
   }
-  const int sid = id - C * B;
-  score_valu_body<D, G>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, MAXB, P, nch_max, scale,
-                        flags, sid % nsc, sid / nsc, smem);
+  const int eid = id - nsc * B;
+  entropy_chunk_body<VEC>(logits, ld, V, C, temp, part, row_stats, eid % C, eid / C, smem);
 }
 
 struct StepBArgs {
@@ -62,12 +65,6 @@ struct StepBArgs {
   float* h_out;
   float* temp_used;
   float eta, h_target, t_min, t_max;
-  const float* logits;
-  long long ld;
-  int V;
-  const float* stats;
-  const float* uniforms;
-  int* tokens;
   const float* zbuf;
   const float* lse_part;
   const int* ctx_lens;
@@ -81,29 +78,22 @@ struct StepBArgs {
   unsigned* flags;
 };
 
-template <bool VEC>
 __global__ __launch_bounds__(kSelThreads) void step_b_kernel(StepBArgs a) {
   extern __shared__ unsigned keys[];        // [MAXB]
   __shared__ SelectShared ssh;
-  __shared__ SampleShared smp;
-  __shared__ float s_H, s_T;
+  __shared__ float s_H;
   const int b = blockIdx.x;
   const int t = threadIdx.x;
   if (t < 64) {
     const float H = row_entropy(a.part, a.C, b);
     if (t == 0) {
       s_H = H;
-      s_T = a.temp[b];
+      controller_update(b, H, a.temp[b], a.h_prev, a.tau, a.temp, a.h_out, a.temp_used, a.eta,
+                        a.h_target, a.t_min, a.t_max);
     }
   }
   __syncthreads();
-  const float H = s_H, T = s_T;
-  const int tok = sample_body<VEC>(a.logits, a.ld, a.V, a.C, a.stats, T, a.uniforms[b], b, smp);
-  if (t == 0) {
-    a.tokens[b] = tok;
-    controller_update(b, H, T, a.h_prev, a.tau, a.temp, a.h_out, a.temp_used, a.eta, a.h_target,
-                      a.t_min, a.t_max);
-  }
+  const float H = s_H;
   select_body(a.zbuf, a.lse_part, a.ctx_lens, H, a.scores, a.theta, a.kept, a.n_kept, a.Hq,
               a.MAXB, a.chunk, a.nch_max, a.eps_h, a.h_min, a.log_v, a.kappa_min, a.b_min,
               a.flags, b, keys, ssh);
@@ -117,10 +107,8 @@ hipError_t launch_step_a(const ent_ctx* c, int B, const float* logits, long long
   const int Hq = cf.num_q_heads;
   if (cf.kv_dtype == ENT_BF16) {
     const int nsc = (cf.max_blocks_per_seq + kMfmaChunk - 1) / kMfmaChunk;
-    const size_t lds = static_cast<size_t>(kMfmaChunk) * Hq * sizeof(float) +
-                       static_cast<size_t>(Hq) * D * sizeof(uint16_t);
     hipLaunchKernelGGL((step_a_mfma_kernel<VEC, D>), dim3(c->chunks * B + nsc * B),
-                       dim3(kChunkThreads), lds, s, logits, ld, cf.vocab, c->chunks, temp,
+                       dim3(kChunkThreads), 0, s, logits, ld, cf.vocab, c->chunks, temp,
                        c->ent_part, row_stats, static_cast<const uint16_t*>(q), ksum, tables,
                        ctx_lens, c->zbuf, c->lse_part, B, cf.num_kv_heads, c->group,
                        cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, nsc, cf.scale,
@@ -184,12 +172,6 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   a.h_target = cf.h_target;
   a.t_min = cf.t_min;
   a.t_max = cf.t_max;
-  a.logits = logits;
-  a.ld = ld;
-  a.V = cf.vocab;
-  a.stats = stats;
-  a.uniforms = uniforms;
-  a.tokens = tokens;
   a.zbuf = c->zbuf;
   a.lse_part = c->lse_part;
   a.ctx_lens = ctx_lens;
@@ -208,13 +190,20 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   a.b_min = cf.b_min;
   a.flags = c->dev_flags;
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-  if (vec)
-    hipLaunchKernelGGL(step_b_kernel<true>, dim3(B), dim3(kSelThreads), lds, s, a);
-  else
-    hipLaunchKernelGGL(step_b_kernel<false>, dim3(B), dim3(kSelThreads), lds, s, a);
+  hipLaunchKernelGGL(step_b_kernel, dim3(B), dim3(kSelThreads), lds, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s);
+  SampleArgs sa;
+  sa.logits = logits;
+  sa.ld = ld;
+  sa.V = cf.vocab;
+  sa.C = c->chunks;
+  sa.stats = stats;
+  sa.temp_used = temp_used;
+  sa.uniforms = uniforms;
+  sa.tokens = tokens;
+  return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s,
+                       &sa);
 }
 
 }  // namespace ent
