@@ -73,7 +73,8 @@ typedef struct {
                               H_q <= 128, H_kv * head_dim <= 2048 */
   int head_dim;            /* d: 64 or 128 */
   int block_size;          /* tokens per KV block: must be 16 */
-  int max_blocks_per_seq;  /* MAXB: row length of block_tables, <= 16384 */
+  int max_blocks_per_seq;  /* MAXB: row length of block_tables, <= 16384;
+                              max_batch * MAXB * H_kv < 2^31 */
   int num_pool_blocks;     /* P: physical blocks in k_cache / v_cache */
   int vocab;               /* |V|: logits per row */
   int kv_dtype;            /* ENT_BF16 or ENT_F32 (K, V and queries) */

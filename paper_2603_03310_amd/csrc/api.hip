@@ -51,6 +51,8 @@ std::string check_config(const ent_config* c, int* code) {
   if (c->max_blocks_per_seq > ent::kMaxBlocksPerSeq) return "max_blocks_per_seq must be <= 16384";
   if (c->num_kv_heads * c->head_dim > 2048) return "num_kv_heads * head_dim must be <= 2048";
   if (c->vocab > kMaxVocab) return "vocab must be <= 1048576";
+  if (static_cast<long long>(c->max_batch) * c->max_blocks_per_seq * c->num_kv_heads >= (1ll << 31))
+    return "max_batch * max_blocks_per_seq * num_kv_heads must be < 2^31";
   *code = ENT_OK;
   return "";
 }
@@ -142,6 +144,7 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->chunks = ent_row_stats_chunks(f.vocab);
   c->lse_chunks = (f.max_blocks_per_seq + ent::kMinScoreChunk - 1) / ent::kMinScoreChunk;
   c->decode_grid = ent::decode_grid_size(c);
+  c->prologue_grid = ent::prologue_grid_size(c);
 
   const size_t Bm = static_cast<size_t>(f.max_batch);
   const size_t sz_ent_part = align_up(Bm * c->chunks * 3 * sizeof(float));

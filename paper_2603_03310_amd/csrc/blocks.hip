@@ -12,7 +12,7 @@
 //
 // Kernels:
 //   summary_kernel   per-block mean keys (setup)
-//   score_mfma_kernel   z for 64 blocks x all heads per workgroup (bf16, MFMA)
+//   (bf16 scoring runs in the persistent kernel of prologue.hip)
 //   score_valu_kernel   z for 16 blocks x all heads per workgroup (fp32, VALU)
 //   select_kernel       per sequence: merges the per-chunk log-sum-exp
 //                       partials into L_h, computes
@@ -97,15 +97,6 @@ __global__ __launch_bounds__(kThreads) void append_kernel(
 }
 
 // Per-stage kernels over the shared bodies.
-template <int D>
-__global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
-    const uint16_t* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
-    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
-    int Hkv, int G, int MAXB, int P, int nch_max, float scale, unsigned* flags) {
-  score_mfma_body<D>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, G, MAXB, P, nch_max, scale,
-                     flags, blockIdx.x, blockIdx.y);
-}
-
 template <int D, int G>
 __global__ __launch_bounds__(kScoreThreads) void score_valu_kernel(
     const float* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
@@ -130,24 +121,15 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 }
 
 template <int D>
-hipError_t launch_score_d(const ent_ctx* c, int B, const void* q, const float* ksum,
-                          const int* tables, const int* ctx_lens, hipStream_t s) {
+hipError_t launch_score_valu_d(const ent_ctx* c, int B, const float* q, const float* ksum,
+                               const int* tables, const int* ctx_lens, hipStream_t s) {
   const ent_config& cf = c->cfg;
   const int Hq = cf.num_q_heads;
-  if (cf.kv_dtype == ENT_BF16) {
-    const dim3 grid((cf.max_blocks_per_seq + kMfmaChunk - 1) / kMfmaChunk, B);
-    hipLaunchKernelGGL(score_mfma_kernel<D>, grid, dim3(kScoreThreads), 0, s,
-                       static_cast<const uint16_t*>(q), ksum, tables, ctx_lens, c->zbuf,
-                       c->lse_part, cf.num_kv_heads, c->group, cf.max_blocks_per_seq,
-                       cf.num_pool_blocks, c->lse_chunks, cf.scale, c->dev_flags);
-    return hipGetLastError();
-  }
   const dim3 grid((cf.max_blocks_per_seq + kValuChunk - 1) / kValuChunk, B);
   const size_t lds = (static_cast<size_t>(Hq) * D + static_cast<size_t>(kValuChunk) * Hq) * sizeof(float);
-  const float* qq = static_cast<const float*>(q);
 #define ENT_SCORE_CASE(GG)                                                                    \
   case GG:                                                                                    \
-    hipLaunchKernelGGL((score_valu_kernel<D, GG>), grid, dim3(kScoreThreads), lds, s, qq,     \
+    hipLaunchKernelGGL((score_valu_kernel<D, GG>), grid, dim3(kScoreThreads), lds, s, q,      \
                        ksum, tables, ctx_lens, c->zbuf, c->lse_part, cf.num_kv_heads,         \
                        cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, cf.scale,    \
                        c->dev_flags);                                                         \
@@ -184,12 +166,39 @@ hipError_t launch_block_summary(const ent_ctx* c, int B, const void* k_cache, co
   return hipGetLastError();
 }
 
+hipError_t launch_score_valu(const ent_ctx* c, int B, const void* q, const float* ksum,
+                             const int* tables, const int* ctx_lens, hipStream_t s) {
+  const float* qq = static_cast<const float*>(q);
+  return c->cfg.head_dim == 128 ? launch_score_valu_d<128>(c, B, qq, ksum, tables, ctx_lens, s)
+                                : launch_score_valu_d<64>(c, B, qq, ksum, tables, ctx_lens, s);
+}
+
 hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const float* ksum,
                                const int* tables, const int* ctx_lens, const float* h, int* kept,
                                int* n_kept, float* scores, float* theta, hipStream_t s) {
   const ent_config& cf = c->cfg;
-  const hipError_t e = cf.head_dim == 128 ? launch_score_d<128>(c, B, q, ksum, tables, ctx_lens, s)
-                                          : launch_score_d<64>(c, B, q, ksum, tables, ctx_lens, s);
+  hipError_t e;
+  if (cf.kv_dtype == ENT_BF16) {
+    PrologueArgs a{};
+    a.B = B;
+    a.do_score = 1;
+    a.q = static_cast<const uint16_t*>(q);
+    a.ksum = ksum;
+    a.tables = tables;
+    a.ctx_lens = ctx_lens;
+    a.zbuf = c->zbuf;
+    a.lse_part = c->lse_part;
+    a.Hkv = cf.num_kv_heads;
+    a.G = c->group;
+    a.MAXB = cf.max_blocks_per_seq;
+    a.P = cf.num_pool_blocks;
+    a.nch_max = c->lse_chunks;
+    a.scale = cf.scale;
+    a.flags = c->dev_flags;
+    e = launch_prologue(c, a, s);
+  } else {
+    e = launch_score_valu(c, B, q, ksum, tables, ctx_lens, s);
+  }
   if (e != hipSuccess) return e;
   const int chunk = cf.kv_dtype == ENT_BF16 ? kMfmaChunk : kValuChunk;
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);

@@ -1,5 +1,6 @@
 // Device bodies of the block scoring and selection stages, shared by the
-// per-stage kernels (blocks.hip) and the fused step kernels (step.hip).
+// per-stage kernels (blocks.hip, prologue.hip) and the fused step kernels
+// (step.hip).
 //
 // Block entropic contribution (Section 3.2 of the paper): I_b is the
 // attention-weighted surprisal of block b's tokens.  Weights come from the
@@ -32,16 +33,13 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p) { return
 // and, per chunk of blocks and head, the log-sum-exp partial (max, sum) of
 // l_bh = z_bh + ln n_b over the chunk's blocks.
 //
-// bf16 queries (MFMA).  A workgroup of 4 waves takes a tile of 16 blocks and
-// splits the KV heads among its waves.  For each KV head g the tile's logits
-// are one small contraction
+// bf16 queries (MFMA).  A wave takes a tile of 16 blocks and two KV heads.
+// For each KV head g the tile's logits are one small contraction
 //   Z[16 blocks x 16] = Kbar_g[16 x d] . Q_g^T[d x 16]   (columns: the G query
 // heads of g, zero-padded), on v_mfma_f32_16x16x32_bf16.  The fp32 summaries
-// are split exactly into three bf16 parts (hi + mid + lo: x - hi and the
-// remainder after mid are exact in fp32 and fit bf16), so three MFMAs per
-// k-step give the fp32 dot product of exact bf16 products.  A operands come
-// straight from global memory (8 dims per lane), as do the B operands (the
-// queries, 16 bytes per lane per k-step, cache-resident).
+// are split exactly into three bf16 parts (hi + mid + lo), so three MFMAs per
+// k-step give the fp32 dot product of exact bf16 products.  Both operands
+// come straight from global memory (the queries are cache-resident).
 //
 // fp32 queries (VALU).  A workgroup of 4 waves takes 16 blocks, 4 per wave;
 // a block's summary is read as NP passes of 256 floats, one float4 per lane
@@ -54,7 +52,6 @@ constexpr int kMfmaChunk = 16;                 // blocks per MFMA scoring workgr
 constexpr int kValuChunk = 16;                 // blocks per VALU scoring workgroup
 constexpr int kValuPerWave = kValuChunk / kScoreWaves;
 
-typedef __bf16 sbf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float sf32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
 
 // Per-head log-sum-exp partial of l = z + ln n over the chunk's nblk blocks
@@ -79,84 +76,119 @@ __device__ __forceinline__ void chunk_lse(const float* zt, int nblk, int Hq, int
   }
 }
 
-// Exact three-way bf16 split of 8 floats (two float4) into packed bf16x8.
-__device__ __forceinline__ void split3(const float4& x0, const float4& x1, sbf16x8_t& hi,
-                                       sbf16x8_t& mid, sbf16x8_t& lo) {
-  const float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-  uint32_t h[4], m[4], l[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    uint32_t hb[2], mb[2], lb[2];
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const uint32_t ux = __float_as_uint(v[2 * i + k]);
-      const uint32_t uh = ux & 0xFFFF0000u;
-      const float r = v[2 * i + k] - __uint_as_float(uh);
-      const uint32_t um = __float_as_uint(r) & 0xFFFF0000u;
-      const uint32_t ul = __float_as_uint(r - __uint_as_float(um));
-      hb[k] = uh;
-      mb[k] = um;
-      lb[k] = ul;
-    }
-    h[i] = (hb[0] >> 16) | hb[1];
-    m[i] = (mb[0] >> 16) | mb[1];
-    l[i] = (lb[0] >> 16) | (lb[1] & 0xFFFF0000u);
-  }
-  hi = __builtin_bit_cast(sbf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
-  mid = __builtin_bit_cast(sbf16x8_t, make_uint4(m[0], m[1], m[2], m[3]));
-  lo = __builtin_bit_cast(sbf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
-}
+// One scoring item: a tile of kMfmaChunk = 16 blocks of sequence b (tile
+// ch) and up to two KV heads g0, g0 + 1, by one wave.  The item's summaries
+// (16 blocks x 2 heads x d fp32) are loaded first (score_pair_load), so that
+// a wave can have the next item's loads in flight while it computes one.
+constexpr int kScorePairSlots = 16;     // float4 slots per lane (d <= 128)
 
-// One tile of kMfmaChunk = 16 blocks of sequence b, by one workgroup of 4
-// waves; wave w takes the KV heads w, w + 4, ... two at a time (both heads'
-// summaries in flight at once).  No LDS and no barrier: each wave reduces the
-// log-sum-exp partial of its own query heads over the tile with shuffles.
-template <int D>
-__device__ __forceinline__ void score_mfma_body(
-    const uint16_t* __restrict__ q, const float* __restrict__ ksum, const int* __restrict__ tables,
-    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
-    int Hkv, int G, int MAXB, int P, int nch_max, float scale, unsigned* flags, int ch, int b) {
-  constexpr int KS = D / 32;
-  const int Hq = Hkv * G;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r16 = lane & 15, gq = lane >> 4;
-  const int jt = ch * kMfmaChunk;
-  // Table entry of block jt + r16, read before the context length is known
-  // (in bounds of the MAXB-entry row); masked below.
-  int p = 0;
-  if (jt + r16 < MAXB) p = tables[static_cast<long long>(b) * MAXB + jt + r16];
-  const int N = ctx_lens[b];
-  if (N < 0 || N > MAXB * kBlock) return;    // flagged by the selection kernel
-  const int nb = (N + kBlock - 1) / kBlock;
-  if (jt >= nb || wave >= Hkv) return;
-  const bool row_ok = jt + r16 < nb;
-  if (row_ok && (p < 0 || p >= P)) {
+// Physical block of tile row r16 (lane & 15), validated; 0 for rows past the
+// sequence's nb blocks.
+__device__ __forceinline__ int score_tile_block(const int* __restrict__ tables, int b, int ch,
+                                                int MAXB, int nb, int P, unsigned* flags) {
+  const int r16 = threadIdx.x & 15;
+  const int j = ch * kMfmaChunk + r16;
+  if (j >= nb) return 0;
+  int p = tables[static_cast<long long>(b) * MAXB + j];
+  if (p < 0 || p >= P) {
     raise_flag(flags, ENT_DEV_BAD_TABLE);
     p = 0;
   }
-  if (!row_ok) p = 0;
+  return p;
+}
+
+// Lane (r16, gq) loads, for head g0 + h of block row r16, the float4 slots
+// j = 0 .. D/16 - 1 at dims 16 j + 4 gq .. +3 (the four lanes of a row read
+// 64 contiguous bytes per slot) into buf[h D/16 + j].
+template <int D>
+__device__ __forceinline__ void score_pair_load(const float* __restrict__ ksum, int p, int Hkv,
+                                                int g0, int ng,
+                                                float4 (&buf)[kScorePairSlots]) {
+  constexpr int NJ = D / 16;
+  static_assert(2 * NJ <= kScorePairSlots, "slots");
+  const int gq = (threadIdx.x & 63) >> 4;
+  const float* src = ksum + (static_cast<long long>(p) * Hkv + g0) * D + gq * 4;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (h < ng) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        buf[h * NJ + j] = *reinterpret_cast<const float4*>(src + h * D + 16 * j);
+    }
+  }
+}
+
+typedef float sf32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 sbf16x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 sbf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
+
+// Exact three-way split x = hi + mid + lo of 8 floats into bf16 parts, each
+// part rounded to nearest from the remainder of the previous ones: the
+// remainders are exact in fp32 (they are differences of nearby floats) and
+// the last one has at most 8 significant bits, so lo is exact in bf16.
+__device__ __forceinline__ void split3(const float4& x0, const float4& x1, sbf16x8_t& hi,
+                                       sbf16x8_t& mid, sbf16x8_t& lo) {
+  const sf32x2_t v[4] = {{x0.x, x0.y}, {x0.z, x0.w}, {x1.x, x1.y}, {x1.z, x1.w}};
+  sbf16x2_t h[4], m[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    h[i] = __builtin_convertvector(v[i], sbf16x2_t);
+    const sf32x2_t r = v[i] - __builtin_convertvector(h[i], sf32x2_t);
+    m[i] = __builtin_convertvector(r, sbf16x2_t);
+    const sf32x2_t r2 = r - __builtin_convertvector(m[i], sf32x2_t);
+    l[i] = __builtin_convertvector(r2, sbf16x2_t);
+  }
+  hi = sbf16x8_t{h[0].x, h[0].y, h[1].x, h[1].y, h[2].x, h[2].y, h[3].x, h[3].y};
+  mid = sbf16x8_t{m[0].x, m[0].y, m[1].x, m[1].y, m[2].x, m[2].y, m[3].x, m[3].y};
+  lo = sbf16x8_t{l[0].x, l[0].y, l[1].x, l[1].y, l[2].x, l[2].y, l[3].x, l[3].y};
+}
+
+// Block logits z of the item's heads (written to zbuf) and each head's
+// log-sum-exp partial (max, sum) of z + ln n_b over the tile (lse_part).
+// z[16 blocks x 16] = Kbar_g[16 x d] Q_g^T[d x 16] on
+// v_mfma_f32_16x16x32_bf16 (columns: the G query heads of g, zero-padded),
+// three MFMAs per k-step over the exact split of the fp32 summaries, so
+// every product is exact and only the fp32 accumulation rounds.  K-slot
+// (gq, e) of step ks is dim 32 ks + 4 gq + e for e < 4 and
+// 32 ks + 16 + 4 gq + (e - 4) for e >= 4, in both operands.
+template <int D>
+__device__ __forceinline__ void score_pair_compute(
+    const uint16_t* __restrict__ q, const float4 (&buf)[kScorePairSlots],
+    float* __restrict__ zbuf, float* __restrict__ lse_part, int b, int ch, int g0, int ng,
+    int N, int nb, int Hkv, int G, int MAXB, int nch_max, float scale) {
+  constexpr int NJ = D / 16;
+  constexpr int KS = D / 32;
+  const int Hq = Hkv * G;
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, gq = lane >> 4;
+  const int jt = ch * kMfmaChunk;
   const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
   const float ln_full = logf(static_cast<float>(kBlock));
-  const float* src = ksum + static_cast<long long>(p) * Hkv * D + gq * 8;
-  const uint16_t* qrow = q + static_cast<long long>(b) * Hq * D + gq * 8;
+  const uint16_t* qrow = q + static_cast<long long>(b) * Hq * D + gq * 4;
   float* zrow = zbuf + (static_cast<long long>(b) * MAXB + jt) * Hq;
   float* lp = lse_part + (static_cast<long long>(b) * nch_max + ch) * Hq * 2;
-
-  auto load_g = [&](int g, float4 (&buf)[2 * KS]) {
+  // Query operands of both heads first: their latency overlaps the splits.
+  uint2 qv[2][2 * KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      buf[2 * ks] = *reinterpret_cast<const float4*>(src + g * D + ks * 32);
-      buf[2 * ks + 1] = *reinterpret_cast<const float4*>(src + g * D + ks * 32 + 4);
+  for (int h = 0; h < 2; ++h) {
+    const uint16_t* qh = qrow + static_cast<long long>((g0 + h) * G + r16) * D;
+#pragma unroll
+    for (int j = 0; j < 2 * KS; ++j) {
+      qv[h][j] = make_uint2(0u, 0u);
+      if (h < ng && r16 < G) qv[h][j] = *reinterpret_cast<const uint2*>(qh + 16 * j);
     }
-  };
-  auto score_g = [&](int g, const float4 (&buf)[2 * KS]) {
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (h >= ng) break;
+    const int g = g0 + h;
     sf32x4_t acc = sf32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       sbf16x8_t hi, mid, lo;
-      split3(buf[2 * ks], buf[2 * ks + 1], hi, mid, lo);
-      uint4 qb = make_uint4(0u, 0u, 0u, 0u);
-      if (r16 < G) qb = *reinterpret_cast<const uint4*>(qrow + (g * G + r16) * D + ks * 32);
+      split3(buf[h * NJ + 2 * ks], buf[h * NJ + 2 * ks + 1], hi, mid, lo);
+      const uint4 qb = make_uint4(qv[h][2 * ks].x, qv[h][2 * ks].y, qv[h][2 * ks + 1].x,
+                                  qv[h][2 * ks + 1].y);
       const sbf16x8_t bq = __builtin_bit_cast(sbf16x8_t, qb);
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq, acc, 0, 0, 0);
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mid, bq, acc, 0, 0, 0);
@@ -185,15 +217,6 @@ __device__ __forceinline__ void score_mfma_body(
       lp[(g * G + r16) * 2 + 0] = m;
       lp[(g * G + r16) * 2 + 1] = sum;
     }
-  };
-
-  float4 k0[2 * KS], k1[2 * KS];
-  for (int g0 = wave; g0 < Hkv; g0 += 2 * kScoreWaves) {
-    const int g1 = g0 + kScoreWaves;
-    load_g(g0, k0);
-    if (g1 < Hkv) load_g(g1, k1);
-    score_g(g0, k0);
-    if (g1 < Hkv) score_g(g1, k1);
   }
 }
 

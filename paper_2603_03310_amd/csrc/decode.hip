@@ -44,6 +44,8 @@ constexpr int kCombineMaxSplits = 64;        // partials staged in LDS per pass
 typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef short s16x4_t __attribute__((__vector_size__(4 * sizeof(short))));
 typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 struct DecodeArgs {
   const void* q;
@@ -102,16 +104,16 @@ __device__ void build_plan(const DecodeArgs& a, int* s_pref, int* s_nk, int* s_N
   __syncthreads();
 }
 
-__device__ __forceinline__ long long range_begin(int w, long long U, int W) {
-  return static_cast<long long>(w) * U / W;
+__device__ __forceinline__ int range_begin(int w, int U, int W) {
+  return static_cast<int>(static_cast<long long>(w) * U / W);
 }
 // The wave whose range holds unit x (U > 0).
-__device__ __forceinline__ int wave_of(long long x, long long U, int W) {
+__device__ __forceinline__ int wave_of(int x, int U, int W) {
   return static_cast<int>(((x + 1) * W - 1) / U);
 }
 
 // Sequence holding unit x: the largest b with s_pref[b] <= x.
-__device__ __forceinline__ int seq_of(long long x, const int* s_pref, int B) {
+__device__ __forceinline__ int seq_of(int x, const int* s_pref, int B) {
   int lo = 0, hi = B;
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
@@ -127,7 +129,7 @@ struct UnitMeta {
   int nv;    // valid tokens of the block
 };
 
-__device__ __forceinline__ UnitMeta unit_meta(const DecodeArgs& a, long long x, long long u1,
+__device__ __forceinline__ UnitMeta unit_meta(const DecodeArgs& a, int x, int u1,
                                               const int* s_pref, const int* s_nk, const int* s_N) {
   UnitMeta m{-1, -1, 0};
   if (x >= u1) return m;
@@ -173,11 +175,11 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   int* s_nk = s_mem + a.B + 1;
   int* s_N = s_nk + a.B;
   build_plan(a, s_pref, s_nk, s_N, s_red);
-  const long long U = s_pref[a.B];
+  const int U = s_pref[a.B];
   const int lane = threadIdx.x & 63;
   const int w = blockIdx.x * kWaves + (threadIdx.x >> 6);
   if (U == 0) return;
-  const long long u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
+  const int u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
   if (u0 >= u1) return;
   const int r16 = lane & 15, gq = lane >> 4;
   const int G = a.G;
@@ -187,7 +189,7 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   const uint16_t* kc = static_cast<const uint16_t*>(a.kc);
   const uint16_t* vc = static_cast<const uint16_t*>(a.vc);
 
-  long long ubase = u0;
+  int ubase = u0;
   UnitMeta win = unit_meta(a, ubase + lane, u1, s_pref, s_nk, s_N);
 
   bf16x8_t kcur[KS], knxt[KS];
@@ -215,8 +217,8 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
     float l_tot = l_run + __shfl_xor(l_run, 16);
     l_tot += __shfl_xor(l_tot, 32);
     const int b = cur_seg / a.Hkv, g = cur_seg % a.Hkv;
-    const long long seg_start = s_pref[b] + static_cast<long long>(g) * s_nk[b];
-    const long long seg_end = seg_start + s_nk[b];
+    const int seg_start = s_pref[b] + g * s_nk[b];
+    const int seg_end = seg_start + s_nk[b];
     if (!head_ok) return;
     if (seg_start >= u0 && seg_end <= u1) {
       const long long oh = static_cast<long long>(b) * Hq + g * G + r16;
@@ -240,13 +242,16 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
     }
   };
 
-  for (long long u = u0; u < u1; ++u) {
+  // One unit: compute on the tiles in (kc, vc) while the next unit's tiles
+  // stream into (kn, vn); the loop below alternates the two buffers.
+  auto unit = [&](int u, bf16x8_t (&kc)[KS], s16x4_t (&vc)[MT], bf16x8_t (&kn)[KS],
+                  s16x4_t (&vn)[MT]) {
     int i = static_cast<int>(u - ubase);
     if (i == kWindow) {
       ubase = u;
       i = 0;
       win = unit_meta(a, ubase + lane, u1, s_pref, s_nk, s_N);
-      load_tiles(0, kcur, vcur);
+      load_tiles(0, kc, vc);
     }
     const int seg = __shfl(win.seg, i);
     if (seg != cur_seg) {
@@ -264,14 +269,14 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
 #pragma unroll
       for (int m = 0; m < MT; ++m) oacc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
-    if (i + 1 < kWindow && u + 1 < u1) load_tiles(i + 1, knxt, vnxt);
+    if (i + 1 < kWindow && u + 1 < u1) load_tiles(i + 1, kn, vn);
     const int p = __shfl(win.p, i);
     const int nv = __shfl(win.nv, i);
     if (p >= 0) {
       f32x4_t sacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kcur[ks], qreg[ks], sacc, 0, 0, 0);
+        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc[ks], qreg[ks], sacc, 0, 0, 0);
       float sc[4];
       bool up = false;
 #pragma unroll
@@ -285,40 +290,47 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
         mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
         mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
         const float m_new = fmaxf(m_run, mloc);
-        const float alpha = exp2f(m_run - m_new);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
         l_run *= alpha;
 #pragma unroll
         for (int m = 0; m < MT; ++m) oacc[m] *= alpha;
         m_run = m_new;
       }
-      float pe[4];
+      // Arguments are <= 0; the hardware exp2 flushes results below 2^-126,
+      // which are negligible next to the running maximum's weight of 1.
+      bf16x2_t ph[2], pl[2];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pe[e] = exp2f(sc[e] - m_run);
-      l_run += (pe[0] + pe[1]) + (pe[2] + pe[3]);
-      s16x4_t phi, plo;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint16_t hb = f32_to_bf16_rne(pe[e]);
-        phi[e] = static_cast<short>(hb);
-        plo[e] = static_cast<short>(f32_to_bf16_rne(pe[e] - bf16_to_f32(hb)));
+      for (int k = 0; k < 2; ++k) {
+        const f32x2_t pe = {__builtin_amdgcn_exp2f(sc[2 * k] - m_run),
+                            __builtin_amdgcn_exp2f(sc[2 * k + 1] - m_run)};
+        l_run += pe.x + pe.y;
+        // P = high bf16 part + bf16 remainder (both rounded to nearest).
+        ph[k] = __builtin_convertvector(pe, bf16x2_t);
+        pl[k] = __builtin_convertvector(pe - __builtin_convertvector(ph[k], f32x2_t), bf16x2_t);
       }
+      const s16x4_t phi = __builtin_bit_cast(s16x4_t, make_uint2(__builtin_bit_cast(uint32_t, ph[0]),
+                                                                 __builtin_bit_cast(uint32_t, ph[1])));
+      const s16x4_t plo = __builtin_bit_cast(s16x4_t, make_uint2(__builtin_bit_cast(uint32_t, pl[0]),
+                                                                 __builtin_bit_cast(uint32_t, pl[1])));
       if (nv < kBlock) {
 #pragma unroll
         for (int m = 0; m < MT; ++m)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (4 * gq + e >= nv) vcur[m][e] = 0;
+            if (4 * gq + e >= nv) vc[m][e] = 0;
       }
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
-        oacc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vcur[m], phi, oacc[m], 0, 0, 0);
-        oacc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vcur[m], plo, oacc[m], 0, 0, 0);
+        oacc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vc[m], phi, oacc[m], 0, 0, 0);
+        oacc[m] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vc[m], plo, oacc[m], 0, 0, 0);
       }
     }
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kcur[ks] = knxt[ks];
-#pragma unroll
-    for (int m = 0; m < MT; ++m) vcur[m] = vnxt[m];
+  };
+  for (int u = u0; u < u1;) {
+    unit(u, kcur, vcur, knxt, vnxt);
+    if (++u >= u1) break;
+    unit(u, knxt, vnxt, kcur, vcur);
+    ++u;
   }
   flush();
 }
@@ -332,11 +344,11 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
   int* s_nk = s_mem + a.B + 1;
   int* s_N = s_nk + a.B;
   build_plan(a, s_pref, s_nk, s_N, s_red);
-  const long long U = s_pref[a.B];
+  const int U = s_pref[a.B];
   const int lane = threadIdx.x & 63;
   const int w = blockIdx.x * kWaves + (threadIdx.x >> 6);
   if (U == 0) return;
-  const long long u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
+  const int u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
   if (u0 >= u1) return;
   const int t16 = lane & 15, hs = lane >> 4;
   const int G = a.G;
@@ -345,7 +357,7 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
   const float* kc = static_cast<const float*>(a.kc);
   const float* vc = static_cast<const float*>(a.vc);
 
-  long long ubase = u0;
+  int ubase = u0;
   UnitMeta win = unit_meta(a, ubase + lane, u1, s_pref, s_nk, s_N);
   int cur_seg = -1;
   long long qbase = 0;
@@ -353,8 +365,8 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
 
   auto flush = [&]() {
     const int b = cur_seg / a.Hkv, g = cur_seg % a.Hkv;
-    const long long seg_start = s_pref[b] + static_cast<long long>(g) * s_nk[b];
-    const long long seg_end = seg_start + s_nk[b];
+    const int seg_start = s_pref[b] + g * s_nk[b];
+    const int seg_end = seg_start + s_nk[b];
     const bool whole = seg_start >= u0 && seg_end <= u1;
     const long long slot = static_cast<long long>(w) + cur_seg;
 #pragma unroll
@@ -378,7 +390,7 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
     }
   };
 
-  for (long long u = u0; u < u1; ++u) {
+  for (int u = u0; u < u1; ++u) {
     int i = static_cast<int>(u - ubase);
     if (i == kWindow) {
       ubase = u;
@@ -469,7 +481,7 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int seg) {
   int* s_nk = s_mem + a.B + 1;
   int* s_N = s_nk + a.B;
   build_plan(a, s_pref, s_nk, s_N, s_red);
-  const long long U = s_pref[a.B];
+  const int U = s_pref[a.B];
   const int t = threadIdx.x;
   const int b = seg / a.Hkv, g = seg % a.Hkv;
   const int G = a.G;
@@ -484,7 +496,7 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int seg) {
     }
     return;
   }
-  const long long seg_start = s_pref[b] + static_cast<long long>(g) * nk;
+  const int seg_start = s_pref[b] + g * nk;
   const int w0 = wave_of(seg_start, U, a.W);
   const int w1 = wave_of(seg_start + nk - 1, U, a.W);
   if (w0 == w1) return;                      // written whole by the decode kernel

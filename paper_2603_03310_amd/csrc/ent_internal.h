@@ -28,6 +28,7 @@ struct ent_ctx {
   int chunks = 0;           // entropy chunks per logit row
   int lse_chunks = 0;       // log-sum-exp partials per sequence (finest chunking)
   int decode_grid = 0;      // persistent decode workgroups
+  int prologue_grid = 0;    // persistent entropy / scoring workgroups
 
   void* ws = nullptr;       // one workspace allocation
   size_t ws_bytes = 0;
@@ -58,6 +59,34 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
                                const int* tables, const int* ctx_lens, const float* h,
                                int* kept, int* n_kept, float* scores, float* theta,
                                hipStream_t s);
+// The persistent pass over logits and block summaries that opens a step:
+// entropy chunk triples / row statistics (do_entropy) and block scoring of
+// bf16 queries (do_score), in one grid.
+struct PrologueArgs {
+  int B;
+  int do_entropy;
+  const float* logits;
+  long long ld;
+  int V, C;
+  const float* temp;
+  float* part;          // chunk triples (nullable)
+  float* row_stats;     // chunk (max, sum) (nullable)
+  int do_score;
+  const uint16_t* q;
+  const float* ksum;
+  const int* tables;
+  const int* ctx_lens;
+  float* zbuf;
+  float* lse_part;
+  int Hkv, G, MAXB, P, nch_max;
+  float scale;
+  unsigned* flags;
+};
+hipError_t launch_prologue(const ent_ctx* c, const PrologueArgs& a, hipStream_t s);
+int prologue_grid_size(const ent_ctx* c);
+hipError_t launch_score_valu(const ent_ctx* c, int B, const void* q, const float* ksum,
+                             const int* tables, const int* ctx_lens, hipStream_t s);
+
 // Sampling issued in the launch that merges the decode partials (the fused
 // step); the arguments of ent_sample.
 struct SampleArgs {

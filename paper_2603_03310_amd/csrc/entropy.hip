@@ -1,18 +1,11 @@
 // Per-stage kernels of the entropy / controller and sampling entry points
-// (device bodies and their description in entropy_dev.h).
+// (device bodies and their description in entropy_dev.h; the chunk passes run
+// in the persistent kernel of prologue.hip).
 
 #include "entropy_dev.h"
 
 namespace ent {
 namespace {
-
-template <bool VEC>
-__global__ __launch_bounds__(kChunkThreads) void entropy_chunk_kernel(
-    const float* __restrict__ logits, long long ld, int V, int C, const float* __restrict__ temp,
-    float* __restrict__ part, float* __restrict__ row_stats) {
-  __shared__ float red[16];
-  entropy_chunk_body<VEC>(logits, ld, V, C, temp, part, row_stats, blockIdx.x, blockIdx.y, red);
-}
 
 // One wave per row: merge of the row's chunk triples, then the controller.
 __global__ __launch_bounds__(256) void entropy_finalize_kernel(
@@ -44,15 +37,23 @@ hipError_t launch_entropy(const ent_ctx* c, int B, const float* logits, long lon
                           ent_state st, float* h_out, float* temp_used, float* row_stats,
                           bool controller, hipStream_t s) {
   const ent_config& cf = c->cfg;
-  const dim3 grid(c->chunks, B);
-  const bool vec = row_vec_ok(logits, ld);
-  auto k = vec ? entropy_chunk_kernel<true> : entropy_chunk_kernel<false>;
   // Without the controller (statistics for the sampler) the temperatures are
   // the ones passed in temp_used.
-  const float* T = controller ? st.temp : temp_used;
-  hipLaunchKernelGGL(k, grid, dim3(kChunkThreads), 0, s, logits, ld, cf.vocab, c->chunks, T,
-                     controller ? c->ent_part : nullptr, row_stats);
-  hipError_t e = hipGetLastError();
+  PrologueArgs a{};
+  a.B = B;
+  a.do_entropy = 1;
+  a.logits = logits;
+  a.ld = ld;
+  a.V = cf.vocab;
+  a.C = c->chunks;
+  a.temp = controller ? st.temp : temp_used;
+  a.part = controller ? c->ent_part : nullptr;
+  a.row_stats = row_stats;
+  a.Hkv = cf.num_kv_heads;
+  a.G = c->group;
+  a.MAXB = cf.max_blocks_per_seq;
+  a.flags = c->dev_flags;
+  hipError_t e = launch_prologue(c, a, s);
   if (e != hipSuccess || !controller) return e;
   hipLaunchKernelGGL(entropy_finalize_kernel, dim3((B + 3) / 4), dim3(256), 0, s, B, c->chunks,
                      c->ent_part, st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta,

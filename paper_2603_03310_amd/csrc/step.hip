@@ -3,10 +3,10 @@
 // bit-identical to calling ent_entropy_temperature, ent_block_select,
 // ent_sparse_paged_decode and ent_sample in sequence:
 //
-//   A  block scoring and the entropy chunk passes, as disjoint workgroup
-//      ranges of one grid (scoring first: its workgroups run longer): both
-//      stream from HBM (block summaries, logits) and do not depend on each
-//      other, so one launch overlaps them;
+//   A  block scoring and the entropy chunk passes in one persistent grid
+//      (prologue.hip): both stream from HBM (block summaries, logits) and
+//      do not depend on each other (fp32 queries: scoring is a second
+//      launch, on the VALU);
 //   B  one workgroup per sequence: the row's entropy from the chunk triples,
 //      the controller update, and the kept-block selection under the
 //      entropy-driven budget;
@@ -19,42 +19,6 @@
 
 namespace ent {
 namespace {
-
-template <bool VEC, int D>
-__global__ __launch_bounds__(kChunkThreads) void step_a_mfma_kernel(
-    const float* __restrict__ logits, long long ld, int V, int C, const float* __restrict__ temp,
-    float* __restrict__ part, float* __restrict__ row_stats, const uint16_t* __restrict__ q,
-    const float* __restrict__ ksum, const int* __restrict__ tables,
-    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
-    int B, int Hkv, int G, int MAXB, int P, int nch_max, int nsc, float scale, unsigned* flags) {
-  __shared__ float red[16];
-  const int id = blockIdx.x;
-  if (id < nsc * B) {
-    score_mfma_body<D>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, G, MAXB, P, nch_max,
-                       scale, flags, id % nsc, id / nsc);
-    return;
-  }
-  const int eid = id - nsc * B;
-  entropy_chunk_body<VEC>(logits, ld, V, C, temp, part, row_stats, eid % C, eid / C, red);
-}
-
-template <bool VEC, int D, int G>
-__global__ __launch_bounds__(kChunkThreads) void step_a_valu_kernel(
-    const float* __restrict__ logits, long long ld, int V, int C, const float* __restrict__ temp,
-    float* __restrict__ part, float* __restrict__ row_stats, const float* __restrict__ q,
-    const float* __restrict__ ksum, const int* __restrict__ tables,
-    const int* __restrict__ ctx_lens, float* __restrict__ zbuf, float* __restrict__ lse_part,
-    int B, int Hkv, int MAXB, int P, int nch_max, int nsc, float scale, unsigned* flags) {
-  extern __shared__ float smem[];
-  const int id = blockIdx.x;
-  if (id < nsc * B) {
-    score_valu_body<D, G>(q, ksum, tables, ctx_lens, zbuf, lse_part, Hkv, MAXB, P, nch_max,
-                          scale, flags, id % nsc, id / nsc, smem);
-    return;
-  }
-  const int eid = id - nsc * B;
-  entropy_chunk_body<VEC>(logits, ld, V, C, temp, part, row_stats, eid % C, eid / C, smem);
-}
 
 struct StepBArgs {
   const float* part;
@@ -99,46 +63,6 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(StepBArgs a) {
               a.flags, b, keys, ssh);
 }
 
-template <bool VEC, int D>
-hipError_t launch_step_a(const ent_ctx* c, int B, const float* logits, long long ld,
-                         const float* temp, float* row_stats, const void* q, const float* ksum,
-                         const int* tables, const int* ctx_lens, hipStream_t s) {
-  const ent_config& cf = c->cfg;
-  const int Hq = cf.num_q_heads;
-  if (cf.kv_dtype == ENT_BF16) {
-    const int nsc = (cf.max_blocks_per_seq + kMfmaChunk - 1) / kMfmaChunk;
-    hipLaunchKernelGGL((step_a_mfma_kernel<VEC, D>), dim3(c->chunks * B + nsc * B),
-                       dim3(kChunkThreads), 0, s, logits, ld, cf.vocab, c->chunks, temp,
-                       c->ent_part, row_stats, static_cast<const uint16_t*>(q), ksum, tables,
-                       ctx_lens, c->zbuf, c->lse_part, B, cf.num_kv_heads, c->group,
-                       cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, nsc, cf.scale,
-                       c->dev_flags);
-    return hipGetLastError();
-  }
-  const int nsc = (cf.max_blocks_per_seq + kValuChunk - 1) / kValuChunk;
-  const size_t lds = (static_cast<size_t>(Hq) * D + static_cast<size_t>(kValuChunk) * Hq) * sizeof(float);
-  const float* qq = static_cast<const float*>(q);
-#define ENT_STEPA_CASE(GG)                                                                     \
-  case GG:                                                                                     \
-    hipLaunchKernelGGL((step_a_valu_kernel<VEC, D, GG>), dim3(c->chunks * B + nsc * B),        \
-                       dim3(kChunkThreads), lds, s, logits, ld, cf.vocab, c->chunks, temp,     \
-                       c->ent_part, row_stats, qq, ksum, tables, ctx_lens, c->zbuf,            \
-                       c->lse_part, B, cf.num_kv_heads, cf.max_blocks_per_seq,                 \
-                       cf.num_pool_blocks, c->lse_chunks, nsc, cf.scale, c->dev_flags);        \
-    break;
-  switch (c->group) {
-    ENT_STEPA_CASE(1)
-    ENT_STEPA_CASE(2)
-    ENT_STEPA_CASE(4)
-    ENT_STEPA_CASE(8)
-    ENT_STEPA_CASE(16)
-    default:
-      return hipErrorInvalidValue;
-  }
-#undef ENT_STEPA_CASE
-  return hipGetLastError();
-}
-
 }  // namespace
 
 hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
@@ -150,15 +74,37 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
                               hipStream_t s) {
   const ent_config& cf = c->cfg;
   float* stats = row_stats ? row_stats : c->stats_tmp;
-  const bool vec = row_vec_ok(logits, ld);
-  hipError_t e;
-  if (cf.head_dim == 128)
-    e = vec ? launch_step_a<true, 128>(c, B, logits, ld, st.temp, stats, q, ksum, tables, ctx_lens, s)
-            : launch_step_a<false, 128>(c, B, logits, ld, st.temp, stats, q, ksum, tables, ctx_lens, s);
-  else
-    e = vec ? launch_step_a<true, 64>(c, B, logits, ld, st.temp, stats, q, ksum, tables, ctx_lens, s)
-            : launch_step_a<false, 64>(c, B, logits, ld, st.temp, stats, q, ksum, tables, ctx_lens, s);
+  const bool bf16 = cf.kv_dtype == ENT_BF16;
+  PrologueArgs pa{};
+  pa.B = B;
+  pa.do_entropy = 1;
+  pa.logits = logits;
+  pa.ld = ld;
+  pa.V = cf.vocab;
+  pa.C = c->chunks;
+  pa.temp = st.temp;
+  pa.part = c->ent_part;
+  pa.row_stats = stats;
+  pa.do_score = bf16 ? 1 : 0;
+  pa.q = static_cast<const uint16_t*>(q);
+  pa.ksum = ksum;
+  pa.tables = tables;
+  pa.ctx_lens = ctx_lens;
+  pa.zbuf = c->zbuf;
+  pa.lse_part = c->lse_part;
+  pa.Hkv = cf.num_kv_heads;
+  pa.G = c->group;
+  pa.MAXB = cf.max_blocks_per_seq;
+  pa.P = cf.num_pool_blocks;
+  pa.nch_max = c->lse_chunks;
+  pa.scale = cf.scale;
+  pa.flags = c->dev_flags;
+  hipError_t e = launch_prologue(c, pa, s);
   if (e != hipSuccess) return e;
+  if (!bf16) {
+    e = launch_score_valu(c, B, q, ksum, tables, ctx_lens, s);
+    if (e != hipSuccess) return e;
+  }
 
   StepBArgs a;
   a.part = c->ent_part;
