@@ -33,7 +33,17 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 METRIC = "decode steps/sec and achieved HBM GB/s (kept KV + logits) vs peak, 1 MI355X"
 COUNTERS = os.path.join(ROOT, "profiles", "decode_counters.json")
-DECODE_SRC = os.path.join(ROOT, "paper_2603_03310_amd", "csrc", "decode.hip")
+# Sources of the decode entry point's kernels (attention and segment merge).
+DECODE_SRCS = [os.path.join(ROOT, "paper_2603_03310_amd", "csrc", f)
+               for f in ("decode.hip", "ent_internal.h")]
+
+
+def decode_src_digest() -> str:
+    h = hashlib.sha256()
+    for f in DECODE_SRCS:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def parse():
@@ -96,8 +106,7 @@ def traffic_from_counters():
         return None
     with open(COUNTERS) as f:
         c = json.load(f)
-    src = hashlib.sha256(open(DECODE_SRC, "rb").read()).hexdigest()
-    if c.get("decode_src_sha256") != src:
+    if c.get("decode_src_sha256") != decode_src_digest():
         return None
     return c.get("hbm_bytes_per_launch")
 
