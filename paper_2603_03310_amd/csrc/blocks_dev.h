@@ -33,7 +33,7 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p) { return
 // and, per chunk of blocks and head, the log-sum-exp partial (max, sum) of
 // l_bh = z_bh + ln n_b over the chunk's blocks.
 //
-// bf16 queries (MFMA).  A wave takes a tile of 16 blocks and two KV heads.
+// bf16 queries (MFMA).  A wave takes a tile of 16 blocks and one KV head.
 // For each KV head g the tile's logits are one small contraction
 //   Z[16 blocks x 16] = Kbar_g[16 x d] . Q_g^T[d x 16]   (columns: the G query
 // heads of g, zero-padded), on v_mfma_f32_16x16x32_bf16.  The fp32 summaries
@@ -77,10 +77,9 @@ __device__ __forceinline__ void chunk_lse(const float* zt, int nblk, int Hq, int
 }
 
 // One scoring item: a tile of kMfmaChunk = 16 blocks of sequence b (tile
-// ch) and up to two KV heads g0, g0 + 1, by one wave.  The item's summaries
-// (16 blocks x 2 heads x d fp32) are loaded first (score_pair_load), so that
-// a wave can have the next item's loads in flight while it computes one.
-constexpr int kScorePairSlots = 16;     // float4 slots per lane (d <= 128)
+// ch) and one KV head g, by one wave: the summaries (16 blocks x d fp32) are
+// loaded with score_head_load and reduced with score_head_compute.
+constexpr int kScoreSlots = 8;          // float4 slots per lane (d <= 128)
 
 // Physical block of tile row r16 (lane & 15), validated; 0 for rows past the
 // sequence's nb blocks.
@@ -97,25 +96,18 @@ __device__ __forceinline__ int score_tile_block(const int* __restrict__ tables, 
   return p;
 }
 
-// Lane (r16, gq) loads, for head g0 + h of block row r16, the float4 slots
+// Lane (r16, gq) loads, for head g of block row r16, the float4 slots
 // j = 0 .. D/16 - 1 at dims 16 j + 4 gq .. +3 (the four lanes of a row read
-// 64 contiguous bytes per slot) into buf[h D/16 + j].
+// 64 contiguous bytes per slot).
 template <int D>
-__device__ __forceinline__ void score_pair_load(const float* __restrict__ ksum, int p, int Hkv,
-                                                int g0, int ng,
-                                                float4 (&buf)[kScorePairSlots]) {
+__device__ __forceinline__ void score_head_load(const float* __restrict__ ksum, int p, int Hkv,
+                                                int g, float4 (&buf)[kScoreSlots]) {
   constexpr int NJ = D / 16;
-  static_assert(2 * NJ <= kScorePairSlots, "slots");
+  static_assert(NJ <= kScoreSlots, "slots");
   const int gq = (threadIdx.x & 63) >> 4;
-  const float* src = ksum + (static_cast<long long>(p) * Hkv + g0) * D + gq * 4;
+  const float* src = ksum + (static_cast<long long>(p) * Hkv + g) * D + gq * 4;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    if (h < ng) {
-#pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        buf[h * NJ + j] = *reinterpret_cast<const float4*>(src + h * D + 16 * j);
-    }
-  }
+  for (int j = 0; j < NJ; ++j) buf[j] = *reinterpret_cast<const float4*>(src + 16 * j);
 }
 
 typedef float sf32x2_t __attribute__((ext_vector_type(2)));
@@ -143,80 +135,66 @@ __device__ __forceinline__ void split3(const float4& x0, const float4& x1, sbf16
   lo = sbf16x8_t{l[0].x, l[0].y, l[1].x, l[1].y, l[2].x, l[2].y, l[3].x, l[3].y};
 }
 
-// Block logits z of the item's heads (written to zbuf) and each head's
-// log-sum-exp partial (max, sum) of z + ln n_b over the tile (lse_part).
-// z[16 blocks x 16] = Kbar_g[16 x d] Q_g^T[d x 16] on
+// Block logits z of head g's query heads (written to zbuf) and each query
+// head's log-sum-exp partial (max, sum) of z + ln n_b over the tile
+// (lse_part).  z[16 blocks x 16] = Kbar_g[16 x d] Q_g^T[d x 16] on
 // v_mfma_f32_16x16x32_bf16 (columns: the G query heads of g, zero-padded),
 // three MFMAs per k-step over the exact split of the fp32 summaries, so
 // every product is exact and only the fp32 accumulation rounds.  K-slot
 // (gq, e) of step ks is dim 32 ks + 4 gq + e for e < 4 and
 // 32 ks + 16 + 4 gq + (e - 4) for e >= 4, in both operands.
 template <int D>
-__device__ __forceinline__ void score_pair_compute(
-    const uint16_t* __restrict__ q, const float4 (&buf)[kScorePairSlots],
-    float* __restrict__ zbuf, float* __restrict__ lse_part, int b, int ch, int g0, int ng,
-    int N, int nb, int Hkv, int G, int MAXB, int nch_max, float scale) {
-  constexpr int NJ = D / 16;
+__device__ __forceinline__ void score_head_compute(
+    const uint16_t* __restrict__ q, const float4 (&buf)[kScoreSlots],
+    float* __restrict__ zbuf, float* __restrict__ lse_part, int b, int ch, int g, int N, int nb,
+    int Hkv, int G, int MAXB, int nch_max, float scale) {
   constexpr int KS = D / 32;
   const int Hq = Hkv * G;
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, gq = lane >> 4;
   const int jt = ch * kMfmaChunk;
+  const uint16_t* qh = q + (static_cast<long long>(b) * Hq + g * G + r16) * D + gq * 4;
+  sf32x4_t acc = sf32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    uint2 q0 = make_uint2(0u, 0u), q1 = make_uint2(0u, 0u);
+    if (r16 < G) {
+      q0 = *reinterpret_cast<const uint2*>(qh + 32 * ks);
+      q1 = *reinterpret_cast<const uint2*>(qh + 32 * ks + 16);
+    }
+    sbf16x8_t hi, mid, lo;
+    split3(buf[2 * ks], buf[2 * ks + 1], hi, mid, lo);
+    const sbf16x8_t bq = __builtin_bit_cast(sbf16x8_t, make_uint4(q0.x, q0.y, q1.x, q1.y));
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mid, bq, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, bq, acc, 0, 0, 0);
+  }
+  // acc[e]: block jt + 4 gq + e, query head g G + r16 (columns r16 >= G are padding).
   const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
   const float ln_full = logf(static_cast<float>(kBlock));
-  const uint16_t* qrow = q + static_cast<long long>(b) * Hq * D + gq * 4;
   float* zrow = zbuf + (static_cast<long long>(b) * MAXB + jt) * Hq;
-  float* lp = lse_part + (static_cast<long long>(b) * nch_max + ch) * Hq * 2;
-  // Query operands of both heads first: their latency overlaps the splits.
-  uint2 qv[2][2 * KS];
+  float l[4];
+  float m = -INFINITY;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const uint16_t* qh = qrow + static_cast<long long>((g0 + h) * G + r16) * D;
-#pragma unroll
-    for (int j = 0; j < 2 * KS; ++j) {
-      qv[h][j] = make_uint2(0u, 0u);
-      if (h < ng && r16 < G) qv[h][j] = *reinterpret_cast<const uint2*>(qh + 16 * j);
-    }
+  for (int e = 0; e < 4; ++e) {
+    const int j = jt + 4 * gq + e;
+    const float z = acc[e] * scale;
+    const bool ok = j < nb;
+    if (ok && r16 < G) zrow[(4 * gq + e) * Hq + g * G + r16] = z;
+    l[e] = ok ? z + ((j == nb - 1) ? ln_last : ln_full) : -INFINITY;
+    m = fmaxf(m, l[e]);
   }
+  m = fmaxf(m, __shfl_xor(m, 16));
+  m = fmaxf(m, __shfl_xor(m, 32));
+  float sum = 0.f;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    if (h >= ng) break;
-    const int g = g0 + h;
-    sf32x4_t acc = sf32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      sbf16x8_t hi, mid, lo;
-      split3(buf[h * NJ + 2 * ks], buf[h * NJ + 2 * ks + 1], hi, mid, lo);
-      const uint4 qb = make_uint4(qv[h][2 * ks].x, qv[h][2 * ks].y, qv[h][2 * ks + 1].x,
-                                  qv[h][2 * ks + 1].y);
-      const sbf16x8_t bq = __builtin_bit_cast(sbf16x8_t, qb);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mid, bq, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, bq, acc, 0, 0, 0);
-    }
-    // acc[e]: block jt + 4 gq + e, query head g G + r16 (columns r16 >= G are padding).
-    float l[4];
-    float m = -INFINITY;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int j = jt + 4 * gq + e;
-      const float z = acc[e] * scale;
-      const bool ok = j < nb;
-      if (ok && r16 < G) zrow[(4 * gq + e) * Hq + g * G + r16] = z;
-      l[e] = ok ? z + ((j == nb - 1) ? ln_last : ln_full) : -INFINITY;
-      m = fmaxf(m, l[e]);
-    }
-    m = fmaxf(m, __shfl_xor(m, 16));
-    m = fmaxf(m, __shfl_xor(m, 32));
-    float sum = 0.f;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) sum += (l[e] == -INFINITY) ? 0.f : expf(l[e] - m);
-    sum += __shfl_xor(sum, 16);
-    sum += __shfl_xor(sum, 32);
-    if (gq == 0 && r16 < G) {
-      lp[(g * G + r16) * 2 + 0] = m;
-      lp[(g * G + r16) * 2 + 1] = sum;
-    }
+  for (int e = 0; e < 4; ++e) sum += (l[e] == -INFINITY) ? 0.f : expf(l[e] - m);
+  sum += __shfl_xor(sum, 16);
+  sum += __shfl_xor(sum, 32);
+  if (gq == 0 && r16 < G) {
+    float* lp = lse_part + ((static_cast<long long>(b) * nch_max + ch) * Hq + g * G + r16) * 2;
+    lp[0] = m;
+    lp[1] = sum;
   }
 }
 

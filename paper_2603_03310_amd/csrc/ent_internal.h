@@ -28,7 +28,6 @@ struct ent_ctx {
   int chunks = 0;           // entropy chunks per logit row
   int lse_chunks = 0;       // log-sum-exp partials per sequence (finest chunking)
   int decode_grid = 0;      // persistent decode workgroups
-  int prologue_grid = 0;    // persistent entropy / scoring workgroups
 
   void* ws = nullptr;       // one workspace allocation
   size_t ws_bytes = 0;
@@ -59,7 +58,7 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
                                const int* tables, const int* ctx_lens, const float* h,
                                int* kept, int* n_kept, float* scores, float* theta,
                                hipStream_t s);
-// The persistent pass over logits and block summaries that opens a step:
+// The pass over logits and block summaries that opens a step:
 // entropy chunk triples / row statistics (do_entropy) and block scoring of
 // bf16 queries (do_score), in one grid.
 struct PrologueArgs {
@@ -83,7 +82,6 @@ struct PrologueArgs {
   unsigned* flags;
 };
 hipError_t launch_prologue(const ent_ctx* c, const PrologueArgs& a, hipStream_t s);
-int prologue_grid_size(const ent_ctx* c);
 hipError_t launch_score_valu(const ent_ctx* c, int B, const void* q, const float* ksum,
                              const int* tables, const int* ctx_lens, hipStream_t s);
 

@@ -4,8 +4,8 @@
 //
 // Entropy (Section 2 and Section 2.1 of the paper): H = -sum_x p(x) ln p(x)
 // with p = softmax(z / T).  One pass over each logit row: the row is cut into
-// chunks of ENT_ROW_CHUNK logits, one wave per (row, chunk); each lane holds
-// 64 logits in registers, so the chunk's maximum and the sums
+// chunks of ENT_ROW_CHUNK logits, one 256-thread workgroup per (chunk, row);
+// each thread holds 16 logits in registers, so the chunk's maximum and the sums
 //   S = sum 2^(t - M),  W = sum 2^(t - M) (t - M)   (t = z log2(e) / T)
 // come from one read of HBM.  One wave per row then merges the chunk triples:
 //   H = ln 2 (log2 S - W / S)
@@ -60,56 +60,53 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return r;
 }
 
-// Chunk pass by one wave: the 4096 logits of chunk c of a row, 64 per lane
-// in 16 float4 slots; slot i of lane l holds positions
-// c*4096 + (64 i + l)*4 + {0..3} (coalesced 1 KB per slot).  Positions past
-// the vocabulary read as -inf (zero probability).
-constexpr int kWaveSlots = kRowChunk / (64 * 4);
-static_assert(kWaveSlots == 16, "chunk layout");
-
+// The thread's 16 logits of chunk c, scaled to log2 units: t = z * c2.
+// Positions past the vocabulary read as -inf (zero probability).
 template <bool VEC>
-__device__ __forceinline__ void chunk_load_wave(const float* __restrict__ row, int V, int c,
-                                                float4 (&buf)[kWaveSlots]) {
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ void load_chunk(const float* __restrict__ row, int V, int c,
+                                           float c2, float (&v)[kPerThread]) {
   const int base = c * kRowChunk;
+  if (VEC && base + kRowChunk <= V) {
 #pragma unroll
-  for (int i = 0; i < kWaveSlots; ++i) {
-    const int idx = base + (64 * i + lane) * 4;
-    if (VEC && idx + 3 < V) {
-      buf[i] = *reinterpret_cast<const float4*>(row + idx);
-    } else {
-      buf[i].x = idx + 0 < V ? row[idx + 0] : -INFINITY;
-      buf[i].y = idx + 1 < V ? row[idx + 1] : -INFINITY;
-      buf[i].z = idx + 2 < V ? row[idx + 2] : -INFINITY;
-      buf[i].w = idx + 3 < V ? row[idx + 3] : -INFINITY;
+    for (int i = 0; i < 4; ++i) {
+      const float4 x = *reinterpret_cast<const float4*>(row + base + (i * kChunkThreads + threadIdx.x) * 4);
+      v[4 * i + 0] = x.x * c2;
+      v[4 * i + 1] = x.y * c2;
+      v[4 * i + 2] = x.z * c2;
+      v[4 * i + 3] = x.w * c2;
     }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int idx = base + (i * kChunkThreads + threadIdx.x) * 4 + k;
+        v[4 * i + k] = idx < V ? row[idx] * c2 : -INFINITY;
+      }
   }
 }
 
-// Reduction of one loaded chunk at temperature T: with t = z log2(e) / T,
-// M = max t, S = sum 2^(t - M), W = sum 2^(t - M) (t - M).  Writes (M, S, W)
-// to part[o] (when non-null) and (M, S) to row_stats[o] (when non-null), o
-// the (row, chunk) index.  Every lane of the wave calls it.
-__device__ __forceinline__ void chunk_reduce_wave(const float4 (&buf)[kWaveSlots], float T,
-                                                  float* __restrict__ part,
-                                                  float* __restrict__ row_stats, long long o) {
+// Chunk pass of (chunk c, row b) by a 256-thread workgroup: writes the triple
+// (M, S, W) to part (when non-null) and (M, S) to row_stats (when non-null).
+template <bool VEC>
+__device__ __forceinline__ void entropy_chunk_body(const float* __restrict__ logits, long long ld,
+                                                   int V, int C, const float* __restrict__ temp,
+                                                   float* __restrict__ part,
+                                                   float* __restrict__ row_stats, int c, int b,
+                                                   float* red) {
+  const float T = temp[b];
   const float c2 = __fdiv_rn(kLog2e, T);
-  float v[4 * kWaveSlots];
-#pragma unroll
-  for (int i = 0; i < kWaveSlots; ++i) {
-    v[4 * i + 0] = buf[i].x * c2;
-    v[4 * i + 1] = buf[i].y * c2;
-    v[4 * i + 2] = buf[i].z * c2;
-    v[4 * i + 3] = buf[i].w * c2;
-  }
+  const float* row = logits + static_cast<long long>(b) * ld;
+  float v[kPerThread];
+  load_chunk<VEC>(row, V, c, c2, v);
   float m = v[0];
 #pragma unroll
-  for (int i = 1; i < 4 * kWaveSlots; ++i) m = fmaxf(m, v[i]);
-  const float M = wave_max(m);
+  for (int i = 1; i < kPerThread; ++i) m = fmaxf(m, v[i]);
+  const float M = block_max<kChunkThreads>(m, red);
   float S = 0.f, W = 0.f;
   if (M != -INFINITY) {
 #pragma unroll
-    for (int i = 0; i < 4 * kWaveSlots; ++i) {
+    for (int i = 0; i < kPerThread; ++i) {
       // d <= 0: the hardware exp2 (no denormal-range fix-up; terms below
       // 2^-126 of the chunk maximum do not change S or W).
       const float d = v[i] - M;
@@ -118,9 +115,10 @@ __device__ __forceinline__ void chunk_reduce_wave(const float4 (&buf)[kWaveSlots
       W += (e > 0.f) ? e * d : 0.f;
     }
   }
-  S = wave_sum(S);
-  W = wave_sum(W);
-  if ((threadIdx.x & 63) == 0) {
+  S = block_sum<kChunkThreads>(S, red);
+  W = block_sum<kChunkThreads>(W, red);
+  if (threadIdx.x == 0) {
+    const long long o = static_cast<long long>(b) * C + c;
     if (row_stats) {
       row_stats[2 * o + 0] = M;
       row_stats[2 * o + 1] = S;
