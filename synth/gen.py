@@ -129,7 +129,7 @@ def generate(w: Workload, seed: Optional[int] = None, ctx_lens=None) -> Inputs:
     scales = g.uniform(w.logit_scale[0], w.logit_scale[1], size=B)
     h_prev = g.uniform(0.0, math.log(V), size=B).astype(np.float32)
     uniforms = g.random(size=(S, B), dtype=np.float32)
-    appended = S - 1 if S > 1 else 0
+    appended = S if S > 1 else 0            # every step of a closed loop appends its token
     nb_alloc = (ctx.astype(np.int64) + appended + bs - 1) // bs
     P = int(nb_alloc.sum())
     perm = g.permutation(P).astype(np.int32)

@@ -189,3 +189,57 @@ def test_full_size_llama3_8b_sampled(torch_cuda):
     print(f"[parity] full-size llama3_8b_decode, sampled sequences {seqs}", flush=True)
     reps, dev = _run(torch_cuda, x, default_params(LLAMA3_8B), seqs=seqs)
     _assert_ok(reps)
+
+
+def _sampled(batch, n, seed):
+    rng = np.random.default_rng(seed)
+    return sorted(rng.choice(batch, size=min(n, batch), replace=False).tolist())
+
+
+def test_full_size_long_context_sampled(torch_cuda):
+    """Full long-context step (B=16, N up to 131072): parity on two sampled
+    sequences, and the planted high-similarity run's full blocks outrank the
+    rest: they are kept whenever the budget covers them."""
+    x = generate(LONG_CONTEXT)
+    seqs = _sampled(LONG_CONTEXT.batch, 2, 1)
+    print(f"[parity] full-size long_context, sampled sequences {seqs}", flush=True)
+    reps, dev = _run(torch_cuda, x, default_params(LONG_CONTEXT), seqs=seqs)
+    _assert_ok(reps)
+    scores = dev.scores.cpu().numpy()
+    n_kept = dev.n_kept.cpu().numpy()
+    kept = dev.kept.cpu().numpy()
+    for s in range(LONG_CONTEXT.batch):
+        off = int(x.planted[s])
+        if off < 0:
+            continue
+        full = [j for j in range(-(-off // 16), (off + LONG_CONTEXT.planted_run) // 16)]
+        nb = -(-int(x.ctx_lens[s]) // 16)
+        sc = scores[s, :nb]
+        order = np.argsort(-sc, kind="stable")
+        # The (up to two) partly planted blocks at the run's ends may rank among them.
+        top = len(full) + 2
+        assert set(full) <= set(order[:top].tolist()), f"seq {s}: planted blocks not top-ranked"
+        if int(n_kept[s]) >= top:
+            assert set(full) <= set(kept[s, : int(n_kept[s])].tolist()), f"seq {s}: planted block pruned"
+
+
+def test_full_size_skewed_sampled(torch_cuda):
+    """Full skewed batch (B=256, lognormal contexts, Zipf and flat logit rows)
+    on sampled sequences of both logit kinds."""
+    x = generate(SKEWED)
+    seqs = sorted(set(_sampled(SKEWED.batch, 6, 2)) | {0, 1})
+    print(f"[parity] full-size skewed_mixed, sampled sequences {seqs}", flush=True)
+    reps, _ = _run(torch_cuda, x, default_params(SKEWED), seqs=seqs)
+    _assert_ok(reps)
+
+
+def test_full_size_70b_loop_three_steps(torch_cuda):
+    """70B-shaped batch at full size (B=128, 64/8 heads, N in [4096,16384]):
+    three closed-loop steps with appends, parity on sampled sequences."""
+    w = small(LLAMA70B_LOOP, LLAMA70B_LOOP.batch, steps=3, suffix="full3")
+    x = generate(w)
+    seqs = _sampled(w.batch, 4, 3)
+    print(f"[parity] full-size llama70b shapes, 3 steps, sampled sequences {seqs}", flush=True)
+    reps, dev = _run(torch_cuda, x, default_params(w), steps=3, seqs=seqs)
+    _assert_ok(reps)
+    assert list(dev.ctx_lens.cpu().numpy()) == list(x.ctx_lens + 3)
