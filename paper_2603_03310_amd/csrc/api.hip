@@ -150,12 +150,14 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   const size_t sz_stats = align_up(Bm * c->chunks * 2 * sizeof(float));
   const size_t sz_z = align_up(Bm * f.max_blocks_per_seq * f.num_q_heads * sizeof(float));
   const size_t sz_lse = align_up(Bm * c->lse_chunks * f.num_q_heads * 2 * sizeof(float));
+  const size_t sz_lrow = align_up(Bm * f.num_q_heads * sizeof(float));
+  const size_t sz_isc = align_up(Bm * f.max_blocks_per_seq * sizeof(float));
   const size_t nslots = static_cast<size_t>(
       ent::decode_partial_slots(c->decode_grid, f.max_batch, f.num_kv_heads));
   const size_t sz_acc = align_up(nslots * c->group * f.head_dim * sizeof(float));
   const size_t sz_ml = align_up(nslots * c->group * 2 * sizeof(float));
   const size_t sz_flags = align_up(sizeof(unsigned));
-  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_acc + sz_ml + sz_flags;
+  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_lrow + sz_isc + sz_acc + sz_ml + sz_flags;
   e = hipMalloc(&c->ws, c->ws_bytes);
   if (e != hipSuccess) {
     g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
@@ -176,6 +178,8 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->stats_tmp = reinterpret_cast<float*>(take(sz_stats));
   c->zbuf = reinterpret_cast<float*>(take(sz_z));
   c->lse_part = reinterpret_cast<float*>(take(sz_lse));
+  c->lrow = reinterpret_cast<float*>(take(sz_lrow));
+  c->iscores = reinterpret_cast<float*>(take(sz_isc));
   c->dec_acc = reinterpret_cast<float*>(take(sz_acc));
   c->dec_ml = reinterpret_cast<float*>(take(sz_ml));
   c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));

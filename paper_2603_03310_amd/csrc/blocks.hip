@@ -14,9 +14,9 @@
 //   summary_kernel   per-block mean keys (setup)
 //   (bf16 scoring runs in the persistent kernel of prologue.hip)
 //   score_valu_kernel   z for 16 blocks x all heads per workgroup (fp32, VALU)
-//   select_kernel       per sequence: merges the per-chunk log-sum-exp
-//                       partials into L_h, computes
-//                       I_b, the budget, a 4-pass 8-bit radix select of the
+//   lse_merge_kernel    per sequence: L_h from the per-tile log-sum-exp partials
+//   block_score_kernel  per 64 blocks: I_b
+//   select_kernel       per sequence: the budget, an 8-bit radix select of the
 //                       k-th largest score, ascending compaction with ballots
 //   append_kernel    writes one token and refreshes its block's mean key
 
@@ -107,17 +107,30 @@ __global__ __launch_bounds__(kScoreThreads) void score_valu_kernel(
                         flags, blockIdx.x, blockIdx.y, smem);
 }
 
+__global__ __launch_bounds__(kRowThreads) void lse_merge_kernel(
+    const float* __restrict__ lse_part, const int* __restrict__ ctx_lens, float* __restrict__ L,
+    int Hq, int MAXB, int nch_max) {
+  __shared__ float s_pm[kRowThreads], s_ps[kRowThreads];
+  lse_merge_body(lse_part, ctx_lens, L, Hq, MAXB, nch_max, blockIdx.x, s_pm, s_ps);
+}
+
+__global__ __launch_bounds__(kRowThreads) void block_score_kernel(
+    const float* __restrict__ zbuf, const float* __restrict__ L, const int* __restrict__ ctx_lens,
+    float* __restrict__ scores, int Hq, int MAXB) {
+  __shared__ float sL[128];
+  block_score_body(zbuf, L, ctx_lens, scores, Hq, MAXB, blockIdx.y, blockIdx.x * kTileBlocks, sL);
+}
+
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
-    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, const float* __restrict__ hvec,
-    float* __restrict__ scores_out, float* __restrict__ theta_out, int* __restrict__ kept,
-    int* __restrict__ n_kept, int Hq, int MAXB, int chunk, int nch_max, float eps_h, float h_min,
-    float log_v, float kappa_min, int b_min, unsigned* flags) {
+    const float* __restrict__ scores, const int* __restrict__ ctx_lens,
+    const float* __restrict__ hvec, float* __restrict__ theta_out, int* __restrict__ kept,
+    int* __restrict__ n_kept, int MAXB, float eps_h, float h_min, float log_v, float kappa_min,
+    int b_min, unsigned* flags) {
   extern __shared__ unsigned keys[];        // [MAXB]
   __shared__ SelectShared sh;
   const int b = blockIdx.x;
-  select_body(zbuf, lse_part, ctx_lens, hvec[b], scores_out, theta_out, kept, n_kept, Hq, MAXB,
-              chunk, nch_max, eps_h, h_min, log_v, kappa_min, b_min, flags, b, keys, sh);
+  select_row_body(scores, ctx_lens, hvec[b], theta_out, kept, n_kept, MAXB, eps_h, h_min, log_v,
+                  kappa_min, b_min, flags, b, keys, sh);
 }
 
 template <int D>
@@ -200,11 +213,32 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
     e = launch_score_valu(c, B, q, ksum, tables, ctx_lens, s);
   }
   if (e != hipSuccess) return e;
-  const int chunk = cf.kv_dtype == ENT_BF16 ? kMfmaChunk : kValuChunk;
+  hipLaunchKernelGGL(lse_merge_kernel, dim3(B), dim3(kRowThreads), 0, s, c->lse_part, ctx_lens,
+                     c->lrow, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  float* sc = scores ? scores : c->iscores;
+  e = launch_block_scores(c, B, ctx_lens, sc, s);
+  if (e != hipSuccess) return e;
+  return launch_select_rows(c, B, ctx_lens, h, sc, theta, kept, n_kept, s);
+}
+
+hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,
+                               hipStream_t s) {
+  const ent_config& cf = c->cfg;
+  const dim3 grid((cf.max_blocks_per_seq + kTileBlocks - 1) / kTileBlocks, B);
+  hipLaunchKernelGGL(block_score_kernel, grid, dim3(kRowThreads), 0, s, c->zbuf, c->lrow, ctx_lens,
+                     scores, cf.num_q_heads, cf.max_blocks_per_seq);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_rows(const ent_ctx* c, int B, const int* ctx_lens, const float* h,
+                              const float* scores, float* theta, int* kept, int* n_kept,
+                              hipStream_t s) {
+  const ent_config& cf = c->cfg;
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelThreads), lds, s, c->zbuf, c->lse_part,
-                     ctx_lens, h, scores, theta, kept, n_kept, cf.num_q_heads,
-                     cf.max_blocks_per_seq, chunk, c->lse_chunks, cf.eps_h, cf.h_min, cf.log_v,
+  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelThreads), lds, s, scores, ctx_lens, h, theta,
+                     kept, n_kept, cf.max_blocks_per_seq, cf.eps_h, cf.h_min, cf.log_v,
                      cf.kappa_min, cf.b_min, c->dev_flags);
   return hipGetLastError();
 }

@@ -51,6 +51,7 @@ constexpr int kScoreWaves = kScoreThreads / 64;
 constexpr int kMfmaChunk = 16;                 // blocks per MFMA scoring workgroup
 constexpr int kValuChunk = 16;                 // blocks per VALU scoring workgroup
 constexpr int kValuPerWave = kValuChunk / kScoreWaves;
+static_assert(kValuChunk == kMfmaChunk, "both scoring paths write partials per 16-block tile");
 
 typedef float sf32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
 
@@ -296,37 +297,107 @@ __device__ __forceinline__ int keep_budget(float h, int nb, float eps_h, float h
   return min(nb, max(min(b_min, nb), k));
 }
 
-// Kept set of one sequence (one workgroup of 512 threads):
-//  1. L_h = ln sum_b n_b e^{z_bh}, merged from the scoring kernel's partials;
-//  2. I_b = (1/H_q) sum_h e^{z_bh + ln n_b - L_h} (L_h - z_bh) for every block,
-//     held in LDS as order-preserving integer keys;
-//  3. budget k from the entropy, the k-th largest key by a 4-pass 8-bit radix
-//     select, and ascending compaction of {b : I_b >= theta} with wave ballots.
-constexpr int kSelThreads = 512;
+// Kept set of one sequence, in three phases:
+//  A. (one workgroup per sequence) L_h = ln sum_b n_b e^{z_bh}, merged from
+//     the scoring pass's per-tile partials;
+//  B. (one workgroup per 64 blocks) I_b = (1/H_q) sum_h e^{z_bh + ln n_b - L_h}
+//     (L_h - z_bh) for every block;
+//  C. (one workgroup per sequence) budget k from the entropy, the k-th
+//     largest score by an 8-bit radix select over the bits in which the
+//     scores differ, and ascending compaction of {b : I_b >= theta} with
+//     wave ballots.
+// Phase B spreads the exponentials of long sequences over the whole chip;
+// the two per-sequence phases only merge and select.
+constexpr int kRowThreads = 256;          // phase A
+constexpr int kTileBlocks = 64;           // phase B: blocks per workgroup (4 lanes each)
+constexpr int kSelThreads = 512;          // phase C
 constexpr int kSelWaves = kSelThreads / 64;
+
+// Phase A for sequence b by kRowThreads threads: writes L_h to L[b * Hq + h]
+// (-inf for an empty or invalid sequence).
+__device__ __forceinline__ void lse_merge_body(const float* __restrict__ lse_part,
+                                               const int* __restrict__ ctx_lens,
+                                               float* __restrict__ L, int Hq, int MAXB,
+                                               int nch_max, int b, float* s_pm, float* s_ps) {
+  const int t = threadIdx.x;
+  const int N = ctx_lens[b];
+  const int nb = (N >= 0 && N <= MAXB * kBlock) ? (N + kBlock - 1) / kBlock : 0;
+  const int nch = (nb + kMfmaChunk - 1) / kMfmaChunk;
+  const int per_head = kRowThreads / Hq;     // threads per head (Hq <= 128)
+  // Each thread folds a strided subset of the tiles of head t % Hq: first
+  // their maximum, then the rescaled sums (independent loads, no serial
+  // rescaling chain).
+  float m = -INFINITY, sum = 0.f;
+  if (t < per_head * Hq) {
+    const int h = t % Hq;
+    const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
+    for (int c = t / Hq; c < nch; c += per_head) m = fmaxf(m, lp[static_cast<long long>(c) * Hq * 2]);
+    if (m != -INFINITY)
+      for (int c = t / Hq; c < nch; c += per_head) {
+        const float mc = lp[static_cast<long long>(c) * Hq * 2];
+        sum += lp[static_cast<long long>(c) * Hq * 2 + 1] * expf(mc - m);
+      }
+  }
+  s_pm[t] = m;
+  s_ps[t] = sum;
+  __syncthreads();
+  if (t < Hq) {
+    float mm = -INFINITY, ss = 0.f;
+    for (int i = 0; i < per_head; ++i) {
+      const float mc = s_pm[i * Hq + t], sc = s_ps[i * Hq + t];
+      if (mc == -INFINITY) continue;
+      const float mn = fmaxf(mm, mc);
+      ss = ss * expf(mm - mn) + sc * expf(mc - mn);
+      mm = mn;
+    }
+    L[static_cast<long long>(b) * Hq + t] = (mm == -INFINITY) ? -INFINITY : mm + logf(ss);
+  }
+}
+
+// Phase B: scores of blocks j0 .. j0 + 63 of sequence b by 256 threads; four
+// lanes per block, lane quarter qq takes heads qq, qq + 4, ...  Writes I_b to
+// scores[b * MAXB + j].
+__device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
+                                                 const float* __restrict__ L,
+                                                 const int* __restrict__ ctx_lens,
+                                                 float* __restrict__ scores, int Hq, int MAXB,
+                                                 int b, int j0, float* sL) {
+  const int t = threadIdx.x;
+  const int N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) return;    // flagged in phase C
+  const int nb = (N + kBlock - 1) / kBlock;
+  if (j0 >= nb) return;
+  for (int h = t; h < Hq; h += kRowThreads) sL[h] = L[static_cast<long long>(b) * Hq + h];
+  __syncthreads();
+  const int j = j0 + (t >> 2), qq = t & 3;
+  float acc = 0.f;
+  if (j < nb) {
+    const float lnn = logf(static_cast<float>(j == nb - 1 ? N - kBlock * (nb - 1) : kBlock));
+    const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq;
+    for (int h = qq; h < Hq; h += 4) {
+      const float z = zr[h];
+      acc += expf(z + lnn - sL[h]) * (sL[h] - z);
+    }
+  }
+  acc += __shfl_xor(acc, 1);
+  acc += __shfl_xor(acc, 2);
+  if (j < nb && qq == 0)
+    scores[static_cast<long long>(b) * MAXB + j] = __fdiv_rn(acc, static_cast<float>(Hq));
+}
 
 struct SelectShared {
   unsigned hist[256];
-  float pm[kSelThreads], ps[kSelThreads], L[128];
+  unsigned red[2 * kSelWaves];
   int digit, krem, wcnt[kSelWaves];
 };
 
-// keys: LDS [MAXB]; h: the sequence's entropy.  Called by all kSelThreads
-// threads of the workgroup.
-__device__ __forceinline__ void select_body(
-    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, float hval,
-    float* __restrict__ scores_out, float* __restrict__ theta_out, int* __restrict__ kept,
-    int* __restrict__ n_kept, int Hq, int MAXB, int chunk, int nch_max, float eps_h, float h_min,
-    float log_v, float kappa_min, int b_min, unsigned* flags, int b, unsigned* keys,
-    SelectShared& sh) {
-  unsigned* hist = sh.hist;
-  float* s_pm = sh.pm;
-  float* s_ps = sh.ps;
-  float* sL = sh.L;
-  int& s_digit = sh.digit;
-  int& s_krem = sh.krem;
-  int* s_wcnt = sh.wcnt;
+// Phase C for sequence b by kSelThreads threads.  keys: LDS [MAXB]; hval: the
+// sequence's entropy; scores: phase B's output.
+__device__ __forceinline__ void select_row_body(
+    const float* __restrict__ scores, const int* __restrict__ ctx_lens, float hval,
+    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
+    float eps_h, float h_min, float log_v, float kappa_min, int b_min, unsigned* flags, int b,
+    unsigned* keys, SelectShared& sh) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int N = ctx_lens[b];
   if (N < 0 || N > MAXB * kBlock) {
@@ -339,96 +410,60 @@ __device__ __forceinline__ void select_body(
   }
   const int nb = (N + kBlock - 1) / kBlock;
   const int k = keep_budget(hval, nb, eps_h, h_min, log_v, kappa_min, b_min);
-  if (nb == 0) {
+  if (nb == 0 || k <= 0) {
     if (t == 0) {
       n_kept[b] = 0;
       if (theta_out) theta_out[b] = INFINITY;
     }
     return;
   }
-  // 1. L_h = ln sum_b n_b e^{z_bh}, merged from the per-chunk partials: each
-  //    thread folds a strided subset of the chunks of head t % Hq, then one
-  //    thread per head folds the subsets.
-  const int nch = (nb + chunk - 1) / chunk;
-  const int per_head = kSelThreads / Hq;     // threads per head (Hq <= 128)
-  {
-    float m = -INFINITY, sum = 0.f;
-    if (t < per_head * Hq) {
-      const int h = t % Hq;
-      const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
-      for (int c = t / Hq; c < nch; c += per_head) {
-        const float mc = lp[static_cast<long long>(c) * Hq * 2], sc = lp[static_cast<long long>(c) * Hq * 2 + 1];
-        const float mn = fmaxf(m, mc);
-        sum = sum * expf(m - mn) + sc * expf(mc - mn);
-        m = mn;
-      }
-    }
-    s_pm[t] = m;
-    s_ps[t] = sum;
+  // Keys in LDS, and the bits in which they differ.
+  const float* sr = scores + static_cast<long long>(b) * MAXB;
+  unsigned kmin = 0xFFFFFFFFu, kmax = 0u;
+  for (int i = t; i < nb; i += kSelThreads) {
+    const unsigned key = float_key(sr[i]);
+    keys[i] = key;
+    kmin = min(kmin, key);
+    kmax = max(kmax, key);
   }
+  kmin = wave_min_u(kmin);
+  kmax = wave_max_u(kmax);
+  if (lane == 0) {
+    sh.red[wave] = kmin;
+    sh.red[kSelWaves + wave] = kmax;
+  }
+  if (t == 0) sh.krem = k;
   __syncthreads();
-  if (t < Hq) {
-    float m = -INFINITY, sum = 0.f;
-    for (int i = 0; i < per_head; ++i) {
-      const float mc = s_pm[i * Hq + t], sc = s_ps[i * Hq + t];
-      if (mc == -INFINITY) continue;
-      const float mn = fmaxf(m, mc);
-      sum = sum * expf(m - mn) + sc * expf(mc - mn);
-      m = mn;
-    }
-    sL[t] = m + logf(sum);
+  kmin = sh.red[0];
+  kmax = sh.red[kSelWaves];
+#pragma unroll
+  for (int w = 1; w < kSelWaves; ++w) {
+    kmin = min(kmin, sh.red[w]);
+    kmax = max(kmax, sh.red[kSelWaves + w]);
   }
-  __syncthreads();
-
-  // 2. Block scores; a thread reads its block's logit row as float4s.
-  const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
-  const float ln_full = logf(static_cast<float>(kBlock));
-  const float* zb = zbuf + static_cast<long long>(b) * MAXB * Hq;
-  for (int j = t; j < nb; j += kSelThreads) {
-    const float lnn = (j == nb - 1) ? ln_last : ln_full;
-    const float* zr = zb + static_cast<long long>(j) * Hq;
-    float acc = 0.f;
-    if ((Hq & 3) == 0) {
-      for (int h = 0; h < Hq; h += 4) {
-        const float4 z4 = *reinterpret_cast<const float4*>(zr + h);
-        acc += expf(z4.x + lnn - sL[h]) * (sL[h] - z4.x);
-        acc += expf(z4.y + lnn - sL[h + 1]) * (sL[h + 1] - z4.y);
-        acc += expf(z4.z + lnn - sL[h + 2]) * (sL[h + 2] - z4.z);
-        acc += expf(z4.w + lnn - sL[h + 3]) * (sL[h + 3] - z4.w);
-      }
-    } else {
-      for (int h = 0; h < Hq; ++h) acc += expf(zr[h] + lnn - sL[h]) * (sL[h] - zr[h]);
-    }
-    const float I = __fdiv_rn(acc, static_cast<float>(Hq));
-    keys[j] = float_key(I);
-    if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j] = I;
-  }
-  if (k <= 0) {
-    if (t == 0) {
-      n_kept[b] = 0;
-      if (theta_out) theta_out[b] = INFINITY;
-    }
-    return;
-  }
-  if (t == 0) s_krem = k;
-  __syncthreads();
-
-  // 3. Radix select of the k-th largest key.
-  unsigned prefix = 0u, mask = 0u;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    if (t < 256) hist[t] = 0u;
+  // Radix select of the k-th largest key over the differing bits, 8 at a
+  // time from the top (the common leading bits are the prefix already).
+  const unsigned diff = kmin ^ kmax;
+  const int top = diff ? 31 - __clz(diff) : -1;    // highest differing bit
+  unsigned mask = diff ? ~((2u << top) - 1u) : 0xFFFFFFFFu;
+  if (top == 31) mask = 0u;
+  unsigned prefix = kmax & mask;
+  for (int hi = top; hi >= 0; hi -= 8) {
+    const int shift = max(hi - 7, 0);
+    const int width = hi - shift + 1;
+    const unsigned dmask = (1u << width) - 1u;
+    if (t < 256) sh.hist[t] = 0u;
     __syncthreads();
     for (int i = t; i < nb; i += kSelThreads) {
       const unsigned key = keys[i];
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      if ((key & mask) == prefix) atomicAdd(&sh.hist[(key >> shift) & dmask], 1u);
     }
     __syncthreads();
     if (wave == 0) {
       // Bins 4*lane .. 4*lane+3; suffix sums over lanes locate the digit
       // holding the k_rem-th largest remaining key.
-      const unsigned c0 = hist[4 * lane], c1 = hist[4 * lane + 1], c2 = hist[4 * lane + 2],
-                     c3 = hist[4 * lane + 3];
+      const unsigned c0 = sh.hist[4 * lane], c1 = sh.hist[4 * lane + 1],
+                     c2 = sh.hist[4 * lane + 2], c3 = sh.hist[4 * lane + 3];
       const unsigned cl = c0 + c1 + c2 + c3;
       unsigned suf = cl;
 #pragma unroll
@@ -436,7 +471,7 @@ __device__ __forceinline__ void select_body(
         const unsigned n = __shfl_down(suf, o);
         if (lane + o < 64) suf += n;
       }
-      const unsigned krem = static_cast<unsigned>(s_krem);
+      const unsigned krem = static_cast<unsigned>(sh.krem);
       const unsigned above = suf - cl;       // keys in higher lanes' bins
       if (above < krem && suf >= krem) {
         unsigned run = above;
@@ -449,13 +484,13 @@ __device__ __forceinline__ void select_body(
           }
           run += cs[x];
         }
-        s_digit = d;
-        s_krem = static_cast<int>(krem - run);
+        sh.digit = d;
+        sh.krem = static_cast<int>(krem - run);
       }
     }
     __syncthreads();
-    prefix |= static_cast<unsigned>(s_digit) << shift;
-    mask |= 255u << shift;
+    prefix |= static_cast<unsigned>(sh.digit) << shift;
+    mask |= dmask << shift;
     __syncthreads();
   }
   const unsigned tkey = prefix;
@@ -468,12 +503,12 @@ __device__ __forceinline__ void select_body(
     const bool f = i < nb && keys[i] >= tkey;
     const unsigned long long bal = __ballot(f);
     const int rank = __popcll(bal & ((1ull << lane) - 1ull));
-    if (lane == 0) s_wcnt[wave] = __popcll(bal);
+    if (lane == 0) sh.wcnt[wave] = __popcll(bal);
     __syncthreads();
     int off = total;
-    for (int w = 0; w < wave; ++w) off += s_wcnt[w];
+    for (int w = 0; w < wave; ++w) off += sh.wcnt[w];
     if (f) krow[off + rank] = i;
-    for (int w = 0; w < kSelWaves; ++w) total += s_wcnt[w];
+    for (int w = 0; w < kSelWaves; ++w) total += sh.wcnt[w];
     __syncthreads();
   }
   if (t == 0) {

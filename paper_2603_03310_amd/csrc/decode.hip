@@ -33,6 +33,8 @@
 
 #include <math.h>
 
+#include <algorithm>
+
 namespace ent {
 namespace {
 
@@ -62,6 +64,7 @@ struct DecodeArgs {
   unsigned* flags;
   int B, Hkv, G, MAXB, P;
   int W;              // waves of the decode grid
+  int nsl;            // merge workgroups per segment
   float scale_log2;   // softmax scale times log2(e)
 };
 
@@ -466,34 +469,47 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
   flush();
 }
 
-// Merge of the partials of every segment that the decode ranges cut (one
-// workgroup per segment).  Segments with nothing kept get zeros and -inf.
-// The (max, sum) pairs of all contributing waves are read at once; per head
-// M = max m, L = sum l 2^(m - M), then out = sum acc 2^(m - M) / L with every
-// thread streaming its outputs' partial accumulators as independent loads.
+// Merge of the partials of every segment that the decode ranges cut.  One
+// workgroup per (segment, slice of its G x d outputs); a.nsl slices per
+// segment (more when segments are cut into many partials).  Segments with
+// nothing kept get zeros and -inf.  Per head, M = max m and
+// L = sum l 2^(m - M); then out = sum_k acc_k 2^(m_k - M) / L.  When a slice
+// has fewer outputs than threads, the threads split the partials into
+// groups (independent loads) and an LDS reduction sums the groups.
+constexpr int kCombinePer = kMaxGroup * 128 / kThreads;   // outputs per thread, at most
+
 template <int D>
-__device__ __forceinline__ void combine_body(const DecodeArgs& a, int seg) {
+__device__ __forceinline__ void combine_body(const DecodeArgs& a, int item) {
   extern __shared__ int s_mem[];
   __shared__ int s_red[kWaves];
   __shared__ float s_m[kCombineMaxSplits * kMaxGroup], s_l[kCombineMaxSplits * kMaxGroup];
   __shared__ float s_M[kMaxGroup], s_L[kMaxGroup];
+  __shared__ float s_acc[kThreads];
   int* s_pref = s_mem;
   int* s_nk = s_mem + a.B + 1;
   int* s_N = s_nk + a.B;
   build_plan(a, s_pref, s_nk, s_N, s_red);
   const int U = s_pref[a.B];
   const int t = threadIdx.x;
-  const int b = seg / a.Hkv, g = seg % a.Hkv;
   const int G = a.G;
+  const int seg = item / a.nsl, slice = item - seg * a.nsl;
+  const int b = seg / a.Hkv, g = seg % a.Hkv;
   const int Hq = a.Hkv * G;
   const int nk = s_nk[b];
+  const int span = G * D / a.nsl;            // outputs of this workgroup (power of two >= 64)
+  const int width = min(span, kThreads);     // threads per partial group
+  const int npg = kThreads / width;          // partial groups
+  const int opt = span / width;              // outputs per thread
+  const int pg = t / width, ol = t - pg * width;
+  const long long ob = static_cast<long long>(b) * Hq + g * G;   // first output head row
   if (nk == 0) {
-    for (int idx = t; idx < G * D; idx += kThreads) {
-      const int r = idx / D, d = idx % D;
-      const long long oh = static_cast<long long>(b) * Hq + g * G + r;
-      a.out[oh * D + d] = 0.f;
-      if (d == 0 && a.lse) a.lse[oh] = -INFINITY;
-    }
+    if (pg == 0)
+      for (int x = 0; x < opt; ++x) {
+        const int o = slice * span + ol + x * width;
+        const int r = o / D, d = o - r * D;
+        a.out[(ob + r) * D + d] = 0.f;
+        if (d == 0 && a.lse) a.lse[ob + r] = -INFINITY;
+      }
     return;
   }
   const int seg_start = s_pref[b] + g * nk;
@@ -502,18 +518,20 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int seg) {
   if (w0 == w1) return;                      // written whole by the decode kernel
   const int ns = w1 - w0 + 1;
 
-  // Pass 1: M and L per head.
+  float acc[kCombinePer];
+#pragma unroll
+  for (int x = 0; x < kCombinePer; ++x) acc[x] = 0.f;
   float M = -INFINITY, L = 0.f;              // meaningful in threads t < G
   for (int c0 = 0; c0 < ns; c0 += kCombineMaxSplits) {
     const int n = min(kCombineMaxSplits, ns - c0);
     for (int e = t; e < n * G; e += kThreads) {
-      const int k = e / G, r = e % G;
+      const int k = e / G, rr = e % G;
       const int wi = w0 + c0 + k;
       // A wave with an empty range (fewer units than waves) wrote no partial.
       const bool live = range_begin(wi + 1, U, a.W) > range_begin(wi, U, a.W);
       const long long slot = static_cast<long long>(wi) + seg;
-      s_m[e] = live ? a.part_ml[(slot * G + r) * 2 + 0] : 0.f;
-      s_l[e] = live ? a.part_ml[(slot * G + r) * 2 + 1] : 0.f;
+      s_m[e] = live ? a.part_ml[(slot * G + rr) * 2 + 0] : 0.f;
+      s_l[e] = live ? a.part_ml[(slot * G + rr) * 2 + 1] : 0.f;
     }
     __syncthreads();
     if (t < G) {
@@ -525,8 +543,32 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int seg) {
         const float l = s_l[k * G + t];
         if (l > 0.f) Lc += l * exp2f(s_m[k * G + t] - Mc);
       }
+      s_M[t] = Mc;
+      s_L[t] = (M == -INFINITY) ? 1.f : exp2f(M - Mc);   // rescales earlier chunks
       M = Mc;
       L = Lc;
+    }
+    __syncthreads();
+    for (int e = t; e < n * G; e += kThreads) {
+      const float l = s_l[e];
+      s_m[e] = (l > 0.f) ? exp2f(s_m[e] - s_M[e % G]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int x = 0; x < kCombinePer; ++x) {
+      if (x < opt) {
+        const int o = slice * span + ol + x * width;
+        const int r = o / D, d = o - r * D;
+        const float* pa = a.part_acc + ((static_cast<long long>(w0 + c0) + seg) * G + r) * D + d;
+        float part = 0.f;
+#pragma unroll 4
+        for (int k = pg; k < n; k += npg) {
+          const float wk = s_m[k * G + r];
+          const float v = pa[static_cast<long long>(k) * G * D];
+          part += wk > 0.f ? wk * v : 0.f;
+        }
+        acc[x] = acc[x] * s_L[r] + part;
+      }
     }
     __syncthreads();
   }
@@ -534,51 +576,19 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int seg) {
     s_M[t] = M;
     s_L[t] = L;
   }
+  if (npg > 1) s_acc[t] = acc[0];            // opt == 1 when the partials are split
   __syncthreads();
-
-  // Pass 2: weighted sum of the partial outputs.
-  constexpr int kPer = (kMaxGroup * D + kThreads - 1) / kThreads;
-  float acc[kPer];
+  if (pg != 0) return;
 #pragma unroll
-  for (int x = 0; x < kPer; ++x) acc[x] = 0.f;
-  for (int c0 = 0; c0 < ns; c0 += kCombineMaxSplits) {
-    const int n = min(kCombineMaxSplits, ns - c0);
-    for (int e = t; e < n * G; e += kThreads) {
-      const int k = e / G, r = e % G;
-      const int wi = w0 + c0 + k;
-      const bool live = range_begin(wi + 1, U, a.W) > range_begin(wi, U, a.W);
-      const long long slot = static_cast<long long>(wi) + seg;
-      const float m = live ? a.part_ml[(slot * G + r) * 2 + 0] : 0.f;
-      const float l = live ? a.part_ml[(slot * G + r) * 2 + 1] : 0.f;
-      s_m[e] = (l > 0.f && s_L[r] > 0.f) ? exp2f(m - s_M[r]) / s_L[r] : 0.f;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int x = 0; x < kPer; ++x) {
-      const int idx = t + x * kThreads;
-      if (idx < G * D) {
-        const int r = idx / D, d = idx % D;
-        const float* pa = a.part_acc + ((static_cast<long long>(w0 + c0) + seg) * G + r) * D + d;
-        float o = 0.f;
-#pragma unroll 8
-        for (int k = 0; k < n; ++k) {
-          const float wk = s_m[k * G + r];
-          const float v = pa[static_cast<long long>(k) * G * D];
-          o += wk > 0.f ? wk * v : 0.f;
-        }
-        acc[x] += o;
-      }
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int x = 0; x < kPer; ++x) {
-    const int idx = t + x * kThreads;
-    if (idx < G * D) {
-      const int r = idx / D, d = idx % D;
-      const long long oh = static_cast<long long>(b) * Hq + g * G + r;
-      a.out[oh * D + d] = acc[x];
-      if (d == 0 && a.lse) a.lse[oh] = s_L[r] > 0.f ? (s_M[r] + log2f(s_L[r])) * kLn2 : -INFINITY;
+  for (int x = 0; x < kCombinePer; ++x) {
+    if (x < opt) {
+      const int o = slice * span + ol + x * width;
+      const int r = o / D, d = o - r * D;
+      float tot = acc[x];
+      for (int q = 1; q < npg; ++q) tot += s_acc[q * width + ol];
+      const float Lr = s_L[r];
+      a.out[(ob + r) * D + d] = Lr > 0.f ? tot / Lr : 0.f;
+      if (d == 0 && a.lse) a.lse[ob + r] = Lr > 0.f ? (s_M[r] + log2f(Lr)) * kLn2 : -INFINITY;
     }
   }
 }
@@ -675,8 +685,13 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // Slices per segment: split the outputs (and the partials across thread
+  // groups) when segments are cut into many partials on average.
+  const int waves_per_seg = a.W / std::max(1, B * cf.num_kv_heads);
+  const int nsl = waves_per_seg >= 8 ? c->group * cf.head_dim / 64 : 1;
+  a.nsl = nsl;
   if (sample) {
-    const dim3 cgrid(B * cf.num_kv_heads + B);
+    const dim3 cgrid(B * cf.num_kv_heads * nsl + B);
     const bool vec = row_vec_ok(sample->logits, sample->ld);
     if (cf.head_dim == 128) {
       if (vec)
@@ -691,7 +706,7 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
     }
     return hipGetLastError();
   }
-  const dim3 cgrid(B * cf.num_kv_heads);
+  const dim3 cgrid(B * cf.num_kv_heads * nsl);
   if (cf.head_dim == 128)
     hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), lds, s, a);
   else

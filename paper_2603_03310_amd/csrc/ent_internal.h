@@ -35,6 +35,8 @@ struct ent_ctx {
   float* stats_tmp = nullptr;     // [max_batch, chunks, 2]  row statistics scratch
   float* zbuf = nullptr;          // [max_batch, MAXB, H_q]  block logits
   float* lse_part = nullptr;      // [max_batch, lse_chunks, H_q, 2]
+  float* lrow = nullptr;          // [max_batch, H_q]  L_h per sequence
+  float* iscores = nullptr;       // [max_batch, MAXB]  block scores when the caller keeps none
   float* dec_acc = nullptr;       // [decode partial slots, G, d]
   float* dec_ml = nullptr;        // [decode partial slots, G, 2]
   unsigned* dev_flags = nullptr;  // [1]
@@ -82,6 +84,12 @@ struct PrologueArgs {
   unsigned* flags;
 };
 hipError_t launch_prologue(const ent_ctx* c, const PrologueArgs& a, hipStream_t s);
+// Selection phases B (block scores from c->lrow) and C (radix select).
+hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,
+                               hipStream_t s);
+hipError_t launch_select_rows(const ent_ctx* c, int B, const int* ctx_lens, const float* h,
+                              const float* scores, float* theta, int* kept, int* n_kept,
+                              hipStream_t s);
 hipError_t launch_score_valu(const ent_ctx* c, int B, const void* q, const float* ksum,
                              const int* tables, const int* ctx_lens, hipStream_t s);
 
@@ -141,6 +149,18 @@ template <typename T>
 __device__ __forceinline__ T wave_max(T v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ unsigned wave_min_u(unsigned v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, static_cast<unsigned>(__shfl_xor(static_cast<int>(v), o)));
+  return v;
+}
+
+__device__ __forceinline__ unsigned wave_max_u(unsigned v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, static_cast<unsigned>(__shfl_xor(static_cast<int>(v), o)));
   return v;
 }
 

@@ -1,4 +1,4 @@
-// One whole decode step in four launches (ent_decode_step).  Each launch runs
+// One whole decode step (ent_decode_step).  Each launch runs
 // the same device bodies as the per-stage entry points, so the results are
 // bit-identical to calling ent_entropy_temperature, ent_block_select,
 // ent_sparse_paged_decode and ent_sample in sequence:
@@ -8,8 +8,9 @@
 //      do not depend on each other (fp32 queries: scoring is a second
 //      launch, on the VALU);
 //   B  one workgroup per sequence: the row's entropy from the chunk triples,
-//      the controller update, and the kept-block selection under the
-//      entropy-driven budget;
+//      the controller update and L_h; then the block scores over the whole
+//      chip, and one workgroup per sequence for the kept-block selection
+//      under the entropy-driven budget;
 //   C  kept-block decode attention;
 //   D  the merge of split decode segments and, in the same launch, sampling
 //      at the temperature the step used (independent of the merge).
@@ -20,47 +21,22 @@
 namespace ent {
 namespace {
 
-struct StepBArgs {
-  const float* part;
-  int C;
-  float* temp;
-  float* h_prev;
-  float* tau;
-  float* h_out;
-  float* temp_used;
-  float eta, h_target, t_min, t_max;
-  const float* zbuf;
-  const float* lse_part;
-  const int* ctx_lens;
-  float* scores;
-  float* theta;
-  int* kept;
-  int* n_kept;
-  int Hq, MAXB, chunk, nch_max;
-  float eps_h, h_min, log_v, kappa_min;
-  int b_min;
-  unsigned* flags;
-};
-
-__global__ __launch_bounds__(kSelThreads) void step_b_kernel(StepBArgs a) {
-  extern __shared__ unsigned keys[];        // [MAXB]
-  __shared__ SelectShared ssh;
-  __shared__ float s_H;
+// Per sequence: the row's entropy from the chunk triples and the controller
+// update (first wave), and L_h for the selection (all threads).
+__global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
+    const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau, float* h_out,
+    float* temp_used, float eta, float h_target, float t_min, float t_max,
+    const float* __restrict__ lse_part, const int* __restrict__ ctx_lens, float* __restrict__ L,
+    int Hq, int MAXB, int nch_max) {
+  __shared__ float s_pm[kRowThreads], s_ps[kRowThreads];
   const int b = blockIdx.x;
-  const int t = threadIdx.x;
-  if (t < 64) {
-    const float H = row_entropy(a.part, a.C, b);
-    if (t == 0) {
-      s_H = H;
-      controller_update(b, H, a.temp[b], a.h_prev, a.tau, a.temp, a.h_out, a.temp_used, a.eta,
-                        a.h_target, a.t_min, a.t_max);
-    }
+  if (threadIdx.x < 64) {
+    const float H = row_entropy(part, C, b);
+    if (threadIdx.x == 0)
+      controller_update(b, H, temp[b], h_prev, tau, temp, h_out, temp_used, eta, h_target, t_min,
+                        t_max);
   }
-  __syncthreads();
-  const float H = s_H;
-  select_body(a.zbuf, a.lse_part, a.ctx_lens, H, a.scores, a.theta, a.kept, a.n_kept, a.Hq,
-              a.MAXB, a.chunk, a.nch_max, a.eps_h, a.h_min, a.log_v, a.kappa_min, a.b_min,
-              a.flags, b, keys, ssh);
+  lse_merge_body(lse_part, ctx_lens, L, Hq, MAXB, nch_max, b, s_pm, s_ps);
 }
 
 }  // namespace
@@ -106,38 +82,16 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
     if (e != hipSuccess) return e;
   }
 
-  StepBArgs a;
-  a.part = c->ent_part;
-  a.C = c->chunks;
-  a.temp = st.temp;
-  a.h_prev = st.h_prev;
-  a.tau = st.tau;
-  a.h_out = h_out;
-  a.temp_used = temp_used;
-  a.eta = cf.eta;
-  a.h_target = cf.h_target;
-  a.t_min = cf.t_min;
-  a.t_max = cf.t_max;
-  a.zbuf = c->zbuf;
-  a.lse_part = c->lse_part;
-  a.ctx_lens = ctx_lens;
-  a.scores = scores;
-  a.theta = theta;
-  a.kept = kept;
-  a.n_kept = n_kept;
-  a.Hq = cf.num_q_heads;
-  a.MAXB = cf.max_blocks_per_seq;
-  a.chunk = cf.kv_dtype == ENT_BF16 ? kMfmaChunk : kValuChunk;
-  a.nch_max = c->lse_chunks;
-  a.eps_h = cf.eps_h;
-  a.h_min = cf.h_min;
-  a.log_v = cf.log_v;
-  a.kappa_min = cf.kappa_min;
-  a.b_min = cf.b_min;
-  a.flags = c->dev_flags;
-  const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-  hipLaunchKernelGGL(step_b_kernel, dim3(B), dim3(kSelThreads), lds, s, a);
+  hipLaunchKernelGGL(step_b0_kernel, dim3(B), dim3(kRowThreads), 0, s, c->ent_part, c->chunks,
+                     st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta, cf.h_target, cf.t_min,
+                     cf.t_max, c->lse_part, ctx_lens, c->lrow, cf.num_q_heads,
+                     cf.max_blocks_per_seq, c->lse_chunks);
   e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  float* sc = scores ? scores : c->iscores;
+  e = launch_block_scores(c, B, ctx_lens, sc, s);
+  if (e != hipSuccess) return e;
+  e = launch_select_rows(c, B, ctx_lens, h_out, sc, theta, kept, n_kept, s);
   if (e != hipSuccess) return e;
   SampleArgs sa;
   sa.logits = logits;
