@@ -28,6 +28,7 @@ struct ent_ctx {
   int chunks = 0;           // entropy chunks per logit row
   int lse_chunks = 0;       // log-sum-exp partials per sequence (finest chunking)
   int decode_grid = 0;      // persistent decode workgroups
+  int prologue_grid = 0;    // resident entropy / scoring workgroups
 
   void* ws = nullptr;       // one workspace allocation
   size_t ws_bytes = 0;
@@ -84,6 +85,7 @@ struct PrologueArgs {
   unsigned* flags;
 };
 hipError_t launch_prologue(const ent_ctx* c, const PrologueArgs& a, hipStream_t s);
+int prologue_grid_size(const ent_ctx* c);
 // Selection phases B (block scores from c->lrow) and C (radix select).
 hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,
                                hipStream_t s);

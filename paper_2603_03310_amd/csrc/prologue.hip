@@ -1,21 +1,27 @@
-// The two streaming passes that open a decode step, as one grid of
-// independent 256-thread workgroups with two roles:
+// The two streaming passes that open a decode step, as one grid of 256-thread
+// workgroups that walk a compact list of jobs of two kinds:
 //
-//   * block scoring (bf16 queries): workgroup (sequence b, tile of 16
-//     blocks, group of four KV heads); wave w takes KV head 4 hg + w
+//   * block scoring (bf16 queries): job (sequence b, tile of 16 blocks,
+//     group of four KV heads); wave w takes KV head 4 hg + w
 //     (score_head_load / score_head_compute, Section 3.2);
-//   * entropy chunk passes: workgroup (row b, chunk c) of 4096 logits
+//   * entropy chunk passes: job (row b, chunk c) of 4096 logits
 //     (entropy_chunk_body, Section 2.1).
 //
 // Both read HBM once (block summaries, logits) at a few flops per byte and
-// do not depend on each other.  Scoring workgroups come first (they run
-// longer).  Every workgroup keeps few registers, so many are resident at
-// once and their loads overlap.  Tiles past a sequence's last block exit at
-// once.  The per-stage entry points launch the same kernel with one role
-// only, which keeps their results bit-identical to the fused step's.
+// do not depend on each other; scoring jobs come first.  Every workgroup
+// keeps few registers, so many jobs' loads are in flight at once.  Two grid
+// forms: dense (one workgroup per job slot; slots for tiles past a
+// sequence's end exit at once) and, when the block tables are much wider
+// than the sequences, compact (the grid is sized to the chip's resident
+// capacity and walks the list of tiles that exist, a prefix over the
+// sequences' tile counts built in LDS by every workgroup).  The per-stage entry
+// points run the same kernel with one kind of job only, which keeps their
+// results bit-identical to the fused step's.
 
 #include "blocks_dev.h"
 #include "entropy_dev.h"
+
+#include <algorithm>
 
 namespace ent {
 namespace {
@@ -23,59 +29,163 @@ namespace {
 constexpr int kProThreads = 256;
 constexpr int kProWaves = kProThreads / 64;
 
-__host__ __device__ inline int score_tiles(int MAXB) { return (MAXB + kMfmaChunk - 1) / kMfmaChunk; }
 __host__ __device__ inline int head_groups(int Hkv) { return (Hkv + kProWaves - 1) / kProWaves; }
 
-template <bool VEC, int D>
+// s_pref[b] = first scoring tile of sequence b (s_pref[B] = all tiles);
+// s_N[b] = its context length (-1 when invalid: no tiles, flagged later).
+__device__ void tile_plan(const int* __restrict__ ctx_lens, int B, int MAXB, int* s_pref, int* s_N,
+                          int* s_red) {
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int per = (B + kProThreads - 1) / kProThreads;
+  int loc = 0;
+  for (int i = 0; i < per; ++i) {
+    const int b = t * per + i;
+    if (b < B) {
+      const int N = ctx_lens[b];
+      const bool ok = N >= 0 && N <= MAXB * kBlock;
+      s_N[b] = ok ? N : -1;
+      loc += ok ? (N + kBlock * kMfmaChunk - 1) / (kBlock * kMfmaChunk) : 0;
+    }
+  }
+  int incl = loc;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int n = __shfl_up(incl, o);
+    if (lane >= o) incl += n;
+  }
+  if (lane == 63) s_red[wave] = incl;
+  __syncthreads();
+  int run = incl - loc;
+  for (int w = 0; w < wave; ++w) run += s_red[w];
+  for (int i = 0; i < per; ++i) {
+    const int b = t * per + i;
+    if (b < B) {
+      s_pref[b] = run;
+      const int N = s_N[b];
+      run += N >= 0 ? (N + kBlock * kMfmaChunk - 1) / (kBlock * kMfmaChunk) : 0;
+    }
+  }
+  if (t == kProThreads - 1) s_pref[B] = run;
+  __syncthreads();
+}
+
+// One scoring job: tile ch of sequence b (context length N), KV heads of
+// group hg (wave w takes head 4 hg + w).
+template <int D>
+__device__ __forceinline__ void score_job(const PrologueArgs& a, int b, int ch, int hg, int N) {
+  const int g = hg * kProWaves + (threadIdx.x >> 6);
+  if (g >= a.Hkv) return;
+  const int nb = (N + kBlock - 1) / kBlock;
+  const int p = score_tile_block(a.tables, b, ch, a.MAXB, nb, a.P, a.flags);
+  float4 buf[kScoreSlots];
+  score_head_load<D>(a.ksum, p, a.Hkv, g, buf);
+  score_head_compute<D>(a.q, buf, a.zbuf, a.lse_part, b, ch, g, N, nb, a.Hkv, a.G, a.MAXB,
+                        a.nch_max, a.scale);
+}
+
+// Dense form: one workgroup per job slot, scoring slots (b, ch, hg) for every
+// tile a sequence could have (slots past its end exit at once), then one per
+// entropy chunk.  Compact form (COMPACT): the grid walks the list of jobs
+// that exist.
+template <bool VEC, int D, bool COMPACT>
 __global__ __launch_bounds__(kProThreads) void prologue_kernel(PrologueArgs a) {
+  extern __shared__ int s_mem[];           // compact: s_pref [B + 1], s_N [B]
+  __shared__ int s_red[kProWaves];
   __shared__ float red[16];
-  const int id = blockIdx.x;
   const int nhg = head_groups(a.Hkv);
-  const int nsc = a.do_score ? a.B * score_tiles(a.MAXB) * nhg : 0;
-  if (id < nsc) {
-    const int per_b = score_tiles(a.MAXB) * nhg;
-    const int b = id / per_b;
-    const int r = id - b * per_b;
-    const int ch = r / nhg;
-    const int g = (r - ch * nhg) * kProWaves + (threadIdx.x >> 6);
-    const int N = a.ctx_lens[b];
-    if (N < 0 || N > a.MAXB * kBlock) return;    // flagged by the selection stage
-    const int nb = (N + kBlock - 1) / kBlock;
-    if (ch * kMfmaChunk >= nb || g >= a.Hkv) return;
-    const int p = score_tile_block(a.tables, b, ch, a.MAXB, nb, a.P, a.flags);
-    float4 buf[kScoreSlots];
-    score_head_load<D>(a.ksum, p, a.Hkv, g, buf);
-    score_head_compute<D>(a.q, buf, a.zbuf, a.lse_part, b, ch, g, N, nb, a.Hkv, a.G, a.MAXB,
-                          a.nch_max, a.scale);
+  if (!COMPACT) {
+    const int tiles = (a.MAXB + kMfmaChunk - 1) / kMfmaChunk;
+    const int nsc = a.do_score ? a.B * tiles * nhg : 0;
+    const int id = blockIdx.x;
+    if (id < nsc) {
+      const int b = id / (tiles * nhg);
+      const int r = id - b * tiles * nhg;
+      const int ch = r / nhg;
+      const int N = a.ctx_lens[b];
+      if (N < 0 || N > a.MAXB * kBlock) return;    // flagged by the selection stage
+      if (ch * kMfmaChunk * kBlock >= N) return;
+      score_job<D>(a, b, ch, r - ch * nhg, N);
+      return;
+    }
+    const int e = id - nsc;
+    const int b = e / a.C;
+    entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats, e - b * a.C,
+                            b, red);
     return;
   }
-  const int e = id - nsc;
-  const int b = e / a.C;
-  entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats, e - b * a.C, b,
-                          red);
+  int* s_pref = s_mem;
+  int* s_N = s_mem + a.B + 1;
+  int n_score = 0;
+  if (a.do_score) {
+    tile_plan(a.ctx_lens, a.B, a.MAXB, s_pref, s_N, s_red);
+    n_score = s_pref[a.B] * nhg;
+  }
+  const int n_jobs = n_score + (a.do_entropy ? a.B * a.C : 0);
+  for (int job = blockIdx.x; job < n_jobs; job += gridDim.x) {
+    if (job < n_score) {
+      const int tile = job / nhg;
+      int lo = 0, hi = a.B;                 // largest b with s_pref[b] <= tile
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (s_pref[mid] <= tile) lo = mid; else hi = mid;
+      }
+      score_job<D>(a, lo, tile - s_pref[lo], job - tile * nhg, s_N[lo]);
+    } else {
+      const int e = job - n_score;
+      const int b = e / a.C;
+      entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats,
+                              e - b * a.C, b, red);
+    }
+  }
+}
+
+template <bool VEC, int D>
+int prologue_per_cu() {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, prologue_kernel<VEC, D, true>, kProThreads, 0) !=
+          hipSuccess || n < 1)
+    n = 1;
+  return n;
 }
 
 }  // namespace
 
+int prologue_grid_size(const ent_ctx* c) {
+  const int n = c->cfg.head_dim == 128
+                    ? std::min(prologue_per_cu<true, 128>(), prologue_per_cu<false, 128>())
+                    : std::min(prologue_per_cu<true, 64>(), prologue_per_cu<false, 64>());
+  return c->num_cu * n;
+}
+
 hipError_t launch_prologue(const ent_ctx* c, const PrologueArgs& a, hipStream_t s) {
   const ent_config& cf = c->cfg;
-  long long grid = 0;
-  if (a.do_score) grid += static_cast<long long>(a.B) * score_tiles(a.MAXB) * head_groups(a.Hkv);
-  if (a.do_entropy) grid += static_cast<long long>(a.B) * a.C;
-  if (grid == 0) return hipSuccess;
+  // Dense job slots (every sequence at its largest length).
+  long long slots = 0;
+  if (a.do_score)
+    slots += static_cast<long long>(a.B) * ((cf.max_blocks_per_seq + kMfmaChunk - 1) / kMfmaChunk) *
+             head_groups(a.Hkv);
+  if (a.do_entropy) slots += static_cast<long long>(a.B) * a.C;
+  if (slots == 0) return hipSuccess;
+  // Dispatching a workgroup costs time even when it exits at once: when the
+  // dense slots outnumber what the chip holds many times over (short
+  // sequences under a large block-table width), walk the compact job list.
+  const bool compact = slots > 16ll * c->prologue_grid;
+  const unsigned grid = static_cast<unsigned>(compact ? c->prologue_grid : slots);
+  const size_t lds = compact ? static_cast<size_t>(2 * a.B + 1) * sizeof(int) : 0;
   const bool vec = !a.do_entropy || row_vec_ok(a.logits, a.ld);
-  const dim3 g(static_cast<unsigned>(grid));
+#define ENT_PRO_LAUNCH(V, DD)                                                                  \
+  do {                                                                                         \
+    if (compact)                                                                               \
+      hipLaunchKernelGGL((prologue_kernel<V, DD, true>), dim3(grid), dim3(kProThreads), lds, s, a); \
+    else                                                                                       \
+      hipLaunchKernelGGL((prologue_kernel<V, DD, false>), dim3(grid), dim3(kProThreads), 0, s, a); \
+  } while (0)
   if (cf.head_dim == 128) {
-    if (vec)
-      hipLaunchKernelGGL((prologue_kernel<true, 128>), g, dim3(kProThreads), 0, s, a);
-    else
-      hipLaunchKernelGGL((prologue_kernel<false, 128>), g, dim3(kProThreads), 0, s, a);
+    if (vec) ENT_PRO_LAUNCH(true, 128); else ENT_PRO_LAUNCH(false, 128);
   } else {
-    if (vec)
-      hipLaunchKernelGGL((prologue_kernel<true, 64>), g, dim3(kProThreads), 0, s, a);
-    else
-      hipLaunchKernelGGL((prologue_kernel<false, 64>), g, dim3(kProThreads), 0, s, a);
+    if (vec) ENT_PRO_LAUNCH(true, 64); else ENT_PRO_LAUNCH(false, 64);
   }
+#undef ENT_PRO_LAUNCH
   return hipGetLastError();
 }
 
