@@ -64,6 +64,7 @@ struct DecodeArgs {
   unsigned* flags;
   int B, Hkv, G, MAXB, P;
   int W;              // waves of the decode grid
+  int R;              // ranges that write partials (workgroups for bf16, waves for fp32)
   int nsl;            // merge workgroups per segment
   float scale_log2;   // softmax scale times log2(e)
 };
@@ -172,20 +173,28 @@ template <int D>
 __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) {
   constexpr int KS = D / 32;      // QK k-steps (32 dims each)
   constexpr int MT = D / 16;      // PV output tiles (16 dims each)
-  extern __shared__ int s_mem[];
+  extern __shared__ __attribute__((aligned(16))) int s_mem[];
   __shared__ int s_red[kWaves];
-  int* s_pref = s_mem;
-  int* s_nk = s_mem + a.B + 1;
+  __shared__ int s_cseg[2 * kWaves];
+  // Dynamic LDS: cut partials first (16-byte aligned), then the plan.
+  float* s_cacc = reinterpret_cast<float*>(s_mem);
+  float* s_cml = s_cacc + 2 * kWaves * a.G * D;
+  int* s_pref = reinterpret_cast<int*>(s_cml + 2 * kWaves * kMaxGroup * 2);
+  int* s_nk = s_pref + a.B + 1;
   int* s_N = s_nk + a.B;
   build_plan(a, s_pref, s_nk, s_N, s_red);
   const int U = s_pref[a.B];
   const int lane = threadIdx.x & 63;
-  const int w = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  const int wave = threadIdx.x >> 6;
+  const int w = blockIdx.x * kWaves + wave;
   if (U == 0) return;
-  const int u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
-  if (u0 >= u1) return;
-  const int r16 = lane & 15, gq = lane >> 4;
   const int G = a.G;
+  // Cut partials of this workgroup's waves, merged in LDS at the end:
+  // slot 2 i (wave i's first segment, begun before its range) and 2 i + 1
+  // (its last, continuing after it): G x D sums and (max, sum) per head.
+  if (lane < 2) s_cseg[2 * wave + lane] = -1;
+  const int u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
+  const int r16 = lane & 15, gq = lane >> 4;
   const int Hq = a.Hkv * G;
   const bool head_ok = r16 < G;
   const uint16_t* q = static_cast<const uint16_t*>(a.q);
@@ -194,6 +203,7 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
 
   int ubase = u0;
   UnitMeta win = unit_meta(a, ubase + lane, u1, s_pref, s_nk, s_N);
+  const bool busy = u0 < u1;
 
   bf16x8_t kcur[KS], knxt[KS];
   s16x4_t vcur[MT], vnxt[MT];
@@ -209,7 +219,7 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
 #pragma unroll
     for (int m = 0; m < MT; ++m) vr[m] = load_s16x4(vc + tile + (16 * m + r16) * kBlock + 4 * gq);
   };
-  load_tiles(0, kcur, vcur);
+  if (busy) load_tiles(0, kcur, vcur);
 
   int cur_seg = -1;
   bf16x8_t qreg[KS];
@@ -233,14 +243,17 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
       }
       if (gq == 0 && a.lse) a.lse[oh] = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
     } else {
-      const long long slot = static_cast<long long>(w) + cur_seg;
+      // Cut by this wave's range: keep the partial for the workgroup merge.
+      const int cs = 2 * wave + (seg_start < u0 ? 0 : 1);
+      if (lane == 0) s_cseg[cs] = cur_seg;
+      float* acc = s_cacc + (static_cast<long long>(cs) * G + r16) * D;
 #pragma unroll
       for (int m = 0; m < MT; ++m)
-        *reinterpret_cast<float4*>(a.part_acc + (slot * G + r16) * D + 16 * m + 4 * gq) =
+        *reinterpret_cast<float4*>(acc + 16 * m + 4 * gq) =
             make_float4(oacc[m][0], oacc[m][1], oacc[m][2], oacc[m][3]);
       if (gq == 0) {
-        a.part_ml[(slot * G + r16) * 2 + 0] = m_run;
-        a.part_ml[(slot * G + r16) * 2 + 1] = l_tot;
+        s_cml[(cs * kMaxGroup + r16) * 2 + 0] = m_run;
+        s_cml[(cs * kMaxGroup + r16) * 2 + 1] = l_tot;
       }
     }
   };
@@ -335,7 +348,58 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
     unit(u, knxt, vnxt, kcur, vcur);
     ++u;
   }
-  flush();
+  if (busy) flush();
+
+  // Workgroup merge: consecutive slots of one segment (in unit order) are one
+  // group; a group whose segment lies inside the workgroup's range is final,
+  // else it becomes the workgroup's partial of that segment (slot wg + seg).
+  __syncthreads();
+  const int wg = blockIdx.x;
+  const int g0 = range_begin(wg * kWaves, U, a.W), g1 = range_begin(wg * kWaves + kWaves, U, a.W);
+  int i = 0;
+  while (i < 2 * kWaves) {
+    const int seg = s_cseg[i];
+    if (seg < 0) {
+      ++i;
+      continue;
+    }
+    int j = i + 1;
+    while (j < 2 * kWaves && (s_cseg[j] == seg || s_cseg[j] < 0)) ++j;
+    // Slots i .. j-1 with s_cseg == seg form the group.
+    const int b = seg / a.Hkv, g = seg % a.Hkv;
+    const int seg_start = s_pref[b] + g * s_nk[b];
+    const int seg_end = seg_start + s_nk[b];
+    const bool whole = seg_start >= g0 && seg_end <= g1;
+    const long long slot = static_cast<long long>(wg) + seg;
+    for (int o = threadIdx.x; o < G * D; o += kThreads) {
+      const int r = o / D, d = o - r * D;
+      float M = -INFINITY;
+      for (int k = i; k < j; ++k)
+        if (s_cseg[k] == seg && s_cml[(k * kMaxGroup + r) * 2 + 1] > 0.f)
+          M = fmaxf(M, s_cml[(k * kMaxGroup + r) * 2]);
+      float L = 0.f, acc = 0.f;
+      for (int k = i; k < j; ++k) {
+        if (s_cseg[k] != seg) continue;
+        const float l = s_cml[(k * kMaxGroup + r) * 2 + 1];
+        if (!(l > 0.f)) continue;
+        const float f = exp2f(s_cml[(k * kMaxGroup + r) * 2] - M);
+        L += l * f;
+        acc += f * s_cacc[(static_cast<long long>(k) * G + r) * D + d];
+      }
+      if (whole) {
+        const long long oh = static_cast<long long>(b) * Hq + g * G + r;
+        a.out[oh * D + d] = L > 0.f ? acc / L : 0.f;
+        if (d == 0 && a.lse) a.lse[oh] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+      } else {
+        a.part_acc[(slot * G + r) * D + d] = acc;
+        if (d == 0) {
+          a.part_ml[(slot * G + r) * 2 + 0] = M;
+          a.part_ml[(slot * G + r) * 2 + 1] = L;
+        }
+      }
+    }
+    i = j;
+  }
 }
 
 template <int D>
@@ -513,8 +577,8 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int item) {
     return;
   }
   const int seg_start = s_pref[b] + g * nk;
-  const int w0 = wave_of(seg_start, U, a.W);
-  const int w1 = wave_of(seg_start + nk - 1, U, a.W);
+  const int w0 = wave_of(seg_start, U, a.R);
+  const int w1 = wave_of(seg_start + nk - 1, U, a.R);
   if (w0 == w1) return;                      // written whole by the decode kernel
   const int ns = w1 - w0 + 1;
 
@@ -528,7 +592,7 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int item) {
       const int k = e / G, rr = e % G;
       const int wi = w0 + c0 + k;
       // A wave with an empty range (fewer units than waves) wrote no partial.
-      const bool live = range_begin(wi + 1, U, a.W) > range_begin(wi, U, a.W);
+      const bool live = range_begin(wi + 1, U, a.R) > range_begin(wi, U, a.R);
       const long long slot = static_cast<long long>(wi) + seg;
       s_m[e] = live ? a.part_ml[(slot * G + rr) * 2 + 0] : 0.f;
       s_l[e] = live ? a.part_ml[(slot * G + rr) * 2 + 1] : 0.f;
@@ -625,15 +689,22 @@ int occupancy_blocks(K kernel, size_t lds) {
 
 size_t plan_lds_bytes(int B) { return static_cast<size_t>(3 * B + 1) * sizeof(int); }
 
+// bf16 decode: the workgroup's cut partials, then the plan.
+size_t decode_lds_bytes(int B, int G, int D) {
+  return static_cast<size_t>(2 * kWaves) * (static_cast<size_t>(G) * D + kMaxGroup * 2) * sizeof(float) +
+         plan_lds_bytes(B);
+}
+
 }  // namespace
 
 int decode_grid_size(const ent_ctx* c) {
   const ent_config& cf = c->cfg;
   const size_t lds = plan_lds_bytes(cf.max_batch);
+  const size_t lds16 = decode_lds_bytes(cf.max_batch, c->group, cf.head_dim);
   int per_cu = 1;
   if (cf.kv_dtype == ENT_BF16)
-    per_cu = cf.head_dim == 128 ? occupancy_blocks(decode_bf16_kernel<128>, lds)
-                                : occupancy_blocks(decode_bf16_kernel<64>, lds);
+    per_cu = cf.head_dim == 128 ? occupancy_blocks(decode_bf16_kernel<128>, lds16)
+                                : occupancy_blocks(decode_bf16_kernel<64>, lds16);
   else
     per_cu = cf.head_dim == 128 ? occupancy_blocks(decode_f32_kernel<128>, lds)
                                 : occupancy_blocks(decode_f32_kernel<64>, lds);
@@ -669,14 +740,16 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   a.MAXB = cf.max_blocks_per_seq;
   a.P = cf.num_pool_blocks;
   a.W = c->decode_grid * kWaves;
+  a.R = cf.kv_dtype == ENT_BF16 ? c->decode_grid : a.W;
   a.scale_log2 = cf.scale * kLog2e;
   const size_t lds = plan_lds_bytes(B);
   const dim3 grid(c->decode_grid);
   if (cf.kv_dtype == ENT_BF16) {
+    const size_t lds16 = decode_lds_bytes(B, c->group, cf.head_dim);
     if (cf.head_dim == 128)
-      hipLaunchKernelGGL(decode_bf16_kernel<128>, grid, dim3(kThreads), lds, s, a);
+      hipLaunchKernelGGL(decode_bf16_kernel<128>, grid, dim3(kThreads), lds16, s, a);
     else
-      hipLaunchKernelGGL(decode_bf16_kernel<64>, grid, dim3(kThreads), lds, s, a);
+      hipLaunchKernelGGL(decode_bf16_kernel<64>, grid, dim3(kThreads), lds16, s, a);
   } else {
     if (cf.head_dim == 128)
       hipLaunchKernelGGL(decode_f32_kernel<128>, grid, dim3(kThreads), lds, s, a);
@@ -687,7 +760,7 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   if (e != hipSuccess) return e;
   // Slices per segment: split the outputs (and the partials across thread
   // groups) when segments are cut into many partials on average.
-  const int waves_per_seg = a.W / std::max(1, B * cf.num_kv_heads);
+  const int waves_per_seg = a.R / std::max(1, B * cf.num_kv_heads);
   const int nsl = waves_per_seg >= 8 ? c->group * cf.head_dim / 64 : 1;
   a.nsl = nsl;
   if (sample) {
