@@ -285,7 +285,10 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
 #pragma unroll
       for (int m = 0; m < MT; ++m) oacc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
-    if (i + 1 < kWindow && u + 1 < u1) load_tiles(i + 1, kn, vn);
+    // The next unit's tiles, issued unconditionally so that the wait below
+    // covers only the current unit's loads; past the end of the window or of
+    // the range the current tiles are re-read (cache hits) and discarded.
+    load_tiles((i + 1 < kWindow && u + 1 < u1) ? i + 1 : i, kn, vn);
     const int p = __shfl(win.p, i);
     const int nv = __shfl(win.nv, i);
     if (p >= 0) {
