@@ -14,10 +14,12 @@
 //   summary_kernel   per-block mean keys (setup)
 //   (bf16 scoring runs in the persistent kernel of prologue.hip)
 //   score_valu_kernel   z for 16 blocks x all heads per workgroup (fp32, VALU)
-//   lse_merge_kernel    per sequence: L_h from the per-tile log-sum-exp partials
-//   block_score_kernel  per 64 blocks: I_b
-//   select_kernel       per sequence: the budget, an 8-bit radix select of the
-//                       k-th largest score, ascending compaction with ballots
+//   select_fused_kernel per sequence (short block tables): L_h, I_b, the
+//                       budget, an 8-bit radix select of the k-th largest
+//                       score, ascending compaction with ballots
+//   lse_merge_kernel,   the same in three launches for long block tables:
+//   block_score_kernel, per sequence L_h; per 64 blocks I_b; per sequence
+//   select_kernel       the selection
 //   append_kernel    writes one token and refreshes its block's mean key
 
 #include "blocks_dev.h"
@@ -111,7 +113,8 @@ __global__ __launch_bounds__(kRowThreads) void lse_merge_kernel(
     const float* __restrict__ lse_part, const int* __restrict__ ctx_lens, float* __restrict__ L,
     int Hq, int MAXB, int nch_max) {
   __shared__ float s_pm[kRowThreads], s_ps[kRowThreads];
-  lse_merge_body(lse_part, ctx_lens, L, Hq, MAXB, nch_max, blockIdx.x, s_pm, s_ps);
+  lse_merge_body(lse_part, ctx_lens, L + static_cast<long long>(blockIdx.x) * Hq, Hq, MAXB, nch_max,
+                 blockIdx.x, s_pm, s_ps);
 }
 
 __global__ __launch_bounds__(kRowThreads) void block_score_kernel(
@@ -131,6 +134,20 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   const int b = blockIdx.x;
   select_row_body(scores, ctx_lens, hvec[b], theta_out, kept, n_kept, MAXB, eps_h, h_min, log_v,
                   kappa_min, b_min, flags, b, keys, sh);
+}
+
+// All three selection steps per sequence (short block tables).
+__global__ __launch_bounds__(kSelThreads) void select_fused_kernel(
+    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, const float* __restrict__ hvec, float* __restrict__ scores,
+    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int Hq,
+    int MAXB, int nch_max, float eps_h, float h_min, float log_v, float kappa_min, int b_min,
+    unsigned* flags) {
+  extern __shared__ unsigned keys[];        // [MAXB]
+  __shared__ SelectShared sh;
+  const int b = blockIdx.x;
+  select_fused_body(zbuf, lse_part, ctx_lens, hvec[b], scores, theta_out, kept, n_kept, Hq, MAXB,
+                    nch_max, eps_h, h_min, log_v, kappa_min, b_min, flags, b, keys, sh);
 }
 
 template <int D>
@@ -213,9 +230,23 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
     e = launch_score_valu(c, B, q, ksum, tables, ctx_lens, s);
   }
   if (e != hipSuccess) return e;
+  return launch_selection(c, B, ctx_lens, h, scores, theta, kept, n_kept, s);
+}
+
+hipError_t launch_selection(const ent_ctx* c, int B, const int* ctx_lens, const float* h,
+                            float* scores, float* theta, int* kept, int* n_kept, hipStream_t s) {
+  const ent_config& cf = c->cfg;
+  const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
+  if (cf.max_blocks_per_seq <= kFusedSelectMaxBlocks) {
+    hipLaunchKernelGGL(select_fused_kernel, dim3(B), dim3(kSelThreads), lds, s, c->zbuf,
+                       c->lse_part, ctx_lens, h, scores, theta, kept, n_kept, cf.num_q_heads,
+                       cf.max_blocks_per_seq, c->lse_chunks, cf.eps_h, cf.h_min, cf.log_v,
+                       cf.kappa_min, cf.b_min, c->dev_flags);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(lse_merge_kernel, dim3(B), dim3(kRowThreads), 0, s, c->lse_part, ctx_lens,
                      c->lrow, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks);
-  e = hipGetLastError();
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   float* sc = scores ? scores : c->iscores;
   e = launch_block_scores(c, B, ctx_lens, sc, s);

@@ -297,28 +297,32 @@ __device__ __forceinline__ int keep_budget(float h, int nb, float eps_h, float h
   return min(nb, max(min(b_min, nb), k));
 }
 
-// Kept set of one sequence, in three phases:
-//  A. (one workgroup per sequence) L_h = ln sum_b n_b e^{z_bh}, merged from
-//     the scoring pass's per-tile partials;
-//  B. (one workgroup per 64 blocks) I_b = (1/H_q) sum_h e^{z_bh + ln n_b - L_h}
-//     (L_h - z_bh) for every block;
-//  C. (one workgroup per sequence) budget k from the entropy, the k-th
-//     largest score by an 8-bit radix select over the bits in which the
-//     scores differ, and ascending compaction of {b : I_b >= theta} with
-//     wave ballots.
-// Phase B spreads the exponentials of long sequences over the whole chip;
-// the two per-sequence phases only merge and select.
-constexpr int kRowThreads = 256;          // phase A
-constexpr int kTileBlocks = 64;           // phase B: blocks per workgroup (4 lanes each)
-constexpr int kSelThreads = 512;          // phase C
+// Kept set of one sequence.  Three steps:
+//  A. L_h = ln sum_b n_b e^{z_bh}, merged from the scoring pass's per-tile
+//     partials (one workgroup per sequence);
+//  B. I_b = (1/H_q) sum_h e^{z_bh + ln n_b - L_h} (L_h - z_bh) for every
+//     block, four lanes per block;
+//  C. budget k from the entropy, the k-th largest score by an 8-bit radix
+//     select over the bits in which the scores differ, and ascending
+//     compaction of {b : I_b >= theta} with wave ballots.
+// When the block tables are short (kFusedSelectMaxBlocks), one workgroup per
+// sequence runs all three; otherwise B runs as its own chip-wide launch (one
+// workgroup per 64 blocks) between two per-sequence launches, so long
+// sequences spread their exponentials over the chip.  Both forms perform the
+// same arithmetic in the same order, so their results are identical.
+constexpr int kRowThreads = 256;          // threads of the L merge
+constexpr int kTileBlocks = 64;           // blocks per scoring workgroup of step B
+constexpr int kSelThreads = 512;          // step C (and the one-launch form)
 constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kFusedSelectMaxBlocks = 1024;
 
-// Phase A for sequence b by kRowThreads threads: writes L_h to L[b * Hq + h]
-// (-inf for an empty or invalid sequence).
+// Step A for sequence b: the first kRowThreads threads fold, every thread of
+// the workgroup must call it.  Writes L_h to Lout[h] (-inf for an empty or
+// invalid sequence); Lout may be global or LDS memory.
 __device__ __forceinline__ void lse_merge_body(const float* __restrict__ lse_part,
-                                               const int* __restrict__ ctx_lens,
-                                               float* __restrict__ L, int Hq, int MAXB,
-                                               int nch_max, int b, float* s_pm, float* s_ps) {
+                                               const int* __restrict__ ctx_lens, float* Lout,
+                                               int Hq, int MAXB, int nch_max, int b, float* s_pm,
+                                               float* s_ps) {
   const int t = threadIdx.x;
   const int N = ctx_lens[b];
   const int nb = (N >= 0 && N <= MAXB * kBlock) ? (N + kBlock - 1) / kBlock : 0;
@@ -327,19 +331,21 @@ __device__ __forceinline__ void lse_merge_body(const float* __restrict__ lse_par
   // Each thread folds a strided subset of the tiles of head t % Hq: first
   // their maximum, then the rescaled sums (independent loads, no serial
   // rescaling chain).
-  float m = -INFINITY, sum = 0.f;
-  if (t < per_head * Hq) {
-    const int h = t % Hq;
-    const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
-    for (int c = t / Hq; c < nch; c += per_head) m = fmaxf(m, lp[static_cast<long long>(c) * Hq * 2]);
-    if (m != -INFINITY)
-      for (int c = t / Hq; c < nch; c += per_head) {
-        const float mc = lp[static_cast<long long>(c) * Hq * 2];
-        sum += lp[static_cast<long long>(c) * Hq * 2 + 1] * expf(mc - m);
-      }
+  if (t < kRowThreads) {
+    float m = -INFINITY, sum = 0.f;
+    if (t < per_head * Hq) {
+      const int h = t % Hq;
+      const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
+      for (int c = t / Hq; c < nch; c += per_head) m = fmaxf(m, lp[static_cast<long long>(c) * Hq * 2]);
+      if (m != -INFINITY)
+        for (int c = t / Hq; c < nch; c += per_head) {
+          const float mc = lp[static_cast<long long>(c) * Hq * 2];
+          sum += lp[static_cast<long long>(c) * Hq * 2 + 1] * expf(mc - m);
+        }
+    }
+    s_pm[t] = m;
+    s_ps[t] = sum;
   }
-  s_pm[t] = m;
-  s_ps[t] = sum;
   __syncthreads();
   if (t < Hq) {
     float mm = -INFINITY, ss = 0.f;
@@ -350,26 +356,16 @@ __device__ __forceinline__ void lse_merge_body(const float* __restrict__ lse_par
       ss = ss * expf(mm - mn) + sc * expf(mc - mn);
       mm = mn;
     }
-    L[static_cast<long long>(b) * Hq + t] = (mm == -INFINITY) ? -INFINITY : mm + logf(ss);
+    Lout[t] = (mm == -INFINITY) ? -INFINITY : mm + logf(ss);
   }
 }
 
-// Phase B: scores of blocks j0 .. j0 + 63 of sequence b by 256 threads; four
-// lanes per block, lane quarter qq takes heads qq, qq + 4, ...  Writes I_b to
-// scores[b * MAXB + j].
-__device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
-                                                 const float* __restrict__ L,
-                                                 const int* __restrict__ ctx_lens,
-                                                 float* __restrict__ scores, int Hq, int MAXB,
-                                                 int b, int j0, float* sL) {
-  const int t = threadIdx.x;
-  const int N = ctx_lens[b];
-  if (N < 0 || N > MAXB * kBlock) return;    // flagged in phase C
-  const int nb = (N + kBlock - 1) / kBlock;
-  if (j0 >= nb) return;
-  for (int h = t; h < Hq; h += kRowThreads) sL[h] = L[static_cast<long long>(b) * Hq + h];
-  __syncthreads();
-  const int j = j0 + (t >> 2), qq = t & 3;
+// Step B for block j of sequence b (context N, nb blocks) by the four lanes
+// qq = 0..3 of a lane quad (heads qq, qq + 4, ...); the score in every lane
+// of the quad.  sL: L_h in LDS.
+__device__ __forceinline__ float block_score_quad(const float* __restrict__ zbuf, const float* sL,
+                                                  int Hq, int MAXB, int b, int j, int N, int nb,
+                                                  int qq) {
   float acc = 0.f;
   if (j < nb) {
     const float lnn = logf(static_cast<float>(j == nb - 1 ? N - kBlock * (nb - 1) : kBlock));
@@ -381,48 +377,43 @@ __device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
   }
   acc += __shfl_xor(acc, 1);
   acc += __shfl_xor(acc, 2);
-  if (j < nb && qq == 0)
-    scores[static_cast<long long>(b) * MAXB + j] = __fdiv_rn(acc, static_cast<float>(Hq));
+  return __fdiv_rn(acc, static_cast<float>(Hq));
+}
+
+// Step B as its own launch: blocks j0 .. j0 + 63 of sequence b by 256 threads.
+__device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
+                                                 const float* __restrict__ L,
+                                                 const int* __restrict__ ctx_lens,
+                                                 float* __restrict__ scores, int Hq, int MAXB,
+                                                 int b, int j0, float* sL) {
+  const int t = threadIdx.x;
+  const int N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) return;    // flagged in step C
+  const int nb = (N + kBlock - 1) / kBlock;
+  if (j0 >= nb) return;
+  for (int h = t; h < Hq; h += kRowThreads) sL[h] = L[static_cast<long long>(b) * Hq + h];
+  __syncthreads();
+  const int j = j0 + (t >> 2);
+  const float I = block_score_quad(zbuf, sL, Hq, MAXB, b, j, N, nb, t & 3);
+  if (j < nb && (t & 3) == 0) scores[static_cast<long long>(b) * MAXB + j] = I;
 }
 
 struct SelectShared {
   unsigned hist[256];
   unsigned red[2 * kSelWaves];
+  float pm[kRowThreads], ps[kRowThreads], L[128];
   int digit, krem, wcnt[kSelWaves];
 };
 
-// Phase C for sequence b by kSelThreads threads.  keys: LDS [MAXB]; hval: the
-// sequence's entropy; scores: phase B's output.
-__device__ __forceinline__ void select_row_body(
-    const float* __restrict__ scores, const int* __restrict__ ctx_lens, float hval,
-    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
-    float eps_h, float h_min, float log_v, float kappa_min, int b_min, unsigned* flags, int b,
-    unsigned* keys, SelectShared& sh) {
+// Step C core: the nb keys of sequence b are in LDS (keys), k >= 1.
+__device__ __forceinline__ void select_core(unsigned* keys, int nb, int k,
+                                            float* __restrict__ theta_out, int* __restrict__ kept,
+                                            int* __restrict__ n_kept, int MAXB, int b,
+                                            SelectShared& sh) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int N = ctx_lens[b];
-  if (N < 0 || N > MAXB * kBlock) {
-    if (t == 0) {
-      raise_flag(flags, ENT_DEV_BAD_CTXLEN);
-      n_kept[b] = 0;
-      if (theta_out) theta_out[b] = INFINITY;
-    }
-    return;
-  }
-  const int nb = (N + kBlock - 1) / kBlock;
-  const int k = keep_budget(hval, nb, eps_h, h_min, log_v, kappa_min, b_min);
-  if (nb == 0 || k <= 0) {
-    if (t == 0) {
-      n_kept[b] = 0;
-      if (theta_out) theta_out[b] = INFINITY;
-    }
-    return;
-  }
-  // Keys in LDS, and the bits in which they differ.
-  const float* sr = scores + static_cast<long long>(b) * MAXB;
   unsigned kmin = 0xFFFFFFFFu, kmax = 0u;
   for (int i = t; i < nb; i += kSelThreads) {
-    const unsigned key = float_key(sr[i]);
-    keys[i] = key;
+    const unsigned key = keys[i];
     kmin = min(kmin, key);
     kmax = max(kmax, key);
   }
@@ -515,6 +506,94 @@ __device__ __forceinline__ void select_row_body(
     n_kept[b] = total;
     if (theta_out) theta_out[b] = key_float(tkey);
   }
+}
+
+// No block kept: the outputs of sequence b.
+__device__ __forceinline__ void select_none(float* __restrict__ theta_out, int* __restrict__ n_kept,
+                                            int b) {
+  if (threadIdx.x == 0) {
+    n_kept[b] = 0;
+    if (theta_out) theta_out[b] = INFINITY;
+  }
+}
+
+// Validates sequence b's context and returns its blocks and budget; false
+// (outputs written) when the context is invalid or empty.  Uniform across
+// the workgroup.
+__device__ __forceinline__ bool select_prepare(const int* __restrict__ ctx_lens, float hval,
+                                               float* __restrict__ theta_out,
+                                               int* __restrict__ n_kept, int MAXB, float eps_h,
+                                               float h_min, float log_v, float kappa_min,
+                                               int b_min, unsigned* flags, int b, int& N, int& nb,
+                                               int& k) {
+  const int t = threadIdx.x;
+  N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) {
+    if (t == 0) {
+      raise_flag(flags, ENT_DEV_BAD_CTXLEN);
+      n_kept[b] = 0;
+      if (theta_out) theta_out[b] = INFINITY;
+    }
+    return false;
+  }
+  nb = (N + kBlock - 1) / kBlock;
+  k = keep_budget(hval, nb, eps_h, h_min, log_v, kappa_min, b_min);
+  if (nb == 0) {
+    select_none(theta_out, n_kept, b);
+    return false;
+  }
+  return true;
+}
+
+// Step C as its own launch: keys from step B's scores.
+__device__ __forceinline__ void select_row_body(
+    const float* __restrict__ scores, const int* __restrict__ ctx_lens, float hval,
+    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
+    float eps_h, float h_min, float log_v, float kappa_min, int b_min, unsigned* flags, int b,
+    unsigned* keys, SelectShared& sh) {
+  int N, nb, k;
+  if (!select_prepare(ctx_lens, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min,
+                      b_min, flags, b, N, nb, k))
+    return;
+  if (k <= 0) {
+    select_none(theta_out, n_kept, b);
+    return;
+  }
+  const float* sr = scores + static_cast<long long>(b) * MAXB;
+  for (int i = threadIdx.x; i < nb; i += kSelThreads) keys[i] = float_key(sr[i]);
+  __syncthreads();
+  select_core(keys, nb, k, theta_out, kept, n_kept, MAXB, b, sh);
+}
+
+// Steps A, B and C in one workgroup (short block tables).  scores_out
+// (nullable) receives I_b.
+__device__ __forceinline__ void select_fused_body(
+    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, float hval, float* __restrict__ scores_out,
+    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int Hq,
+    int MAXB, int nch_max, float eps_h, float h_min, float log_v, float kappa_min, int b_min,
+    unsigned* flags, int b, unsigned* keys, SelectShared& sh) {
+  int N, nb, k;
+  if (!select_prepare(ctx_lens, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min,
+                      b_min, flags, b, N, nb, k))
+    return;
+  lse_merge_body(lse_part, ctx_lens, sh.L, Hq, MAXB, nch_max, b, sh.pm, sh.ps);
+  __syncthreads();
+  const int t = threadIdx.x;
+  for (int j0 = 0; j0 < nb; j0 += kSelThreads / 4) {
+    const int j = j0 + (t >> 2);
+    const float I = block_score_quad(zbuf, sh.L, Hq, MAXB, b, j, N, nb, t & 3);
+    if (j < nb && (t & 3) == 0) {
+      keys[j] = float_key(I);
+      if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j] = I;
+    }
+  }
+  __syncthreads();
+  if (k <= 0) {
+    select_none(theta_out, n_kept, b);
+    return;
+  }
+  select_core(keys, nb, k, theta_out, kept, n_kept, MAXB, b, sh);
 }
 
 }  // namespace

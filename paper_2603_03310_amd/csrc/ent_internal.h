@@ -86,6 +86,10 @@ struct PrologueArgs {
 };
 hipError_t launch_prologue(const ent_ctx* c, const PrologueArgs& a, hipStream_t s);
 int prologue_grid_size(const ent_ctx* c);
+// The kept-block selection after scoring (L merge, block scores, radix
+// select), given each sequence's entropy h.
+hipError_t launch_selection(const ent_ctx* c, int B, const int* ctx_lens, const float* h,
+                            float* scores, float* theta, int* kept, int* n_kept, hipStream_t s);
 // Selection phases B (block scores from c->lrow) and C (radix select).
 hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,
                                hipStream_t s);

@@ -8,9 +8,10 @@
 //      do not depend on each other (fp32 queries: scoring is a second
 //      launch, on the VALU);
 //   B  one workgroup per sequence: the row's entropy from the chunk triples,
-//      the controller update and L_h; then the block scores over the whole
-//      chip, and one workgroup per sequence for the kept-block selection
-//      under the entropy-driven budget;
+//      the controller update and the kept-block selection under the
+//      entropy-driven budget (for long block tables: entropy, controller and
+//      L_h per sequence, the block scores over the whole chip, then the
+//      selection per sequence);
 //   C  kept-block decode attention;
 //   D  the merge of split decode segments and, in the same launch, sampling
 //      at the temperature the step used (independent of the merge).
@@ -36,7 +37,34 @@ __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
       controller_update(b, H, temp[b], h_prev, tau, temp, h_out, temp_used, eta, h_target, t_min,
                         t_max);
   }
-  lse_merge_body(lse_part, ctx_lens, L, Hq, MAXB, nch_max, b, s_pm, s_ps);
+  lse_merge_body(lse_part, ctx_lens, L + static_cast<long long>(b) * Hq, Hq, MAXB, nch_max, b,
+                 s_pm, s_ps);
+}
+
+// Per sequence, short block tables: the row's entropy and the controller
+// update (first wave), then the whole kept-block selection.
+__global__ __launch_bounds__(kSelThreads) void step_b_kernel(
+    const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau, float* h_out,
+    float* temp_used, float eta, float h_target, float t_min, float t_max,
+    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, float* __restrict__ scores, float* __restrict__ theta,
+    int* __restrict__ kept, int* __restrict__ n_kept, int Hq, int MAXB, int nch_max, float eps_h,
+    float h_min, float log_v, float kappa_min, int b_min, unsigned* flags) {
+  extern __shared__ unsigned keys[];        // [MAXB]
+  __shared__ SelectShared sh;
+  __shared__ float s_H;
+  const int b = blockIdx.x;
+  if (threadIdx.x < 64) {
+    const float H = row_entropy(part, C, b);
+    if (threadIdx.x == 0) {
+      s_H = H;
+      controller_update(b, H, temp[b], h_prev, tau, temp, h_out, temp_used, eta, h_target, t_min,
+                        t_max);
+    }
+  }
+  __syncthreads();
+  select_fused_body(zbuf, lse_part, ctx_lens, s_H, scores, theta, kept, n_kept, Hq, MAXB, nch_max,
+                    eps_h, h_min, log_v, kappa_min, b_min, flags, b, keys, sh);
 }
 
 }  // namespace
@@ -82,17 +110,28 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
     if (e != hipSuccess) return e;
   }
 
-  hipLaunchKernelGGL(step_b0_kernel, dim3(B), dim3(kRowThreads), 0, s, c->ent_part, c->chunks,
-                     st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta, cf.h_target, cf.t_min,
-                     cf.t_max, c->lse_part, ctx_lens, c->lrow, cf.num_q_heads,
-                     cf.max_blocks_per_seq, c->lse_chunks);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  float* sc = scores ? scores : c->iscores;
-  e = launch_block_scores(c, B, ctx_lens, sc, s);
-  if (e != hipSuccess) return e;
-  e = launch_select_rows(c, B, ctx_lens, h_out, sc, theta, kept, n_kept, s);
-  if (e != hipSuccess) return e;
+  if (cf.max_blocks_per_seq <= kFusedSelectMaxBlocks) {
+    const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
+    hipLaunchKernelGGL(step_b_kernel, dim3(B), dim3(kSelThreads), lds, s, c->ent_part, c->chunks,
+                       st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta, cf.h_target,
+                       cf.t_min, cf.t_max, c->zbuf, c->lse_part, ctx_lens, scores, theta, kept,
+                       n_kept, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks, cf.eps_h,
+                       cf.h_min, cf.log_v, cf.kappa_min, cf.b_min, c->dev_flags);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  } else {
+    hipLaunchKernelGGL(step_b0_kernel, dim3(B), dim3(kRowThreads), 0, s, c->ent_part, c->chunks,
+                       st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta, cf.h_target,
+                       cf.t_min, cf.t_max, c->lse_part, ctx_lens, c->lrow, cf.num_q_heads,
+                       cf.max_blocks_per_seq, c->lse_chunks);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    float* sc = scores ? scores : c->iscores;
+    e = launch_block_scores(c, B, ctx_lens, sc, s);
+    if (e != hipSuccess) return e;
+    e = launch_select_rows(c, B, ctx_lens, h_out, sc, theta, kept, n_kept, s);
+    if (e != hipSuccess) return e;
+  }
   SampleArgs sa;
   sa.logits = logits;
   sa.ld = ld;
