@@ -137,17 +137,18 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 }
 
 // All three selection steps per sequence (short block tables).
+template <int HPL>
 __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, const float* __restrict__ hvec, float* __restrict__ scores,
-    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int Hq,
-    int MAXB, int nch_max, float eps_h, float h_min, float log_v, float kappa_min, int b_min,
+    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
+    int nch_max, float eps_h, float h_min, float log_v, float kappa_min, int b_min,
     unsigned* flags) {
   extern __shared__ unsigned keys[];        // [MAXB]
   __shared__ SelectShared sh;
   const int b = blockIdx.x;
-  select_fused_body(zbuf, lse_part, ctx_lens, hvec[b], scores, theta_out, kept, n_kept, Hq, MAXB,
-                    nch_max, eps_h, h_min, log_v, kappa_min, b_min, flags, b, keys, sh);
+  select_fused_body<HPL>(zbuf, lse_part, ctx_lens, hvec[b], scores, theta_out, kept, n_kept, MAXB,
+                         nch_max, eps_h, h_min, log_v, kappa_min, b_min, flags, b, keys, sh);
 }
 
 template <int D>
@@ -237,11 +238,25 @@ hipError_t launch_selection(const ent_ctx* c, int B, const int* ctx_lens, const 
                             float* scores, float* theta, int* kept, int* n_kept, hipStream_t s) {
   const ent_config& cf = c->cfg;
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-  if (cf.max_blocks_per_seq <= kFusedSelectMaxBlocks) {
-    hipLaunchKernelGGL(select_fused_kernel, dim3(B), dim3(kSelThreads), lds, s, c->zbuf,
-                       c->lse_part, ctx_lens, h, scores, theta, kept, n_kept, cf.num_q_heads,
-                       cf.max_blocks_per_seq, c->lse_chunks, cf.eps_h, cf.h_min, cf.log_v,
-                       cf.kappa_min, cf.b_min, c->dev_flags);
+  const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
+  if (hpl) {
+    const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
+#define ENT_SEL_CASE(HH)                                                                       \
+  case HH:                                                                                     \
+    hipLaunchKernelGGL((select_fused_kernel<HH>), dim3(B), dim3(kSelThreads), lds, s, c->zbuf, \
+                       c->lse_part, ctx_lens, h, scores, theta, kept, n_kept,                  \
+                       cf.max_blocks_per_seq, c->lse_chunks, cf.eps_h, cf.h_min, cf.log_v,     \
+                       cf.kappa_min, cf.b_min, c->dev_flags);                                  \
+    break;
+    switch (hpl) {
+      ENT_SEL_CASE(1)
+      ENT_SEL_CASE(2)
+      ENT_SEL_CASE(4)
+      ENT_SEL_CASE(8)
+      default:
+        return hipErrorInvalidValue;
+    }
+#undef ENT_SEL_CASE
     return hipGetLastError();
   }
   hipLaunchKernelGGL(lse_merge_kernel, dim3(B), dim3(kRowThreads), 0, s, c->lse_part, ctx_lens,

@@ -520,14 +520,12 @@ __device__ __forceinline__ void select_none(float* __restrict__ theta_out, int* 
 // Validates sequence b's context and returns its blocks and budget; false
 // (outputs written) when the context is invalid or empty.  Uniform across
 // the workgroup.
-__device__ __forceinline__ bool select_prepare(const int* __restrict__ ctx_lens, float hval,
-                                               float* __restrict__ theta_out,
+__device__ __forceinline__ bool select_prepare(int N, float hval, float* __restrict__ theta_out,
                                                int* __restrict__ n_kept, int MAXB, float eps_h,
                                                float h_min, float log_v, float kappa_min,
-                                               int b_min, unsigned* flags, int b, int& N, int& nb,
+                                               int b_min, unsigned* flags, int b, int& nb,
                                                int& k) {
   const int t = threadIdx.x;
-  N = ctx_lens[b];
   if (N < 0 || N > MAXB * kBlock) {
     if (t == 0) {
       raise_flag(flags, ENT_DEV_BAD_CTXLEN);
@@ -551,9 +549,10 @@ __device__ __forceinline__ void select_row_body(
     float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
     float eps_h, float h_min, float log_v, float kappa_min, int b_min, unsigned* flags, int b,
     unsigned* keys, SelectShared& sh) {
-  int N, nb, k;
-  if (!select_prepare(ctx_lens, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min,
-                      b_min, flags, b, N, nb, k))
+  const int N = ctx_lens[b];
+  int nb, k;
+  if (!select_prepare(N, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min,
+                      flags, b, nb, k))
     return;
   if (k <= 0) {
     select_none(theta_out, n_kept, b);
@@ -565,35 +564,151 @@ __device__ __forceinline__ void select_row_body(
   select_core(keys, nb, k, theta_out, kept, n_kept, MAXB, b, sh);
 }
 
-// Steps A, B and C in one workgroup (short block tables).  scores_out
-// (nullable) receives I_b.
-__device__ __forceinline__ void select_fused_body(
-    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, float hval, float* __restrict__ scores_out,
-    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int Hq,
-    int MAXB, int nch_max, float eps_h, float h_min, float log_v, float kappa_min, int b_min,
-    unsigned* flags, int b, unsigned* keys, SelectShared& sh) {
-  int N, nb, k;
-  if (!select_prepare(ctx_lens, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min,
-                      b_min, flags, b, N, nb, k))
-    return;
-  lse_merge_body(lse_part, ctx_lens, sh.L, Hq, MAXB, nch_max, b, sh.pm, sh.ps);
-  __syncthreads();
+// Steps A, B and C in one workgroup (short block tables), in two parts so
+// that a caller can overlap other work with the loads: select_load issues
+// every global read of the sequence at once (its block logits, four lanes
+// per block and HPL = H_q / 4 heads per lane, and the per-tile log-sum-exp
+// partials of the L merge) into registers; select_finish merges L, scores
+// the blocks and selects.  The arithmetic, and its order, is that of the
+// three-launch form (lse_merge_body, block_score_quad, select_core).
+constexpr int kFusedRegs = 32;            // logits per lane, at most
+constexpr int kFusedTiles = 8;            // L-merge tiles per thread, at most
+
+template <int HPL>
+struct SelectRegs {
+  static constexpr int kPasses = kFusedRegs / HPL;   // 128 blocks per pass
+  float z[kFusedRegs];
+  float2 pr[kFusedTiles];
+};
+
+// Whether the one-launch form applies (both the staged and the fused step
+// decide with this, so they take the same form).
+__host__ __device__ inline int select_one_launch_hpl(int MAXB, int Hq) {
+  if (MAXB > kFusedSelectMaxBlocks || (Hq != 4 && Hq != 8 && Hq != 16 && Hq != 32)) return 0;
+  const int hpl = Hq / 4;
+  const int nch = (MAXB + kMfmaChunk - 1) / kMfmaChunk;
+  const int per_head = kRowThreads / Hq;
+  if (MAXB > (kFusedRegs / hpl) * (kSelThreads / 4)) return 0;
+  if ((nch + per_head - 1) / per_head > kFusedTiles) return 0;
+  return hpl;
+}
+
+template <int HPL>
+__device__ __forceinline__ void select_load(const float* __restrict__ zbuf,
+                                            const float* __restrict__ lse_part, int MAXB,
+                                            int nch_max, int b, int nb, SelectRegs<HPL>& R) {
+  constexpr int Hq = 4 * HPL;
+  const int t = threadIdx.x, qq = t & 3;
+#pragma unroll
+  for (int p = 0; p < SelectRegs<HPL>::kPasses; ++p) {
+    const int j = p * (kSelThreads / 4) + (t >> 2);
+    if (j < nb) {
+      const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq;
+#pragma unroll
+      for (int i = 0; i < HPL; ++i) R.z[p * HPL + i] = zr[qq + 4 * i];
+    }
+  }
+  const int nch = (nb + kMfmaChunk - 1) / kMfmaChunk;
+  constexpr int per_head = kRowThreads / Hq;
+  if (t < per_head * Hq) {
+    const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + t % Hq) * 2;
+#pragma unroll
+    for (int i = 0; i < kFusedTiles; ++i) {
+      const int c = t / Hq + i * per_head;
+      if (c < nch) R.pr[i] = *reinterpret_cast<const float2*>(lp + static_cast<long long>(c) * Hq * 2);
+    }
+  }
+}
+
+template <int HPL>
+__device__ __forceinline__ void select_finish(
+    const SelectRegs<HPL>& R, int N, int nb, float hval, float* __restrict__ scores_out,
+    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
+    float eps_h, float h_min, float log_v, float kappa_min, int b_min, int b, unsigned* keys,
+    SelectShared& sh) {
+  constexpr int Hq = 4 * HPL;
+  constexpr int per_head = kRowThreads / Hq;
   const int t = threadIdx.x;
-  for (int j0 = 0; j0 < nb; j0 += kSelThreads / 4) {
-    const int j = j0 + (t >> 2);
-    const float I = block_score_quad(zbuf, sh.L, Hq, MAXB, b, j, N, nb, t & 3);
-    if (j < nb && (t & 3) == 0) {
+  // Step A (the fold of lse_merge_body, from the registers).
+  const int nch = (nb + kMfmaChunk - 1) / kMfmaChunk;
+  if (t < kRowThreads) {
+    float m = -INFINITY, sum = 0.f;
+    if (t < per_head * Hq) {
+#pragma unroll
+      for (int i = 0; i < kFusedTiles; ++i)
+        if (t / Hq + i * per_head < nch) m = fmaxf(m, R.pr[i].x);
+      if (m != -INFINITY) {
+#pragma unroll
+        for (int i = 0; i < kFusedTiles; ++i)
+          if (t / Hq + i * per_head < nch) sum += R.pr[i].y * expf(R.pr[i].x - m);
+      }
+    }
+    sh.pm[t] = m;
+    sh.ps[t] = sum;
+  }
+  __syncthreads();
+  if (t < Hq) {
+    float mm = -INFINITY, ss = 0.f;
+    for (int i = 0; i < per_head; ++i) {
+      const float mc = sh.pm[i * Hq + t], sc = sh.ps[i * Hq + t];
+      if (mc == -INFINITY) continue;
+      const float mn = fmaxf(mm, mc);
+      ss = ss * expf(mm - mn) + sc * expf(mc - mn);
+      mm = mn;
+    }
+    sh.L[t] = (mm == -INFINITY) ? -INFINITY : mm + logf(ss);
+  }
+  __syncthreads();
+  // Step B (block_score_quad on the registers).
+  const int qq = t & 3;
+#pragma unroll
+  for (int p = 0; p < SelectRegs<HPL>::kPasses; ++p) {
+    const int j = p * (kSelThreads / 4) + (t >> 2);
+    if (p * (kSelThreads / 4) >= nb) break;
+    float acc = 0.f;
+    if (j < nb) {
+      const float lnn = logf(static_cast<float>(j == nb - 1 ? N - kBlock * (nb - 1) : kBlock));
+#pragma unroll
+      for (int i = 0; i < HPL; ++i) {
+        const int h = qq + 4 * i;
+        const float z = R.z[p * HPL + i];
+        acc += expf(z + lnn - sh.L[h]) * (sh.L[h] - z);
+      }
+    }
+    acc += __shfl_xor(acc, 1);
+    acc += __shfl_xor(acc, 2);
+    const float I = __fdiv_rn(acc, static_cast<float>(Hq));
+    if (j < nb && qq == 0) {
       keys[j] = float_key(I);
       if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j] = I;
     }
   }
   __syncthreads();
+  const int k = keep_budget(hval, nb, eps_h, h_min, log_v, kappa_min, b_min);
   if (k <= 0) {
     select_none(theta_out, n_kept, b);
     return;
   }
   select_core(keys, nb, k, theta_out, kept, n_kept, MAXB, b, sh);
+}
+
+// The one-launch selection of sequence b with its entropy in hval.
+template <int HPL>
+__device__ __forceinline__ void select_fused_body(
+    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, float hval, float* __restrict__ scores_out,
+    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
+    int nch_max, float eps_h, float h_min, float log_v, float kappa_min, int b_min,
+    unsigned* flags, int b, unsigned* keys, SelectShared& sh) {
+  const int N = ctx_lens[b];
+  int nb, k;
+  if (!select_prepare(N, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min,
+                      flags, b, nb, k))
+    return;
+  SelectRegs<HPL> R;
+  select_load<HPL>(zbuf, lse_part, MAXB, nch_max, b, nb, R);
+  select_finish<HPL>(R, N, nb, hval, scores_out, theta_out, kept, n_kept, MAXB, eps_h, h_min,
+                     log_v, kappa_min, b_min, b, keys, sh);
 }
 
 }  // namespace

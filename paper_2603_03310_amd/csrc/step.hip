@@ -41,19 +41,26 @@ __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
                  s_pm, s_ps);
 }
 
-// Per sequence, short block tables: the row's entropy and the controller
-// update (first wave), then the whole kept-block selection.
+// Per sequence, short block tables: the selection's loads are issued first,
+// then the first wave computes the row's entropy and the controller update
+// while they are in flight, then the whole kept-block selection.
+template <int HPL>
 __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau, float* h_out,
     float* temp_used, float eta, float h_target, float t_min, float t_max,
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, float* __restrict__ scores, float* __restrict__ theta,
-    int* __restrict__ kept, int* __restrict__ n_kept, int Hq, int MAXB, int nch_max, float eps_h,
+    int* __restrict__ kept, int* __restrict__ n_kept, int MAXB, int nch_max, float eps_h,
     float h_min, float log_v, float kappa_min, int b_min, unsigned* flags) {
   extern __shared__ unsigned keys[];        // [MAXB]
   __shared__ SelectShared sh;
   __shared__ float s_H;
   const int b = blockIdx.x;
+  const int N = ctx_lens[b];
+  const bool ok = N >= 0 && N <= MAXB * kBlock;
+  const int nb = ok ? (N + kBlock - 1) / kBlock : 0;
+  SelectRegs<HPL> R;
+  select_load<HPL>(zbuf, lse_part, MAXB, nch_max, b, nb, R);
   if (threadIdx.x < 64) {
     const float H = row_entropy(part, C, b);
     if (threadIdx.x == 0) {
@@ -63,10 +70,14 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     }
   }
   __syncthreads();
-  select_fused_body(zbuf, lse_part, ctx_lens, s_H, scores, theta, kept, n_kept, Hq, MAXB, nch_max,
-                    eps_h, h_min, log_v, kappa_min, b_min, flags, b, keys, sh);
+  const float H = s_H;
+  int nb2, k;
+  if (!select_prepare(N, H, theta, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min, flags, b,
+                      nb2, k))
+    return;
+  select_finish<HPL>(R, N, nb, H, scores, theta, kept, n_kept, MAXB, eps_h, h_min, log_v,
+                     kappa_min, b_min, b, keys, sh);
 }
-
 }  // namespace
 
 hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
@@ -110,13 +121,26 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
     if (e != hipSuccess) return e;
   }
 
-  if (cf.max_blocks_per_seq <= kFusedSelectMaxBlocks) {
+  const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
+  if (hpl) {
     const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-    hipLaunchKernelGGL(step_b_kernel, dim3(B), dim3(kSelThreads), lds, s, c->ent_part, c->chunks,
-                       st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta, cf.h_target,
-                       cf.t_min, cf.t_max, c->zbuf, c->lse_part, ctx_lens, scores, theta, kept,
-                       n_kept, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks, cf.eps_h,
-                       cf.h_min, cf.log_v, cf.kappa_min, cf.b_min, c->dev_flags);
+#define ENT_STEPB_CASE(HH)                                                                     \
+  case HH:                                                                                     \
+    hipLaunchKernelGGL((step_b_kernel<HH>), dim3(B), dim3(kSelThreads), lds, s, c->ent_part,   \
+                       c->chunks, st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta,        \
+                       cf.h_target, cf.t_min, cf.t_max, c->zbuf, c->lse_part, ctx_lens,        \
+                       scores, theta, kept, n_kept, cf.max_blocks_per_seq, c->lse_chunks,      \
+                       cf.eps_h, cf.h_min, cf.log_v, cf.kappa_min, cf.b_min, c->dev_flags);    \
+    break;
+    switch (hpl) {
+      ENT_STEPB_CASE(1)
+      ENT_STEPB_CASE(2)
+      ENT_STEPB_CASE(4)
+      ENT_STEPB_CASE(8)
+      default:
+        return hipErrorInvalidValue;
+    }
+#undef ENT_STEPB_CASE
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   } else {
