@@ -75,7 +75,7 @@ typedef struct {
   int block_size;          /* tokens per KV block: must be 16 */
   int max_blocks_per_seq;  /* MAXB: row length of block_tables, <= 16384;
                               max_batch * MAXB * H_kv < 2^31 */
-  int num_pool_blocks;     /* P: physical blocks in k_cache / v_cache */
+  int num_pool_blocks;     /* P: physical blocks in k_cache / v_cache, < 2^30 */
   int vocab;               /* |V|: logits per row */
   int kv_dtype;            /* ENT_BF16 or ENT_F32 (K, V and queries) */
   float scale;             /* softmax scale of scoring and attention, e.g. 1/sqrt(d) */

@@ -51,6 +51,7 @@ std::string check_config(const ent_config* c, int* code) {
   if (c->max_blocks_per_seq > ent::kMaxBlocksPerSeq) return "max_blocks_per_seq must be <= 16384";
   if (c->num_kv_heads * c->head_dim > 2048) return "num_kv_heads * head_dim must be <= 2048";
   if (c->vocab > kMaxVocab) return "vocab must be <= 1048576";
+  if (c->num_pool_blocks >= (1 << 30)) return "num_pool_blocks must be < 2^30";
   if (static_cast<long long>(c->max_batch) * c->max_blocks_per_seq * c->num_kv_heads >= (1ll << 31))
     return "max_batch * max_blocks_per_seq * num_kv_heads must be < 2^31";
   *code = ENT_OK;
@@ -153,12 +154,13 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   const size_t sz_lse = align_up(Bm * c->lse_chunks * f.num_q_heads * 2 * sizeof(float));
   const size_t sz_lrow = align_up(Bm * f.num_q_heads * sizeof(float));
   const size_t sz_isc = align_up(Bm * f.max_blocks_per_seq * sizeof(float));
+  const size_t sz_kphys = align_up(Bm * f.max_blocks_per_seq * sizeof(int));
   const size_t nslots = static_cast<size_t>(
       ent::decode_partial_slots(c->decode_grid, f.max_batch, f.num_kv_heads));
   const size_t sz_acc = align_up(nslots * c->group * f.head_dim * sizeof(float));
   const size_t sz_ml = align_up(nslots * c->group * 2 * sizeof(float));
   const size_t sz_flags = align_up(sizeof(unsigned));
-  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_lrow + sz_isc + sz_acc + sz_ml + sz_flags;
+  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_lrow + sz_isc + sz_kphys + sz_acc + sz_ml + sz_flags;
   e = hipMalloc(&c->ws, c->ws_bytes);
   if (e != hipSuccess) {
     g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
@@ -181,6 +183,7 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->lse_part = reinterpret_cast<float*>(take(sz_lse));
   c->lrow = reinterpret_cast<float*>(take(sz_lrow));
   c->iscores = reinterpret_cast<float*>(take(sz_isc));
+  c->kept_phys = reinterpret_cast<int*>(take(sz_kphys));
   c->dec_acc = reinterpret_cast<float*>(take(sz_acc));
   c->dec_ml = reinterpret_cast<float*>(take(sz_ml));
   c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));

@@ -126,29 +126,32 @@ __global__ __launch_bounds__(kRowThreads) void block_score_kernel(
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const float* __restrict__ scores, const int* __restrict__ ctx_lens,
-    const float* __restrict__ hvec, float* __restrict__ theta_out, int* __restrict__ kept,
-    int* __restrict__ n_kept, int MAXB, float eps_h, float h_min, float log_v, float kappa_min,
-    int b_min, unsigned* flags) {
-  extern __shared__ unsigned keys[];        // [MAXB]
+    const int* __restrict__ tables, const float* __restrict__ hvec, float* __restrict__ theta_out,
+    int* __restrict__ kept, int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P,
+    float eps_h, float h_min, float log_v, float kappa_min, int b_min, unsigned* flags) {
+  extern __shared__ unsigned keys[];        // [MAXB] keys, then [MAXB] encoded blocks
   __shared__ SelectShared sh;
   const int b = blockIdx.x;
-  select_row_body(scores, ctx_lens, hvec[b], theta_out, kept, n_kept, MAXB, eps_h, h_min, log_v,
-                  kappa_min, b_min, flags, b, keys, sh);
+  select_row_body(scores, ctx_lens, tables, hvec[b], theta_out, kept, kphys, n_kept, MAXB, P,
+                  eps_h, h_min, log_v, kappa_min, b_min, flags, b, keys,
+                  reinterpret_cast<int*>(keys + MAXB), sh);
 }
 
 // All three selection steps per sequence (short block tables).
 template <int HPL>
 __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, const float* __restrict__ hvec, float* __restrict__ scores,
-    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
+    const int* __restrict__ ctx_lens, const int* __restrict__ tables,
+    const float* __restrict__ hvec, float* __restrict__ scores, float* __restrict__ theta_out,
+    int* __restrict__ kept, int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P,
     int nch_max, float eps_h, float h_min, float log_v, float kappa_min, int b_min,
     unsigned* flags) {
-  extern __shared__ unsigned keys[];        // [MAXB]
+  extern __shared__ unsigned keys[];        // [MAXB] keys, then [MAXB] encoded blocks
   __shared__ SelectShared sh;
   const int b = blockIdx.x;
-  select_fused_body<HPL>(zbuf, lse_part, ctx_lens, hvec[b], scores, theta_out, kept, n_kept, MAXB,
-                         nch_max, eps_h, h_min, log_v, kappa_min, b_min, flags, b, keys, sh);
+  select_fused_body<HPL>(zbuf, lse_part, ctx_lens, tables, hvec[b], scores, theta_out, kept,
+                         kphys, n_kept, MAXB, P, nch_max, eps_h, h_min, log_v, kappa_min, b_min,
+                         flags, b, keys, reinterpret_cast<int*>(keys + MAXB), sh);
 }
 
 template <int D>
@@ -231,22 +234,23 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
     e = launch_score_valu(c, B, q, ksum, tables, ctx_lens, s);
   }
   if (e != hipSuccess) return e;
-  return launch_selection(c, B, ctx_lens, h, scores, theta, kept, n_kept, s);
+  return launch_selection(c, B, tables, ctx_lens, h, scores, theta, kept, n_kept, s);
 }
 
-hipError_t launch_selection(const ent_ctx* c, int B, const int* ctx_lens, const float* h,
-                            float* scores, float* theta, int* kept, int* n_kept, hipStream_t s) {
+hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const int* ctx_lens,
+                            const float* h, float* scores, float* theta, int* kept, int* n_kept,
+                            hipStream_t s) {
   const ent_config& cf = c->cfg;
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
   const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
   if (hpl) {
-    const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
+    const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
 #define ENT_SEL_CASE(HH)                                                                       \
   case HH:                                                                                     \
     hipLaunchKernelGGL((select_fused_kernel<HH>), dim3(B), dim3(kSelThreads), lds, s, c->zbuf, \
-                       c->lse_part, ctx_lens, h, scores, theta, kept, n_kept,                  \
-                       cf.max_blocks_per_seq, c->lse_chunks, cf.eps_h, cf.h_min, cf.log_v,     \
-                       cf.kappa_min, cf.b_min, c->dev_flags);                                  \
+                       c->lse_part, ctx_lens, tables, h, scores, theta, kept, c->kept_phys,    \
+                       n_kept, cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks,       \
+                       cf.eps_h, cf.h_min, cf.log_v, cf.kappa_min, cf.b_min, c->dev_flags);    \
     break;
     switch (hpl) {
       ENT_SEL_CASE(1)
@@ -266,7 +270,7 @@ hipError_t launch_selection(const ent_ctx* c, int B, const int* ctx_lens, const 
   float* sc = scores ? scores : c->iscores;
   e = launch_block_scores(c, B, ctx_lens, sc, s);
   if (e != hipSuccess) return e;
-  return launch_select_rows(c, B, ctx_lens, h, sc, theta, kept, n_kept, s);
+  return launch_select_rows(c, B, tables, ctx_lens, h, sc, theta, kept, n_kept, s);
 }
 
 hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,
@@ -278,14 +282,15 @@ hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, flo
   return hipGetLastError();
 }
 
-hipError_t launch_select_rows(const ent_ctx* c, int B, const int* ctx_lens, const float* h,
-                              const float* scores, float* theta, int* kept, int* n_kept,
-                              hipStream_t s) {
+hipError_t launch_select_rows(const ent_ctx* c, int B, const int* tables, const int* ctx_lens,
+                              const float* h, const float* scores, float* theta, int* kept,
+                              int* n_kept, hipStream_t s) {
   const ent_config& cf = c->cfg;
-  const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelThreads), lds, s, scores, ctx_lens, h, theta,
-                     kept, n_kept, cf.max_blocks_per_seq, cf.eps_h, cf.h_min, cf.log_v,
-                     cf.kappa_min, cf.b_min, c->dev_flags);
+  const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
+  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelThreads), lds, s, scores, ctx_lens, tables,
+                     h, theta, kept, c->kept_phys, n_kept, cf.max_blocks_per_seq,
+                     cf.num_pool_blocks, cf.eps_h, cf.h_min, cf.log_v, cf.kappa_min, cf.b_min,
+                     c->dev_flags);
   return hipGetLastError();
 }
 

@@ -405,11 +405,21 @@ struct SelectShared {
   int digit, krem, wcnt[kSelWaves];
 };
 
+// Physical block p of logical block j (of nb) for the decode's unit lists:
+// p, with bit 30 set for the sequence's last block; -1 when p is outside the
+// pool (the decode flags it).  Pools hold fewer than 2^30 blocks.
+__device__ __forceinline__ int encode_phys(int p, int j, int nb, int P) {
+  if (p < 0 || p >= P) return -1;
+  return p | (j == nb - 1 ? (1 << 30) : 0);
+}
+
 // Step C core: the nb keys of sequence b are in LDS (keys), k >= 1.
-__device__ __forceinline__ void select_core(unsigned* keys, int nb, int k,
+// tbl: LDS [nb] physical block of each block, encoded (encode_phys);
+// kphys (global [B, MAXB]) receives them in kept order.
+__device__ __forceinline__ void select_core(unsigned* keys, const int* tbl, int nb, int k,
                                             float* __restrict__ theta_out, int* __restrict__ kept,
-                                            int* __restrict__ n_kept, int MAXB, int b,
-                                            SelectShared& sh) {
+                                            int* __restrict__ kphys, int* __restrict__ n_kept,
+                                            int MAXB, int b, SelectShared& sh) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   unsigned kmin = 0xFFFFFFFFu, kmax = 0u;
   for (int i = t; i < nb; i += kSelThreads) {
@@ -498,7 +508,10 @@ __device__ __forceinline__ void select_core(unsigned* keys, int nb, int k,
     __syncthreads();
     int off = total;
     for (int w = 0; w < wave; ++w) off += sh.wcnt[w];
-    if (f) krow[off + rank] = i;
+    if (f) {
+      krow[off + rank] = i;
+      kphys[static_cast<long long>(b) * MAXB + off + rank] = tbl[i];
+    }
     for (int w = 0; w < kSelWaves; ++w) total += sh.wcnt[w];
     __syncthreads();
   }
@@ -545,10 +558,11 @@ __device__ __forceinline__ bool select_prepare(int N, float hval, float* __restr
 
 // Step C as its own launch: keys from step B's scores.
 __device__ __forceinline__ void select_row_body(
-    const float* __restrict__ scores, const int* __restrict__ ctx_lens, float hval,
-    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
+    const float* __restrict__ scores, const int* __restrict__ ctx_lens,
+    const int* __restrict__ tables, float hval, float* __restrict__ theta_out,
+    int* __restrict__ kept, int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P,
     float eps_h, float h_min, float log_v, float kappa_min, int b_min, unsigned* flags, int b,
-    unsigned* keys, SelectShared& sh) {
+    unsigned* keys, int* tbl, SelectShared& sh) {
   const int N = ctx_lens[b];
   int nb, k;
   if (!select_prepare(N, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min,
@@ -559,9 +573,13 @@ __device__ __forceinline__ void select_row_body(
     return;
   }
   const float* sr = scores + static_cast<long long>(b) * MAXB;
-  for (int i = threadIdx.x; i < nb; i += kSelThreads) keys[i] = float_key(sr[i]);
+  const int* tr = tables + static_cast<long long>(b) * MAXB;
+  for (int i = threadIdx.x; i < nb; i += kSelThreads) {
+    keys[i] = float_key(sr[i]);
+    tbl[i] = encode_phys(tr[i], i, nb, P);
+  }
   __syncthreads();
-  select_core(keys, nb, k, theta_out, kept, n_kept, MAXB, b, sh);
+  select_core(keys, tbl, nb, k, theta_out, kept, kphys, n_kept, MAXB, b, sh);
 }
 
 // Steps A, B and C in one workgroup (short block tables), in two parts so
@@ -579,6 +597,7 @@ struct SelectRegs {
   static constexpr int kPasses = kFusedRegs / HPL;   // 128 blocks per pass
   float z[kFusedRegs];
   float2 pr[kFusedTiles];
+  int tb[kPasses];                         // table entries (lanes qq == 0)
 };
 
 // Whether the one-launch form applies (both the staged and the fused step
@@ -595,7 +614,8 @@ __host__ __device__ inline int select_one_launch_hpl(int MAXB, int Hq) {
 
 template <int HPL>
 __device__ __forceinline__ void select_load(const float* __restrict__ zbuf,
-                                            const float* __restrict__ lse_part, int MAXB,
+                                            const float* __restrict__ lse_part,
+                                            const int* __restrict__ tables, int MAXB,
                                             int nch_max, int b, int nb, SelectRegs<HPL>& R) {
   constexpr int Hq = 4 * HPL;
   const int t = threadIdx.x, qq = t & 3;
@@ -606,6 +626,7 @@ __device__ __forceinline__ void select_load(const float* __restrict__ zbuf,
       const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq;
 #pragma unroll
       for (int i = 0; i < HPL; ++i) R.z[p * HPL + i] = zr[qq + 4 * i];
+      if (qq == 0) R.tb[p] = tables[static_cast<long long>(b) * MAXB + j];
     }
   }
   const int nch = (nb + kMfmaChunk - 1) / kMfmaChunk;
@@ -623,9 +644,9 @@ __device__ __forceinline__ void select_load(const float* __restrict__ zbuf,
 template <int HPL>
 __device__ __forceinline__ void select_finish(
     const SelectRegs<HPL>& R, int N, int nb, float hval, float* __restrict__ scores_out,
-    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
-    float eps_h, float h_min, float log_v, float kappa_min, int b_min, int b, unsigned* keys,
-    SelectShared& sh) {
+    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ kphys,
+    int* __restrict__ n_kept, int MAXB, int P, float eps_h, float h_min, float log_v,
+    float kappa_min, int b_min, int b, unsigned* keys, int* tbl, SelectShared& sh) {
   constexpr int Hq = 4 * HPL;
   constexpr int per_head = kRowThreads / Hq;
   const int t = threadIdx.x;
@@ -680,6 +701,7 @@ __device__ __forceinline__ void select_finish(
     const float I = __fdiv_rn(acc, static_cast<float>(Hq));
     if (j < nb && qq == 0) {
       keys[j] = float_key(I);
+      tbl[j] = encode_phys(R.tb[p], j, nb, P);
       if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j] = I;
     }
   }
@@ -689,26 +711,27 @@ __device__ __forceinline__ void select_finish(
     select_none(theta_out, n_kept, b);
     return;
   }
-  select_core(keys, nb, k, theta_out, kept, n_kept, MAXB, b, sh);
+  select_core(keys, tbl, nb, k, theta_out, kept, kphys, n_kept, MAXB, b, sh);
 }
 
 // The one-launch selection of sequence b with its entropy in hval.
 template <int HPL>
 __device__ __forceinline__ void select_fused_body(
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, float hval, float* __restrict__ scores_out,
-    float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ n_kept, int MAXB,
-    int nch_max, float eps_h, float h_min, float log_v, float kappa_min, int b_min,
-    unsigned* flags, int b, unsigned* keys, SelectShared& sh) {
+    const int* __restrict__ ctx_lens, const int* __restrict__ tables, float hval,
+    float* __restrict__ scores_out, float* __restrict__ theta_out, int* __restrict__ kept,
+    int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P, int nch_max, float eps_h,
+    float h_min, float log_v, float kappa_min, int b_min, unsigned* flags, int b, unsigned* keys,
+    int* tbl, SelectShared& sh) {
   const int N = ctx_lens[b];
   int nb, k;
   if (!select_prepare(N, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min,
                       flags, b, nb, k))
     return;
   SelectRegs<HPL> R;
-  select_load<HPL>(zbuf, lse_part, MAXB, nch_max, b, nb, R);
-  select_finish<HPL>(R, N, nb, hval, scores_out, theta_out, kept, n_kept, MAXB, eps_h, h_min,
-                     log_v, kappa_min, b_min, b, keys, sh);
+  select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, nb, R);
+  select_finish<HPL>(R, N, nb, hval, scores_out, theta_out, kept, kphys, n_kept, MAXB, P, eps_h,
+                     h_min, log_v, kappa_min, b_min, b, keys, tbl, sh);
 }
 
 }  // namespace

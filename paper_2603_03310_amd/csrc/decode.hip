@@ -56,6 +56,7 @@ struct DecodeArgs {
   const int* tables;
   const int* ctx_lens;
   const int* kept;
+  const int* kept_phys;   // nullable: encoded physical blocks of the kept lists
   const int* n_kept;
   float* out;
   float* lse;
@@ -145,6 +146,17 @@ __device__ __forceinline__ UnitMeta unit_meta(const DecodeArgs& a, int x, int u1
   const int N = s_N[b];
   const int nb = (N + kBlock - 1) / kBlock;
   const long long row = static_cast<long long>(b) * a.MAXB;
+  if (a.kept_phys) {
+    // The selection's encoding: physical block, bit 30 = the sequence's last block.
+    const int v = a.kept_phys[row + j];
+    if (v >= 0) {
+      m.p = v & ((1 << 30) - 1);
+      m.nv = (v >> 30) ? N - kBlock * (nb - 1) : kBlock;
+    } else if (g == 0) {
+      raise_flag(a.flags, ENT_DEV_BAD_TABLE);
+    }
+    return m;
+  }
   const int kid = a.kept[row + j];
   if (kid >= 0 && kid < nb) {
     const int p = a.tables[row + kid];
@@ -225,6 +237,19 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   bf16x8_t qreg[KS];
   float m_run = -INFINITY, l_run = 0.f;
   f32x4_t oacc[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) oacc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // The first segment's queries load together with the first tiles.
+  if (busy) {
+    cur_seg = __shfl(win.seg, 0);
+    const int b = cur_seg / a.Hkv, g = cur_seg % a.Hkv;
+    const long long qh = static_cast<long long>(b) * Hq + g * G + r16;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (head_ok) qreg[ks] = load_bf16x8(q + qh * D + ks * 32 + gq * 8);
+      else qreg[ks] = __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+    }
+  }
 
   auto flush = [&]() {
     float l_tot = l_run + __shfl_xor(l_run, 16);
@@ -722,7 +747,7 @@ long long decode_partial_slots(int decode_grid, int max_batch, int num_kv_heads)
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
-                         hipStream_t s, const SampleArgs* sample) {
+                         hipStream_t s, const SampleArgs* sample, const int* kept_phys) {
   const ent_config& cf = c->cfg;
   DecodeArgs a;
   a.q = q;
@@ -731,6 +756,7 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   a.tables = tables;
   a.ctx_lens = ctx_lens;
   a.kept = kept;
+  a.kept_phys = kept_phys;
   a.n_kept = n_kept;
   a.out = out;
   a.lse = lse;

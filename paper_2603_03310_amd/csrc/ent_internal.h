@@ -38,6 +38,7 @@ struct ent_ctx {
   float* lse_part = nullptr;      // [max_batch, lse_chunks, H_q, 2]
   float* lrow = nullptr;          // [max_batch, H_q]  L_h per sequence
   float* iscores = nullptr;       // [max_batch, MAXB]  block scores when the caller keeps none
+  int* kept_phys = nullptr;       // [max_batch, MAXB]  physical blocks of the kept lists
   float* dec_acc = nullptr;       // [decode partial slots, G, d]
   float* dec_ml = nullptr;        // [decode partial slots, G, 2]
   unsigned* dev_flags = nullptr;  // [1]
@@ -88,14 +89,15 @@ hipError_t launch_prologue(const ent_ctx* c, const PrologueArgs& a, hipStream_t 
 int prologue_grid_size(const ent_ctx* c);
 // The kept-block selection after scoring (L merge, block scores, radix
 // select), given each sequence's entropy h.
-hipError_t launch_selection(const ent_ctx* c, int B, const int* ctx_lens, const float* h,
-                            float* scores, float* theta, int* kept, int* n_kept, hipStream_t s);
+hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const int* ctx_lens,
+                            const float* h, float* scores, float* theta, int* kept, int* n_kept,
+                            hipStream_t s);
 // Selection phases B (block scores from c->lrow) and C (radix select).
 hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,
                                hipStream_t s);
-hipError_t launch_select_rows(const ent_ctx* c, int B, const int* ctx_lens, const float* h,
-                              const float* scores, float* theta, int* kept, int* n_kept,
-                              hipStream_t s);
+hipError_t launch_select_rows(const ent_ctx* c, int B, const int* tables, const int* ctx_lens,
+                              const float* h, const float* scores, float* theta, int* kept,
+                              int* n_kept, hipStream_t s);
 hipError_t launch_score_valu(const ent_ctx* c, int B, const void* q, const float* ksum,
                              const int* tables, const int* ctx_lens, hipStream_t s);
 
@@ -111,11 +113,13 @@ struct SampleArgs {
   int* tokens;
 };
 
+// kept_phys (nullable): the selection's encoded physical blocks of the same
+// kept lists, read instead of kept + tables.
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
                          hipStream_t s,
-                         const SampleArgs* sample = nullptr);
+                         const SampleArgs* sample = nullptr, const int* kept_phys = nullptr);
 hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
                               ent_state st, const void* q, const void* k_cache,
                               const void* v_cache, const float* ksum, const int* tables,

@@ -49,10 +49,11 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau, float* h_out,
     float* temp_used, float eta, float h_target, float t_min, float t_max,
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, float* __restrict__ scores, float* __restrict__ theta,
-    int* __restrict__ kept, int* __restrict__ n_kept, int MAXB, int nch_max, float eps_h,
-    float h_min, float log_v, float kappa_min, int b_min, unsigned* flags) {
-  extern __shared__ unsigned keys[];        // [MAXB]
+    const int* __restrict__ ctx_lens, const int* __restrict__ tables, float* __restrict__ scores,
+    float* __restrict__ theta, int* __restrict__ kept, int* __restrict__ kphys,
+    int* __restrict__ n_kept, int MAXB, int P, int nch_max, float eps_h, float h_min, float log_v,
+    float kappa_min, int b_min, unsigned* flags) {
+  extern __shared__ unsigned keys[];        // [MAXB] keys, then [MAXB] encoded blocks
   __shared__ SelectShared sh;
   __shared__ float s_H;
   const int b = blockIdx.x;
@@ -60,7 +61,7 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
   const bool ok = N >= 0 && N <= MAXB * kBlock;
   const int nb = ok ? (N + kBlock - 1) / kBlock : 0;
   SelectRegs<HPL> R;
-  select_load<HPL>(zbuf, lse_part, MAXB, nch_max, b, nb, R);
+  select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, nb, R);
   if (threadIdx.x < 64) {
     const float H = row_entropy(part, C, b);
     if (threadIdx.x == 0) {
@@ -75,8 +76,8 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
   if (!select_prepare(N, H, theta, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min, flags, b,
                       nb2, k))
     return;
-  select_finish<HPL>(R, N, nb, H, scores, theta, kept, n_kept, MAXB, eps_h, h_min, log_v,
-                     kappa_min, b_min, b, keys, sh);
+  select_finish<HPL>(R, N, nb, H, scores, theta, kept, kphys, n_kept, MAXB, P, eps_h, h_min,
+                     log_v, kappa_min, b_min, b, keys, reinterpret_cast<int*>(keys + MAXB), sh);
 }
 }  // namespace
 
@@ -123,14 +124,15 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
 
   const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
   if (hpl) {
-    const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
+    const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
 #define ENT_STEPB_CASE(HH)                                                                     \
   case HH:                                                                                     \
     hipLaunchKernelGGL((step_b_kernel<HH>), dim3(B), dim3(kSelThreads), lds, s, c->ent_part,   \
                        c->chunks, st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta,        \
                        cf.h_target, cf.t_min, cf.t_max, c->zbuf, c->lse_part, ctx_lens,        \
-                       scores, theta, kept, n_kept, cf.max_blocks_per_seq, c->lse_chunks,      \
-                       cf.eps_h, cf.h_min, cf.log_v, cf.kappa_min, cf.b_min, c->dev_flags);    \
+                       tables, scores, theta, kept, c->kept_phys, n_kept,                      \
+                       cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, cf.eps_h,     \
+                       cf.h_min, cf.log_v, cf.kappa_min, cf.b_min, c->dev_flags);              \
     break;
     switch (hpl) {
       ENT_STEPB_CASE(1)
@@ -153,7 +155,7 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
     float* sc = scores ? scores : c->iscores;
     e = launch_block_scores(c, B, ctx_lens, sc, s);
     if (e != hipSuccess) return e;
-    e = launch_select_rows(c, B, ctx_lens, h_out, sc, theta, kept, n_kept, s);
+    e = launch_select_rows(c, B, tables, ctx_lens, h_out, sc, theta, kept, n_kept, s);
     if (e != hipSuccess) return e;
   }
   SampleArgs sa;
@@ -166,7 +168,7 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   sa.uniforms = uniforms;
   sa.tokens = tokens;
   return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s,
-                       &sa);
+                       &sa, c->kept_phys);
 }
 
 }  // namespace ent
