@@ -7,8 +7,9 @@ library and its Python binding never do, and it shares no code with them.
 
 Modules, each following the paper's definitions (section cited per function):
 
-* ``entropy``    -- exact Shannon entropy of the tempered softmax, entropic
-                    time, and the temperature control law.
+* ``entropy``    -- exact Shannon entropy of the tempered softmax, the top-k
+                    and tail-corrected estimates of it, entropic time, and
+                    the temperature control law.
 * ``blocks``     -- per-block mean keys, block entropic contributions, the
                     entropy-driven block budget and the kept-block set.
 * ``attention``  -- decode attention restricted to the kept blocks.

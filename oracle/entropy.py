@@ -32,6 +32,74 @@ def entropy(z: np.ndarray, temp: float) -> float:
     return float(-np.sum(p[pos] * logp[pos]))
 
 
+def _topk_split(z: np.ndarray, temp: float, k: int):
+    """The k largest log-probabilities of the tempered softmax (the top-k set
+    K_t of Section 2.1) and the rest.  With ties at the k-th value any choice
+    of members gives the same multiset of probabilities, so everything below
+    is well defined.  k is clamped to [1, |V|]."""
+    logp = tempered_log_softmax(z, temp)
+    kk = min(max(int(k), 1), logp.size)
+    desc = np.sort(logp)[::-1]
+    return desc[:kk], desc[kk:], kk
+
+
+def topk_entropy(z: np.ndarray, temp: float, k: int):
+    """Top-k truncated entropy (Section 2.1, top-k approximation).
+
+    K = the k most probable tokens under p; m = sum_{x in K} p(x);
+    p~(x) = p(x) / m on K and 0 elsewhere; H~ = -sum_{x in K} p~(x) ln p~(x).
+    Returns (H~, m, mbar) with mbar = 1 - m summed directly over the tokens
+    outside K (more accurate than 1 - m when the tail is small)."""
+    top, rest, _ = _topk_split(z, temp, k)
+    p = np.exp(top)
+    m = float(np.sum(p))
+    mbar = float(np.sum(np.exp(rest))) if rest.size else 0.0
+    pos = p > 0.0
+    log_pt = top[pos] - math.log(m)           # log p~ on K
+    h_tilde = float(-np.sum(np.exp(log_pt) * log_pt))
+    return h_tilde, m, mbar
+
+
+def binary_entropy(x: float) -> float:
+    """h(x) = -x ln x - (1 - x) ln(1 - x), with h(0) = h(1) = 0."""
+    x = float(x)
+    if x <= 0.0 or x >= 1.0:
+        return 0.0
+    return -x * math.log(x) - (1.0 - x) * math.log1p(-x)
+
+
+def tail_corrected_entropy(z: np.ndarray, temp: float, k: int) -> float:
+    """Tail-corrected estimate (Section 2.1, tail-corrected estimator):
+
+      H^ = H~ + h(mbar) + mbar ln(|V| - k)
+
+    the bound on H obtained by taking the mass outside the top-k set as
+    uniform over the |V| - k remaining tokens.  With k >= |V| there is no tail
+    and the last term is 0 (0 ln 0 = 0)."""
+    h_tilde, _, mbar = topk_entropy(z, temp, k)
+    V = np.asarray(z).size
+    kk = min(max(int(k), 1), V)
+    tail = mbar * math.log(V - kk) if V > kk else 0.0
+    return h_tilde + binary_entropy(mbar) + tail
+
+
+# Estimator codes (the same values as the library configuration field).
+EXACT, TOPK, TAIL = 0, 1, 2
+
+
+def entropy_estimate(z: np.ndarray, temp: float, estimator: int = EXACT, k: int = 0) -> float:
+    """The entropy the controller acts on (Section 3.3, estimator in the
+    control loop): the exact H_t, the top-k H~_t, or the tail-corrected
+    H^_t."""
+    if estimator == EXACT:
+        return entropy(z, temp)
+    if estimator == TOPK:
+        return topk_entropy(z, temp, k)[0]
+    if estimator == TAIL:
+        return tail_corrected_entropy(z, temp, k)
+    raise ValueError(f"unknown estimator {estimator}")
+
+
 def entropic_time(tau: float, h_prev: float, h: float) -> float:
     """tau + max(0, H_{t-1} - H_t)  (Section 2: entropy flow Delta H_t, its
     positive part, and entropic time as their running sum).
@@ -59,14 +127,18 @@ def control_step(logits: np.ndarray, h_prev: np.ndarray, tau: np.ndarray, temp: 
     """One controller update for a batch of logit rows [B, V].
 
     H_t is measured at the current temperature T_t; sampling uses the same
-    T_t; the updated temperature applies to the next step.  Returns H_t,
-    the updated tau, the temperature used and the next temperature."""
+    T_t; the updated temperature applies to the next step.  The controller
+    acts on the configured estimate (exact by default; `params.estimator`,
+    `params.est_k`).  Returns H_t, the updated tau, the temperature used and
+    the next temperature."""
     B = logits.shape[0]
     h = np.empty(B)
     tau_out = np.empty(B)
     t_next = np.empty(B)
+    est = int(getattr(params, "estimator", EXACT))
+    est_k = int(getattr(params, "est_k", 0))
     for b in range(B):
-        h[b] = entropy(logits[b], float(temp[b]))
+        h[b] = entropy_estimate(logits[b], float(temp[b]), est, est_k)
         tau_out[b] = entropic_time(float(tau[b]), float(h_prev[b]), h[b])
         t_next[b] = temperature_next(float(temp[b]), h[b], params.h_target, params.eta,
                                      params.t_min, params.t_max)

@@ -31,7 +31,8 @@ def sequence_step(s: int, *, k_pool, v_pool, tables, ctx_lens, q, logits, h_prev
     N = int(ctx_lens[s])
     z = np.asarray(logits[s], dtype=np.float64)
     T = float(temp[s])
-    h = entropy.entropy(z, T)
+    h = entropy.entropy_estimate(z, T, int(getattr(params, "estimator", entropy.EXACT)),
+                                 int(getattr(params, "est_k", 0)))
     out = {
         "h": h,
         "tau": entropy.entropic_time(float(tau[s]), float(h_prev[s]), h),

@@ -32,6 +32,8 @@ class Params:
     b_min: int            # smallest number of kept blocks
     log_v: float          # log |V| rounded to float32
     t0: float = 1.0       # initial temperature
+    estimator: int = 0    # entropy the controller acts on: 0 exact, 1 top-k, 2 tail-corrected
+    est_k: int = 256      # k of the top-k and tail-corrected estimators
 
     def __post_init__(self):
         # Every float is held at float32 precision: the library receives
