@@ -159,8 +159,10 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
       ent::decode_partial_slots(c->decode_grid, f.max_batch, f.num_kv_heads));
   const size_t sz_acc = align_up(nslots * c->group * f.head_dim * sizeof(float));
   const size_t sz_ml = align_up(nslots * c->group * 2 * sizeof(float));
+  const size_t sz_rec = align_up(static_cast<size_t>(c->decode_grid) * 4 * sizeof(int4));
   const size_t sz_flags = align_up(sizeof(unsigned));
-  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_lrow + sz_isc + sz_kphys + sz_acc + sz_ml + sz_flags;
+  c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_lrow + sz_isc + sz_kphys + sz_acc + sz_ml +
+                sz_rec + sz_flags;
   e = hipMalloc(&c->ws, c->ws_bytes);
   if (e != hipSuccess) {
     g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
@@ -186,6 +188,7 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->kept_phys = reinterpret_cast<int*>(take(sz_kphys));
   c->dec_acc = reinterpret_cast<float*>(take(sz_acc));
   c->dec_ml = reinterpret_cast<float*>(take(sz_ml));
+  c->dec_rec = reinterpret_cast<int4*>(take(sz_rec));
   c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));
   *out = c;
   return ENT_OK;

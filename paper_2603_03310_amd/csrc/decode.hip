@@ -11,9 +11,11 @@
 // parallel) and a one-block-ahead register prefetch of the K and V tiles.
 // Where its range covers a whole segment it writes the output directly;
 // where it covers part of one it writes an unnormalised partial
-// (max, sum, output) to slot (wave + segment), which is unique because both
-// partitions are ordered intervals.  A second kernel merges the partials of
-// every segment that was cut.  The kept counts stay on the device.
+// (max, sum, output) to slot (range + segment), which is unique because both
+// partitions are ordered intervals.  The range in which a cut segment begins
+// also writes a record (segment, last range holding it, total units), so a
+// second kernel merges the partials of every cut segment from that record
+// alone, without rebuilding the plan.  The kept counts stay on the device.
 //
 // bf16 path (MFMA, gfx950).  Per kept block of 16 tokens:
 //   S^T[16 tok x 16 heads] = K[16 x d] . Q^T[d x 16]   v_mfma_f32_16x16x32_bf16,
@@ -29,7 +31,6 @@
 // fp32 path (VALU): the same decomposition with scalar dot products.
 
 #include "ent_internal.h"
-#include "entropy_dev.h"
 
 #include <math.h>
 
@@ -41,7 +42,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kWindow = 64;                  // units of metadata per window
-constexpr int kCombineMaxSplits = 64;        // partials staged in LDS per pass
 
 typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef short s16x4_t __attribute__((__vector_size__(4 * sizeof(short))));
@@ -62,6 +62,7 @@ struct DecodeArgs {
   float* lse;
   float* part_acc;    // [W + S, G, D]
   float* part_ml;     // [W + S, G, 2]
+  int4* rec;          // [R] cut-segment record of each range: (segment or -1, last range, U, 0)
   unsigned* flags;
   int B, Hkv, G, MAXB, P;
   int W;              // waves of the decode grid
@@ -107,6 +108,20 @@ __device__ void build_plan(const DecodeArgs& a, int* s_pref, int* s_nk, int* s_N
   }
   if (t == kThreads - 1) s_pref[a.B] = run;
   __syncthreads();
+}
+
+// Sequences with nothing kept (or an invalid context length) get out = 0 and
+// lse = -inf, written by workgroup b % gridDim.x.  s_nk is in LDS (uniform).
+template <int D>
+__device__ __forceinline__ void zero_empty(const DecodeArgs& a, const int* s_nk) {
+  const int Hq = a.Hkv * a.G;
+  for (int b = blockIdx.x; b < a.B; b += gridDim.x) {
+    if (s_nk[b] != 0) continue;
+    float* o = a.out + static_cast<long long>(b) * Hq * D;
+    for (int e = threadIdx.x; e < Hq * D; e += blockDim.x) o[e] = 0.f;
+    if (a.lse)
+      for (int h = threadIdx.x; h < Hq; h += blockDim.x) a.lse[static_cast<long long>(b) * Hq + h] = -INFINITY;
+  }
 }
 
 __device__ __forceinline__ int range_begin(int w, int U, int W) {
@@ -199,7 +214,11 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int w = blockIdx.x * kWaves + wave;
-  if (U == 0) return;
+  zero_empty<D>(a, s_nk);
+  if (U == 0) {
+    if (threadIdx.x == 0) a.rec[blockIdx.x] = make_int4(-1, 0, 0, 0);
+    return;
+  }
   const int G = a.G;
   // Cut partials of this workgroup's waves, merged in LDS at the end:
   // slot 2 i (wave i's first segment, begun before its range) and 2 i + 1
@@ -384,6 +403,7 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   __syncthreads();
   const int wg = blockIdx.x;
   const int g0 = range_begin(wg * kWaves, U, a.W), g1 = range_begin(wg * kWaves + kWaves, U, a.W);
+  int owner = -1, owner_last = 0;            // cut segment that begins in this range
   int i = 0;
   while (i < 2 * kWaves) {
     const int seg = s_cseg[i];
@@ -399,6 +419,10 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
     const int seg_end = seg_start + s_nk[b];
     const bool whole = seg_start >= g0 && seg_end <= g1;
     const long long slot = static_cast<long long>(wg) + seg;
+    if (!whole && seg_start >= g0) {
+      owner = seg;
+      owner_last = wave_of(seg_end - 1, U, a.R);
+    }
     for (int o = threadIdx.x; o < G * D; o += kThreads) {
       const int r = o / D, d = o - r * D;
       float M = -INFINITY;
@@ -428,6 +452,7 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
     }
     i = j;
   }
+  if (threadIdx.x == 0) a.rec[wg] = make_int4(owner, owner_last, U, 0);
 }
 
 template <int D>
@@ -442,6 +467,10 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
   const int U = s_pref[a.B];
   const int lane = threadIdx.x & 63;
   const int w = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  zero_empty<D>(a, s_nk);
+  // This wave's record; replaced below (same lane, program order) when a
+  // segment that begins in its range is cut.
+  if (lane == 0) a.rec[w] = make_int4(-1, 0, 0, 0);
   if (U == 0) return;
   const int u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
   if (u0 >= u1) return;
@@ -475,6 +504,8 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
         if (lane == 0 && a.lse)
           a.lse[oh] = l_run[h] > 0.f ? (m_run[h] + log2f(l_run[h])) * kLn2 : -INFINITY;
       } else {
+        if (h == 0 && lane == 0 && seg_start >= u0)
+          a.rec[w] = make_int4(cur_seg, wave_of(seg_end - 1, U, a.W), U, 0);
 #pragma unroll
         for (int y = 0; y < DPL; ++y) a.part_acc[(slot * G + h) * D + lane + 64 * y] = o[h][y];
         if (lane == 0) {
@@ -562,149 +593,62 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
 }
 
 // Merge of the partials of every segment that the decode ranges cut.  One
-// workgroup per (segment, slice of its G x d outputs); a.nsl slices per
-// segment (more when segments are cut into many partials).  Segments with
-// nothing kept get zeros and -inf.  Per head, M = max m and
-// L = sum l 2^(m - M); then out = sum_k acc_k 2^(m_k - M) / L.  When a slice
-// has fewer outputs than threads, the threads split the partials into
-// groups (independent loads) and an LDS reduction sums the groups.
-constexpr int kCombinePer = kMaxGroup * 128 / kThreads;   // outputs per thread, at most
+// workgroup per (decode range, slice of the G x d outputs); the range's
+// record names the cut segment that begins in it, if any, and the last range
+// holding a piece of it; a.nsl slices of at most 256 outputs per segment.
+// Each thread merges one output on its own, in
+// range order, with a running (max, sum, output) rescaled as the maximum
+// grows; the loads of eight partials are issued together, so one memory
+// round trip follows the record for segments cut into at most eight pieces.
+// Ranges with no units (fewer units than ranges) wrote no partial.
+constexpr int kCombinePrefetch = 8;        // partials whose loads are issued together
 
 template <int D>
 __device__ __forceinline__ void combine_body(const DecodeArgs& a, int item) {
-  extern __shared__ int s_mem[];
-  __shared__ int s_red[kWaves];
-  __shared__ float s_m[kCombineMaxSplits * kMaxGroup], s_l[kCombineMaxSplits * kMaxGroup];
-  __shared__ float s_M[kMaxGroup], s_L[kMaxGroup];
-  __shared__ float s_acc[kThreads];
-  int* s_pref = s_mem;
-  int* s_nk = s_mem + a.B + 1;
-  int* s_N = s_nk + a.B;
-  build_plan(a, s_pref, s_nk, s_N, s_red);
-  const int U = s_pref[a.B];
-  const int t = threadIdx.x;
+  const int range = item / a.nsl, slice = item - range * a.nsl;
+  const int4 rec = a.rec[range];
+  const int seg = rec.x;
+  if (seg < 0) return;                       // no cut segment begins in this range
+  const int U = rec.z;
+  const int w0 = range, w1 = rec.y;
   const int G = a.G;
-  const int seg = item / a.nsl, slice = item - seg * a.nsl;
   const int b = seg / a.Hkv, g = seg % a.Hkv;
   const int Hq = a.Hkv * G;
-  const int nk = s_nk[b];
-  const int span = G * D / a.nsl;            // outputs of this workgroup (power of two >= 64)
-  const int width = min(span, kThreads);     // threads per partial group
-  const int npg = kThreads / width;          // partial groups
-  const int opt = span / width;              // outputs per thread
-  const int pg = t / width, ol = t - pg * width;
+  const int span = G * D / a.nsl;            // outputs of this workgroup, <= kThreads
+  const int o = slice * span + static_cast<int>(threadIdx.x);
+  if (static_cast<int>(threadIdx.x) >= span) return;
+  const int r = o / D, d = o - r * D;
   const long long ob = static_cast<long long>(b) * Hq + g * G;   // first output head row
-  if (nk == 0) {
-    if (pg == 0)
-      for (int x = 0; x < opt; ++x) {
-        const int o = slice * span + ol + x * width;
-        const int r = o / D, d = o - r * D;
-        a.out[(ob + r) * D + d] = 0.f;
-        if (d == 0 && a.lse) a.lse[ob + r] = -INFINITY;
-      }
-    return;
-  }
-  const int seg_start = s_pref[b] + g * nk;
-  const int w0 = wave_of(seg_start, U, a.R);
-  const int w1 = wave_of(seg_start + nk - 1, U, a.R);
-  if (w0 == w1) return;                      // written whole by the decode kernel
-  const int ns = w1 - w0 + 1;
-
-  float acc[kCombinePer];
+  float M = -INFINITY, L = 0.f, acc = 0.f;
+  for (int c0 = w0; c0 <= w1; c0 += kCombinePrefetch) {
+    float m[kCombinePrefetch], l[kCombinePrefetch], v[kCombinePrefetch];
 #pragma unroll
-  for (int x = 0; x < kCombinePer; ++x) acc[x] = 0.f;
-  float M = -INFINITY, L = 0.f;              // meaningful in threads t < G
-  for (int c0 = 0; c0 < ns; c0 += kCombineMaxSplits) {
-    const int n = min(kCombineMaxSplits, ns - c0);
-    for (int e = t; e < n * G; e += kThreads) {
-      const int k = e / G, rr = e % G;
-      const int wi = w0 + c0 + k;
-      // A wave with an empty range (fewer units than waves) wrote no partial.
-      const bool live = range_begin(wi + 1, U, a.R) > range_begin(wi, U, a.R);
+    for (int k = 0; k < kCombinePrefetch; ++k) {
+      const int wi = c0 + k;
+      const bool ok = wi <= w1 && range_begin(wi + 1, U, a.R) > range_begin(wi, U, a.R);
       const long long slot = static_cast<long long>(wi) + seg;
-      s_m[e] = live ? a.part_ml[(slot * G + rr) * 2 + 0] : 0.f;
-      s_l[e] = live ? a.part_ml[(slot * G + rr) * 2 + 1] : 0.f;
+      m[k] = ok ? a.part_ml[(slot * G + r) * 2 + 0] : -INFINITY;
+      l[k] = ok ? a.part_ml[(slot * G + r) * 2 + 1] : 0.f;
+      v[k] = ok ? a.part_acc[(slot * G + r) * D + d] : 0.f;
     }
-    __syncthreads();
-    if (t < G) {
-      float Mc = M;
-      for (int k = 0; k < n; ++k)
-        if (s_l[k * G + t] > 0.f) Mc = fmaxf(Mc, s_m[k * G + t]);
-      float Lc = (L > 0.f) ? L * exp2f(M - Mc) : 0.f;
-      for (int k = 0; k < n; ++k) {
-        const float l = s_l[k * G + t];
-        if (l > 0.f) Lc += l * exp2f(s_m[k * G + t] - Mc);
-      }
-      s_M[t] = Mc;
-      s_L[t] = (M == -INFINITY) ? 1.f : exp2f(M - Mc);   // rescales earlier chunks
-      M = Mc;
-      L = Lc;
-    }
-    __syncthreads();
-    for (int e = t; e < n * G; e += kThreads) {
-      const float l = s_l[e];
-      s_m[e] = (l > 0.f) ? exp2f(s_m[e] - s_M[e % G]) : 0.f;
-    }
-    __syncthreads();
 #pragma unroll
-    for (int x = 0; x < kCombinePer; ++x) {
-      if (x < opt) {
-        const int o = slice * span + ol + x * width;
-        const int r = o / D, d = o - r * D;
-        const float* pa = a.part_acc + ((static_cast<long long>(w0 + c0) + seg) * G + r) * D + d;
-        float part = 0.f;
-#pragma unroll 4
-        for (int k = pg; k < n; k += npg) {
-          const float wk = s_m[k * G + r];
-          const float v = pa[static_cast<long long>(k) * G * D];
-          part += wk > 0.f ? wk * v : 0.f;
-        }
-        acc[x] = acc[x] * s_L[r] + part;
-      }
-    }
-    __syncthreads();
-  }
-  if (t < G) {
-    s_M[t] = M;
-    s_L[t] = L;
-  }
-  if (npg > 1) s_acc[t] = acc[0];            // opt == 1 when the partials are split
-  __syncthreads();
-  if (pg != 0) return;
-#pragma unroll
-  for (int x = 0; x < kCombinePer; ++x) {
-    if (x < opt) {
-      const int o = slice * span + ol + x * width;
-      const int r = o / D, d = o - r * D;
-      float tot = acc[x];
-      for (int q = 1; q < npg; ++q) tot += s_acc[q * width + ol];
-      const float Lr = s_L[r];
-      a.out[(ob + r) * D + d] = Lr > 0.f ? tot / Lr : 0.f;
-      if (d == 0 && a.lse) a.lse[ob + r] = Lr > 0.f ? (s_M[r] + log2f(Lr)) * kLn2 : -INFINITY;
+    for (int k = 0; k < kCombinePrefetch; ++k) {
+      if (!(l[k] > 0.f)) continue;
+      const float Mn = fmaxf(M, m[k]);
+      const float f_old = (M == -INFINITY) ? 0.f : exp2f(M - Mn);
+      const float f_new = exp2f(m[k] - Mn);
+      L = L * f_old + l[k] * f_new;
+      acc = acc * f_old + v[k] * f_new;
+      M = Mn;
     }
   }
+  a.out[(ob + r) * D + d] = L > 0.f ? acc / L : 0.f;
+  if (d == 0 && a.lse) a.lse[ob + r] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
 }
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
   combine_body<D>(a, blockIdx.x);
-}
-
-// The merge above, and in the same launch (workgroups 0 .. B-1, first) the
-// sampling of every row: the two are independent, and the sampling
-// workgroups run in the merge's shadow.
-template <int D, bool VEC>
-__global__ __launch_bounds__(kThreads) void combine_sample_kernel(DecodeArgs a, SampleArgs sa) {
-  static_assert(kThreads == kSampleThreads, "sampling workgroup size");
-  __shared__ SampleShared sh;
-  if (static_cast<int>(blockIdx.x) < a.B) {
-    const int b = blockIdx.x;
-    const int tok = sample_body<VEC>(sa.logits, sa.ld, sa.V, sa.C, sa.stats, sa.temp_used[b],
-                                     sa.uniforms[b], b, sh);
-    if (threadIdx.x == 0) sa.tokens[b] = tok;
-    return;
-  }
-  combine_body<D>(a, blockIdx.x - a.B);
 }
 
 template <typename K>
@@ -747,7 +691,7 @@ long long decode_partial_slots(int decode_grid, int max_batch, int num_kv_heads)
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
-                         hipStream_t s, const SampleArgs* sample, const int* kept_phys) {
+                         hipStream_t s, const int* kept_phys) {
   const ent_config& cf = c->cfg;
   DecodeArgs a;
   a.q = q;
@@ -762,6 +706,7 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   a.lse = lse;
   a.part_acc = c->dec_acc;
   a.part_ml = c->dec_ml;
+  a.rec = c->dec_rec;
   a.flags = c->dev_flags;
   a.B = B;
   a.Hkv = cf.num_kv_heads;
@@ -787,32 +732,13 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // Slices per segment: split the outputs (and the partials across thread
-  // groups) when segments are cut into many partials on average.
-  const int waves_per_seg = a.R / std::max(1, B * cf.num_kv_heads);
-  const int nsl = waves_per_seg >= 8 ? c->group * cf.head_dim / 64 : 1;
-  a.nsl = nsl;
-  if (sample) {
-    const dim3 cgrid(B * cf.num_kv_heads * nsl + B);
-    const bool vec = row_vec_ok(sample->logits, sample->ld);
-    if (cf.head_dim == 128) {
-      if (vec)
-        hipLaunchKernelGGL((combine_sample_kernel<128, true>), cgrid, dim3(kThreads), lds, s, a, *sample);
-      else
-        hipLaunchKernelGGL((combine_sample_kernel<128, false>), cgrid, dim3(kThreads), lds, s, a, *sample);
-    } else {
-      if (vec)
-        hipLaunchKernelGGL((combine_sample_kernel<64, true>), cgrid, dim3(kThreads), lds, s, a, *sample);
-      else
-        hipLaunchKernelGGL((combine_sample_kernel<64, false>), cgrid, dim3(kThreads), lds, s, a, *sample);
-    }
-    return hipGetLastError();
-  }
-  const dim3 cgrid(B * cf.num_kv_heads * nsl);
+  // Slices per segment: one output per merge thread.
+  a.nsl = std::max(1, c->group * cf.head_dim / kThreads);
+  const dim3 cgrid(a.R * a.nsl);
   if (cf.head_dim == 128)
-    hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), lds, s, a);
+    hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), 0, s, a);
   else
-    hipLaunchKernelGGL(combine_kernel<64>, cgrid, dim3(kThreads), lds, s, a);
+    hipLaunchKernelGGL(combine_kernel<64>, cgrid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -41,6 +41,7 @@ struct ent_ctx {
   int* kept_phys = nullptr;       // [max_batch, MAXB]  physical blocks of the kept lists
   float* dec_acc = nullptr;       // [decode partial slots, G, d]
   float* dec_ml = nullptr;        // [decode partial slots, G, 2]
+  int4* dec_rec = nullptr;        // [decode waves]  cut-segment records of the decode ranges
   unsigned* dev_flags = nullptr;  // [1]
 
   std::string err;
@@ -74,6 +75,7 @@ struct PrologueArgs {
   const float* temp;
   float* part;          // chunk triples (nullable)
   float* row_stats;     // chunk (max, sum) (nullable)
+  float* temp_used;     // nullable: receives temp[b] (written by chunk 0's job)
   int do_score;
   const uint16_t* q;
   const float* ksum;
@@ -101,8 +103,8 @@ hipError_t launch_select_rows(const ent_ctx* c, int B, const int* tables, const 
 hipError_t launch_score_valu(const ent_ctx* c, int B, const void* q, const float* ksum,
                              const int* tables, const int* ctx_lens, hipStream_t s);
 
-// Sampling issued in the launch that merges the decode partials (the fused
-// step); the arguments of ent_sample.
+// Sampling issued in the launch that runs the kept-block selection (the
+// fused step), on workgroups of its own; the arguments of ent_sample.
 struct SampleArgs {
   const float* logits;
   long long ld;
@@ -118,8 +120,7 @@ struct SampleArgs {
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
-                         hipStream_t s,
-                         const SampleArgs* sample = nullptr, const int* kept_phys = nullptr);
+                         hipStream_t s, const int* kept_phys = nullptr);
 hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
                               ent_state st, const void* q, const void* k_cache,
                               const void* v_cache, const float* ksum, const int* tables,

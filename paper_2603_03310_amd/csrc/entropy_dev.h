@@ -160,14 +160,15 @@ __device__ __forceinline__ float row_entropy(const float* __restrict__ part, int
   }
 }
 
-// Controller update of sequence b given its entropy H at temperature T.
+// Controller update of sequence b given its entropy H at temperature T
+// (temp_used nullable: the fused step records T_t earlier).
 __device__ __forceinline__ void controller_update(int b, float H, float T, float* h_prev,
                                                   float* tau, float* temp, float* h_out,
                                                   float* temp_used, float eta, float h_target,
                                                   float t_min, float t_max) {
 #pragma clang fp contract(off)
   h_out[b] = H;
-  temp_used[b] = T;
+  if (temp_used) temp_used[b] = T;
   const float hp = h_prev[b];
   float ta = tau[b];
   if (!isnan(hp)) ta += fmaxf(0.f, hp - H);

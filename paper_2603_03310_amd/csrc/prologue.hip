@@ -5,7 +5,10 @@
 //     group of four KV heads); wave w takes KV head 4 hg + w
 //     (score_head_load / score_head_compute, Section 3.2);
 //   * entropy chunk passes: job (row b, chunk c) of 4096 logits
-//     (entropy_chunk_body, Section 2.1).
+//     (entropy_chunk_body, Section 2.1); chunk 0's job also records the
+//     row's temperature T_t in temp_used when asked (the fused step's
+//     sampler reads it in the next launch, while the controller replaces
+//     temp with T_{t+1}).
 //
 // Both read HBM once (block summaries, logits) at a few flops per byte and
 // do not depend on each other; scoring jobs come first.  Every workgroup
@@ -111,6 +114,7 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(PrologueArgs a) {
     const int b = e / a.C;
     entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats, e - b * a.C,
                             b, red);
+    if (e == b * a.C && threadIdx.x == 0 && a.temp_used) a.temp_used[b] = a.temp[b];
     return;
   }
   int* s_pref = s_mem;
@@ -135,6 +139,7 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(PrologueArgs a) {
       const int b = e / a.C;
       entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats,
                               e - b * a.C, b, red);
+      if (e == b * a.C && threadIdx.x == 0 && a.temp_used) a.temp_used[b] = a.temp[b];
     }
   }
 }

@@ -6,15 +6,16 @@
 //   A  block scoring and the entropy chunk passes in one persistent grid
 //      (prologue.hip): both stream from HBM (block summaries, logits) and
 //      do not depend on each other (fp32 queries: scoring is a second
-//      launch, on the VALU);
+//      launch, on the VALU); each row's T_t is recorded in temp_used;
 //   B  one workgroup per sequence: the row's entropy from the chunk triples,
 //      the controller update and the kept-block selection under the
 //      entropy-driven budget (for long block tables: entropy, controller and
 //      L_h per sequence, the block scores over the whole chip, then the
-//      selection per sequence);
+//      selection per sequence); in the same launch, on workgroups of their
+//      own, sampling at T_t (it needs only the row statistics of A, so it
+//      runs on the CUs the per-sequence selection leaves idle);
 //   C  kept-block decode attention;
-//   D  the merge of split decode segments and, in the same launch, sampling
-//      at the temperature the step used (independent of the merge).
+//   D  the merge of split decode segments.
 
 #include "blocks_dev.h"
 #include "entropy_dev.h"
@@ -22,19 +23,36 @@
 namespace ent {
 namespace {
 
+// Sampling of row b - B by a workgroup of the launch that runs the
+// per-sequence stage (blockIdx.x >= B); every thread must call it.
+template <bool VEC>
+__device__ __forceinline__ void step_sample(const SampleArgs& sa, int b, SampleShared& sh) {
+  const int tok = sample_body<VEC>(sa.logits, sa.ld, sa.V, sa.C, sa.stats, sa.temp_used[b],
+                                   sa.uniforms[b], b, sh);
+  if (threadIdx.x == 0) sa.tokens[b] = tok;
+}
+
 // Per sequence: the row's entropy from the chunk triples and the controller
-// update (first wave), and L_h for the selection (all threads).
+// update (first wave), and L_h for the selection (all threads); workgroups
+// B .. 2B-1 sample.
+template <bool VEC>
 __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
-    const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau, float* h_out,
-    float* temp_used, float eta, float h_target, float t_min, float t_max,
+    int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
+    float* h_out, float eta, float h_target, float t_min, float t_max,
     const float* __restrict__ lse_part, const int* __restrict__ ctx_lens, float* __restrict__ L,
-    int Hq, int MAXB, int nch_max) {
+    int Hq, int MAXB, int nch_max, SampleArgs sa) {
+  static_assert(kRowThreads >= kSampleThreads, "sampling workgroup size");
   __shared__ float s_pm[kRowThreads], s_ps[kRowThreads];
+  __shared__ SampleShared ssh;
   const int b = blockIdx.x;
+  if (b >= B) {
+    step_sample<VEC>(sa, b - B, ssh);
+    return;
+  }
   if (threadIdx.x < 64) {
     const float H = row_entropy(part, C, b);
     if (threadIdx.x == 0)
-      controller_update(b, H, temp[b], h_prev, tau, temp, h_out, temp_used, eta, h_target, t_min,
+      controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min,
                         t_max);
   }
   lse_merge_body(lse_part, ctx_lens, L + static_cast<long long>(b) * Hq, Hq, MAXB, nch_max, b,
@@ -43,20 +61,27 @@ __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
 
 // Per sequence, short block tables: the selection's loads are issued first,
 // then the first wave computes the row's entropy and the controller update
-// while they are in flight, then the whole kept-block selection.
-template <int HPL>
+// while they are in flight, then the whole kept-block selection; workgroups
+// B .. 2B-1 sample.
+template <int HPL, bool VEC>
 __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
-    const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau, float* h_out,
-    float* temp_used, float eta, float h_target, float t_min, float t_max,
+    int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
+    float* h_out, float eta, float h_target, float t_min, float t_max,
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, const int* __restrict__ tables, float* __restrict__ scores,
     float* __restrict__ theta, int* __restrict__ kept, int* __restrict__ kphys,
     int* __restrict__ n_kept, int MAXB, int P, int nch_max, float eps_h, float h_min, float log_v,
-    float kappa_min, int b_min, unsigned* flags) {
+    float kappa_min, int b_min, unsigned* flags, SampleArgs sa) {
+  static_assert(kSelThreads >= kSampleThreads, "sampling workgroup size");
   extern __shared__ unsigned keys[];        // [MAXB] keys, then [MAXB] encoded blocks
   __shared__ SelectShared sh;
+  __shared__ SampleShared ssh;
   __shared__ float s_H;
   const int b = blockIdx.x;
+  if (b >= B) {
+    step_sample<VEC>(sa, b - B, ssh);
+    return;
+  }
   const int N = ctx_lens[b];
   const bool ok = N >= 0 && N <= MAXB * kBlock;
   const int nb = ok ? (N + kBlock - 1) / kBlock : 0;
@@ -66,7 +91,7 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     const float H = row_entropy(part, C, b);
     if (threadIdx.x == 0) {
       s_H = H;
-      controller_update(b, H, temp[b], h_prev, tau, temp, h_out, temp_used, eta, h_target, t_min,
+      controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min,
                         t_max);
     }
   }
@@ -101,6 +126,7 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   pa.temp = st.temp;
   pa.part = c->ent_part;
   pa.row_stats = stats;
+  pa.temp_used = temp_used;
   pa.do_score = bf16 ? 1 : 0;
   pa.q = static_cast<const uint16_t*>(q);
   pa.ksum = ksum;
@@ -122,42 +148,6 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
     if (e != hipSuccess) return e;
   }
 
-  const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
-  if (hpl) {
-    const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-#define ENT_STEPB_CASE(HH)                                                                     \
-  case HH:                                                                                     \
-    hipLaunchKernelGGL((step_b_kernel<HH>), dim3(B), dim3(kSelThreads), lds, s, c->ent_part,   \
-                       c->chunks, st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta,        \
-                       cf.h_target, cf.t_min, cf.t_max, c->zbuf, c->lse_part, ctx_lens,        \
-                       tables, scores, theta, kept, c->kept_phys, n_kept,                      \
-                       cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, cf.eps_h,     \
-                       cf.h_min, cf.log_v, cf.kappa_min, cf.b_min, c->dev_flags);              \
-    break;
-    switch (hpl) {
-      ENT_STEPB_CASE(1)
-      ENT_STEPB_CASE(2)
-      ENT_STEPB_CASE(4)
-      ENT_STEPB_CASE(8)
-      default:
-        return hipErrorInvalidValue;
-    }
-#undef ENT_STEPB_CASE
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  } else {
-    hipLaunchKernelGGL(step_b0_kernel, dim3(B), dim3(kRowThreads), 0, s, c->ent_part, c->chunks,
-                       st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta, cf.h_target,
-                       cf.t_min, cf.t_max, c->lse_part, ctx_lens, c->lrow, cf.num_q_heads,
-                       cf.max_blocks_per_seq, c->lse_chunks);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    float* sc = scores ? scores : c->iscores;
-    e = launch_block_scores(c, B, ctx_lens, sc, s);
-    if (e != hipSuccess) return e;
-    e = launch_select_rows(c, B, tables, ctx_lens, h_out, sc, theta, kept, n_kept, s);
-    if (e != hipSuccess) return e;
-  }
   SampleArgs sa;
   sa.logits = logits;
   sa.ld = ld;
@@ -167,8 +157,50 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   sa.temp_used = temp_used;
   sa.uniforms = uniforms;
   sa.tokens = tokens;
+  const bool vec = row_vec_ok(logits, ld);
+  const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
+  if (hpl) {
+    const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
+#define ENT_STEPB_CASE(HH, VV)                                                                 \
+  hipLaunchKernelGGL((step_b_kernel<HH, VV>), dim3(2 * B), dim3(kSelThreads), lds, s, B,       \
+                     c->ent_part, c->chunks, st.temp, st.h_prev, st.tau, h_out, cf.eta,        \
+                     cf.h_target, cf.t_min, cf.t_max, c->zbuf, c->lse_part, ctx_lens, tables,  \
+                     scores, theta, kept, c->kept_phys, n_kept, cf.max_blocks_per_seq,         \
+                     cf.num_pool_blocks, c->lse_chunks, cf.eps_h, cf.h_min, cf.log_v,          \
+                     cf.kappa_min, cf.b_min, c->dev_flags, sa)
+#define ENT_STEPB_HPL(HH)                   \
+  case HH:                                  \
+    if (vec) ENT_STEPB_CASE(HH, true);      \
+    else ENT_STEPB_CASE(HH, false);         \
+    break;
+    switch (hpl) {
+      ENT_STEPB_HPL(1)
+      ENT_STEPB_HPL(2)
+      ENT_STEPB_HPL(4)
+      ENT_STEPB_HPL(8)
+      default:
+        return hipErrorInvalidValue;
+    }
+#undef ENT_STEPB_HPL
+#undef ENT_STEPB_CASE
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  } else {
+    auto k0 = vec ? step_b0_kernel<true> : step_b0_kernel<false>;
+    hipLaunchKernelGGL(k0, dim3(2 * B), dim3(kRowThreads), 0, s, B, c->ent_part, c->chunks,
+                       st.temp, st.h_prev, st.tau, h_out, cf.eta, cf.h_target, cf.t_min,
+                       cf.t_max, c->lse_part, ctx_lens, c->lrow, cf.num_q_heads,
+                       cf.max_blocks_per_seq, c->lse_chunks, sa);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    float* sc = scores ? scores : c->iscores;
+    e = launch_block_scores(c, B, ctx_lens, sc, s);
+    if (e != hipSuccess) return e;
+    e = launch_select_rows(c, B, tables, ctx_lens, h_out, sc, theta, kept, n_kept, s);
+    if (e != hipSuccess) return e;
+  }
   return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s,
-                       &sa, c->kept_phys);
+                       c->kept_phys);
 }
 
 }  // namespace ent
