@@ -52,6 +52,15 @@ enum {
 
 enum { ENT_F32 = 0, ENT_BF16 = 1 };
 
+/* Entropy the controller acts on (Section 2.1 and Section 3.3, "Entropy
+ * estimator in the control loop"): the exact entropy, the top-k truncated
+ * entropy H~ of the renormalised top-k distribution, or the tail-corrected
+ * estimate H^ = H~ + h(mbar) + mbar ln(|V| - k) (mbar = probability mass
+ * outside the top-k set, h the binary entropy).  With k >= |V| both
+ * estimates equal the exact entropy. */
+enum { ENT_EST_EXACT = 0, ENT_EST_TOPK = 1, ENT_EST_TAIL = 2 };
+#define ENT_EST_MAX_K 512
+
 /* Tokens per logical row chunk of the entropy reduction; row statistics hold
  * one (max, sum) pair per chunk: ent_row_stats_chunks(vocab) chunks per row. */
 #define ENT_ROW_CHUNK 4096
@@ -87,6 +96,9 @@ typedef struct {
   float kappa_min;         /* smallest kept fraction of blocks, in [0, 1] */
   int b_min;               /* smallest number of kept blocks, >= 0 */
   float log_v;             /* log |V| as float32; must exceed h_min */
+  int estimator;           /* ENT_EST_EXACT, ENT_EST_TOPK or ENT_EST_TAIL; with an estimate,
+                              eps_h is its error bound and enters the block budget */
+  int est_k;               /* k of the estimators, 1 <= k <= ENT_EST_MAX_K (ignored when exact) */
 } ent_config;
 
 /* Per-sequence controller state, device arrays of B floats each, read and
@@ -100,7 +112,8 @@ typedef struct {
 
 /* Defaults: Llama-3-8B decode shapes (32/8 heads, d = 128, bf16, |V| = 128256),
  * eta = -0.05, H* = 2.5, T in [0.05, 5], eps_H = 0, H_min = H*, kappa_min = 0.05,
- * B_min = 4.  max_batch, max_blocks_per_seq and num_pool_blocks must be set. */
+ * B_min = 4, exact entropy (est_k = 256 for the estimators).  max_batch,
+ * max_blocks_per_seq and num_pool_blocks must be set. */
 void ent_default_config(ent_config* out);
 
 /* Host-only check of a configuration (no HIP call).  Returns ENT_OK, or
@@ -129,11 +142,13 @@ const char* ent_last_error(const ent_ctx* c);
 int ent_device_status(ent_ctx* c, void* stream, unsigned* flags);
 
 /* Entropy and controller (Section 2: H_t, Delta H_t, entropic time tau;
- * Section 2.1: exact entropy of the tempered softmax; Section 3.3: the
- * temperature law T_{t+1} = clip(T_t exp(eta (H_t - H*)), T_min, T_max)).
+ * Section 2.1: exact entropy of the tempered softmax and its top-k and
+ * tail-corrected estimates; Section 3.3: the temperature law
+ * T_{t+1} = clip(T_t exp(eta (H_t - H*)), T_min, T_max)).
  *
  * For each row b < B of logits (fp32, row stride ld >= vocab elements):
  *   H_t      = -sum_x p(x) ln p(x),  p = softmax(z / T_t),  T_t = st.temp[b]
+ *              (or the configured estimate of it, cfg.estimator)
  *   h_out[b] = H_t;  temp_used[b] = T_t
  *   st.tau[b]   += max(0, st.h_prev[b] - H_t)   (unchanged if h_prev is NaN)
  *   st.h_prev[b] = H_t;  st.temp[b] = T_{t+1}

@@ -43,6 +43,10 @@ std::string check_config(const ent_config* c, int* code) {
     return "need finite h_min < log_v";
   if (!(c->kappa_min >= 0.f && c->kappa_min <= 1.f)) return "kappa_min must be in [0, 1]";
   if (c->b_min < 0) return "b_min must be >= 0";
+  if (c->estimator != ENT_EST_EXACT && c->estimator != ENT_EST_TOPK && c->estimator != ENT_EST_TAIL)
+    return "estimator must be ENT_EST_EXACT, ENT_EST_TOPK or ENT_EST_TAIL";
+  if (c->estimator != ENT_EST_EXACT && (c->est_k < 1 || c->est_k > ENT_EST_MAX_K))
+    return "est_k must be in [1, ENT_EST_MAX_K]";
   *code = ENT_E_UNSUPPORTED;
   if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
   if (!is_pow2_group(c->num_q_heads / c->num_kv_heads))
@@ -104,6 +108,8 @@ void ent_default_config(ent_config* out) {
   out->kappa_min = 0.05f;
   out->b_min = 4;
   out->log_v = static_cast<float>(log(128256.0));
+  out->estimator = ENT_EST_EXACT;
+  out->est_k = 256;
 }
 
 int ent_check_config(const ent_config* cfg, char* msg, int msg_len) {
@@ -160,9 +166,12 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   const size_t sz_acc = align_up(nslots * c->group * f.head_dim * sizeof(float));
   const size_t sz_ml = align_up(nslots * c->group * 2 * sizeof(float));
   const size_t sz_rec = align_up(static_cast<size_t>(c->decode_grid) * 4 * sizeof(int4));
+  const size_t sz_tmax = f.estimator == ENT_EST_EXACT
+                             ? 0
+                             : align_up(Bm * c->chunks * ent::kEstChunkThreads * sizeof(float));
   const size_t sz_flags = align_up(sizeof(unsigned));
   c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_lrow + sz_isc + sz_kphys + sz_acc + sz_ml +
-                sz_rec + sz_flags;
+                sz_rec + sz_tmax + sz_flags;
   e = hipMalloc(&c->ws, c->ws_bytes);
   if (e != hipSuccess) {
     g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
@@ -189,6 +198,7 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->dec_acc = reinterpret_cast<float*>(take(sz_acc));
   c->dec_ml = reinterpret_cast<float*>(take(sz_ml));
   c->dec_rec = reinterpret_cast<int4*>(take(sz_rec));
+  c->tmax = sz_tmax ? reinterpret_cast<float*>(take(sz_tmax)) : nullptr;
   c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));
   *out = c;
   return ENT_OK;

@@ -82,20 +82,26 @@ __device__ __forceinline__ void chunk_lse(const float* zt, int nblk, int Hq, int
 // loaded with score_head_load and reduced with score_head_compute.
 constexpr int kScoreSlots = 8;          // float4 slots per lane (d <= 128)
 
-// Physical block of tile row r16 (lane & 15), validated; 0 for rows past the
-// sequence's nb blocks.
-__device__ __forceinline__ int score_tile_block(const int* __restrict__ tables, int b, int ch,
-                                                int MAXB, int nb, int P, unsigned* flags) {
-  const int r16 = threadIdx.x & 15;
-  const int j = ch * kMfmaChunk + r16;
+// Table entry of tile row r16 (lane & 15), read before the context length
+// is known (-1 past the row); score_tile_check validates it once nb is.
+__device__ __forceinline__ int score_tile_entry(const int* __restrict__ tables, int b, int ch,
+                                                int MAXB) {
+  const int j = ch * kMfmaChunk + (threadIdx.x & 15);
+  return j < MAXB ? tables[static_cast<long long>(b) * MAXB + j] : -1;
+}
+
+// Physical block of tile row r16 from its table entry, validated; 0 for rows
+// past the sequence's nb blocks.
+__device__ __forceinline__ int score_tile_check(int p, int ch, int nb, int P, unsigned* flags) {
+  const int j = ch * kMfmaChunk + (threadIdx.x & 15);
   if (j >= nb) return 0;
-  int p = tables[static_cast<long long>(b) * MAXB + j];
   if (p < 0 || p >= P) {
     raise_flag(flags, ENT_DEV_BAD_TABLE);
     p = 0;
   }
   return p;
 }
+
 
 // Lane (r16, gq) loads, for head g of block row r16, the float4 slots
 // j = 0 .. D/16 - 1 at dims 16 j + 4 gq .. +3 (the four lanes of a row read
@@ -586,8 +592,10 @@ __device__ __forceinline__ void select_row_body(
 // that a caller can overlap other work with the loads: select_load issues
 // every global read of the sequence at once (its block logits, four lanes
 // per block and HPL = H_q / 4 heads per lane, and the per-tile log-sum-exp
-// partials of the L merge) into registers; select_finish merges L, scores
-// the blocks and selects.  The arithmetic, and its order, is that of the
+// partials of the L merge) into registers, for the whole block-table row,
+// so that no load waits for the context length (entries past the sequence's
+// blocks are read and never used); select_finish merges L, scores the blocks
+// and selects.  The arithmetic, and its order, is that of the
 // three-launch form (lse_merge_body, block_score_quad, select_core).
 constexpr int kFusedRegs = 32;            // logits per lane, at most
 constexpr int kFusedTiles = 8;            // L-merge tiles per thread, at most
@@ -616,9 +624,10 @@ template <int HPL>
 __device__ __forceinline__ void select_load(const float* __restrict__ zbuf,
                                             const float* __restrict__ lse_part,
                                             const int* __restrict__ tables, int MAXB,
-                                            int nch_max, int b, int nb, SelectRegs<HPL>& R) {
+                                            int nch_max, int b, SelectRegs<HPL>& R) {
   constexpr int Hq = 4 * HPL;
   const int t = threadIdx.x, qq = t & 3;
+  const int nb = MAXB;
 #pragma unroll
   for (int p = 0; p < SelectRegs<HPL>::kPasses; ++p) {
     const int j = p * (kSelThreads / 4) + (t >> 2);
@@ -723,13 +732,13 @@ __device__ __forceinline__ void select_fused_body(
     int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P, int nch_max, float eps_h,
     float h_min, float log_v, float kappa_min, int b_min, unsigned* flags, int b, unsigned* keys,
     int* tbl, SelectShared& sh) {
+  SelectRegs<HPL> R;
+  select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, R);
   const int N = ctx_lens[b];
   int nb, k;
   if (!select_prepare(N, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min,
                       flags, b, nb, k))
     return;
-  SelectRegs<HPL> R;
-  select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, nb, R);
   select_finish<HPL>(R, N, nb, hval, scores_out, theta_out, kept, kphys, n_kept, MAXB, P, eps_h,
                      h_min, log_v, kappa_min, b_min, b, keys, tbl, sh);
 }

@@ -15,6 +15,7 @@ constexpr int kRowChunk = ENT_ROW_CHUNK;    // logits per entropy chunk
 constexpr int kMinScoreChunk = 16;          // smallest scoring chunk (blocks)
 constexpr int kMaxGroup = 16;               // query heads per KV head
 constexpr int kMaxBlocksPerSeq = 16384;     // selection keeps all scores in LDS
+constexpr int kEstChunkThreads = 256;       // threads of an entropy chunk job (maxima per chunk)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -42,12 +43,19 @@ struct ent_ctx {
   float* dec_acc = nullptr;       // [decode partial slots, G, d]
   float* dec_ml = nullptr;        // [decode partial slots, G, 2]
   int4* dec_rec = nullptr;        // [decode waves]  cut-segment records of the decode ranges
+  float* tmax = nullptr;          // [max_batch, chunks, 256]  per-thread logit maxima (estimators)
   unsigned* dev_flags = nullptr;  // [1]
 
   std::string err;
 };
 
 namespace ent {
+
+// Whether the controller acts on an estimate (top-k or tail-corrected) of
+// the entropy: with k >= |V| both estimates are the exact entropy.
+inline bool uses_estimate(const ent_config& cf) {
+  return cf.estimator != ENT_EST_EXACT && cf.est_k < cf.vocab;
+}
 
 // Launchers (one per kernel family); each returns the launch status.
 hipError_t launch_entropy(const ent_ctx* c, int B, const float* logits, long long ld,
@@ -76,6 +84,7 @@ struct PrologueArgs {
   float* part;          // chunk triples (nullable)
   float* row_stats;     // chunk (max, sum) (nullable)
   float* temp_used;     // nullable: receives temp[b] (written by chunk 0's job)
+  float* tmax;          // nullable: per-thread maxima of the chunk, [B, C, 256] (estimators)
   int do_score;
   const uint16_t* q;
   const float* ksum;

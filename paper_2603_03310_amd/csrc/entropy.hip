@@ -2,10 +2,26 @@
 // (device bodies and their description in entropy_dev.h; the chunk passes run
 // in the persistent kernel of prologue.hip).
 
-#include "entropy_dev.h"
+#include "estimate_dev.h"
 
 namespace ent {
 namespace {
+
+// One workgroup per row: the top-k or tail-corrected estimate from the chunk
+// triples, the thread maxima and the re-read logits, then the controller.
+__global__ __launch_bounds__(kEstThreads) void estimate_finalize_kernel(
+    int est, int k, int V, int C, const float* __restrict__ part, const float* __restrict__ tmax,
+    const float* __restrict__ logits, long long ld, float* __restrict__ temp,
+    float* __restrict__ h_prev, float* __restrict__ tau, float* __restrict__ h_out,
+    float* __restrict__ temp_used, float eta, float h_target, float t_min, float t_max) {
+  extern __shared__ unsigned est_lds[];
+  __shared__ EstShared esh;
+  const int b = blockIdx.x;
+  const float T = temp[b];
+  const float H = row_estimate(est, k, part, tmax, logits, ld, V, C, T, b, est_lds, esh);
+  if (threadIdx.x == 0)
+    controller_update(b, H, T, h_prev, tau, temp, h_out, temp_used, eta, h_target, t_min, t_max);
+}
 
 // One wave per row: merge of the row's chunk triples, then the controller.
 __global__ __launch_bounds__(256) void entropy_finalize_kernel(
@@ -49,12 +65,21 @@ hipError_t launch_entropy(const ent_ctx* c, int B, const float* logits, long lon
   a.temp = controller ? st.temp : temp_used;
   a.part = controller ? c->ent_part : nullptr;
   a.row_stats = row_stats;
+  const bool est = controller && uses_estimate(cf);
+  a.tmax = est ? c->tmax : nullptr;
   a.Hkv = cf.num_kv_heads;
   a.G = c->group;
   a.MAXB = cf.max_blocks_per_seq;
   a.flags = c->dev_flags;
   hipError_t e = launch_prologue(c, a, s);
   if (e != hipSuccess || !controller) return e;
+  if (est) {
+    hipLaunchKernelGGL(estimate_finalize_kernel, dim3(B), dim3(kEstThreads),
+                       est_lds_bytes(c->chunks, cf.est_k), s, cf.estimator, cf.est_k, cf.vocab,
+                       c->chunks, c->ent_part, c->tmax, logits, ld, st.temp, st.h_prev, st.tau,
+                       h_out, temp_used, cf.eta, cf.h_target, cf.t_min, cf.t_max);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(entropy_finalize_kernel, dim3((B + 3) / 4), dim3(256), 0, s, B, c->chunks,
                      c->ent_part, st.temp, st.h_prev, st.tau, h_out, temp_used, cf.eta,
                      cf.h_target, cf.t_min, cf.t_max);

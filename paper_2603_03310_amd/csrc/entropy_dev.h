@@ -87,13 +87,17 @@ __device__ __forceinline__ void load_chunk(const float* __restrict__ row, int V,
 }
 
 // Chunk pass of (chunk c, row b) by a 256-thread workgroup: writes the triple
-// (M, S, W) to part (when non-null) and (M, S) to row_stats (when non-null).
+// (M, S, W) to part (when non-null), (M, S) to row_stats (when non-null) and
+// each thread's largest scaled logit to tmax[b, c, thread] (when non-null:
+// the top-k estimators select from these).
 template <bool VEC>
 __device__ __forceinline__ void entropy_chunk_body(const float* __restrict__ logits, long long ld,
                                                    int V, int C, const float* __restrict__ temp,
                                                    float* __restrict__ part,
-                                                   float* __restrict__ row_stats, int c, int b,
+                                                   float* __restrict__ row_stats,
+                                                   float* __restrict__ tmax, int c, int b,
                                                    float* red) {
+  static_assert(kChunkThreads == kEstChunkThreads, "thread maxima per chunk");
   const float T = temp[b];
   const float c2 = __fdiv_rn(kLog2e, T);
   const float* row = logits + static_cast<long long>(b) * ld;
@@ -102,6 +106,7 @@ __device__ __forceinline__ void entropy_chunk_body(const float* __restrict__ log
   float m = v[0];
 #pragma unroll
   for (int i = 1; i < kPerThread; ++i) m = fmaxf(m, v[i]);
+  if (tmax) tmax[(static_cast<long long>(b) * C + c) * kChunkThreads + threadIdx.x] = m;
   const float M = block_max<kChunkThreads>(m, red);
   float S = 0.f, W = 0.f;
   if (M != -INFINITY) {

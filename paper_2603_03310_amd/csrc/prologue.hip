@@ -73,13 +73,15 @@ __device__ void tile_plan(const int* __restrict__ ctx_lens, int B, int MAXB, int
 }
 
 // One scoring job: tile ch of sequence b (context length N), KV heads of
-// group hg (wave w takes head 4 hg + w).
+// group hg (wave w takes head 4 hg + w); entry: the lane's table entry
+// (score_tile_entry).
 template <int D>
-__device__ __forceinline__ void score_job(const PrologueArgs& a, int b, int ch, int hg, int N) {
+__device__ __forceinline__ void score_job(const PrologueArgs& a, int b, int ch, int hg, int N,
+                                          int entry) {
   const int g = hg * kProWaves + (threadIdx.x >> 6);
   if (g >= a.Hkv) return;
   const int nb = (N + kBlock - 1) / kBlock;
-  const int p = score_tile_block(a.tables, b, ch, a.MAXB, nb, a.P, a.flags);
+  const int p = score_tile_check(entry, ch, nb, a.P, a.flags);
   float4 buf[kScoreSlots];
   score_head_load<D>(a.ksum, p, a.Hkv, g, buf);
   score_head_compute<D>(a.q, buf, a.zbuf, a.lse_part, b, ch, g, N, nb, a.Hkv, a.G, a.MAXB,
@@ -104,16 +106,18 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(PrologueArgs a) {
       const int b = id / (tiles * nhg);
       const int r = id - b * tiles * nhg;
       const int ch = r / nhg;
+      // The context length and the tile's table entries load together.
+      const int entry = score_tile_entry(a.tables, b, ch, a.MAXB);
       const int N = a.ctx_lens[b];
       if (N < 0 || N > a.MAXB * kBlock) return;    // flagged by the selection stage
       if (ch * kMfmaChunk * kBlock >= N) return;
-      score_job<D>(a, b, ch, r - ch * nhg, N);
+      score_job<D>(a, b, ch, r - ch * nhg, N, entry);
       return;
     }
     const int e = id - nsc;
     const int b = e / a.C;
-    entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats, e - b * a.C,
-                            b, red);
+    entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats, a.tmax,
+                            e - b * a.C, b, red);
     if (e == b * a.C && threadIdx.x == 0 && a.temp_used) a.temp_used[b] = a.temp[b];
     return;
   }
@@ -133,11 +137,12 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(PrologueArgs a) {
         const int mid = (lo + hi) >> 1;
         if (s_pref[mid] <= tile) lo = mid; else hi = mid;
       }
-      score_job<D>(a, lo, tile - s_pref[lo], job - tile * nhg, s_N[lo]);
+      const int ch = tile - s_pref[lo];
+      score_job<D>(a, lo, ch, job - tile * nhg, s_N[lo], score_tile_entry(a.tables, lo, ch, a.MAXB));
     } else {
       const int e = job - n_score;
       const int b = e / a.C;
-      entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats,
+      entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats, a.tmax,
                               e - b * a.C, b, red);
       if (e == b * a.C && threadIdx.x == 0 && a.temp_used) a.temp_used[b] = a.temp[b];
     }

@@ -18,7 +18,7 @@
 //   D  the merge of split decode segments.
 
 #include "blocks_dev.h"
-#include "entropy_dev.h"
+#include "estimate_dev.h"
 
 namespace ent {
 namespace {
@@ -40,16 +40,25 @@ __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
     int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
     float* h_out, float eta, float h_target, float t_min, float t_max,
     const float* __restrict__ lse_part, const int* __restrict__ ctx_lens, float* __restrict__ L,
-    int Hq, int MAXB, int nch_max, SampleArgs sa) {
-  static_assert(kRowThreads >= kSampleThreads, "sampling workgroup size");
+    int Hq, int MAXB, int nch_max, SampleArgs sa, int est, int est_k,
+    const float* __restrict__ tmax) {
+  static_assert(kRowThreads >= kSampleThreads && kRowThreads >= kEstThreads, "workgroup size");
+  extern __shared__ unsigned est_lds[];
   __shared__ float s_pm[kRowThreads], s_ps[kRowThreads];
   __shared__ SampleShared ssh;
+  __shared__ EstShared esh;
   const int b = blockIdx.x;
   if (b >= B) {
     step_sample<VEC>(sa, b - B, ssh);
     return;
   }
-  if (threadIdx.x < 64) {
+  if (est != ENT_EST_EXACT) {
+    const float T = temp[b];
+    const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T, b, est_lds,
+                                 esh);
+    if (threadIdx.x == 0)
+      controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min, t_max);
+  } else if (threadIdx.x < 64) {
     const float H = row_entropy(part, C, b);
     if (threadIdx.x == 0)
       controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min,
@@ -71,10 +80,12 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     const int* __restrict__ ctx_lens, const int* __restrict__ tables, float* __restrict__ scores,
     float* __restrict__ theta, int* __restrict__ kept, int* __restrict__ kphys,
     int* __restrict__ n_kept, int MAXB, int P, int nch_max, float eps_h, float h_min, float log_v,
-    float kappa_min, int b_min, unsigned* flags, SampleArgs sa) {
-  static_assert(kSelThreads >= kSampleThreads, "sampling workgroup size");
-  extern __shared__ unsigned keys[];        // [MAXB] keys, then [MAXB] encoded blocks
+    float kappa_min, int b_min, unsigned* flags, SampleArgs sa, int est, int est_k,
+    const float* __restrict__ tmax) {
+  static_assert(kSelThreads >= kSampleThreads && kSelThreads >= kEstThreads, "workgroup size");
+  extern __shared__ unsigned keys[];        // [MAXB] keys, [MAXB] encoded blocks, estimator
   __shared__ SelectShared sh;
+  __shared__ EstShared esh;
   __shared__ SampleShared ssh;
   __shared__ float s_H;
   const int b = blockIdx.x;
@@ -82,12 +93,20 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     step_sample<VEC>(sa, b - B, ssh);
     return;
   }
+  SelectRegs<HPL> R;
+  select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, R);
   const int N = ctx_lens[b];
   const bool ok = N >= 0 && N <= MAXB * kBlock;
   const int nb = ok ? (N + kBlock - 1) / kBlock : 0;
-  SelectRegs<HPL> R;
-  select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, nb, R);
-  if (threadIdx.x < 64) {
+  if (est != ENT_EST_EXACT) {
+    const float T = temp[b];
+    const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T, b,
+                                 keys + 2 * MAXB, esh);
+    if (threadIdx.x == 0) {
+      s_H = H;
+      controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min, t_max);
+    }
+  } else if (threadIdx.x < 64) {
     const float H = row_entropy(part, C, b);
     if (threadIdx.x == 0) {
       s_H = H;
@@ -127,6 +146,10 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   pa.part = c->ent_part;
   pa.row_stats = stats;
   pa.temp_used = temp_used;
+  const bool est = uses_estimate(cf);
+  const int est_mode = est ? cf.estimator : ENT_EST_EXACT;
+  const size_t est_lds = est ? est_lds_bytes(c->chunks, cf.est_k) : 0;
+  pa.tmax = est ? c->tmax : nullptr;
   pa.do_score = bf16 ? 1 : 0;
   pa.q = static_cast<const uint16_t*>(q);
   pa.ksum = ksum;
@@ -160,14 +183,14 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   const bool vec = row_vec_ok(logits, ld);
   const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
   if (hpl) {
-    const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
+    const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned) + est_lds;
 #define ENT_STEPB_CASE(HH, VV)                                                                 \
   hipLaunchKernelGGL((step_b_kernel<HH, VV>), dim3(2 * B), dim3(kSelThreads), lds, s, B,       \
                      c->ent_part, c->chunks, st.temp, st.h_prev, st.tau, h_out, cf.eta,        \
                      cf.h_target, cf.t_min, cf.t_max, c->zbuf, c->lse_part, ctx_lens, tables,  \
                      scores, theta, kept, c->kept_phys, n_kept, cf.max_blocks_per_seq,         \
                      cf.num_pool_blocks, c->lse_chunks, cf.eps_h, cf.h_min, cf.log_v,          \
-                     cf.kappa_min, cf.b_min, c->dev_flags, sa)
+                     cf.kappa_min, cf.b_min, c->dev_flags, sa, est_mode, cf.est_k, c->tmax)
 #define ENT_STEPB_HPL(HH)                   \
   case HH:                                  \
     if (vec) ENT_STEPB_CASE(HH, true);      \
@@ -187,10 +210,10 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
     if (e != hipSuccess) return e;
   } else {
     auto k0 = vec ? step_b0_kernel<true> : step_b0_kernel<false>;
-    hipLaunchKernelGGL(k0, dim3(2 * B), dim3(kRowThreads), 0, s, B, c->ent_part, c->chunks,
+    hipLaunchKernelGGL(k0, dim3(2 * B), dim3(kRowThreads), est_lds, s, B, c->ent_part, c->chunks,
                        st.temp, st.h_prev, st.tau, h_out, cf.eta, cf.h_target, cf.t_min,
                        cf.t_max, c->lse_part, ctx_lens, c->lrow, cf.num_q_heads,
-                       cf.max_blocks_per_seq, c->lse_chunks, sa);
+                       cf.max_blocks_per_seq, c->lse_chunks, sa, est_mode, cf.est_k, c->tmax);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     float* sc = scores ? scores : c->iscores;

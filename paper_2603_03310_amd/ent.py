@@ -17,6 +17,8 @@ LIB_PATH = os.path.join(HERE, "libent.so")
 
 ENT_OK, ENT_E_INVAL, ENT_E_NOMEM, ENT_E_HIP, ENT_E_UNSUPPORTED = 0, -1, -2, -3, -4
 ENT_F32, ENT_BF16 = 0, 1
+ENT_EST_EXACT, ENT_EST_TOPK, ENT_EST_TAIL = 0, 1, 2
+ENT_EST_MAX_K = 512
 ENT_ROW_CHUNK = 4096
 ENT_BLOCK_SIZE = 16
 ENT_DEV_BAD_TABLE, ENT_DEV_BAD_CTXLEN, ENT_DEV_CACHE_FULL = 1, 2, 4
@@ -36,7 +38,7 @@ class ent_config(ctypes.Structure):
         ("scale", ctypes.c_float), ("eta", ctypes.c_float), ("h_target", ctypes.c_float),
         ("t_min", ctypes.c_float), ("t_max", ctypes.c_float), ("eps_h", ctypes.c_float),
         ("h_min", ctypes.c_float), ("kappa_min", ctypes.c_float), ("b_min", ctypes.c_int),
-        ("log_v", ctypes.c_float),
+        ("log_v", ctypes.c_float), ("estimator", ctypes.c_int), ("est_k", ctypes.c_int),
     ]
 
 

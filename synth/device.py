@@ -23,7 +23,8 @@ def config_fields(w: Workload, p: Params, num_pool_blocks: int,
         num_pool_blocks=max(1, num_pool_blocks), vocab=w.vocab,
         kv_dtype=1 if w.kv_dtype == "bf16" else 0,
         scale=p.scale, eta=p.eta, h_target=p.h_target, t_min=p.t_min, t_max=p.t_max,
-        eps_h=p.eps_h, h_min=p.h_min, kappa_min=p.kappa_min, b_min=p.b_min, log_v=p.log_v)
+        eps_h=p.eps_h, h_min=p.h_min, kappa_min=p.kappa_min, b_min=p.b_min, log_v=p.log_v,
+        estimator=p.estimator, est_k=p.est_k)
 
 
 def _tensor(a: np.ndarray, device):

@@ -4,7 +4,8 @@ Per stage, the oracle is fed the GPU's own upstream values (teacher forcing):
 its entropy for the block budget, its block summaries for the scores, its
 kept list for attention, its temperature for sampling.  Bands:
 
-* entropy, entropic time, temperature: |delta| <= 1e-4 (nats / absolute);
+* entropy (or its top-k / tail-corrected estimate), entropic time,
+  temperature: |delta| <= 1e-4 (nats / absolute);
 * kept list: bit-exact, except blocks whose oracle score lies within 1e-6
   of the oracle threshold; the GPU's list must also be exactly the blocks
   whose GPU score reaches the k-th largest GPU score, with k the budget the
@@ -86,8 +87,8 @@ def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev,
         N = int(ctx_lens[s])
         z = np.asarray(logits[s], dtype=np.float64)
         T = float(temp[s])
-        # Stage 1: entropy and controller.
-        h_o = OE.entropy(z, T)
+        # Stage 1: entropy (or the configured estimate of it) and controller.
+        h_o = OE.entropy_estimate(z, T, int(params.estimator), int(params.est_k))
         dh = abs(float(gpu.h[s]) - h_o)
         rep.max_h_err = max(rep.max_h_err, dh)
         if dh > H_TOL:

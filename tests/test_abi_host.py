@@ -36,7 +36,8 @@ def test_default_config_is_valid_and_checks_reject_bad_ones():
            ("head_dim", 96, ent.ENT_E_UNSUPPORTED), ("t_min", 0.0, ent.ENT_E_INVAL),
            ("log_v", 1.0, ent.ENT_E_INVAL), ("kappa_min", 1.5, ent.ENT_E_INVAL),
            ("max_batch", 0, ent.ENT_E_INVAL), ("max_blocks_per_seq", 20000, ent.ENT_E_UNSUPPORTED),
-           ("vocab", 2_000_000, ent.ENT_E_UNSUPPORTED), ("kv_dtype", 7, ent.ENT_E_INVAL)]
+           ("vocab", 2_000_000, ent.ENT_E_UNSUPPORTED), ("kv_dtype", 7, ent.ENT_E_INVAL),
+           ("estimator", 3, ent.ENT_E_INVAL)]
     for field, val, code in bad:
         c = ent.ent_default_config()
         c.num_pool_blocks = 100
@@ -47,6 +48,17 @@ def test_default_config_is_valid_and_checks_reject_bad_ones():
     c.num_pool_blocks = 100
     c.num_q_heads = 48          # G = 6
     assert ent.ent_check_config(c)[0] == ent.ENT_E_UNSUPPORTED
+    # Estimator k: checked only when an estimator is configured.
+    for est, k, code in [(ent.ENT_EST_TOPK, 0, ent.ENT_E_INVAL),
+                         (ent.ENT_EST_TAIL, ent.ENT_EST_MAX_K + 1, ent.ENT_E_INVAL),
+                         (ent.ENT_EST_TAIL, ent.ENT_EST_MAX_K, ent.ENT_OK),
+                         (ent.ENT_EST_EXACT, 0, ent.ENT_OK)]:
+        c = ent.ent_default_config()
+        c.num_pool_blocks = 100
+        c.estimator, c.est_k = est, k
+        assert ent.ent_check_config(c)[0] == code, (est, k)
+    d = ent.ent_default_config()
+    assert d.estimator == ent.ENT_EST_EXACT and d.est_k == 256
 
 
 def test_row_stats_chunks():
