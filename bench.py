@@ -18,6 +18,7 @@ events on the launch stream), and the float64 oracle timed on the host's
 cores on a bounded sample of the same workload.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+                    [--estimator exact|topk|tail] [--est-k K] [--eps-h E]
 """
 from __future__ import annotations
 
@@ -56,6 +57,11 @@ def parse():
     ap.add_argument("--copies", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--estimator", choices=["exact", "topk", "tail"], default="exact",
+                    help="entropy the controller acts on (top-k / tail-corrected estimates)")
+    ap.add_argument("--est-k", type=int, default=256)
+    ap.add_argument("--eps-h", type=float, default=None,
+                    help="estimator error bound in the block budget (default 0)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -130,6 +136,11 @@ def main():
     if w.steps != 1:
         raise SystemExit("bench.py times single decode steps; closed loops are parity cases")
     p = default_params(w)
+    est = {"exact": 0, "topk": 1, "tail": 2}[args.estimator]
+    if est:
+        p = p.replace(estimator=est, est_k=args.est_k)
+    if args.eps_h is not None:
+        p = p.replace(eps_h=args.eps_h)
     t0 = time.perf_counter()
     x = generate(w)
     print(f"[bench] generated {w.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
@@ -265,7 +276,9 @@ def main():
         "data": "synthetic (seeded; shapes and value recipes of the workload)",
         "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": w.num_kv_heads,
                    "head_dim": d, "block_size": 16, "ctx": list(w.ctx), "vocab": w.vocab,
-                   "kv_dtype": w.kv_dtype},
+                   "kv_dtype": w.kv_dtype, "entropy": args.estimator,
+                   **({"est_k": args.est_k} if est else {}),
+                   **({"eps_h": p.eps_h} if p.eps_h else {})},
         "hbm_gbps_kept_kv_plus_logits": round(gbps, 1),
         "hbm_frac_kept_kv_plus_logits": round(gbps / HBM_PEAK_GBPS, 4),
         "metric_bytes_per_step": int(metric_bytes),

@@ -9,12 +9,14 @@ namespace {
 
 // One workgroup per row: the top-k or tail-corrected estimate from the chunk
 // triples, the thread maxima and the re-read logits, then the controller.
-__global__ __launch_bounds__(kEstThreads) void estimate_finalize_kernel(
+constexpr int kEstFinalizeThreads = 512;
+
+__global__ __launch_bounds__(kEstFinalizeThreads) void estimate_finalize_kernel(
     int est, int k, int V, int C, const float* __restrict__ part, const float* __restrict__ tmax,
     const float* __restrict__ logits, long long ld, float* __restrict__ temp,
     float* __restrict__ h_prev, float* __restrict__ tau, float* __restrict__ h_out,
     float* __restrict__ temp_used, float eta, float h_target, float t_min, float t_max) {
-  extern __shared__ unsigned est_lds[];
+  extern __shared__ __attribute__((aligned(16))) unsigned est_lds[];
   __shared__ EstShared esh;
   const int b = blockIdx.x;
   const float T = temp[b];
@@ -74,7 +76,7 @@ hipError_t launch_entropy(const ent_ctx* c, int B, const float* logits, long lon
   hipError_t e = launch_prologue(c, a, s);
   if (e != hipSuccess || !controller) return e;
   if (est) {
-    hipLaunchKernelGGL(estimate_finalize_kernel, dim3(B), dim3(kEstThreads),
+    hipLaunchKernelGGL(estimate_finalize_kernel, dim3(B), dim3(kEstFinalizeThreads),
                        est_lds_bytes(c->chunks, cf.est_k), s, cf.estimator, cf.est_k, cf.vocab,
                        c->chunks, c->ent_part, c->tmax, logits, ld, st.temp, st.h_prev, st.tau,
                        h_out, temp_used, cf.eta, cf.h_target, cf.t_min, cf.t_max);

@@ -43,7 +43,7 @@ __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
     int Hq, int MAXB, int nch_max, SampleArgs sa, int est, int est_k,
     const float* __restrict__ tmax) {
   static_assert(kRowThreads >= kSampleThreads && kRowThreads >= kEstThreads, "workgroup size");
-  extern __shared__ unsigned est_lds[];
+  extern __shared__ __attribute__((aligned(16))) unsigned est_lds[];
   __shared__ float s_pm[kRowThreads], s_ps[kRowThreads];
   __shared__ SampleShared ssh;
   __shared__ EstShared esh;
@@ -83,7 +83,7 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     float kappa_min, int b_min, unsigned* flags, SampleArgs sa, int est, int est_k,
     const float* __restrict__ tmax) {
   static_assert(kSelThreads >= kSampleThreads && kSelThreads >= kEstThreads, "workgroup size");
-  extern __shared__ unsigned keys[];        // [MAXB] keys, [MAXB] encoded blocks, estimator
+  extern __shared__ __attribute__((aligned(16))) unsigned keys[];   // [MAXB] keys, [MAXB] blocks, estimator
   __shared__ SelectShared sh;
   __shared__ EstShared esh;
   __shared__ SampleShared ssh;
@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
   if (est != ENT_EST_EXACT) {
     const float T = temp[b];
     const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T, b,
-                                 keys + 2 * MAXB, esh);
+                                 keys + est_lds_offset(2 * MAXB), esh);
     if (threadIdx.x == 0) {
       s_H = H;
       controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min, t_max);
@@ -183,7 +183,8 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   const bool vec = row_vec_ok(logits, ld);
   const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
   if (hpl) {
-    const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned) + est_lds;
+    const size_t lds =
+        static_cast<size_t>(est_lds_offset(2 * cf.max_blocks_per_seq)) * sizeof(unsigned) + est_lds;
 #define ENT_STEPB_CASE(HH, VV)                                                                 \
   hipLaunchKernelGGL((step_b_kernel<HH, VV>), dim3(2 * B), dim3(kSelThreads), lds, s, B,       \
                      c->ent_part, c->chunks, st.temp, st.h_prev, st.tau, h_out, cf.eta,        \
