@@ -74,25 +74,39 @@ def block_scores(q: np.ndarray, kbar: np.ndarray, counts: np.ndarray, scale: flo
     return I_h.mean(axis=1), I_h, z
 
 
-def keep_budget(h: float, nb: int, params) -> int:
-    """Number of blocks to keep, k, from the entropy H_t (reading of the
-    entropy-driven threshold and its guards; Sections 3.2, 3.3, 5).
+def kept_fraction(h: float, params, kappa_prev: float = math.nan) -> np.float32:
+    """Kept fraction kappa from the entropy H_t (reading of the
+    entropy-driven threshold and its guards; Sections 3.2, 3.3, 5):
 
       H_g   = max(H + eps_H, H_min)                  conservative, floored entropy
       u     = clip((H_g - H_min) / (log|V| - H_min), 0, 1)
-      kappa = kappa_min + (1 - kappa_min) u          kept fraction
-      k     = min(nb, max(min(B_min, nb), ceil(kappa nb)))
+      kappa = kappa_min + (1 - kappa_min) u
+
+    and the bounded rate of change of Section 5 (guard iii), read as a bound
+    on how fast pruning may tighten: kappa >= kappa_prev - dkappa when the
+    previous step's fraction is known (NaN: no previous step); a larger
+    fraction is always allowed.
 
     Evaluated in float32 with exactly this operation order (no fused
-    multiply-add), because k is an integer decided by floating point and
-    both sides must take that decision in the same precision."""
-    if nb <= 0:
-        return 0
+    multiply-add): the block count is an integer decided by floating point,
+    and both sides must take that decision in the same precision."""
     f = np.float32
     hg = max(f(h) + f(params.eps_h), f(params.h_min))
     u = (hg - f(params.h_min)) / (f(params.log_v) - f(params.h_min))
     u = min(max(u, f(0.0)), f(1.0))
     kappa = f(params.kappa_min) + (f(1.0) - f(params.kappa_min)) * u
+    if not math.isnan(kappa_prev):
+        kappa = max(kappa, f(kappa_prev) - f(getattr(params, "dkappa", 1.0)))
+    return f(kappa)
+
+
+def keep_budget(h: float, nb: int, params, kappa_prev: float = math.nan) -> int:
+    """Number of blocks to keep, k = min(nb, max(min(B_min, nb), ceil(kappa nb)))
+    with kappa = kept_fraction(h, params, kappa_prev) (float32)."""
+    if nb <= 0:
+        return 0
+    f = np.float32
+    kappa = kept_fraction(h, params, kappa_prev)
     k = int(np.ceil(f(kappa * f(nb))))
     return min(nb, max(min(int(params.b_min), nb), k))
 

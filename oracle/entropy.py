@@ -100,6 +100,25 @@ def entropy_estimate(z: np.ndarray, temp: float, estimator: int = EXACT, k: int 
     raise ValueError(f"unknown estimator {estimator}")
 
 
+def effective_temperature(temp: float, params) -> float:
+    """Temperature of every softmax over the vocabulary in a step: the
+    controlled T_t times the calibration temperature T_cal (Section 5,
+    calibration-aware entropy, read as a post-hoc wrapper on the logits,
+    p^cal proportional to exp(z / T_cal), to which the sampling temperature
+    then applies; T_cal = 1 leaves the step unchanged)."""
+    return float(temp) * float(getattr(params, "t_cal", 1.0))
+
+
+def control_entropy(z: np.ndarray, temp: float, params) -> float:
+    """The entropy the controller and the block budget act on: the
+    configured estimate (exact, top-k or tail-corrected) of the entropy at
+    the effective temperature, plus the injected bias of the miscalibration
+    stress tests (Section 5, "injecting entropy bias"; 0 by default)."""
+    h = entropy_estimate(z, effective_temperature(temp, params),
+                         int(getattr(params, "estimator", EXACT)), int(getattr(params, "est_k", 0)))
+    return h + float(getattr(params, "h_bias", 0.0))
+
+
 def entropic_time(tau: float, h_prev: float, h: float) -> float:
     """tau + max(0, H_{t-1} - H_t)  (Section 2: entropy flow Delta H_t, its
     positive part, and entropic time as their running sum).
@@ -111,14 +130,22 @@ def entropic_time(tau: float, h_prev: float, h: float) -> float:
 
 
 def temperature_next(temp: float, h: float, h_target: float, eta: float,
-                     t_min: float, t_max: float) -> float:
+                     t_min: float, t_max: float, rho_t: float = math.inf) -> float:
     """T_{t+1} = clip(T_t exp(eta (H_t - H*)), T_min, T_max)  (Section 3.3).
 
     Reading: `eta` is a signed gain.  With the positive gain as printed the
     loop feeds back positively, because dH/dT >= 0 for a softmax; the
     stabilising law the paper describes (high entropy driven toward
-    commitment) and its linearisation in Section 7 need eta < 0 here."""
-    t = float(temp) * math.exp(float(eta) * (float(h) - float(h_target)))
+    commitment) and its linearisation in Section 7 need eta < 0 here.
+
+    Bounded rate of change (Section 5, guard iii): the multiplicative step
+    exp(eta (H - H*)) is clipped to [exp(-rho_t), exp(rho_t)] before the
+    clip to [T_min, T_max], so |ln T_{t+1} - ln T_t| <= rho_t inside the
+    bounds; rho_t = inf leaves the law unchanged."""
+    step = math.exp(float(eta) * (float(h) - float(h_target)))
+    if math.isfinite(float(rho_t)):
+        step = min(max(step, math.exp(-float(rho_t))), math.exp(float(rho_t)))
+    t = float(temp) * step
     return min(max(t, float(t_min)), float(t_max))
 
 
@@ -135,12 +162,11 @@ def control_step(logits: np.ndarray, h_prev: np.ndarray, tau: np.ndarray, temp: 
     h = np.empty(B)
     tau_out = np.empty(B)
     t_next = np.empty(B)
-    est = int(getattr(params, "estimator", EXACT))
-    est_k = int(getattr(params, "est_k", 0))
     for b in range(B):
-        h[b] = entropy_estimate(logits[b], float(temp[b]), est, est_k)
+        h[b] = control_entropy(logits[b], float(temp[b]), params)
         tau_out[b] = entropic_time(float(tau[b]), float(h_prev[b]), h[b])
         t_next[b] = temperature_next(float(temp[b]), h[b], params.h_target, params.eta,
-                                     params.t_min, params.t_max)
+                                     params.t_min, params.t_max,
+                                     float(getattr(params, "rho_t", math.inf)))
     return {"h": h, "tau": tau_out, "temp_used": np.asarray(temp, dtype=np.float64).copy(),
             "temp_next": t_next}

@@ -25,20 +25,22 @@ from . import attention, blocks, entropy, layout, sample
 
 def sequence_step(s: int, *, k_pool, v_pool, tables, ctx_lens, q, logits, h_prev, tau, temp,
                   uniforms, params, block_size: int, h_override: Optional[float] = None,
-                  ksum_pool: Optional[np.ndarray] = None, want_exact: bool = False) -> dict:
+                  ksum_pool: Optional[np.ndarray] = None, want_exact: bool = False,
+                  kappa=None) -> dict:
     """Every output of the step for sequence s.  Array arguments are the
-    batch's buffers in the library's layouts (one step's q/logits/uniforms)."""
+    batch's buffers in the library's layouts (one step's q/logits/uniforms);
+    `kappa` holds the previous step's kept fractions (None or NaN: none)."""
     N = int(ctx_lens[s])
     z = np.asarray(logits[s], dtype=np.float64)
     T = float(temp[s])
-    h = entropy.entropy_estimate(z, T, int(getattr(params, "estimator", entropy.EXACT)),
-                                 int(getattr(params, "est_k", 0)))
+    h = entropy.control_entropy(z, T, params)
     out = {
         "h": h,
         "tau": entropy.entropic_time(float(tau[s]), float(h_prev[s]), h),
         "temp_used": T,
         "temp_next": entropy.temperature_next(T, h, params.h_target, params.eta,
-                                              params.t_min, params.t_max),
+                                              params.t_min, params.t_max,
+                                              float(getattr(params, "rho_t", math.inf))),
     }
     K, V = layout.gather_sequence(k_pool, v_pool, tables[s], N, block_size)
     qs = layout.to_f64(q[s])
@@ -54,12 +56,14 @@ def sequence_step(s: int, *, k_pool, v_pool, tables, ctx_lens, q, logits, h_prev
     else:
         I = np.zeros(0)
     h_budget = h if h_override is None else float(h_override)
-    k = blocks.keep_budget(h_budget, nb, params)
+    kp = math.nan if kappa is None else float(kappa[s])
+    k = blocks.keep_budget(h_budget, nb, params, kp)
+    out["kappa"] = float(blocks.kept_fraction(h_budget, params, kp)) if nb else kp
     kept, theta = blocks.select_blocks(I, k)
     out.update(scores=I, k=k, kept=kept, theta=theta, nb=nb)
     o, lse = attention.sparse_decode(qs, K, V, kept, block_size, params.scale)
     out.update(o=o, lse=lse)
-    tok, margin = sample.sample(z, T, float(uniforms[s]))
+    tok, margin = sample.sample(z, entropy.effective_temperature(T, params), float(uniforms[s]))
     out.update(token=tok, margin=margin)
     if want_exact and nb:
         out["exact_scores"] = blocks.exact_token_scores(qs, K, block_size, params.scale)

@@ -34,6 +34,10 @@ class Params:
     t0: float = 1.0       # initial temperature
     estimator: int = 0    # entropy the controller acts on: 0 exact, 1 top-k, 2 tail-corrected
     est_k: int = 256      # k of the top-k and tail-corrected estimators
+    t_cal: float = 1.0    # calibration temperature wrapping the logits (1 = none)
+    rho_t: float = math.inf   # bound on |ln T_{t+1} - ln T_t| before clipping (inf = none)
+    dkappa: float = 1.0   # largest decrease of the kept fraction per step (1 = none)
+    h_bias: float = 0.0   # offset added to the entropy the controller acts on (stress tests)
 
     def __post_init__(self):
         # Every float is held at float32 precision: the library receives

@@ -50,6 +50,7 @@ class StepResult:
     out: np.ndarray
     lse: np.ndarray
     tokens: np.ndarray
+    kappa: Optional[np.ndarray] = None
 
 
 @dataclass
@@ -67,20 +68,22 @@ class Report:
         return not self.failures
 
 
-def collect(dev) -> StepResult:
+def collect(dev, with_kappa: bool = False) -> StepResult:
     c = lambda t: t.detach().cpu().numpy().copy()  # noqa: E731
     return StepResult(h=c(dev.h), tau=c(dev.tau), temp_next=c(dev.temp), temp_used=c(dev.temp_used),
                       ksum=c(dev.ksum), kept=c(dev.kept), n_kept=c(dev.n_kept), scores=c(dev.scores),
-                      theta=c(dev.theta), out=c(dev.out), lse=c(dev.lse), tokens=c(dev.tokens))
+                      theta=c(dev.theta), out=c(dev.out), lse=c(dev.lse), tokens=c(dev.tokens),
+                      kappa=c(dev.kappa) if with_kappa else None)
 
 
 def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev, tau, temp,
                params, gpu: StepResult, block_size: int = 16, seqs: Optional[Iterable[int]] = None,
-               check_ksum: bool = True, report: Optional[Report] = None) -> Report:
+               check_ksum: bool = True, report: Optional[Report] = None, kappa=None) -> Report:
     """Compare the GPU step `gpu` with the oracle on sequences `seqs` (default all).
 
     The input arrays are the host copies of what the GPU step consumed
-    (state before the step)."""
+    (state before the step; `kappa`: the kept-fraction state, None when the
+    step ran without it)."""
     rep = report or Report()
     B = len(ctx_lens)
     for s in (range(B) if seqs is None else seqs):
@@ -88,7 +91,7 @@ def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev,
         z = np.asarray(logits[s], dtype=np.float64)
         T = float(temp[s])
         # Stage 1: entropy (or the configured estimate of it) and controller.
-        h_o = OE.entropy_estimate(z, T, int(params.estimator), int(params.est_k))
+        h_o = OE.control_entropy(z, T, params)
         dh = abs(float(gpu.h[s]) - h_o)
         rep.max_h_err = max(rep.max_h_err, dh)
         if dh > H_TOL:
@@ -96,7 +99,8 @@ def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev,
         tau_o = OE.entropic_time(float(tau[s]), float(h_prev[s]), h_o)
         if abs(float(gpu.tau[s]) - tau_o) > H_TOL:
             rep.fail(f"seq {s}: tau {gpu.tau[s]} vs oracle {tau_o}")
-        tn_o = OE.temperature_next(T, h_o, params.h_target, params.eta, params.t_min, params.t_max)
+        tn_o = OE.temperature_next(T, h_o, params.h_target, params.eta, params.t_min, params.t_max,
+                                   params.rho_t)
         if abs(float(gpu.temp_next[s]) - tn_o) > H_TOL:
             rep.fail(f"seq {s}: next temperature {gpu.temp_next[s]} vs oracle {tn_o}")
         if float(gpu.temp_used[s]) != np.float32(T):
@@ -114,7 +118,12 @@ def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev,
             if np.any(err > 1e-5 + 1e-5 * np.abs(kbar_o)):
                 rep.fail(f"seq {s}: block summaries differ by {err.max():.3g}")
         qs = OL.to_f64(q[s])
-        k_o = OB.keep_budget(float(gpu.h[s]), nb, params)
+        kp = math.nan if kappa is None else float(kappa[s])
+        k_o = OB.keep_budget(float(gpu.h[s]), nb, params, kp)
+        if gpu.kappa is not None and nb:
+            ka_o = OB.kept_fraction(float(gpu.h[s]), params, kp)
+            if np.float32(gpu.kappa[s]) != ka_o:
+                rep.fail(f"seq {s}: kept-fraction state {gpu.kappa[s]} vs oracle {ka_o}")
         nk = int(gpu.n_kept[s])
         kept_g = gpu.kept[s][:nk].astype(np.int64)
         if nb == 0:
@@ -162,7 +171,7 @@ def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev,
             rep.fail(f"seq {s}: attention log-sum-exp differs")
 
         # Stage 4: sampling at the GPU's temperature.
-        Tu = float(gpu.temp_used[s])
+        Tu = OE.effective_temperature(float(gpu.temp_used[s]), params)
         u = float(uniforms[s])
         x_o, margin = OS.sample(z, Tu, u)
         x_g = int(gpu.tokens[s])
