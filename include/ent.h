@@ -99,21 +99,36 @@ typedef struct {
   int estimator;           /* ENT_EST_EXACT, ENT_EST_TOPK or ENT_EST_TAIL; with an estimate,
                               eps_h is its error bound and enters the block budget */
   int est_k;               /* k of the estimators, 1 <= k <= ENT_EST_MAX_K (ignored when exact) */
+  /* Calibration and safe control (Section 5).  Neutral values leave the
+   * step unchanged: t_cal = 1, rho_t = INFINITY, dkappa = 1, h_bias = 0. */
+  float t_cal;             /* calibration temperature, > 0: every softmax over the vocabulary
+                              (entropy, estimates, sampling) uses z / (t_cal * T_t) */
+  float rho_t;             /* bound on |ln T_{t+1} - ln T_t|: the temperature step
+                              exp(eta (H - H*)) is clipped to [e^-rho_t, e^rho_t]; >= 0 or INFINITY */
+  float dkappa;            /* largest decrease of a sequence's kept fraction per step, in [0, 1];
+                              needs the kept-fraction state (ent_state.kappa) */
+  float h_bias;            /* offset added to the entropy the controller and budget act on
+                              (miscalibration stress tests); finite */
 } ent_config;
 
 /* Per-sequence controller state, device arrays of B floats each, read and
  * updated in place by ent_entropy_temperature: the previous step's entropy
- * H_{t-1} (NaN = no previous step), entropic time tau, and temperature T_t. */
+ * H_{t-1} (NaN = no previous step), entropic time tau, and temperature T_t.
+ * kappa (nullable): the previous step's kept fraction of blocks (NaN = none),
+ * read and updated by the block selection; the rate guard dkappa applies
+ * only when it is given. */
 typedef struct {
   float* h_prev;
   float* tau;
   float* temp;
+  float* kappa;
 } ent_state;
 
 /* Defaults: Llama-3-8B decode shapes (32/8 heads, d = 128, bf16, |V| = 128256),
  * eta = -0.05, H* = 2.5, T in [0.05, 5], eps_H = 0, H_min = H*, kappa_min = 0.05,
- * B_min = 4, exact entropy (est_k = 256 for the estimators).  max_batch,
- * max_blocks_per_seq and num_pool_blocks must be set. */
+ * B_min = 4, exact entropy (est_k = 256 for the estimators), no calibration or
+ * rate guards, no bias.  max_batch, max_blocks_per_seq and num_pool_blocks
+ * must be set. */
 void ent_default_config(ent_config* out);
 
 /* Host-only check of a configuration (no HIP call).  Returns ENT_OK, or
@@ -170,13 +185,18 @@ int ent_block_summary(ent_ctx* c, int B, const void* k_cache, const int* block_t
 
 /* Block scores and kept-block selection (Section 3.2: block entropic
  * contribution I_b and the kept set B_t = {b : I_b >= theta_t}; Section 3.3
- * and Section 5: the safety floor and the minimum block budget).
+ * and Section 5: the safety floor, the minimum block budget and the bounded
+ * rate of change of the threshold).
  *   z_bh  = scale <q_h, ksum[p_b, h / G]>,  weights a_bh = e^{z_bh} / sum_b' n_b' e^{z_b'h}
  *   I_b   = (1/H_q) sum_h n_b a_bh (-ln a_bh)
  *   H_g   = max(h[b] + eps_H, H_min);  u = clip((H_g - H_min)/(log_v - H_min), 0, 1)
- *   k     = min(nb, max(min(B_min, nb), ceil((kappa_min + (1 - kappa_min) u) nb)))
+ *   kappa = kappa_min + (1 - kappa_min) u, then max(kappa, kappa[b] - dkappa) when the
+ *           state kappa is given and kappa[b] is not NaN
+ *   k     = min(nb, max(min(B_min, nb), ceil(kappa nb)))
  *           (float32, in exactly this order, no fused multiply-add)
  *   theta = k-th largest I_b;  kept = {b : I_b >= theta} in ascending order
+ * kappa (nullable, in/out): the kept-fraction state; receives this step's
+ * fraction for every sequence with blocks.
  * q: [B, H_q, d] (kv_dtype); ksum from ent_block_summary; h: float [B] (the
  * entropy from ent_entropy_temperature).  Outputs: kept int [B, MAXB] (first
  * n_kept[b] entries valid, logical block ids), n_kept int [B]; scores
@@ -184,7 +204,7 @@ int ent_block_summary(ent_ctx* c, int B, const void* k_cache, const int* block_t
  * (+inf when nothing is kept). */
 int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum,
                      const int* block_tables, const int* ctx_lens, const float* h, int* kept,
-                     int* n_kept, float* scores, float* theta, void* stream);
+                     int* n_kept, float* scores, float* theta, float* kappa, void* stream);
 
 /* Decode attention over the kept blocks only (Section 3.2: attention is
  * restricted to B_t).  For query head h (KV head g = h / G), over the valid

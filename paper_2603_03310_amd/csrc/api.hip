@@ -47,6 +47,10 @@ std::string check_config(const ent_config* c, int* code) {
     return "estimator must be ENT_EST_EXACT, ENT_EST_TOPK or ENT_EST_TAIL";
   if (c->estimator != ENT_EST_EXACT && (c->est_k < 1 || c->est_k > ENT_EST_MAX_K))
     return "est_k must be in [1, ENT_EST_MAX_K]";
+  if (!(c->t_cal > 0.f) || !isfinite(c->t_cal)) return "t_cal must be finite and > 0";
+  if (!(c->rho_t >= 0.f)) return "rho_t must be >= 0 (INFINITY: no bound)";
+  if (!(c->dkappa >= 0.f && c->dkappa <= 1.f)) return "dkappa must be in [0, 1]";
+  if (!isfinite(c->h_bias)) return "h_bias must be finite";
   *code = ENT_E_UNSUPPORTED;
   if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
   if (!is_pow2_group(c->num_q_heads / c->num_kv_heads))
@@ -110,6 +114,10 @@ void ent_default_config(ent_config* out) {
   out->log_v = static_cast<float>(log(128256.0));
   out->estimator = ENT_EST_EXACT;
   out->est_k = 256;
+  out->t_cal = 1.0f;
+  out->rho_t = INFINITY;
+  out->dkappa = 1.0f;
+  out->h_bias = 0.0f;
 }
 
 int ent_check_config(const ent_config* cfg, char* msg, int msg_len) {
@@ -262,7 +270,7 @@ int ent_block_summary(ent_ctx* c, int B, const void* k_cache, const int* block_t
 
 int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum, const int* block_tables,
                      const int* ctx_lens, const float* h, int* kept, int* n_kept, float* scores,
-                     float* theta, void* stream) {
+                     float* theta, float* kappa, void* stream) {
   if (!c) return ENT_E_INVAL;
   if (int r = check_batch(c, B)) return r;
   if (B == 0) return ENT_OK;
@@ -271,7 +279,7 @@ int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum, const 
   if (!aligned(q, 16) || !aligned(ksum, 16))
     return fail(c, ENT_E_INVAL, "ent_block_select: q or ksum misaligned");
   const hipError_t e = ent::launch_block_select(c, B, q, ksum, block_tables, ctx_lens, h, kept,
-                                                n_kept, scores, theta,
+                                                n_kept, scores, theta, kappa,
                                                 static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(c, e, "ent_block_select launch");
   c->err.clear();

@@ -128,13 +128,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const float* __restrict__ scores, const int* __restrict__ ctx_lens,
     const int* __restrict__ tables, const float* __restrict__ hvec, float* __restrict__ theta_out,
     int* __restrict__ kept, int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P,
-    float eps_h, float h_min, float log_v, float kappa_min, int b_min, unsigned* flags) {
+    Budget bu, unsigned* flags) {
   extern __shared__ unsigned keys[];        // [MAXB] keys, then [MAXB] encoded blocks
   __shared__ SelectShared sh;
   const int b = blockIdx.x;
-  select_row_body(scores, ctx_lens, tables, hvec[b], theta_out, kept, kphys, n_kept, MAXB, P,
-                  eps_h, h_min, log_v, kappa_min, b_min, flags, b, keys,
-                  reinterpret_cast<int*>(keys + MAXB), sh);
+  select_row_body(scores, ctx_lens, tables, hvec[b], theta_out, kept, kphys, n_kept, MAXB, P, bu,
+                  flags, b, keys, reinterpret_cast<int*>(keys + MAXB), sh);
 }
 
 // All three selection steps per sequence (short block tables).
@@ -144,14 +143,13 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(
     const int* __restrict__ ctx_lens, const int* __restrict__ tables,
     const float* __restrict__ hvec, float* __restrict__ scores, float* __restrict__ theta_out,
     int* __restrict__ kept, int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P,
-    int nch_max, float eps_h, float h_min, float log_v, float kappa_min, int b_min,
-    unsigned* flags) {
+    int nch_max, Budget bu, unsigned* flags) {
   extern __shared__ unsigned keys[];        // [MAXB] keys, then [MAXB] encoded blocks
   __shared__ SelectShared sh;
   const int b = blockIdx.x;
   select_fused_body<HPL>(zbuf, lse_part, ctx_lens, tables, hvec[b], scores, theta_out, kept,
-                         kphys, n_kept, MAXB, P, nch_max, eps_h, h_min, log_v, kappa_min, b_min,
-                         flags, b, keys, reinterpret_cast<int*>(keys + MAXB), sh);
+                         kphys, n_kept, MAXB, P, nch_max, bu, flags, b, keys,
+                         reinterpret_cast<int*>(keys + MAXB), sh);
 }
 
 template <int D>
@@ -207,9 +205,22 @@ hipError_t launch_score_valu(const ent_ctx* c, int B, const void* q, const float
                                 : launch_score_valu_d<64>(c, B, qq, ksum, tables, ctx_lens, s);
 }
 
+Budget make_budget(const ent_config& cf, float* kappa) {
+  Budget bu;
+  bu.eps_h = cf.eps_h;
+  bu.h_min = cf.h_min;
+  bu.log_v = cf.log_v;
+  bu.kappa_min = cf.kappa_min;
+  bu.dkappa = cf.dkappa;
+  bu.b_min = cf.b_min;
+  bu.kappa = kappa;
+  return bu;
+}
+
 hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const float* ksum,
                                const int* tables, const int* ctx_lens, const float* h, int* kept,
-                               int* n_kept, float* scores, float* theta, hipStream_t s) {
+                               int* n_kept, float* scores, float* theta, float* kappa,
+                               hipStream_t s) {
   const ent_config& cf = c->cfg;
   hipError_t e;
   if (cf.kv_dtype == ENT_BF16) {
@@ -234,13 +245,14 @@ hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const flo
     e = launch_score_valu(c, B, q, ksum, tables, ctx_lens, s);
   }
   if (e != hipSuccess) return e;
-  return launch_selection(c, B, tables, ctx_lens, h, scores, theta, kept, n_kept, s);
+  return launch_selection(c, B, tables, ctx_lens, h, scores, theta, kept, n_kept, kappa, s);
 }
 
 hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const int* ctx_lens,
                             const float* h, float* scores, float* theta, int* kept, int* n_kept,
-                            hipStream_t s) {
+                            float* kappa, hipStream_t s) {
   const ent_config& cf = c->cfg;
+  const Budget bu = make_budget(cf, kappa);
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
   const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
   if (hpl) {
@@ -249,8 +261,8 @@ hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const in
   case HH:                                                                                     \
     hipLaunchKernelGGL((select_fused_kernel<HH>), dim3(B), dim3(kSelThreads), lds, s, c->zbuf, \
                        c->lse_part, ctx_lens, tables, h, scores, theta, kept, c->kept_phys,    \
-                       n_kept, cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks,       \
-                       cf.eps_h, cf.h_min, cf.log_v, cf.kappa_min, cf.b_min, c->dev_flags);    \
+                       n_kept, cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, bu,   \
+                       c->dev_flags);                                                          \
     break;
     switch (hpl) {
       ENT_SEL_CASE(1)
@@ -270,7 +282,7 @@ hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const in
   float* sc = scores ? scores : c->iscores;
   e = launch_block_scores(c, B, ctx_lens, sc, s);
   if (e != hipSuccess) return e;
-  return launch_select_rows(c, B, tables, ctx_lens, h, sc, theta, kept, n_kept, s);
+  return launch_select_rows(c, B, tables, ctx_lens, h, sc, theta, kept, n_kept, kappa, s);
 }
 
 hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,
@@ -284,13 +296,12 @@ hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, flo
 
 hipError_t launch_select_rows(const ent_ctx* c, int B, const int* tables, const int* ctx_lens,
                               const float* h, const float* scores, float* theta, int* kept,
-                              int* n_kept, hipStream_t s) {
+                              int* n_kept, float* kappa, hipStream_t s) {
   const ent_config& cf = c->cfg;
   const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
   hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelThreads), lds, s, scores, ctx_lens, tables,
                      h, theta, kept, c->kept_phys, n_kept, cf.max_blocks_per_seq,
-                     cf.num_pool_blocks, cf.eps_h, cf.h_min, cf.log_v, cf.kappa_min, cf.b_min,
-                     c->dev_flags);
+                     cf.num_pool_blocks, make_budget(cf, kappa), c->dev_flags);
   return hipGetLastError();
 }
 

@@ -291,16 +291,40 @@ __device__ __forceinline__ float key_float(unsigned k) {
 }
 
 // Budget k in float32, operation by operation (no contraction), so that the
-// integer matches a float32 evaluation of the same formula elsewhere.
-__device__ __forceinline__ int keep_budget(float h, int nb, float eps_h, float h_min,
-                                           float log_v, float kappa_min, int b_min) {
+// integer matches a float32 evaluation of the same formula elsewhere: the
+// kept fraction from the guarded entropy, bounded below by the previous
+// step's fraction minus dkappa (kprev NaN: no previous step), then
+// k = min(nb, max(min(B_min, nb), ceil(kappa nb))).  kappa_used (nullable)
+// receives the fraction.
+__device__ __forceinline__ int keep_budget(float h, int nb, const Budget& bu, float kprev,
+                                           float* kappa_used = nullptr) {
+  // Plain operators under this pragma: the _rn intrinsics are header
+  // functions whose bodies the pragma does not reach, and after inlining the
+  // compiler would fuse kappa_min + (1 - kappa_min) u into one multiply-add.
+#pragma clang fp contract(off)
   if (nb <= 0) return 0;
-  const float hg = fmaxf(__fadd_rn(h, eps_h), h_min);
-  float u = __fdiv_rn(__fsub_rn(hg, h_min), __fsub_rn(log_v, h_min));
+  const float hg = fmaxf(h + bu.eps_h, bu.h_min);
+  float u = __fdiv_rn(hg - bu.h_min, bu.log_v - bu.h_min);
   u = fminf(fmaxf(u, 0.f), 1.f);
-  const float kappa = __fadd_rn(kappa_min, __fmul_rn(__fsub_rn(1.f, kappa_min), u));
-  const int k = static_cast<int>(ceilf(__fmul_rn(kappa, static_cast<float>(nb))));
-  return min(nb, max(min(b_min, nb), k));
+  const float span = 1.f - bu.kappa_min;
+  const float grow = span * u;
+  float kappa = bu.kappa_min + grow;
+  if (!isnan(kprev)) kappa = fmaxf(kappa, kprev - bu.dkappa);
+  if (kappa_used) *kappa_used = kappa;
+  const float kn = kappa * static_cast<float>(nb);
+  const int k = static_cast<int>(ceilf(kn));
+  return min(nb, max(min(bu.b_min, nb), k));
+}
+
+// The previous step's kept fraction of sequence b (NaN when there is none
+// or no state array).
+__device__ __forceinline__ float budget_prev(const Budget& bu, int b) {
+  return bu.kappa ? bu.kappa[b] : NAN;
+}
+
+// Records the kept fraction of a sequence with blocks (first thread).
+__device__ __forceinline__ void budget_record(const Budget& bu, int b, float kappa) {
+  if (bu.kappa && threadIdx.x == 0) bu.kappa[b] = kappa;
 }
 
 // Kept set of one sequence.  Three steps:
@@ -540,10 +564,9 @@ __device__ __forceinline__ void select_none(float* __restrict__ theta_out, int* 
 // (outputs written) when the context is invalid or empty.  Uniform across
 // the workgroup.
 __device__ __forceinline__ bool select_prepare(int N, float hval, float* __restrict__ theta_out,
-                                               int* __restrict__ n_kept, int MAXB, float eps_h,
-                                               float h_min, float log_v, float kappa_min,
-                                               int b_min, unsigned* flags, int b, int& nb,
-                                               int& k) {
+                                               int* __restrict__ n_kept, int MAXB,
+                                               const Budget& bu, float kprev, unsigned* flags,
+                                               int b, int& nb, int& k) {
   const int t = threadIdx.x;
   if (N < 0 || N > MAXB * kBlock) {
     if (t == 0) {
@@ -554,7 +577,7 @@ __device__ __forceinline__ bool select_prepare(int N, float hval, float* __restr
     return false;
   }
   nb = (N + kBlock - 1) / kBlock;
-  k = keep_budget(hval, nb, eps_h, h_min, log_v, kappa_min, b_min);
+  k = keep_budget(hval, nb, bu, kprev);
   if (nb == 0) {
     select_none(theta_out, n_kept, b);
     return false;
@@ -567,13 +590,18 @@ __device__ __forceinline__ void select_row_body(
     const float* __restrict__ scores, const int* __restrict__ ctx_lens,
     const int* __restrict__ tables, float hval, float* __restrict__ theta_out,
     int* __restrict__ kept, int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P,
-    float eps_h, float h_min, float log_v, float kappa_min, int b_min, unsigned* flags, int b,
-    unsigned* keys, int* tbl, SelectShared& sh) {
+    const Budget& bu, unsigned* flags, int b, unsigned* keys, int* tbl, SelectShared& sh) {
   const int N = ctx_lens[b];
+  const float kprev = budget_prev(bu, b);
   int nb, k;
-  if (!select_prepare(N, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min,
-                      flags, b, nb, k))
+  if (!select_prepare(N, hval, theta_out, n_kept, MAXB, bu, kprev, flags, b, nb, k))
     return;
+  {
+    float ku;
+    keep_budget(hval, nb, bu, kprev, &ku);
+    __syncthreads();              // every thread has read the previous fraction
+    budget_record(bu, b, ku);
+  }
   if (k <= 0) {
     select_none(theta_out, n_kept, b);
     return;
@@ -654,8 +682,8 @@ template <int HPL>
 __device__ __forceinline__ void select_finish(
     const SelectRegs<HPL>& R, int N, int nb, float hval, float* __restrict__ scores_out,
     float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ kphys,
-    int* __restrict__ n_kept, int MAXB, int P, float eps_h, float h_min, float log_v,
-    float kappa_min, int b_min, int b, unsigned* keys, int* tbl, SelectShared& sh) {
+    int* __restrict__ n_kept, int MAXB, int P, const Budget& bu, float kprev, int b,
+    unsigned* keys, int* tbl, SelectShared& sh) {
   constexpr int Hq = 4 * HPL;
   constexpr int per_head = kRowThreads / Hq;
   const int t = threadIdx.x;
@@ -715,7 +743,9 @@ __device__ __forceinline__ void select_finish(
     }
   }
   __syncthreads();
-  const int k = keep_budget(hval, nb, eps_h, h_min, log_v, kappa_min, b_min);
+  float ku;
+  const int k = keep_budget(hval, nb, bu, kprev, &ku);
+  budget_record(bu, b, ku);       // every thread read kprev before the barriers above
   if (k <= 0) {
     select_none(theta_out, n_kept, b);
     return;
@@ -729,18 +759,17 @@ __device__ __forceinline__ void select_fused_body(
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, const int* __restrict__ tables, float hval,
     float* __restrict__ scores_out, float* __restrict__ theta_out, int* __restrict__ kept,
-    int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P, int nch_max, float eps_h,
-    float h_min, float log_v, float kappa_min, int b_min, unsigned* flags, int b, unsigned* keys,
-    int* tbl, SelectShared& sh) {
+    int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P, int nch_max,
+    const Budget& bu, unsigned* flags, int b, unsigned* keys, int* tbl, SelectShared& sh) {
   SelectRegs<HPL> R;
   select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, R);
   const int N = ctx_lens[b];
+  const float kprev = budget_prev(bu, b);
   int nb, k;
-  if (!select_prepare(N, hval, theta_out, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min,
-                      flags, b, nb, k))
+  if (!select_prepare(N, hval, theta_out, n_kept, MAXB, bu, kprev, flags, b, nb, k))
     return;
-  select_finish<HPL>(R, N, nb, hval, scores_out, theta_out, kept, kphys, n_kept, MAXB, P, eps_h,
-                     h_min, log_v, kappa_min, b_min, b, keys, tbl, sh);
+  select_finish<HPL>(R, N, nb, hval, scores_out, theta_out, kept, kphys, n_kept, MAXB, P, bu,
+                     kprev, b, keys, tbl, sh);
 }
 
 }  // namespace

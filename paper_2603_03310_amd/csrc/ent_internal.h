@@ -19,6 +19,23 @@ constexpr int kEstChunkThreads = 256;       // threads of an entropy chunk job (
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
+// Parameters of the controller (Section 3.3 and Section 5): the signed gain,
+// the target entropy, the temperature bounds, the bound on the temperature's
+// log step per update, and the entropy offset of the stress tests.
+struct Control {
+  float eta, h_target, t_min, t_max, rho_t, h_bias;
+};
+Control make_control(const ent_config& cf);
+
+// Parameters of the block budget and the kept-fraction state (Sections
+// 3.2, 3.3, 5): the guarded entropy, the floor, the smallest fraction and
+// count, and the bound on how fast the kept fraction may fall.
+struct Budget {
+  float eps_h, h_min, log_v, kappa_min, dkappa;
+  int b_min;
+  float* kappa;   // nullable [B]: previous kept fraction (NaN = none), updated in place
+};
+
 }  // namespace ent
 
 struct ent_ctx {
@@ -70,7 +87,8 @@ hipError_t launch_block_summary(const ent_ctx* c, int B, const void* k_cache,
 hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const float* ksum,
                                const int* tables, const int* ctx_lens, const float* h,
                                int* kept, int* n_kept, float* scores, float* theta,
-                               hipStream_t s);
+                               float* kappa, hipStream_t s);
+Budget make_budget(const ent_config& cf, float* kappa);
 // The pass over logits and block summaries that opens a step:
 // entropy chunk triples / row statistics (do_entropy) and block scoring of
 // bf16 queries (do_score), in one grid.
@@ -85,6 +103,7 @@ struct PrologueArgs {
   float* row_stats;     // chunk (max, sum) (nullable)
   float* temp_used;     // nullable: receives temp[b] (written by chunk 0's job)
   float* tmax;          // nullable: per-thread maxima of the chunk, [B, C, 256] (estimators)
+  float t_cal;          // calibration temperature: the chunk pass uses temp[b] * t_cal
   int do_score;
   const uint16_t* q;
   const float* ksum;
@@ -102,13 +121,13 @@ int prologue_grid_size(const ent_ctx* c);
 // select), given each sequence's entropy h.
 hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const int* ctx_lens,
                             const float* h, float* scores, float* theta, int* kept, int* n_kept,
-                            hipStream_t s);
+                            float* kappa, hipStream_t s);
 // Selection phases B (block scores from c->lrow) and C (radix select).
 hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,
                                hipStream_t s);
 hipError_t launch_select_rows(const ent_ctx* c, int B, const int* tables, const int* ctx_lens,
                               const float* h, const float* scores, float* theta, int* kept,
-                              int* n_kept, hipStream_t s);
+                              int* n_kept, float* kappa, hipStream_t s);
 hipError_t launch_score_valu(const ent_ctx* c, int B, const void* q, const float* ksum,
                              const int* tables, const int* ctx_lens, hipStream_t s);
 
@@ -122,6 +141,7 @@ struct SampleArgs {
   const float* temp_used;
   const float* uniforms;
   int* tokens;
+  float t_cal;          // calibration temperature: sampling at temp_used[b] * t_cal
 };
 
 // kept_phys (nullable): the selection's encoded physical blocks of the same

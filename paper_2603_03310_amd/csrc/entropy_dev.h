@@ -93,12 +93,12 @@ __device__ __forceinline__ void load_chunk(const float* __restrict__ row, int V,
 template <bool VEC>
 __device__ __forceinline__ void entropy_chunk_body(const float* __restrict__ logits, long long ld,
                                                    int V, int C, const float* __restrict__ temp,
-                                                   float* __restrict__ part,
+                                                   float t_cal, float* __restrict__ part,
                                                    float* __restrict__ row_stats,
                                                    float* __restrict__ tmax, int c, int b,
                                                    float* red) {
   static_assert(kChunkThreads == kEstChunkThreads, "thread maxima per chunk");
-  const float T = temp[b];
+  const float T = temp[b] * t_cal;          // effective temperature (calibration wrapper)
   const float c2 = __fdiv_rn(kLog2e, T);
   const float* row = logits + static_cast<long long>(b) * ld;
   float v[kPerThread];
@@ -165,23 +165,30 @@ __device__ __forceinline__ float row_entropy(const float* __restrict__ part, int
   }
 }
 
-// Controller update of sequence b given its entropy H at temperature T
-// (temp_used nullable: the fused step records T_t earlier).
-__device__ __forceinline__ void controller_update(int b, float H, float T, float* h_prev,
-                                                  float* tau, float* temp, float* h_out,
-                                                  float* temp_used, float eta, float h_target,
-                                                  float t_min, float t_max) {
+// Controller update of sequence b given its entropy H (or estimate) at its
+// controlled temperature T (temp_used nullable: the fused step records T_t
+// earlier).  The controller acts on H + h_bias (0 outside stress tests); the
+// temperature's multiplicative step exp(eta (H - H*)) is clipped to
+// [e^-rho_t, e^rho_t] (no-op for rho_t = inf) before the clip to
+// [T_min, T_max].  Returns the entropy acted on (the budget's input).
+__device__ __forceinline__ float controller_update(int b, float H, float T, float* h_prev,
+                                                   float* tau, float* temp, float* h_out,
+                                                   float* temp_used, const Control& ct) {
 #pragma clang fp contract(off)
+  H = H + ct.h_bias;
   h_out[b] = H;
   if (temp_used) temp_used[b] = T;
   const float hp = h_prev[b];
   float ta = tau[b];
   if (!isnan(hp)) ta += fmaxf(0.f, hp - H);
-  float tn = T * expf(eta * (H - h_target));
-  tn = fminf(fmaxf(tn, t_min), t_max);
+  float step = expf(ct.eta * (H - ct.h_target));
+  step = fminf(fmaxf(step, expf(-ct.rho_t)), expf(ct.rho_t));
+  float tn = T * step;
+  tn = fminf(fmaxf(tn, ct.t_min), ct.t_max);
   tau[b] = ta;
   h_prev[b] = H;
   temp[b] = tn;
+  return H;
 }
 
 // Exclusive prefix sum (float64) over the first kSampleThreads threads.

@@ -116,8 +116,8 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(PrologueArgs a) {
     }
     const int e = id - nsc;
     const int b = e / a.C;
-    entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats, a.tmax,
-                            e - b * a.C, b, red);
+    entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.t_cal, a.part, a.row_stats,
+                            a.tmax, e - b * a.C, b, red);
     if (e == b * a.C && threadIdx.x == 0 && a.temp_used) a.temp_used[b] = a.temp[b];
     return;
   }
@@ -142,8 +142,8 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(PrologueArgs a) {
     } else {
       const int e = job - n_score;
       const int b = e / a.C;
-      entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.part, a.row_stats, a.tmax,
-                              e - b * a.C, b, red);
+      entropy_chunk_body<VEC>(a.logits, a.ld, a.V, a.C, a.temp, a.t_cal, a.part, a.row_stats,
+                              a.tmax, e - b * a.C, b, red);
       if (e == b * a.C && threadIdx.x == 0 && a.temp_used) a.temp_used[b] = a.temp[b];
     }
   }

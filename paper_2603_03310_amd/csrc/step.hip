@@ -27,7 +27,7 @@ namespace {
 // per-sequence stage (blockIdx.x >= B); every thread must call it.
 template <bool VEC>
 __device__ __forceinline__ void step_sample(const SampleArgs& sa, int b, SampleShared& sh) {
-  const int tok = sample_body<VEC>(sa.logits, sa.ld, sa.V, sa.C, sa.stats, sa.temp_used[b],
+  const int tok = sample_body<VEC>(sa.logits, sa.ld, sa.V, sa.C, sa.stats, sa.temp_used[b] * sa.t_cal,
                                    sa.uniforms[b], b, sh);
   if (threadIdx.x == 0) sa.tokens[b] = tok;
 }
@@ -38,10 +38,9 @@ __device__ __forceinline__ void step_sample(const SampleArgs& sa, int b, SampleS
 template <bool VEC>
 __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
     int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
-    float* h_out, float eta, float h_target, float t_min, float t_max,
-    const float* __restrict__ lse_part, const int* __restrict__ ctx_lens, float* __restrict__ L,
-    int Hq, int MAXB, int nch_max, SampleArgs sa, int est, int est_k,
-    const float* __restrict__ tmax) {
+    float* h_out, Control ct, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, float* __restrict__ L, int Hq, int MAXB, int nch_max,
+    SampleArgs sa, int est, int est_k, const float* __restrict__ tmax) {
   static_assert(kRowThreads >= kSampleThreads && kRowThreads >= kEstThreads, "workgroup size");
   extern __shared__ __attribute__((aligned(16))) unsigned est_lds[];
   __shared__ float s_pm[kRowThreads], s_ps[kRowThreads];
@@ -54,15 +53,12 @@ __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
   }
   if (est != ENT_EST_EXACT) {
     const float T = temp[b];
-    const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T, b, est_lds,
-                                 esh);
-    if (threadIdx.x == 0)
-      controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min, t_max);
+    const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T * sa.t_cal, b,
+                                 est_lds, esh);
+    if (threadIdx.x == 0) controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, ct);
   } else if (threadIdx.x < 64) {
     const float H = row_entropy(part, C, b);
-    if (threadIdx.x == 0)
-      controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min,
-                        t_max);
+    if (threadIdx.x == 0) controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, ct);
   }
   lse_merge_body(lse_part, ctx_lens, L + static_cast<long long>(b) * Hq, Hq, MAXB, nch_max, b,
                  s_pm, s_ps);
@@ -75,13 +71,11 @@ __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
 template <int HPL, bool VEC>
 __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
-    float* h_out, float eta, float h_target, float t_min, float t_max,
-    const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    float* h_out, Control ct, const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, const int* __restrict__ tables, float* __restrict__ scores,
     float* __restrict__ theta, int* __restrict__ kept, int* __restrict__ kphys,
-    int* __restrict__ n_kept, int MAXB, int P, int nch_max, float eps_h, float h_min, float log_v,
-    float kappa_min, int b_min, unsigned* flags, SampleArgs sa, int est, int est_k,
-    const float* __restrict__ tmax) {
+    int* __restrict__ n_kept, int MAXB, int P, int nch_max, Budget bu, unsigned* flags,
+    SampleArgs sa, int est, int est_k, const float* __restrict__ tmax) {
   static_assert(kSelThreads >= kSampleThreads && kSelThreads >= kEstThreads, "workgroup size");
   extern __shared__ __attribute__((aligned(16))) unsigned keys[];   // [MAXB] keys, [MAXB] blocks, estimator
   __shared__ SelectShared sh;
@@ -96,32 +90,25 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
   SelectRegs<HPL> R;
   select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, R);
   const int N = ctx_lens[b];
+  const float kprev = budget_prev(bu, b);
   const bool ok = N >= 0 && N <= MAXB * kBlock;
   const int nb = ok ? (N + kBlock - 1) / kBlock : 0;
   if (est != ENT_EST_EXACT) {
     const float T = temp[b];
-    const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T, b,
+    const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T * sa.t_cal, b,
                                  keys + est_lds_offset(2 * MAXB), esh);
-    if (threadIdx.x == 0) {
-      s_H = H;
-      controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min, t_max);
-    }
+    if (threadIdx.x == 0) s_H = controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, ct);
   } else if (threadIdx.x < 64) {
     const float H = row_entropy(part, C, b);
-    if (threadIdx.x == 0) {
-      s_H = H;
-      controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, eta, h_target, t_min,
-                        t_max);
-    }
+    if (threadIdx.x == 0)
+      s_H = controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, ct);
   }
   __syncthreads();
   const float H = s_H;
   int nb2, k;
-  if (!select_prepare(N, H, theta, n_kept, MAXB, eps_h, h_min, log_v, kappa_min, b_min, flags, b,
-                      nb2, k))
-    return;
-  select_finish<HPL>(R, N, nb, H, scores, theta, kept, kphys, n_kept, MAXB, P, eps_h, h_min,
-                     log_v, kappa_min, b_min, b, keys, reinterpret_cast<int*>(keys + MAXB), sh);
+  if (!select_prepare(N, H, theta, n_kept, MAXB, bu, kprev, flags, b, nb2, k)) return;
+  select_finish<HPL>(R, N, nb, H, scores, theta, kept, kphys, n_kept, MAXB, P, bu, kprev, b, keys,
+                     reinterpret_cast<int*>(keys + MAXB), sh);
 }
 }  // namespace
 
@@ -143,6 +130,7 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   pa.V = cf.vocab;
   pa.C = c->chunks;
   pa.temp = st.temp;
+  pa.t_cal = cf.t_cal;
   pa.part = c->ent_part;
   pa.row_stats = stats;
   pa.temp_used = temp_used;
@@ -180,6 +168,9 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   sa.temp_used = temp_used;
   sa.uniforms = uniforms;
   sa.tokens = tokens;
+  sa.t_cal = cf.t_cal;
+  const Control ct = make_control(cf);
+  const Budget bu = make_budget(cf, st.kappa);
   const bool vec = row_vec_ok(logits, ld);
   const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
   if (hpl) {
@@ -187,11 +178,10 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
         static_cast<size_t>(est_lds_offset(2 * cf.max_blocks_per_seq)) * sizeof(unsigned) + est_lds;
 #define ENT_STEPB_CASE(HH, VV)                                                                 \
   hipLaunchKernelGGL((step_b_kernel<HH, VV>), dim3(2 * B), dim3(kSelThreads), lds, s, B,       \
-                     c->ent_part, c->chunks, st.temp, st.h_prev, st.tau, h_out, cf.eta,        \
-                     cf.h_target, cf.t_min, cf.t_max, c->zbuf, c->lse_part, ctx_lens, tables,  \
-                     scores, theta, kept, c->kept_phys, n_kept, cf.max_blocks_per_seq,         \
-                     cf.num_pool_blocks, c->lse_chunks, cf.eps_h, cf.h_min, cf.log_v,          \
-                     cf.kappa_min, cf.b_min, c->dev_flags, sa, est_mode, cf.est_k, c->tmax)
+                     c->ent_part, c->chunks, st.temp, st.h_prev, st.tau, h_out, ct, c->zbuf,   \
+                     c->lse_part, ctx_lens, tables, scores, theta, kept, c->kept_phys, n_kept, \
+                     cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, bu,             \
+                     c->dev_flags, sa, est_mode, cf.est_k, c->tmax)
 #define ENT_STEPB_HPL(HH)                   \
   case HH:                                  \
     if (vec) ENT_STEPB_CASE(HH, true);      \
@@ -212,15 +202,15 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   } else {
     auto k0 = vec ? step_b0_kernel<true> : step_b0_kernel<false>;
     hipLaunchKernelGGL(k0, dim3(2 * B), dim3(kRowThreads), est_lds, s, B, c->ent_part, c->chunks,
-                       st.temp, st.h_prev, st.tau, h_out, cf.eta, cf.h_target, cf.t_min,
-                       cf.t_max, c->lse_part, ctx_lens, c->lrow, cf.num_q_heads,
-                       cf.max_blocks_per_seq, c->lse_chunks, sa, est_mode, cf.est_k, c->tmax);
+                       st.temp, st.h_prev, st.tau, h_out, ct, c->lse_part, ctx_lens, c->lrow,
+                       cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks, sa, est_mode,
+                       cf.est_k, c->tmax);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     float* sc = scores ? scores : c->iscores;
     e = launch_block_scores(c, B, ctx_lens, sc, s);
     if (e != hipSuccess) return e;
-    e = launch_select_rows(c, B, tables, ctx_lens, h_out, sc, theta, kept, n_kept, s);
+    e = launch_select_rows(c, B, tables, ctx_lens, h_out, sc, theta, kept, n_kept, st.kappa, s);
     if (e != hipSuccess) return e;
   }
   return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s,

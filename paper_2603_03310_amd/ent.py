@@ -39,11 +39,14 @@ class ent_config(ctypes.Structure):
         ("t_min", ctypes.c_float), ("t_max", ctypes.c_float), ("eps_h", ctypes.c_float),
         ("h_min", ctypes.c_float), ("kappa_min", ctypes.c_float), ("b_min", ctypes.c_int),
         ("log_v", ctypes.c_float), ("estimator", ctypes.c_int), ("est_k", ctypes.c_int),
+        ("t_cal", ctypes.c_float), ("rho_t", ctypes.c_float), ("dkappa", ctypes.c_float),
+        ("h_bias", ctypes.c_float),
     ]
 
 
 class ent_state(ctypes.Structure):
-    _fields_ = [("h_prev", ctypes.c_void_p), ("tau", ctypes.c_void_p), ("temp", ctypes.c_void_p)]
+    _fields_ = [("h_prev", ctypes.c_void_p), ("tau", ctypes.c_void_p), ("temp", ctypes.c_void_p),
+                ("kappa", ctypes.c_void_p)]
 
 
 class EntError(RuntimeError):
@@ -75,7 +78,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "ent_device_status": (i, [vp, vp, ctypes.POINTER(ctypes.c_uint)]),
         "ent_entropy_temperature": (i, [vp, i, vp, ll, ent_state, vp, vp, vp, vp]),
         "ent_block_summary": (i, [vp, i, vp, vp, vp, vp, vp]),
-        "ent_block_select": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "ent_block_select": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "ent_sparse_paged_decode": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "ent_sample": (i, [vp, i, vp, ll, vp, vp, vp, vp, vp]),
         "ent_kv_append": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp]),
@@ -152,7 +155,7 @@ def ent_device_status(ctx: int, stream=None) -> int:
 
 def ent_entropy_temperature(ctx, B, logits, ld, h_prev, tau, temp, h_out, temp_used,
                             row_stats=None, stream=None):
-    st = ent_state(ptr(h_prev), ptr(tau), ptr(temp))
+    st = ent_state(ptr(h_prev), ptr(tau), ptr(temp), None)
     _check(ctx, load().ent_entropy_temperature(ctx, B, ptr(logits), ld, st, ptr(h_out),
                                                ptr(temp_used), ptr(row_stats), _stream(stream)))
 
@@ -163,10 +166,10 @@ def ent_block_summary(ctx, B, k_cache, block_tables, ctx_lens, ksum, stream=None
 
 
 def ent_block_select(ctx, B, q, ksum, block_tables, ctx_lens, h, kept, n_kept, scores=None,
-                     theta=None, stream=None):
+                     theta=None, stream=None, kappa=None):
     _check(ctx, load().ent_block_select(ctx, B, ptr(q), ptr(ksum), ptr(block_tables),
                                         ptr(ctx_lens), ptr(h), ptr(kept), ptr(n_kept),
-                                        ptr(scores), ptr(theta), _stream(stream)))
+                                        ptr(scores), ptr(theta), ptr(kappa), _stream(stream)))
 
 
 def ent_sparse_paged_decode(ctx, B, q, k_cache, v_cache, block_tables, ctx_lens, kept, n_kept,
@@ -190,8 +193,9 @@ def ent_kv_append(ctx, B, k_new, v_new, block_tables, ctx_lens, k_cache, v_cache
 
 def ent_decode_step(ctx, B, logits, ld, h_prev, tau, temp, q, k_cache, v_cache, ksum,
                     block_tables, ctx_lens, uniforms, h_out, temp_used, kept, n_kept, out,
-                    tokens, row_stats=None, lse=None, scores=None, theta=None, stream=None):
-    st = ent_state(ptr(h_prev), ptr(tau), ptr(temp))
+                    tokens, row_stats=None, lse=None, scores=None, theta=None, stream=None,
+                    kappa=None):
+    st = ent_state(ptr(h_prev), ptr(tau), ptr(temp), ptr(kappa))
     _check(ctx, load().ent_decode_step(ctx, B, ptr(logits), ld, st, ptr(q), ptr(k_cache),
                                        ptr(v_cache), ptr(ksum), ptr(block_tables), ptr(ctx_lens),
                                        ptr(uniforms), ptr(h_out), ptr(temp_used), ptr(row_stats),

@@ -41,17 +41,17 @@ class Decoder:
 
     def step(self, B, *, logits, h_prev, tau, temp, q, k_cache, v_cache, block_tables, ctx_lens,
              ksum, uniforms, h, temp_used, row_stats, kept, n_kept, out, tokens, lse=None,
-             scores=None, theta=None, stream=None, fused=True):
+             scores=None, theta=None, stream=None, fused=True, kappa=None):
         ld = logits.stride(0)
         if fused:
             ent.ent_decode_step(self.ctx, B, logits, ld, h_prev, tau, temp, q, k_cache, v_cache,
                                 ksum, block_tables, ctx_lens, uniforms, h, temp_used, kept,
-                                n_kept, out, tokens, row_stats, lse, scores, theta, stream)
+                                n_kept, out, tokens, row_stats, lse, scores, theta, stream, kappa)
             return
         ent.ent_entropy_temperature(self.ctx, B, logits, ld, h_prev, tau, temp, h, temp_used,
                                     row_stats, stream)
         ent.ent_block_select(self.ctx, B, q, ksum, block_tables, ctx_lens, h, kept, n_kept,
-                             scores, theta, stream)
+                             scores, theta, stream, kappa)
         ent.ent_sparse_paged_decode(self.ctx, B, q, k_cache, v_cache, block_tables, ctx_lens,
                                     kept, n_kept, out, lse, stream)
         ent.ent_sample(self.ctx, B, logits, ld, row_stats, temp_used, uniforms, tokens, stream)

@@ -24,7 +24,8 @@ def config_fields(w: Workload, p: Params, num_pool_blocks: int,
         kv_dtype=1 if w.kv_dtype == "bf16" else 0,
         scale=p.scale, eta=p.eta, h_target=p.h_target, t_min=p.t_min, t_max=p.t_max,
         eps_h=p.eps_h, h_min=p.h_min, kappa_min=p.kappa_min, b_min=p.b_min, log_v=p.log_v,
-        estimator=p.estimator, est_k=p.est_k)
+        estimator=p.estimator, est_k=p.est_k, t_cal=p.t_cal, rho_t=p.rho_t, dkappa=p.dkappa,
+        h_bias=p.h_bias)
 
 
 def _tensor(a: np.ndarray, device):
@@ -61,6 +62,7 @@ class DeviceInputs:
     out: object
     lse: object
     tokens: object
+    kappa: object      # kept-fraction state (NaN: no previous step)
 
 
 def upload(x: Inputs, device="cuda", copies: int = 1) -> DeviceInputs:
@@ -86,4 +88,4 @@ def upload(x: Inputs, device="cuda", copies: int = 1) -> DeviceInputs:
         kept=torch.full((B, maxb), -1, **i32), n_kept=torch.zeros(B, **i32),
         scores=torch.zeros((B, maxb), **f32), theta=torch.zeros(B, **f32),
         out=torch.zeros((B, Hq, d), **f32), lse=torch.zeros((B, Hq), **f32),
-        tokens=torch.zeros(B, **i32))
+        tokens=torch.zeros(B, **i32), kappa=torch.full((B,), float("nan"), **f32))

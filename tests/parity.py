@@ -187,13 +187,14 @@ def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev,
     return rep
 
 
-def run_step(dec, dev, step: int = 0, stream=None, fused: bool = True):
+def run_step(dec, dev, step: int = 0, stream=None, fused: bool = True, kappa: bool = False):
     """Issue one decode step of the uploaded inputs on the library (no sync):
-    ent_decode_step when `fused`, else the four per-stage entry points."""
+    ent_decode_step when `fused`, else the four per-stage entry points; with
+    `kappa` the kept-fraction state dev.kappa rides along."""
     B = dev.ctx_lens.shape[0]
     dec.step(B, logits=dev.logits[step], h_prev=dev.h_prev, tau=dev.tau, temp=dev.temp,
              q=dev.q[step], k_cache=dev.k_pool, v_cache=dev.v_pool, block_tables=dev.block_tables,
              ctx_lens=dev.ctx_lens, ksum=dev.ksum, uniforms=dev.uniforms[step], h=dev.h,
              temp_used=dev.temp_used, row_stats=dev.row_stats, kept=dev.kept, n_kept=dev.n_kept,
              out=dev.out, tokens=dev.tokens, lse=dev.lse, scores=dev.scores, theta=dev.theta,
-             stream=stream, fused=fused)
+             stream=stream, fused=fused, kappa=dev.kappa if kappa else None)
