@@ -15,10 +15,11 @@ Modules, each following the paper's definitions (section cited per function):
 * ``attention``  -- decode attention restricted to the kept blocks.
 * ``sample``     -- inverse-CDF sampling at the controlled temperature.
 * ``append``     -- appending one token to the paged cache.
+* ``schedule``   -- entropy-aware selection of the sequences of the next batch.
 * ``layout``     -- reading the library's buffer layouts.
 * ``step``       -- the whole step for a batch, built from the above.
 
 Readings where the paper is silent or garbled are stated in each function's
 docstring; the ones that cannot be pinned to the paper say "parity unpinned".
 """
-from . import entropy, blocks, attention, sample, append, layout, step  # noqa: F401
+from . import entropy, blocks, attention, sample, append, layout, step, schedule  # noqa: F401
