@@ -50,9 +50,9 @@ def update_gain(gain: float, tau: float, tau_last: float, ran: bool, lam: float)
 def priority(gain: float, kept_blocks: int, ctx_len: int, age: int, prm) -> np.float32:
     """pi(s) in float32, in this operation order (no fused multiply-add)."""
     num = max(f32(gain), f32(prm.gain_floor))
-    held = f32((int(ctx_len) + 15) // 16)
+    held = f32((max(int(ctx_len), 0) + 15) // 16)
     slack = max(f32(prm.slo) - f32(age), f32(prm.slack_floor))
-    den = f32(prm.alpha) * f32(kept_blocks)
+    den = f32(prm.alpha) * f32(max(int(kept_blocks), 0))
     den = den + f32(prm.beta) * held
     den = den + f32(prm.gamma) * slack
     return f32(num / den)
