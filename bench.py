@@ -118,6 +118,39 @@ def traffic_from_counters():
     return c.get("hbm_bytes_per_launch")
 
 
+def sched_time(ent, torch, ctx, sp, b_sel, K, W):
+    """Average duration of one ent_schedule call over a pool of
+    ENT_SCHED_MAX_POOL sequences (seeded synthetic state)."""
+    import numpy as np
+    n = ent.ENT_SCHED_MAX_POOL
+    rng = np.random.default_rng(1234)
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(a).to(dev)
+    tau = t((rng.random(n) * 50).astype(np.float32))
+    tl = t((rng.random(n) * 50).astype(np.float32))
+    gain = t((rng.random(n) * 0.5).astype(np.float32))
+    age = t(rng.integers(0, 40, n).astype(np.int32))
+    kept = t(rng.integers(0, 512, n).astype(np.int32))
+    lens = t(rng.integers(0, 32768, n).astype(np.int32))
+    sel = torch.empty(n, dtype=torch.int32, device=dev)
+    nsel = torch.empty(1, dtype=torch.int32, device=dev)
+    pri = torch.empty(n, dtype=torch.float32, device=dev)
+    prm = ent.ent_sched_params(1.0, 0.25, 4.0, 16.0, 0.5, 1e-3, 0.25)
+
+    def call():
+        ent.ent_schedule(ctx, n, prm, tau, kept, lens, tl, gain, age, b_sel, sel, nsel, pri, sp)
+
+    for _ in range(W):
+        call()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(torch.cuda.current_stream())
+    for _ in range(K):
+        call()
+    e1.record(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    return {"pool": n, "b_sel": b_sel, "avg_launch_us": round(e0.elapsed_time(e1) / K * 1e3, 2)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -243,6 +276,10 @@ def main():
     d1.record(stream)
     torch.cuda.synchronize()
     dec_us = d0.elapsed_time(d1) / K * 1e3
+    # Pass D: the scheduler that picks the next batch (Section 3.1), over the
+    # largest pool of active sequences, selecting this workload's batch; K
+    # calls back to back between two events.
+    sched = sched_time(ent, torch, ctx, sp, B, K, W)
     flags = ent.ent_device_status(ctx, sp)
     if flags:
         raise SystemExit(f"device flags raised: {flags}")
@@ -292,6 +329,7 @@ def main():
                      "traffic": traffic_from_counters(),
                      "bytes_per_launch": int(dec_bytes), "avg_launch_us": round(dec_us, 2)},
         "cpu_baseline": cpu,
+        "schedule": sched,
     }
     print(json.dumps(line), flush=True)
 

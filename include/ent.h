@@ -256,6 +256,44 @@ int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new,
                   const int* block_tables, int* ctx_lens, void* k_cache, void* v_cache,
                   float* ksum, void* stream);
 
+/* Entropy-aware scheduling over a pool of N active sequences (Section 3.1:
+ * the priority pi(s) = E[Delta H_s] / (alpha C_s + beta M_s + gamma L_s);
+ * Section 7: nonnegative bounded terms, no starvation).  Readings: the
+ * expected gain is a running mean g of the sequence's entropy drops (its
+ * entropic time increments), C_s the blocks it kept at its last step, M_s
+ * the blocks it holds, ceil(N_s / 16), and L_s its slack against a service
+ * objective of slo steps, which shrinks while it waits. */
+typedef struct {
+  float alpha, beta, gamma;  /* cost weights, finite and >= 0 */
+  float slo;                 /* service objective, in steps, finite */
+  float slack_floor;         /* smallest slack, finite and > 0 */
+  float gain_floor;          /* smallest expected gain, finite and > 0 */
+  float ewma_rate;           /* weight lam of the newest drop, in [0, 1] */
+} ent_sched_params;
+#define ENT_SCHED_MAX_POOL 8192
+
+/* One scheduling call (one workgroup; N <= ENT_SCHED_MAX_POOL).  For each
+ * sequence s < N, with a_s = age[s] on entry:
+ *   if a_s == 0 (it ran since the last call):
+ *       gain[s] = (1 - lam) gain[s] + lam (tau[s] - tau_last[s]);  tau_last[s] = tau[s]
+ *   pi_s = max(gain[s], gain_floor) /
+ *          (alpha max(n_kept[s], 0) + beta ceil(max(ctx_lens[s], 0) / 16)
+ *           + gamma max(slo - a_s, slack_floor))
+ *   (float32, in exactly this order, no fused multiply-add)
+ * The min(b_sel, N) largest pi are selected, equal priorities to the lower
+ * index; selected[0 .. n_selected) receives their indices in ascending order
+ * (int [N] of room), *n_selected (device int) their number; age[s] becomes 0
+ * when selected and a_s + 1 otherwise.  tau: float [N], entropic time (as
+ * updated by the decode step); n_kept, ctx_lens: int [N]; tau_last, gain
+ * (float [N]) and age (int [N]) are the scheduler state, updated in place
+ * (start: tau_last = tau, gain = 0 or a prior, age = 0).  priority
+ * (nullable): float [N], receives pi.  b_sel < 0 selects none.  N == 0
+ * launches nothing (n_selected is not written).  c serves for error
+ * messages only. */
+int ent_schedule(ent_ctx* c, int N, const ent_sched_params* prm, const float* tau,
+                 const int* n_kept, const int* ctx_lens, float* tau_last, float* gain, int* age,
+                 int b_sel, int* selected, int* n_selected, float* priority, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -370,4 +370,36 @@ int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new, const
   return ENT_OK;
 }
 
+int ent_schedule(ent_ctx* c, int N, const ent_sched_params* prm, const float* tau,
+                 const int* n_kept, const int* ctx_lens, float* tau_last, float* gain, int* age,
+                 int b_sel, int* selected, int* n_selected, float* priority, void* stream) {
+  if (!c) return ENT_E_INVAL;
+  if (N < 0 || N > ENT_SCHED_MAX_POOL)
+    return fail(c, ENT_E_INVAL, "ent_schedule: N must be in [0, ENT_SCHED_MAX_POOL]");
+  if (!prm) return fail(c, ENT_E_INVAL, "ent_schedule: params is NULL");
+  const ent_sched_params& p = *prm;
+  if (!(p.alpha >= 0.f) || !(p.beta >= 0.f) || !(p.gamma >= 0.f) || !isfinite(p.alpha) ||
+      !isfinite(p.beta) || !isfinite(p.gamma))
+    return fail(c, ENT_E_INVAL, "ent_schedule: alpha, beta and gamma must be finite and >= 0");
+  if (!isfinite(p.slo)) return fail(c, ENT_E_INVAL, "ent_schedule: slo must be finite");
+  if (!(p.slack_floor > 0.f) || !isfinite(p.slack_floor))
+    return fail(c, ENT_E_INVAL, "ent_schedule: slack_floor must be finite and > 0");
+  if (!(p.gain_floor > 0.f) || !isfinite(p.gain_floor))
+    return fail(c, ENT_E_INVAL, "ent_schedule: gain_floor must be finite and > 0");
+  if (!(p.ewma_rate >= 0.f && p.ewma_rate <= 1.f))
+    return fail(c, ENT_E_INVAL, "ent_schedule: ewma_rate must be in [0, 1]");
+  if (N == 0) {
+    c->err.clear();
+    return ENT_OK;
+  }
+  if (!tau || !n_kept || !ctx_lens || !tau_last || !gain || !age || !selected || !n_selected)
+    return fail(c, ENT_E_INVAL, "ent_schedule: NULL required pointer");
+  const hipError_t e = ent::launch_schedule(N, p, tau, n_kept, ctx_lens, tau_last, gain, age, b_sel,
+                                            selected, n_selected, priority,
+                                            static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "ent_schedule launch");
+  c->err.clear();
+  return ENT_OK;
+}
+
 }  // extern "C"

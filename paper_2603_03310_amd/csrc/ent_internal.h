@@ -160,6 +160,9 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
 hipError_t launch_kv_append(const ent_ctx* c, int B, const void* k_new, const void* v_new,
                             const int* tables, int* ctx_lens, void* k_cache, void* v_cache,
                             float* ksum, hipStream_t s);
+hipError_t launch_schedule(int N, const ent_sched_params& p, const float* tau, const int* n_kept,
+                           const int* ctx_lens, float* tau_last, float* gain, int* age, int b_sel,
+                           int* selected, int* n_selected, float* priority, hipStream_t s);
 
 // Occupancy-derived persistent grid of the decode kernel, and the number of
 // partial slots its split segments may use (waves + segments).

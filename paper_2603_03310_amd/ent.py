@@ -26,7 +26,8 @@ ENT_DEV_BAD_TABLE, ENT_DEV_BAD_CTXLEN, ENT_DEV_CACHE_FULL = 1, 2, 4
 EXPORTED = ("ent_default_config", "ent_check_config", "ent_row_stats_chunks", "ent_init",
             "ent_destroy", "ent_last_error", "ent_device_status", "ent_entropy_temperature",
             "ent_block_summary", "ent_block_select", "ent_sparse_paged_decode", "ent_sample",
-            "ent_kv_append", "ent_decode_step")
+            "ent_kv_append", "ent_decode_step", "ent_schedule")
+ENT_SCHED_MAX_POOL = 8192
 
 
 class ent_config(ctypes.Structure):
@@ -42,6 +43,12 @@ class ent_config(ctypes.Structure):
         ("t_cal", ctypes.c_float), ("rho_t", ctypes.c_float), ("dkappa", ctypes.c_float),
         ("h_bias", ctypes.c_float),
     ]
+
+
+class ent_sched_params(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("gamma", ctypes.c_float),
+                ("slo", ctypes.c_float), ("slack_floor", ctypes.c_float),
+                ("gain_floor", ctypes.c_float), ("ewma_rate", ctypes.c_float)]
 
 
 class ent_state(ctypes.Structure):
@@ -83,6 +90,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "ent_sample": (i, [vp, i, vp, ll, vp, vp, vp, vp, vp]),
         "ent_kv_append": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp]),
         "ent_decode_step": (i, [vp, i, vp, ll, ent_state] + [vp] * 18),
+        "ent_schedule": (i, [vp, i, ctypes.POINTER(ent_sched_params)] + [vp] * 6
+                         + [i] + [vp] * 4),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -201,3 +210,11 @@ def ent_decode_step(ctx, B, logits, ld, h_prev, tau, temp, q, k_cache, v_cache, 
                                        ptr(uniforms), ptr(h_out), ptr(temp_used), ptr(row_stats),
                                        ptr(kept), ptr(n_kept), ptr(out), ptr(lse), ptr(tokens),
                                        ptr(scores), ptr(theta), _stream(stream)))
+
+
+def ent_schedule(ctx, N, prm: ent_sched_params, tau, n_kept, ctx_lens, tau_last, gain, age,
+                 b_sel, selected, n_selected, priority=None, stream=None):
+    _check(ctx, load().ent_schedule(ctx, N, ctypes.byref(prm), ptr(tau), ptr(n_kept),
+                                    ptr(ctx_lens), ptr(tau_last), ptr(gain), ptr(age), b_sel,
+                                    ptr(selected), ptr(n_selected), ptr(priority),
+                                    _stream(stream)))

@@ -62,3 +62,8 @@ class Decoder:
 
     def device_status(self, stream=None) -> int:
         return ent.ent_device_status(self.ctx, stream)
+
+    def schedule(self, N, prm, tau, n_kept, ctx_lens, tau_last, gain, age, b_sel, selected,
+                 n_selected, priority=None, stream=None):
+        ent.ent_schedule(self.ctx, N, prm, tau, n_kept, ctx_lens, tau_last, gain, age, b_sel,
+                         selected, n_selected, priority, stream)

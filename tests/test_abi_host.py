@@ -76,3 +76,11 @@ def test_init_rejects_bad_config_without_a_device():
     with pytest.raises(ent.EntError) as e:
         ent.ent_init(c)
     assert e.value.code == ent.ENT_E_INVAL and "block_size" in str(e.value)
+
+
+def test_schedule_rejects_null_context_without_a_device():
+    from paper_2603_03310_amd import ent
+    lib = ent.load()
+    prm = ent.ent_sched_params(1.0, 0.25, 4.0, 16.0, 0.5, 1e-3, 0.25)
+    code = lib.ent_schedule(None, 4, ctypes.byref(prm), *([None] * 6), 2, None, None, None, None)
+    assert code == ent.ENT_E_INVAL
