@@ -19,6 +19,10 @@ surprisal's distribution is, or what form the threshold takes.  Readings:
   the (floored) entropy from kappa_min * nb at H_min to nb at log |V|;
   ties at the threshold are all kept.
 
+The exact token-level weights (every key of the sequence against the current
+query) are the second scoring mode, exact_token_scores.  Optionally the first
+and last blocks of a sequence are always kept (forced_blocks).
+
 These readings are the build's; the paper prints no values to pin them to
 (parity unpinned against the paper; pinned here against closed forms of the
 readings themselves).
@@ -111,22 +115,45 @@ def keep_budget(h: float, nb: int, params, kappa_prev: float = math.nan) -> int:
     return min(nb, max(min(int(params.b_min), nb), k))
 
 
-def select_blocks(scores: np.ndarray, k: int):
+def forced_blocks(nb: int, keep_first: int = 0, keep_last: int = 0) -> np.ndarray:
+    """Blocks always kept: the first keep_first and the last keep_last logical
+    blocks of a sequence of nb blocks (a build option; the paper prunes by
+    score alone)."""
+    f = set(range(min(max(int(keep_first), 0), nb)))
+    f |= set(range(max(nb - max(int(keep_last), 0), 0), nb))
+    return np.array(sorted(f), dtype=np.int64)
+
+
+def select_blocks(scores: np.ndarray, k: int, forced=None):
     """Kept set B_t = {b : I_b >= theta_t} with theta_t the k-th largest score
     (Section 3.2), listed in ascending block order.  Ties at theta are kept.
-    Returns (kept indices, theta); theta is +inf when k == 0."""
+    Returns (kept indices, theta); theta is +inf when k == 0.
+
+    Forced blocks (optional) are always kept and count toward the budget:
+    they rank above every score, the budget becomes max(k, |forced|), and
+    theta is the budget-th largest of those ranks (+inf when the forced
+    blocks fill it)."""
     nb = len(scores)
+    nf = 0 if forced is None else len(forced)
+    if nf:
+        ranked = np.asarray(scores, dtype=np.float64).copy()
+        ranked[np.asarray(forced, dtype=np.int64)] = math.inf
+        k = max(int(k), nf)
+    else:
+        ranked = scores
     if k <= 0 or nb == 0:
         return np.zeros(0, dtype=np.int64), math.inf
-    theta = float(np.sort(scores)[::-1][k - 1])
-    kept = np.nonzero(scores >= theta)[0]
+    theta = float(np.sort(ranked)[::-1][k - 1])
+    kept = np.nonzero(ranked >= theta)[0]
     return kept.astype(np.int64), theta
 
 
 def exact_token_scores(q: np.ndarray, K: np.ndarray, block_size: int, scale: float) -> np.ndarray:
-    """Diagnostic only (not a parity target): block scores from the exact
-    token-level attention weights of the current query, a_i = softmax over
-    all keys, with surprisal -log a_i, averaged over heads."""
+    """Block entropic contributions from the exact token-level attention
+    weights (Section 3.2 taken literally: a_i is the current query's softmax
+    over all valid keys, surprisal -log a_i), I_b = mean_h sum_{i in b}
+    a_i (-log a_i).  The conservative scoring mode: it reads every key of the
+    sequence, where the mean-key reading reads one summary per block."""
     Hq, d = q.shape
     N, Hkv, _ = K.shape
     G = Hq // Hkv

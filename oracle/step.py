@@ -51,7 +51,9 @@ def sequence_step(s: int, *, k_pool, v_pool, tables, ctx_lens, q, logits, h_prev
     else:
         kbar = blocks.block_means(K, block_size)
     out["kbar"] = kbar
-    if nb:
+    if nb and getattr(params, "scoring", 0) == 1:
+        I = blocks.exact_token_scores(qs, K, block_size, params.scale)
+    elif nb:
         I, _, _ = blocks.block_scores(qs, kbar, counts, params.scale)
     else:
         I = np.zeros(0)
@@ -59,7 +61,9 @@ def sequence_step(s: int, *, k_pool, v_pool, tables, ctx_lens, q, logits, h_prev
     kp = math.nan if kappa is None else float(kappa[s])
     k = blocks.keep_budget(h_budget, nb, params, kp)
     out["kappa"] = float(blocks.kept_fraction(h_budget, params, kp)) if nb else kp
-    kept, theta = blocks.select_blocks(I, k)
+    forced = blocks.forced_blocks(nb, getattr(params, "keep_first", 0),
+                                  getattr(params, "keep_last", 0))
+    kept, theta = blocks.select_blocks(I, k, forced)
     out.update(scores=I, k=k, kept=kept, theta=theta, nb=nb)
     o, lse = attention.sparse_decode(qs, K, V, kept, block_size, params.scale)
     out.update(o=o, lse=lse)

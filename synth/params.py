@@ -38,6 +38,9 @@ class Params:
     rho_t: float = math.inf   # bound on |ln T_{t+1} - ln T_t| before clipping (inf = none)
     dkappa: float = 1.0   # largest decrease of the kept fraction per step (1 = none)
     h_bias: float = 0.0   # offset added to the entropy the controller acts on (stress tests)
+    scoring: int = 0      # block scores: 0 mean-key reading, 1 exact token-level weights
+    keep_first: int = 0   # leading blocks always kept
+    keep_last: int = 0    # trailing blocks always kept
 
     def __post_init__(self):
         # Every float is held at float32 precision: the library receives
