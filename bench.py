@@ -62,6 +62,10 @@ def parse():
     ap.add_argument("--est-k", type=int, default=256)
     ap.add_argument("--eps-h", type=float, default=None,
                     help="estimator error bound in the block budget (default 0)")
+    ap.add_argument("--scoring", choices=["meankey", "exact"], default="meankey",
+                    help="block scores from mean keys, or from exact token-level weights")
+    ap.add_argument("--keep-first", type=int, default=0, help="leading blocks always kept")
+    ap.add_argument("--keep-last", type=int, default=0, help="trailing blocks always kept")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -174,6 +178,8 @@ def main():
         p = p.replace(estimator=est, est_k=args.est_k)
     if args.eps_h is not None:
         p = p.replace(eps_h=args.eps_h)
+    p = p.replace(scoring=1 if args.scoring == "exact" else 0, keep_first=args.keep_first,
+                  keep_last=args.keep_last)
     t0 = time.perf_counter()
     x = generate(w)
     print(f"[bench] generated {w.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
@@ -213,7 +219,7 @@ def main():
                                     o.row_stats, sp)
         ev[1].record(stream)
         ent.ent_block_select(ctx, B, c.q[0], c.ksum, c.block_tables, c.ctx_lens, o.h, o.kept,
-                             o.n_kept, None, None, sp)
+                             o.n_kept, None, None, sp, None, c.k_pool)
         ev[2].record(stream)
         ent.ent_sparse_paged_decode(ctx, B, c.q[0], c.k_pool, c.v_pool, c.block_tables,
                                     c.ctx_lens, o.kept, o.n_kept, o.out, o.lse, sp)
@@ -315,7 +321,10 @@ def main():
                    "head_dim": d, "block_size": 16, "ctx": list(w.ctx), "vocab": w.vocab,
                    "kv_dtype": w.kv_dtype, "entropy": args.estimator,
                    **({"est_k": args.est_k} if est else {}),
-                   **({"eps_h": p.eps_h} if p.eps_h else {})},
+                   **({"eps_h": p.eps_h} if p.eps_h else {}),
+                   **({"scoring": args.scoring} if p.scoring else {}),
+                   **({"keep_first": p.keep_first} if p.keep_first else {}),
+                   **({"keep_last": p.keep_last} if p.keep_last else {})},
         "hbm_gbps_kept_kv_plus_logits": round(gbps, 1),
         "hbm_frac_kept_kv_plus_logits": round(gbps / HBM_PEAK_GBPS, 4),
         "metric_bytes_per_step": int(metric_bytes),
@@ -331,6 +340,12 @@ def main():
         "cpu_baseline": cpu,
         "schedule": sched,
     }
+    if p.scoring:
+        # The exact mode reads every valid key once inside the block selection.
+        k_all = int(sum(int(n) for n in x.ctx_lens)) * w.num_kv_heads * w.head_dim * elem
+        sel_us = per_k["block_select"]
+        line["exact_scoring"] = {"k_bytes": k_all, "block_select_us": round(sel_us, 2),
+                                 "gbps_on_k": round(k_all / (sel_us * 1e-6) / 1e9, 1)}
     print(json.dumps(line), flush=True)
 
 

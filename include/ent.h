@@ -61,6 +61,13 @@ enum { ENT_F32 = 0, ENT_BF16 = 1 };
 enum { ENT_EST_EXACT = 0, ENT_EST_TOPK = 1, ENT_EST_TAIL = 2 };
 #define ENT_EST_MAX_K 512
 
+/* Block scoring (Section 3.2: I_b is the attention-weighted surprisal of
+ * block b's tokens).  MEANKEY: the weights of the current query when every
+ * token carries its block's mean key (one summary per block and KV head is
+ * read).  EXACT: the token-level softmax of the current query over every
+ * valid key of the sequence (every key is read: the conservative mode). */
+enum { ENT_SCORE_MEANKEY = 0, ENT_SCORE_EXACT = 1 };
+
 /* Tokens per logical row chunk of the entropy reduction; row statistics hold
  * one (max, sum) pair per chunk: ent_row_stats_chunks(vocab) chunks per row. */
 #define ENT_ROW_CHUNK 4096
@@ -109,6 +116,10 @@ typedef struct {
                               needs the kept-fraction state (ent_state.kappa) */
   float h_bias;            /* offset added to the entropy the controller and budget act on
                               (miscalibration stress tests); finite */
+  int scoring;             /* ENT_SCORE_MEANKEY (default) or ENT_SCORE_EXACT */
+  int keep_first;          /* leading logical blocks always kept, >= 0 (0 = none) */
+  int keep_last;           /* trailing logical blocks always kept, >= 0 (0 = none); forced
+                              blocks count toward the budget k (it becomes max(k, forced)) */
 } ent_config;
 
 /* Per-sequence controller state, device arrays of B floats each, read and
@@ -187,22 +198,30 @@ int ent_block_summary(ent_ctx* c, int B, const void* k_cache, const int* block_t
  * contribution I_b and the kept set B_t = {b : I_b >= theta_t}; Section 3.3
  * and Section 5: the safety floor, the minimum block budget and the bounded
  * rate of change of the threshold).
+ *   ENT_SCORE_MEANKEY:
  *   z_bh  = scale <q_h, ksum[p_b, h / G]>,  weights a_bh = e^{z_bh} / sum_b' n_b' e^{z_b'h}
  *   I_b   = (1/H_q) sum_h n_b a_bh (-ln a_bh)
+ *   ENT_SCORE_EXACT (reads k_cache; ksum unused):
+ *   s_ih  = scale <q_h, k_i>,  a_ih = softmax over the valid tokens i of s_.h
+ *   I_b   = (1/H_q) sum_h sum_{i in b} a_ih (-ln a_ih)
  *   H_g   = max(h[b] + eps_H, H_min);  u = clip((H_g - H_min)/(log_v - H_min), 0, 1)
  *   kappa = kappa_min + (1 - kappa_min) u, then max(kappa, kappa[b] - dkappa) when the
  *           state kappa is given and kappa[b] is not NaN
  *   k     = min(nb, max(min(B_min, nb), ceil(kappa nb)))
  *           (float32, in exactly this order, no fused multiply-add)
- *   theta = k-th largest I_b;  kept = {b : I_b >= theta} in ascending order
+ *   F     = the first keep_first and the last keep_last blocks (forced keeps)
+ *   theta = max(k, |F|)-th largest of I_b, with +inf for the blocks of F;
+ *   kept  = F + {b : I_b >= theta} in ascending order
  * kappa (nullable, in/out): the kept-fraction state; receives this step's
  * fraction for every sequence with blocks.
- * q: [B, H_q, d] (kv_dtype); ksum from ent_block_summary; h: float [B] (the
- * entropy from ent_entropy_temperature).  Outputs: kept int [B, MAXB] (first
+ * q: [B, H_q, d] (kv_dtype); ksum from ent_block_summary (mean-key mode);
+ * k_cache (exact mode; may be NULL otherwise); h: float [B] (the entropy
+ * from ent_entropy_temperature).  Outputs: kept int [B, MAXB] (first
  * n_kept[b] entries valid, logical block ids), n_kept int [B]; scores
- * (nullable) float [B, MAXB] (I_b for b < nb); theta (nullable) float [B]
- * (+inf when nothing is kept). */
-int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum,
+ * (nullable) float [B, MAXB] (I_b for b < nb, forced blocks included);
+ * theta (nullable) float [B] (+inf when nothing is kept, or when the forced
+ * blocks fill the budget). */
+int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum, const void* k_cache,
                      const int* block_tables, const int* ctx_lens, const float* h, int* kept,
                      int* n_kept, float* scores, float* theta, float* kappa, void* stream);
 
@@ -234,7 +253,8 @@ int ent_sample(ent_ctx* c, int B, const float* logits, long long ld, const float
  * temp_used passed from the first to the last).  The entropy passes and the
  * block scoring share one launch; the per-sequence entropy, controller and
  * selection share a second; decode attention follows, and sampling shares
- * the launch that merges the split attention segments.
+ * the launch that merges the split attention segments.  In the exact
+ * scoring mode the step is the four staged calls in order.
  * Arguments as in those calls: st is updated in place (tau, h_prev, temp
  * for the next step); h_out, temp_used, tokens: [B]; kept, n_kept, out as
  * in ent_sparse_paged_decode; row_stats, lse, scores, theta nullable.

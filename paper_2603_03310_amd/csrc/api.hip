@@ -51,6 +51,9 @@ std::string check_config(const ent_config* c, int* code) {
   if (!(c->rho_t >= 0.f)) return "rho_t must be >= 0 (INFINITY: no bound)";
   if (!(c->dkappa >= 0.f && c->dkappa <= 1.f)) return "dkappa must be in [0, 1]";
   if (!isfinite(c->h_bias)) return "h_bias must be finite";
+  if (c->scoring != ENT_SCORE_MEANKEY && c->scoring != ENT_SCORE_EXACT)
+    return "scoring must be ENT_SCORE_MEANKEY or ENT_SCORE_EXACT";
+  if (c->keep_first < 0 || c->keep_last < 0) return "keep_first and keep_last must be >= 0";
   *code = ENT_E_UNSUPPORTED;
   if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
   if (!is_pow2_group(c->num_q_heads / c->num_kv_heads))
@@ -118,6 +121,9 @@ void ent_default_config(ent_config* out) {
   out->rho_t = INFINITY;
   out->dkappa = 1.0f;
   out->h_bias = 0.0f;
+  out->scoring = ENT_SCORE_MEANKEY;
+  out->keep_first = 0;
+  out->keep_last = 0;
 }
 
 int ent_check_config(const ent_config* cfg, char* msg, int msg_len) {
@@ -177,9 +183,12 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   const size_t sz_tmax = f.estimator == ENT_EST_EXACT
                              ? 0
                              : align_up(Bm * c->chunks * ent::kEstChunkThreads * sizeof(float));
+  const size_t sz_ex = f.scoring == ENT_SCORE_EXACT
+                           ? align_up(Bm * f.max_blocks_per_seq * f.num_q_heads * 2 * sizeof(float))
+                           : 0;
   const size_t sz_flags = align_up(sizeof(unsigned));
   c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_lrow + sz_isc + sz_kphys + sz_acc + sz_ml +
-                sz_rec + sz_tmax + sz_flags;
+                sz_rec + sz_tmax + sz_ex + sz_flags;
   e = hipMalloc(&c->ws, c->ws_bytes);
   if (e != hipSuccess) {
     g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
@@ -207,6 +216,7 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->dec_ml = reinterpret_cast<float*>(take(sz_ml));
   c->dec_rec = reinterpret_cast<int4*>(take(sz_rec));
   c->tmax = sz_tmax ? reinterpret_cast<float*>(take(sz_tmax)) : nullptr;
+  c->exbuf = sz_ex ? reinterpret_cast<float2*>(take(sz_ex)) : nullptr;
   c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));
   *out = c;
   return ENT_OK;
@@ -268,18 +278,22 @@ int ent_block_summary(ent_ctx* c, int B, const void* k_cache, const int* block_t
   return ENT_OK;
 }
 
-int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum, const int* block_tables,
-                     const int* ctx_lens, const float* h, int* kept, int* n_kept, float* scores,
-                     float* theta, float* kappa, void* stream) {
+int ent_block_select(ent_ctx* c, int B, const void* q, const float* ksum, const void* k_cache,
+                     const int* block_tables, const int* ctx_lens, const float* h, int* kept,
+                     int* n_kept, float* scores, float* theta, float* kappa, void* stream) {
   if (!c) return ENT_E_INVAL;
   if (int r = check_batch(c, B)) return r;
   if (B == 0) return ENT_OK;
-  if (!q || !ksum || !block_tables || !ctx_lens || !h || !kept || !n_kept)
+  const bool exact = c->cfg.scoring == ENT_SCORE_EXACT;
+  if (!q || !block_tables || !ctx_lens || !h || !kept || !n_kept)
     return fail(c, ENT_E_INVAL, "ent_block_select: NULL required pointer");
-  if (!aligned(q, 16) || !aligned(ksum, 16))
-    return fail(c, ENT_E_INVAL, "ent_block_select: q or ksum misaligned");
-  const hipError_t e = ent::launch_block_select(c, B, q, ksum, block_tables, ctx_lens, h, kept,
-                                                n_kept, scores, theta, kappa,
+  if (exact ? !k_cache : !ksum)
+    return fail(c, ENT_E_INVAL, exact ? "ent_block_select: exact scoring needs k_cache"
+                                      : "ent_block_select: mean-key scoring needs ksum");
+  if (!aligned(q, 16) || (exact ? !aligned(k_cache, 16) : !aligned(ksum, 16)))
+    return fail(c, ENT_E_INVAL, "ent_block_select: q, ksum or k_cache misaligned");
+  const hipError_t e = ent::launch_block_select(c, B, q, ksum, k_cache, block_tables, ctx_lens, h,
+                                                kept, n_kept, scores, theta, kappa,
                                                 static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(c, e, "ent_block_select launch");
   c->err.clear();
@@ -336,6 +350,20 @@ int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_st
   if (!c) return ENT_E_INVAL;
   if (int r = check_batch(c, B)) return r;
   if (B == 0) return ENT_OK;
+  if (c->cfg.scoring == ENT_SCORE_EXACT) {
+    // The conservative scoring mode: the staged calls in order.
+    if (!logits || !uniforms || !out || !tokens || !v_cache)
+      return fail(c, ENT_E_INVAL, "ent_decode_step: NULL required pointer");
+    if (int r = ent_entropy_temperature(c, B, logits, ld, st, h_out, temp_used, row_stats, stream))
+      return r;
+    if (int r = ent_block_select(c, B, q, ksum, k_cache, block_tables, ctx_lens, h_out, kept,
+                                 n_kept, scores, theta, st.kappa, stream))
+      return r;
+    if (int r = ent_sparse_paged_decode(c, B, q, k_cache, v_cache, block_tables, ctx_lens, kept,
+                                        n_kept, out, lse, stream))
+      return r;
+    return ent_sample(c, B, logits, ld, row_stats, temp_used, uniforms, tokens, stream);
+  }
   if (!logits || !st.h_prev || !st.tau || !st.temp || !q || !k_cache || !v_cache || !ksum ||
       !block_tables || !ctx_lens || !uniforms || !h_out || !temp_used || !kept || !n_kept ||
       !out || !tokens)

@@ -213,16 +213,30 @@ Budget make_budget(const ent_config& cf, float* kappa) {
   bu.kappa_min = cf.kappa_min;
   bu.dkappa = cf.dkappa;
   bu.b_min = cf.b_min;
+  bu.keep_first = cf.keep_first;
+  bu.keep_last = cf.keep_last;
   bu.kappa = kappa;
   return bu;
 }
 
 hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const float* ksum,
-                               const int* tables, const int* ctx_lens, const float* h, int* kept,
-                               int* n_kept, float* scores, float* theta, float* kappa,
-                               hipStream_t s) {
+                               const void* k_cache, const int* tables, const int* ctx_lens,
+                               const float* h, int* kept, int* n_kept, float* scores,
+                               float* theta, float* kappa, hipStream_t s) {
   const ent_config& cf = c->cfg;
   hipError_t e;
+  if (cf.scoring == ENT_SCORE_EXACT) {
+    // Exact token-level weights: per-block triples from one pass over K,
+    // then the selection's three phases with the exact block scores.
+    e = launch_exact_scores(c, B, q, k_cache, tables, ctx_lens, s);
+    if (e != hipSuccess) return e;
+    e = launch_lse_merge(c, B, ctx_lens, s);
+    if (e != hipSuccess) return e;
+    float* sc = scores ? scores : c->iscores;
+    e = launch_exact_block_scores(c, B, ctx_lens, sc, s);
+    if (e != hipSuccess) return e;
+    return launch_select_rows(c, B, tables, ctx_lens, h, sc, theta, kept, n_kept, kappa, s);
+  }
   if (cf.kv_dtype == ENT_BF16) {
     PrologueArgs a{};
     a.B = B;
@@ -275,14 +289,19 @@ hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const in
 #undef ENT_SEL_CASE
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(lse_merge_kernel, dim3(B), dim3(kRowThreads), 0, s, c->lse_part, ctx_lens,
-                     c->lrow, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_lse_merge(c, B, ctx_lens, s);
   if (e != hipSuccess) return e;
   float* sc = scores ? scores : c->iscores;
   e = launch_block_scores(c, B, ctx_lens, sc, s);
   if (e != hipSuccess) return e;
   return launch_select_rows(c, B, tables, ctx_lens, h, sc, theta, kept, n_kept, kappa, s);
+}
+
+hipError_t launch_lse_merge(const ent_ctx* c, int B, const int* ctx_lens, hipStream_t s) {
+  const ent_config& cf = c->cfg;
+  hipLaunchKernelGGL(lse_merge_kernel, dim3(B), dim3(kRowThreads), 0, s, c->lse_part, ctx_lens,
+                     c->lrow, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks);
+  return hipGetLastError();
 }
 
 hipError_t launch_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,

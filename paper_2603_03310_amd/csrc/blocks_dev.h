@@ -551,6 +551,20 @@ __device__ __forceinline__ void select_core(unsigned* keys, const int* tbl, int 
   }
 }
 
+// Forced keeps: the first keep_first and the last keep_last of a sequence's
+// nb blocks rank above every score (key of +inf) and count toward the
+// budget, which becomes max(k, their number).
+__device__ __forceinline__ bool forced_block(int j, int nb, const Budget& bu) {
+  return j < bu.keep_first || j >= nb - bu.keep_last;
+}
+__device__ __forceinline__ int forced_budget(int k, int nb, const Budget& bu) {
+  const int nf = min(nb, min(bu.keep_first, nb) + min(bu.keep_last, nb));
+  return max(k, nf);
+}
+__device__ __forceinline__ unsigned select_key(float I, int j, int nb, const Budget& bu) {
+  return forced_block(j, nb, bu) ? float_key(INFINITY) : float_key(I);
+}
+
 // No block kept: the outputs of sequence b.
 __device__ __forceinline__ void select_none(float* __restrict__ theta_out, int* __restrict__ n_kept,
                                             int b) {
@@ -602,6 +616,7 @@ __device__ __forceinline__ void select_row_body(
     __syncthreads();              // every thread has read the previous fraction
     budget_record(bu, b, ku);
   }
+  k = forced_budget(k, nb, bu);
   if (k <= 0) {
     select_none(theta_out, n_kept, b);
     return;
@@ -609,7 +624,7 @@ __device__ __forceinline__ void select_row_body(
   const float* sr = scores + static_cast<long long>(b) * MAXB;
   const int* tr = tables + static_cast<long long>(b) * MAXB;
   for (int i = threadIdx.x; i < nb; i += kSelThreads) {
-    keys[i] = float_key(sr[i]);
+    keys[i] = select_key(sr[i], i, nb, bu);
     tbl[i] = encode_phys(tr[i], i, nb, P);
   }
   __syncthreads();
@@ -737,14 +752,14 @@ __device__ __forceinline__ void select_finish(
     acc += __shfl_xor(acc, 2);
     const float I = __fdiv_rn(acc, static_cast<float>(Hq));
     if (j < nb && qq == 0) {
-      keys[j] = float_key(I);
+      keys[j] = select_key(I, j, nb, bu);
       tbl[j] = encode_phys(R.tb[p], j, nb, P);
       if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j] = I;
     }
   }
   __syncthreads();
   float ku;
-  const int k = keep_budget(hval, nb, bu, kprev, &ku);
+  const int k = forced_budget(keep_budget(hval, nb, bu, kprev, &ku), nb, bu);
   budget_record(bu, b, ku);       // every thread read kprev before the barriers above
   if (k <= 0) {
     select_none(theta_out, n_kept, b);

@@ -33,6 +33,7 @@ Control make_control(const ent_config& cf);
 struct Budget {
   float eps_h, h_min, log_v, kappa_min, dkappa;
   int b_min;
+  int keep_first, keep_last;   // blocks always kept at each end of a sequence
   float* kappa;   // nullable [B]: previous kept fraction (NaN = none), updated in place
 };
 
@@ -61,6 +62,7 @@ struct ent_ctx {
   float* dec_ml = nullptr;        // [decode partial slots, G, 2]
   int4* dec_rec = nullptr;        // [decode waves]  cut-segment records of the decode ranges
   float* tmax = nullptr;          // [max_batch, chunks, 256]  per-thread logit maxima (estimators)
+  float2* exbuf = nullptr;        // [max_batch, MAXB, H_q]  exact mode: (log mass, mean logit) per block
   unsigned* dev_flags = nullptr;  // [1]
 
   std::string err;
@@ -85,9 +87,18 @@ hipError_t launch_block_summary(const ent_ctx* c, int B, const void* k_cache,
                                 const int* tables, const int* ctx_lens, float* ksum,
                                 hipStream_t s);
 hipError_t launch_block_select(const ent_ctx* c, int B, const void* q, const float* ksum,
-                               const int* tables, const int* ctx_lens, const float* h,
-                               int* kept, int* n_kept, float* scores, float* theta,
-                               float* kappa, hipStream_t s);
+                               const void* k_cache, const int* tables, const int* ctx_lens,
+                               const float* h, int* kept, int* n_kept, float* scores,
+                               float* theta, float* kappa, hipStream_t s);
+// Exact token-level scoring: per block and query head (log mass, mean logit)
+// into c->exbuf and the per-tile log-sum-exp partials into c->lse_part.
+hipError_t launch_exact_scores(const ent_ctx* c, int B, const void* q, const void* k_cache,
+                               const int* tables, const int* ctx_lens, hipStream_t s);
+// Block scores of the exact mode from c->exbuf and c->lrow.
+hipError_t launch_exact_block_scores(const ent_ctx* c, int B, const int* ctx_lens, float* scores,
+                                     hipStream_t s);
+// Selection phase A: L_h of every sequence into c->lrow from c->lse_part.
+hipError_t launch_lse_merge(const ent_ctx* c, int B, const int* ctx_lens, hipStream_t s);
 Budget make_budget(const ent_config& cf, float* kappa);
 // The pass over logits and block summaries that opens a step:
 // entropy chunk triples / row statistics (do_entropy) and block scoring of

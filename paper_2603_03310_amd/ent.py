@@ -19,6 +19,7 @@ ENT_OK, ENT_E_INVAL, ENT_E_NOMEM, ENT_E_HIP, ENT_E_UNSUPPORTED = 0, -1, -2, -3, 
 ENT_F32, ENT_BF16 = 0, 1
 ENT_EST_EXACT, ENT_EST_TOPK, ENT_EST_TAIL = 0, 1, 2
 ENT_EST_MAX_K = 512
+ENT_SCORE_MEANKEY, ENT_SCORE_EXACT = 0, 1
 ENT_ROW_CHUNK = 4096
 ENT_BLOCK_SIZE = 16
 ENT_DEV_BAD_TABLE, ENT_DEV_BAD_CTXLEN, ENT_DEV_CACHE_FULL = 1, 2, 4
@@ -41,7 +42,8 @@ class ent_config(ctypes.Structure):
         ("h_min", ctypes.c_float), ("kappa_min", ctypes.c_float), ("b_min", ctypes.c_int),
         ("log_v", ctypes.c_float), ("estimator", ctypes.c_int), ("est_k", ctypes.c_int),
         ("t_cal", ctypes.c_float), ("rho_t", ctypes.c_float), ("dkappa", ctypes.c_float),
-        ("h_bias", ctypes.c_float),
+        ("h_bias", ctypes.c_float), ("scoring", ctypes.c_int), ("keep_first", ctypes.c_int),
+        ("keep_last", ctypes.c_int),
     ]
 
 
@@ -85,7 +87,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "ent_device_status": (i, [vp, vp, ctypes.POINTER(ctypes.c_uint)]),
         "ent_entropy_temperature": (i, [vp, i, vp, ll, ent_state, vp, vp, vp, vp]),
         "ent_block_summary": (i, [vp, i, vp, vp, vp, vp, vp]),
-        "ent_block_select": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "ent_block_select": (i, [vp, i] + [vp] * 12),
         "ent_sparse_paged_decode": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "ent_sample": (i, [vp, i, vp, ll, vp, vp, vp, vp, vp]),
         "ent_kv_append": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp]),
@@ -175,10 +177,11 @@ def ent_block_summary(ctx, B, k_cache, block_tables, ctx_lens, ksum, stream=None
 
 
 def ent_block_select(ctx, B, q, ksum, block_tables, ctx_lens, h, kept, n_kept, scores=None,
-                     theta=None, stream=None, kappa=None):
-    _check(ctx, load().ent_block_select(ctx, B, ptr(q), ptr(ksum), ptr(block_tables),
-                                        ptr(ctx_lens), ptr(h), ptr(kept), ptr(n_kept),
-                                        ptr(scores), ptr(theta), ptr(kappa), _stream(stream)))
+                     theta=None, stream=None, kappa=None, k_cache=None):
+    _check(ctx, load().ent_block_select(ctx, B, ptr(q), ptr(ksum), ptr(k_cache),
+                                        ptr(block_tables), ptr(ctx_lens), ptr(h), ptr(kept),
+                                        ptr(n_kept), ptr(scores), ptr(theta), ptr(kappa),
+                                        _stream(stream)))
 
 
 def ent_sparse_paged_decode(ctx, B, q, k_cache, v_cache, block_tables, ctx_lens, kept, n_kept,

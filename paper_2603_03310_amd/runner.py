@@ -51,7 +51,7 @@ class Decoder:
         ent.ent_entropy_temperature(self.ctx, B, logits, ld, h_prev, tau, temp, h, temp_used,
                                     row_stats, stream)
         ent.ent_block_select(self.ctx, B, q, ksum, block_tables, ctx_lens, h, kept, n_kept,
-                             scores, theta, stream, kappa)
+                             scores, theta, stream, kappa, k_cache)
         ent.ent_sparse_paged_decode(self.ctx, B, q, k_cache, v_cache, block_tables, ctx_lens,
                                     kept, n_kept, out, lse, stream)
         ent.ent_sample(self.ctx, B, logits, ld, row_stats, temp_used, uniforms, tokens, stream)

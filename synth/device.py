@@ -25,7 +25,7 @@ def config_fields(w: Workload, p: Params, num_pool_blocks: int,
         scale=p.scale, eta=p.eta, h_target=p.h_target, t_min=p.t_min, t_max=p.t_max,
         eps_h=p.eps_h, h_min=p.h_min, kappa_min=p.kappa_min, b_min=p.b_min, log_v=p.log_v,
         estimator=p.estimator, est_k=p.est_k, t_cal=p.t_cal, rho_t=p.rho_t, dkappa=p.dkappa,
-        h_bias=p.h_bias)
+        h_bias=p.h_bias, scoring=p.scoring, keep_first=p.keep_first, keep_last=p.keep_last)
 
 
 def _tensor(a: np.ndarray, device):

@@ -60,6 +60,7 @@ class Report:
     band_exempt: int = 0
     max_att_err: float = 0.0
     max_h_err: float = 0.0
+    max_score_err: float = 0.0
 
     def fail(self, msg):
         self.failures.append(msg)
@@ -130,32 +131,46 @@ def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev,
             if nk != 0:
                 rep.fail(f"seq {s}: empty sequence kept {nk} blocks")
         else:
-            I_o, _, _ = OB.block_scores(qs, kbar_g, counts, params.scale)
+            if getattr(params, "scoring", 0) == 1:
+                I_o = OB.exact_token_scores(qs, K, block_size, params.scale)
+            else:
+                I_o, _, _ = OB.block_scores(qs, kbar_g, counts, params.scale)
             I_g = gpu.scores[s][:nb].astype(np.float32)
             serr = np.abs(I_g.astype(np.float64) - I_o)
+            rep.max_score_err = max(rep.max_score_err, float(serr.max(initial=0.0)))
             if np.any(serr > 1e-6 + 1e-4 * np.abs(I_o)):
                 rep.fail(f"seq {s}: block scores differ by {serr.max():.3g}")
-            _, theta_o = OB.select_blocks(I_o, k_o)
-            # GPU self-consistency, bit-exact on its own scores.
-            if k_o > 0:
-                theta_g_expect = np.sort(I_g)[::-1][k_o - 1]
+            forced = OB.forced_blocks(nb, getattr(params, "keep_first", 0),
+                                      getattr(params, "keep_last", 0))
+            _, theta_o = OB.select_blocks(I_o, k_o, forced)
+            k_eff = max(k_o, len(forced))
+            # GPU self-consistency, bit-exact on its own scores (forced blocks
+            # rank above every score).
+            rank_g = I_g.copy()
+            rank_g[forced] = np.float32(np.inf)
+            if k_eff > 0:
+                theta_g_expect = np.sort(rank_g)[::-1][k_eff - 1]
                 if np.float32(gpu.theta[s]) != theta_g_expect:
-                    rep.fail(f"seq {s}: GPU threshold {gpu.theta[s]} is not the k={k_o}-th "
+                    rep.fail(f"seq {s}: GPU threshold {gpu.theta[s]} is not the k={k_eff}-th "
                              f"largest GPU score {theta_g_expect}")
-                expect = np.nonzero(I_g >= np.float32(gpu.theta[s]))[0]
+                expect = np.nonzero(rank_g >= np.float32(gpu.theta[s]))[0]
                 if not np.array_equal(expect, kept_g):
                     rep.fail(f"seq {s}: GPU kept list is not its scores >= its threshold")
             elif nk != 0:
                 rep.fail(f"seq {s}: budget 0 but {nk} blocks kept")
             # Oracle band.
-            must = set(np.nonzero(I_o > theta_o + THETA_BAND)[0].tolist())
-            never = set(np.nonzero(I_o < theta_o - THETA_BAND)[0].tolist())
+            rank_o = I_o.copy()
+            rank_o[forced] = np.inf
+            with np.errstate(invalid="ignore"):
+                must = set(np.nonzero(rank_o > theta_o + THETA_BAND)[0].tolist()) | \
+                    set(forced.tolist())
+                never = set(np.nonzero(rank_o < theta_o - THETA_BAND)[0].tolist())
+                rep.band_exempt += int(np.sum(np.abs(rank_o - theta_o) <= THETA_BAND))
             kg = set(kept_g.tolist())
             if not must <= kg:
                 rep.fail(f"seq {s}: {len(must - kg)} blocks above the threshold band not kept")
             if kg & never:
                 rep.fail(f"seq {s}: {len(kg & never)} blocks below the threshold band kept")
-            rep.band_exempt += int(np.sum(np.abs(I_o - theta_o) <= THETA_BAND))
 
         # Stage 3: attention over the GPU's kept blocks.
         o_ref, lse_ref = OA.sparse_decode(qs, K, V, kept_g, block_size, params.scale)
