@@ -118,12 +118,27 @@ __device__ __forceinline__ int est_block_count(int v, EstShared& sh) {
   return r;
 }
 
+// One histogram update per active lane.  Lanes whose bin equals the first
+// active lane's bin add together (one atomic for all of them): equal keys
+// (ties) would otherwise serialise on one LDS address.
+__device__ __forceinline__ void est_hist_add(unsigned* hist, bool act, unsigned bin) {
+  const unsigned long long am = __ballot(act);
+  if (am == 0ull) return;
+  const int leader = __ffsll(static_cast<long long>(am)) - 1;
+  const unsigned lb = __builtin_amdgcn_readlane(bin, leader);
+  const bool same = act && bin == lb;
+  const unsigned long long sm = __ballot(same);
+  if ((threadIdx.x & 63) == leader) atomicAdd(&hist[lb], static_cast<unsigned>(__popcll(sm)));
+  if (act && !same) atomicAdd(&hist[bin], 1u);
+}
+
 // k-th largest among the keys >= lo of src (4 n4 keys); requires
 // 1 <= k <= their number.  n_gt receives how many of them lie strictly
 // above it.  Radix select over the bits in which those keys differ,
 // kEstDigit bits per pass from the top; every thread of the workgroup calls
 // it and takes part (the result does not depend on the workgroup size).
-template <class Src>
+// Ties: callers whose keys often repeat aggregate equal bins per wave.
+template <class Src, bool kTies = false>
 __device__ __forceinline__ unsigned est_kth_largest(const Src& src, int n4, unsigned lo, int k,
                                                     EstShared& sh, int& n_gt) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -171,8 +186,11 @@ __device__ __forceinline__ unsigned est_kth_largest(const Src& src, int n4, unsi
         const uint4 x = src.load4(i);
         const unsigned e[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (e[j] >= lo && (e[j] & mask) == prefix) atomicAdd(&sh.hist[(e[j] >> shift) & dmask], 1u);
+        for (int j = 0; j < 4; ++j) {
+          const bool act = e[j] >= lo && (e[j] & mask) == prefix;
+          if (kTies) est_hist_add(sh.hist, act, (e[j] >> shift) & dmask);
+          else if (act) atomicAdd(&sh.hist[(e[j] >> shift) & dmask], 1u);
+        }
       }
       __syncthreads();
       if (wave == 0) {

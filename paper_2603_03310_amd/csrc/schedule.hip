@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs a) {
   unsigned theta = 0u;
   int n_gt = 0;
   if (take > 0 && take < N)
-    theta = est_kth_largest(EstLdsKeys{keys}, N4 / 4, 1u, take, esh, n_gt);
+    theta = est_kth_largest<EstLdsKeys, true>(EstLdsKeys{keys}, N4 / 4, 1u, take, esh, n_gt);
   const int quota = take - n_gt;    // ties at theta to take, in index order
   const bool all = take == N;
   // Selected: key > theta, or key == theta among the first `quota` ties.
