@@ -150,9 +150,27 @@ __device__ __forceinline__ void split3(const float4& x0, const float4& x1, sbf16
 // every product is exact and only the fp32 accumulation rounds.  K-slot
 // (gq, e) of step ks is dim 32 ks + 4 gq + e for e < 4 and
 // 32 ks + 16 + 4 gq + (e - 4) for e >= 4, in both operands.
+// The B operand of head g's query heads for lane (r16, gq): slot 2 ks holds
+// dims 32 ks + 4 gq .. +3, slot 2 ks + 1 dims 32 ks + 16 + 4 gq .. +3.
+// Every load is issued at once, from a valid head's address (the padding
+// columns r16 >= G are zeroed where they are used, so nothing waits here).
+template <int D>
+__device__ __forceinline__ void score_q_load(const uint16_t* __restrict__ q, int b, int g, int Hkv,
+                                             int G, uint2 (&qv)[D / 16]) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, gq = lane >> 4;
+  const uint16_t* qh =
+      q + (static_cast<long long>(b) * Hkv * G + g * G + min(r16, G - 1)) * D + gq * 4;
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks) {
+    qv[2 * ks] = *reinterpret_cast<const uint2*>(qh + 32 * ks);
+    qv[2 * ks + 1] = *reinterpret_cast<const uint2*>(qh + 32 * ks + 16);
+  }
+}
+
 template <int D>
 __device__ __forceinline__ void score_head_compute(
-    const uint16_t* __restrict__ q, const float4 (&buf)[kScoreSlots],
+    const uint2 (&qv)[D / 16], const float4 (&buf)[kScoreSlots],
     float* __restrict__ zbuf, float* __restrict__ lse_part, int b, int ch, int g, int N, int nb,
     int Hkv, int G, int MAXB, int nch_max, float scale) {
   constexpr int KS = D / 32;
@@ -160,15 +178,11 @@ __device__ __forceinline__ void score_head_compute(
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, gq = lane >> 4;
   const int jt = ch * kMfmaChunk;
-  const uint16_t* qh = q + (static_cast<long long>(b) * Hq + g * G + r16) * D + gq * 4;
   sf32x4_t acc = sf32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
-    uint2 q0 = make_uint2(0u, 0u), q1 = make_uint2(0u, 0u);
-    if (r16 < G) {
-      q0 = *reinterpret_cast<const uint2*>(qh + 32 * ks);
-      q1 = *reinterpret_cast<const uint2*>(qh + 32 * ks + 16);
-    }
+    const uint2 zero = make_uint2(0u, 0u);
+    const uint2 q0 = r16 < G ? qv[2 * ks] : zero, q1 = r16 < G ? qv[2 * ks + 1] : zero;
     sbf16x8_t hi, mid, lo;
     split3(buf[2 * ks], buf[2 * ks + 1], hi, mid, lo);
     const sbf16x8_t bq = __builtin_bit_cast(sbf16x8_t, make_uint4(q0.x, q0.y, q1.x, q1.y));

@@ -60,28 +60,31 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return r;
 }
 
-// The thread's 16 logits of chunk c, scaled to log2 units: t = z * c2.
-// Positions past the vocabulary read as -inf (zero probability).
+// The thread's 16 logits of chunk c (unscaled).  Positions past the
+// vocabulary read as -inf (zero probability).
 template <bool VEC>
 __device__ __forceinline__ void load_chunk(const float* __restrict__ row, int V, int c,
-                                           float c2, float (&v)[kPerThread]) {
+                                           float (&v)[kPerThread]) {
   const int base = c * kRowChunk;
   if (VEC && base + kRowChunk <= V) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float4 x = *reinterpret_cast<const float4*>(row + base + (i * kChunkThreads + threadIdx.x) * 4);
-      v[4 * i + 0] = x.x * c2;
-      v[4 * i + 1] = x.y * c2;
-      v[4 * i + 2] = x.z * c2;
-      v[4 * i + 3] = x.w * c2;
+      v[4 * i + 0] = x.x;
+      v[4 * i + 1] = x.y;
+      v[4 * i + 2] = x.z;
+      v[4 * i + 3] = x.w;
     }
   } else {
+    // Ragged or unaligned: every load from an index clamped into the row,
+    // so all sixteen are in flight together (no branch per load).
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const int idx = base + (i * kChunkThreads + threadIdx.x) * 4 + k;
-        v[4 * i + k] = idx < V ? row[idx] * c2 : -INFINITY;
+        const float x = row[min(idx, V - 1)];
+        v[4 * i + k] = idx < V ? x : -INFINITY;
       }
   }
 }
@@ -98,11 +101,15 @@ __device__ __forceinline__ void entropy_chunk_body(const float* __restrict__ log
                                                    float* __restrict__ tmax, int c, int b,
                                                    float* red) {
   static_assert(kChunkThreads == kEstChunkThreads, "thread maxima per chunk");
-  const float T = temp[b] * t_cal;          // effective temperature (calibration wrapper)
-  const float c2 = __fdiv_rn(kLog2e, T);
   const float* row = logits + static_cast<long long>(b) * ld;
   float v[kPerThread];
-  load_chunk<VEC>(row, V, c, c2, v);
+  load_chunk<VEC>(row, V, c, v);
+  // The logits are in flight before the temperature is waited for.
+  __builtin_amdgcn_sched_barrier(0);
+  const float T = temp[b] * t_cal;          // effective temperature (calibration wrapper)
+  const float c2 = __fdiv_rn(kLog2e, T);
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) v[i] *= c2;   // log2 units: t = z * c2
   float m = v[0];
 #pragma unroll
   for (int i = 1; i < kPerThread; ++i) m = fmaxf(m, v[i]);
@@ -283,8 +290,10 @@ __device__ __forceinline__ int sample_body(const float* __restrict__ logits, lon
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < kPerThread; ++i)
-      e[i] = (base + i < V) ? exp2f(row[base + i] * c2 - M) : 0.f;
+    for (int i = 0; i < kPerThread; ++i) {
+      const float x = row[min(base + i, V - 1)];   // clamped: loads issue together
+      e[i] = (base + i < V) ? exp2f(x * c2 - M) : 0.f;
+    }
   }
   double local = 0.0;
   int lastpos = -1;

@@ -374,7 +374,8 @@ __device__ __forceinline__ float row_estimate(int est, int k, const float* __res
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const int pos = base + i * kEstChunkThreads * 4 + kk;
-        const float v = pos < V ? row[pos] * c2 : -INFINITY;
+        const float x = row[min(pos, V - 1)];   // clamped: loads issue together
+        const float v = pos < V ? x * c2 : -INFINITY;
         keys[q * 16 + 4 * i + kk] = est_key(v);
       }
   }

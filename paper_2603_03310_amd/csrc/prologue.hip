@@ -84,7 +84,11 @@ __device__ __forceinline__ void score_job(const PrologueArgs& a, int b, int ch, 
   const int p = score_tile_check(entry, ch, nb, a.P, a.flags);
   float4 buf[kScoreSlots];
   score_head_load<D>(a.ksum, p, a.Hkv, g, buf);
-  score_head_compute<D>(a.q, buf, a.zbuf, a.lse_part, b, ch, g, N, nb, a.Hkv, a.G, a.MAXB,
+  uint2 qv[D / 16];
+  score_q_load<D>(a.q, b, g, a.Hkv, a.G, qv);
+  // Every load above is issued before any arithmetic: one memory round trip.
+  __builtin_amdgcn_sched_barrier(0);
+  score_head_compute<D>(qv, buf, a.zbuf, a.lse_part, b, ch, g, N, nb, a.Hkv, a.G, a.MAXB,
                         a.nch_max, a.scale);
 }
 
