@@ -254,7 +254,8 @@ int ent_sample(ent_ctx* c, int B, const float* logits, long long ld, const float
  * block scoring share one launch; the per-sequence entropy, controller and
  * selection share a second; decode attention follows, and sampling shares
  * the launch that merges the split attention segments.  In the exact
- * scoring mode the step is the four staged calls in order.
+ * scoring mode the step is the four staged calls in order and ksum may be
+ * NULL.
  * Arguments as in those calls: st is updated in place (tau, h_prev, temp
  * for the next step); h_out, temp_used, tokens: [B]; kept, n_kept, out as
  * in ent_sparse_paged_decode; row_stats, lse, scores, theta nullable.
@@ -271,7 +272,8 @@ int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_st
  * write k_new[b, g, :] to k_cache[p, g, N%16, :] and v_new[b, g, :] to
  * v_cache[p, g, :, N%16], recompute ksum[p, g, :] over the block's N%16 + 1
  * valid slots (bit-identical to ent_block_summary), and set ctx_lens[b] = N+1.
- * k_new, v_new: [B, H_kv, d] (kv_dtype). */
+ * k_new, v_new: [B, H_kv, d] (kv_dtype).  ksum may be NULL in the exact
+ * scoring mode, which does not read summaries (then none is maintained). */
 int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new,
                   const int* block_tables, int* ctx_lens, void* k_cache, void* v_cache,
                   float* ksum, void* stream);

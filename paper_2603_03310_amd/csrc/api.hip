@@ -350,10 +350,20 @@ int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_st
   if (!c) return ENT_E_INVAL;
   if (int r = check_batch(c, B)) return r;
   if (B == 0) return ENT_OK;
-  if (c->cfg.scoring == ENT_SCORE_EXACT) {
-    // The conservative scoring mode: the staged calls in order.
-    if (!logits || !uniforms || !out || !tokens || !v_cache)
-      return fail(c, ENT_E_INVAL, "ent_decode_step: NULL required pointer");
+  const bool exact = c->cfg.scoring == ENT_SCORE_EXACT;   // ksum unused in exact mode
+  if (!logits || !st.h_prev || !st.tau || !st.temp || !q || !k_cache || !v_cache ||
+      (!exact && !ksum) || !block_tables || !ctx_lens || !uniforms || !h_out || !temp_used ||
+      !kept || !n_kept || !out || !tokens)
+    return fail(c, ENT_E_INVAL, "ent_decode_step: NULL required pointer");
+  if (ld < c->cfg.vocab) return fail(c, ENT_E_INVAL, "ent_decode_step: ld < vocab");
+  if (h_out == st.h_prev) return fail(c, ENT_E_INVAL, "ent_decode_step: h_out aliases h_prev");
+  if (temp_used == st.temp) return fail(c, ENT_E_INVAL, "ent_decode_step: temp_used aliases temp");
+  if (!aligned(q, 16) || (!exact && !aligned(ksum, 16)) || !aligned(k_cache, 16) ||
+      !aligned(v_cache, 16) || !aligned(out, 16))
+    return fail(c, ENT_E_INVAL, "ent_decode_step: q, ksum, caches and out need 16-byte alignment");
+  if (exact) {
+    // The conservative scoring mode: the staged calls in order (every
+    // argument they check was checked above, so none fails part-way).
     if (int r = ent_entropy_temperature(c, B, logits, ld, st, h_out, temp_used, row_stats, stream))
       return r;
     if (int r = ent_block_select(c, B, q, ksum, k_cache, block_tables, ctx_lens, h_out, kept,
@@ -364,16 +374,6 @@ int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_st
       return r;
     return ent_sample(c, B, logits, ld, row_stats, temp_used, uniforms, tokens, stream);
   }
-  if (!logits || !st.h_prev || !st.tau || !st.temp || !q || !k_cache || !v_cache || !ksum ||
-      !block_tables || !ctx_lens || !uniforms || !h_out || !temp_used || !kept || !n_kept ||
-      !out || !tokens)
-    return fail(c, ENT_E_INVAL, "ent_decode_step: NULL required pointer");
-  if (ld < c->cfg.vocab) return fail(c, ENT_E_INVAL, "ent_decode_step: ld < vocab");
-  if (h_out == st.h_prev) return fail(c, ENT_E_INVAL, "ent_decode_step: h_out aliases h_prev");
-  if (temp_used == st.temp) return fail(c, ENT_E_INVAL, "ent_decode_step: temp_used aliases temp");
-  if (!aligned(q, 16) || !aligned(ksum, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
-      !aligned(out, 16))
-    return fail(c, ENT_E_INVAL, "ent_decode_step: q, ksum, caches and out need 16-byte alignment");
   const hipError_t e = ent::launch_decode_step(c, B, logits, ld, st, q, k_cache, v_cache, ksum,
                                                block_tables, ctx_lens, uniforms, h_out,
                                                temp_used, row_stats, kept, n_kept, out, lse,
@@ -389,7 +389,8 @@ int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new, const
   if (!c) return ENT_E_INVAL;
   if (int r = check_batch(c, B)) return r;
   if (B == 0) return ENT_OK;
-  if (!k_new || !v_new || !block_tables || !ctx_lens || !k_cache || !v_cache || !ksum)
+  if (!k_new || !v_new || !block_tables || !ctx_lens || !k_cache || !v_cache ||
+      (!ksum && c->cfg.scoring != ENT_SCORE_EXACT))
     return fail(c, ENT_E_INVAL, "ent_kv_append: NULL required pointer");
   const hipError_t e = ent::launch_kv_append(c, B, k_new, v_new, block_tables, ctx_lens, k_cache,
                                              v_cache, ksum, static_cast<hipStream_t>(stream));

@@ -91,8 +91,9 @@ __global__ __launch_bounds__(kThreads) void append_kernel(
     const T kv = k_new[src];
     kc[tile + slot * D + dd] = kv;
     vc[tile + dd * kBlock + slot] = v_new[src];
-    ksum[(static_cast<long long>(p) * Hkv + g) * D + dd] =
-        block_mean<T>(kc, tile, D, dd, slot + 1, load_elem<T>(&kv));
+    if (ksum)
+      ksum[(static_cast<long long>(p) * Hkv + g) * D + dd] =
+          block_mean<T>(kc, tile, D, dd, slot + 1, load_elem<T>(&kv));
   }
   __syncthreads();
   if (threadIdx.x == 0) ctx_lens[b] = N + 1;

@@ -37,7 +37,8 @@ def test_default_config_is_valid_and_checks_reject_bad_ones():
            ("log_v", 1.0, ent.ENT_E_INVAL), ("kappa_min", 1.5, ent.ENT_E_INVAL),
            ("max_batch", 0, ent.ENT_E_INVAL), ("max_blocks_per_seq", 20000, ent.ENT_E_UNSUPPORTED),
            ("vocab", 2_000_000, ent.ENT_E_UNSUPPORTED), ("kv_dtype", 7, ent.ENT_E_INVAL),
-           ("estimator", 3, ent.ENT_E_INVAL)]
+           ("estimator", 3, ent.ENT_E_INVAL), ("scoring", 2, ent.ENT_E_INVAL),
+           ("keep_first", -1, ent.ENT_E_INVAL), ("keep_last", -2, ent.ENT_E_INVAL)]
     for field, val, code in bad:
         c = ent.ent_default_config()
         c.num_pool_blocks = 100
