@@ -47,13 +47,17 @@ constexpr int kEstBins = 1 << kEstDigit;
 constexpr int kEstMaxRuns = kMaxChunks * kEstChunkThreads / 64;   // runs of 64 maxima
 static_assert(kEstMaxRuns <= kEstBins, "run counts reuse the histogram");
 
+constexpr int kEstRankMax = 64;    // prefix groups this small are finished by counting ranks
+static_assert(kEstRankMax <= kEstBins, "candidates reuse the histogram");
+
 struct EstShared {
-  alignas(16) unsigned hist[kEstBins];   // radix histogram, then the qualifying-run offsets
+  alignas(16) unsigned hist[kEstBins];   // radix histogram, then candidates or run offsets
   unsigned red[2 * kEstMaxWaves];
   float fred[2 * kEstWaves];
   int ired[kEstMaxWaves];
   float M, S;
-  int digit, krem, nq;
+  int digit, krem, nq, ncand, rgt;
+  unsigned rv;
 };
 
 __device__ __forceinline__ unsigned est_key(float f) {
@@ -135,9 +139,12 @@ __device__ __forceinline__ void est_hist_add(unsigned* hist, bool act, unsigned 
 // k-th largest among the keys >= lo of src (4 n4 keys); requires
 // 1 <= k <= their number.  n_gt receives how many of them lie strictly
 // above it.  Radix select over the bits in which those keys differ,
-// kEstDigit bits per pass from the top; every thread of the workgroup calls
-// it and takes part (the result does not depend on the workgroup size).
-// Ties: callers whose keys often repeat aggregate equal bins per wave.
+// kEstDigit bits per pass from the top; once the keys that share the
+// selected prefix are few (at most kEstRankMax) they are gathered into LDS
+// and the answer is found among them by counting ranks, instead of further
+// passes over every key.  Every thread of the workgroup calls it and takes
+// part (the result does not depend on the workgroup size).  Ties: callers
+// whose keys often repeat aggregate equal bins per wave.
 template <class Src, bool kTies = false>
 __device__ __forceinline__ unsigned est_kth_largest(const Src& src, int n4, unsigned lo, int k,
                                                     EstShared& sh, int& n_gt) {
@@ -234,6 +241,43 @@ __device__ __forceinline__ unsigned est_kth_largest(const Src& src, int n4, unsi
       __syncthreads();
       prefix |= static_cast<unsigned>(sh.digit) << shift;
       mask |= dmask << shift;
+      const int c = static_cast<int>(sh.hist[sh.digit]);   // keys sharing the new prefix
+      const int krem = sh.krem;
+      __syncthreads();                       // every thread has read both before reuse
+      if (shift > 0 && c <= kEstRankMax) {
+        // The krem-th largest of those c keys: gather them (any order),
+        // then each counts the keys above it and at or above it.
+        if (t == 0) sh.ncand = 0;
+        __syncthreads();
+        unsigned* cand = sh.hist;
+#pragma unroll 4
+        for (int i = t; i < n4; i += NT) {
+          const uint4 x = src.load4(i);
+          const unsigned e[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (e[j] >= lo && (e[j] & mask) == prefix) cand[atomicAdd(&sh.ncand, 1)] = e[j];
+        }
+        __syncthreads();
+        for (int i = t; i < c; i += NT) {
+          const unsigned v = cand[i];
+          int gt = 0, ge = 0;
+          for (int j = 0; j < c; ++j) {
+            const unsigned x = cand[j];
+            gt += x > v;
+            ge += x >= v;
+          }
+          if (gt < krem && ge >= krem) {     // equal keys write the same values
+            sh.rv = v;
+            sh.rgt = gt;
+          }
+        }
+        __syncthreads();
+        n_gt = k - krem + sh.rgt;
+        const unsigned r = sh.rv;
+        __syncthreads();
+        return r;
+      }
     }
   }
   n_gt = k - sh.krem;
