@@ -442,11 +442,14 @@ __device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
   if (j < nb && (t & 3) == 0) scores[static_cast<long long>(b) * MAXB + j] = I;
 }
 
+constexpr int kSelRankMax = 64;    // prefix groups this small are finished by counting ranks
+
 struct SelectShared {
-  unsigned hist[256];
+  unsigned hist[256];                // radix histogram, then the last candidates
   unsigned red[2 * kSelWaves];
   float pm[kRowThreads], ps[kRowThreads], L[128];
-  int digit, krem, wcnt[kSelWaves];
+  int digit, krem, ncand, wcnt[kSelWaves];
+  unsigned rv;
 };
 
 // Physical block p of logical block j (of nb) for the decode's unit lists:
@@ -487,7 +490,9 @@ __device__ __forceinline__ void select_core(unsigned* keys, const int* tbl, int 
     kmax = max(kmax, sh.red[kSelWaves + w]);
   }
   // Radix select of the k-th largest key over the differing bits, 8 at a
-  // time from the top (the common leading bits are the prefix already).
+  // time from the top (the common leading bits are the prefix already);
+  // once at most kSelRankMax keys share the prefix, the answer is found
+  // among them by counting ranks.
   const unsigned diff = kmin ^ kmax;
   const int top = diff ? 31 - __clz(diff) : -1;    // highest differing bit
   unsigned mask = diff ? ~((2u << top) - 1u) : 0xFFFFFFFFu;
@@ -536,7 +541,31 @@ __device__ __forceinline__ void select_core(unsigned* keys, const int* tbl, int 
     __syncthreads();
     prefix |= static_cast<unsigned>(sh.digit) << shift;
     mask |= dmask << shift;
-    __syncthreads();
+    const int c = static_cast<int>(sh.hist[sh.digit]);   // keys sharing the new prefix
+    const int krem = sh.krem;
+    __syncthreads();                       // every thread has read both before reuse
+    if (shift > 0 && c <= kSelRankMax) {
+      if (t == 0) sh.ncand = 0;
+      __syncthreads();
+      for (int i = t; i < nb; i += kSelThreads) {
+        const unsigned key = keys[i];
+        if ((key & mask) == prefix) sh.hist[atomicAdd(&sh.ncand, 1)] = key;
+      }
+      __syncthreads();
+      if (t < c) {
+        const unsigned v = sh.hist[t];
+        int gt = 0, ge = 0;
+        for (int j = 0; j < c; ++j) {
+          const unsigned x = sh.hist[j];
+          gt += x > v;
+          ge += x >= v;
+        }
+        if (gt < krem && ge >= krem) sh.rv = v;   // equal keys write the same value
+      }
+      __syncthreads();
+      prefix = sh.rv;
+      break;
+    }
   }
   const unsigned tkey = prefix;
 
