@@ -155,6 +155,111 @@ def sched_time(ent, torch, ctx, sp, b_sel, K, W):
     return {"pool": n, "b_sel": b_sel, "avg_launch_us": round(e0.elapsed_time(e1) / K * 1e3, 2)}
 
 
+def closed_loop(args, w, p):
+    """A closed-loop workload: every step is ent_decode_step then
+    ent_kv_append (the new token's K/V), the controller state and the
+    kept-fraction state carried on the device.  The timed region is
+    min(--steps, the workload's steps) consecutive steps after --warmup
+    steps and a reset of the lengths and state; a second, untimed pass over
+    the same steps (the same results: the loop is deterministic) records the
+    kept lists for the byte count."""
+    import numpy as np
+    import torch
+
+    from paper_2603_03310_amd import ent
+    from synth import generate
+    from synth.device import config_fields, upload
+
+    t0 = time.perf_counter()
+    x = generate(w)
+    print(f"[bench] generated {w.name} ({w.steps} steps) in {time.perf_counter() - t0:.1f} s",
+          file=sys.stderr, flush=True)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    d = upload(x, dev)
+    B = w.batch
+    K = min(args.steps, w.steps)
+    W = min(args.warmup, w.steps)
+    cfg = ent.ent_config()
+    for k, v in config_fields(w, p, x.num_pool_blocks).items():
+        setattr(cfg, k, v)
+    ctx = ent.ent_init(cfg)
+    sp = torch.cuda.current_stream().cuda_stream
+    ent.ent_block_summary(ctx, B, d.k_pool, d.block_tables, d.ctx_lens, d.ksum, sp)
+    ld = x.logits.shape[2]
+    init = [torch.from_numpy(a).to(dev) for a in (x.h_prev, x.tau, x.temp, x.ctx_lens)]
+
+    def reset():
+        for dst, src in zip((d.h_prev, d.tau, d.temp, d.ctx_lens), init):
+            dst.copy_(src)
+        d.kappa.fill_(float("nan"))
+
+    def step(t):
+        ent.ent_decode_step(ctx, B, d.logits[t], ld, d.h_prev, d.tau, d.temp, d.q[t], d.k_pool,
+                            d.v_pool, d.ksum, d.block_tables, d.ctx_lens, d.uniforms[t], d.h,
+                            d.temp_used, d.kept, d.n_kept, d.out, d.tokens, d.row_stats, d.lse,
+                            None, None, sp, d.kappa)
+        ent.ent_kv_append(ctx, B, d.k_new[t], d.v_new[t], d.block_tables, d.ctx_lens, d.k_pool,
+                          d.v_pool, d.ksum, sp)
+
+    for t in range(W):
+        step(t)
+    torch.cuda.synchronize()
+    reset()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for t in range(K):
+        step(t)
+    e1.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    ms_step = e0.elapsed_time(e1) / K
+    flags = ent.ent_device_status(ctx, sp)
+    if flags:
+        raise SystemExit(f"device flags raised: {flags}")
+    # Untimed pass: the kept lists of every step (for the bytes moved).
+    reset()
+    elem = 2 if w.kv_dtype == "bf16" else 4
+    kv_kept, blocks_kept, blocks_all = 0, 0, 0
+    xs = type("X", (), {})()
+    xs.workload = w
+    for t in range(K):
+        step(t)
+        torch.cuda.synchronize()
+        xs.ctx_lens = x.ctx_lens + t
+        nk, kp = d.n_kept.cpu().numpy(), d.kept.cpu().numpy()
+        kv_kept += kv_bytes_kept(xs, nk, kp, elem)
+        blocks_kept += int(nk.sum())
+        blocks_all += int(sum(-(-int(n) // 16) for n in xs.ctx_lens))
+    ent.ent_destroy(ctx)
+    metric_bytes = kv_kept / K + 4 * B * w.vocab
+    gbps = metric_bytes / (ms_step * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(x, p, args.cpu_seconds)
+    line = {
+        "metric": METRIC, "value": round(1e3 / ms_step, 3), "unit": "steps/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; shapes and value recipes of the workload)",
+        "config": {"workload": w.name, "batch": B, "q_heads": w.num_q_heads,
+                   "kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "block_size": 16,
+                   "ctx": list(w.ctx), "vocab": w.vocab, "kv_dtype": w.kv_dtype,
+                   "closed_loop_steps": K, "step": "ent_decode_step + ent_kv_append",
+                   "entropy": args.estimator},
+        "hbm_gbps_kept_kv_plus_logits": round(gbps, 1),
+        "hbm_frac_kept_kv_plus_logits": round(gbps / HBM_PEAK_GBPS, 4),
+        "metric_bytes_per_step": int(metric_bytes),
+        "kept_block_fraction": round(blocks_kept / max(1, blocks_all), 4),
+        "wall_ms_per_step": round(wall_ms / K, 5),
+        "roofline": None,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -170,8 +275,6 @@ def main():
 
     ent.load()
     w = WORKLOADS[args.workload]
-    if w.steps != 1:
-        raise SystemExit("bench.py times single decode steps; closed loops are parity cases")
     p = default_params(w)
     est = {"exact": 0, "topk": 1, "tail": 2}[args.estimator]
     if est:
@@ -180,6 +283,8 @@ def main():
         p = p.replace(eps_h=args.eps_h)
     p = p.replace(scoring=1 if args.scoring == "exact" else 0, keep_first=args.keep_first,
                   keep_last=args.keep_last)
+    if w.steps != 1:
+        return closed_loop(args, w, p)
     t0 = time.perf_counter()
     x = generate(w)
     print(f"[bench] generated {w.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
