@@ -87,6 +87,21 @@ def kv_bytes_kept(x, n_kept, kept, elem):
     return tot
 
 
+def total_bytes(w, ctx_lens, kv_kept, elem, scoring):
+    """Every byte the step must move (besides the metric's kept K/V and
+    logits): one logit chunk re-read per row by sampling, the block
+    summaries (mean-key scoring) or every valid key (exact scoring), the
+    queries and the attention outputs."""
+    B, V = w.batch, w.vocab
+    nb = sum(-(-int(n) // 16) for n in ctx_lens)
+    if scoring:
+        scores = int(sum(int(n) for n in ctx_lens)) * w.num_kv_heads * w.head_dim * elem
+    else:
+        scores = nb * w.num_kv_heads * w.head_dim * 4
+    return (4 * B * V + 4 * B * 4096 + scores + kv_kept
+            + B * w.num_q_heads * w.head_dim * (elem + 4))
+
+
 def cpu_baseline(x, p, seconds):
     """The float64 oracle on the host, single thread, over the step's sequences
     in order (cycling) for about `seconds`; scaled to whole steps per second."""
@@ -222,7 +237,7 @@ def closed_loop(args, w, p):
     # Untimed pass: the kept lists of every step (for the bytes moved).
     reset()
     elem = 2 if w.kv_dtype == "bf16" else 4
-    kv_kept, blocks_kept, blocks_all = 0, 0, 0
+    kv_kept, blocks_kept, blocks_all, all_bytes = 0, 0, 0, 0
     xs = type("X", (), {})()
     xs.workload = w
     for t in range(K):
@@ -230,7 +245,9 @@ def closed_loop(args, w, p):
         torch.cuda.synchronize()
         xs.ctx_lens = x.ctx_lens + t
         nk, kp = d.n_kept.cpu().numpy(), d.kept.cpu().numpy()
-        kv_kept += kv_bytes_kept(xs, nk, kp, elem)
+        kv_step = kv_bytes_kept(xs, nk, kp, elem)
+        kv_kept += kv_step
+        all_bytes += total_bytes(w, xs.ctx_lens, kv_step, elem, p.scoring)
         blocks_kept += int(nk.sum())
         blocks_all += int(sum(-(-int(n) // 16) for n in xs.ctx_lens))
     ent.ent_destroy(ctx)
@@ -252,6 +269,9 @@ def closed_loop(args, w, p):
         "hbm_gbps_kept_kv_plus_logits": round(gbps, 1),
         "hbm_frac_kept_kv_plus_logits": round(gbps / HBM_PEAK_GBPS, 4),
         "metric_bytes_per_step": int(metric_bytes),
+        "total_bytes_per_step": int(all_bytes / K),
+        "hbm_gbps_total": round(all_bytes / K / (ms_step * 1e-3) / 1e9, 1),
+        "hbm_frac_total": round(all_bytes / K / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "kept_block_fraction": round(blocks_kept / max(1, blocks_all), 4),
         "wall_ms_per_step": round(wall_ms / K, 5),
         "roofline": None,
@@ -401,6 +421,7 @@ def main():
     kv_kept = kv_bytes_kept(x, n_kept, kept, elem)
     logit_bytes = 4 * B * w.vocab
     metric_bytes = kv_kept + logit_bytes
+    all_bytes = total_bytes(w, x.ctx_lens, kv_kept, elem, p.scoring)
     nb_tot = int(sum(-(-int(n) // 16) for n in x.ctx_lens))
     kept_frac = float(n_kept.sum()) / max(1, nb_tot)
     steps_per_s = 1e3 / ms_step
@@ -433,6 +454,9 @@ def main():
         "hbm_gbps_kept_kv_plus_logits": round(gbps, 1),
         "hbm_frac_kept_kv_plus_logits": round(gbps / HBM_PEAK_GBPS, 4),
         "metric_bytes_per_step": int(metric_bytes),
+        "total_bytes_per_step": int(all_bytes),
+        "hbm_gbps_total": round(all_bytes / (ms_step * 1e-3) / 1e9, 1),
+        "hbm_frac_total": round(all_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "kept_block_fraction": round(kept_frac, 4),
         "per_stage_us": {k: round(v, 2) for k, v in per_k.items()},
         "staged_ms_per_step": round(sum(per_k.values()) * 1e-3, 5),
