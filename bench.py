@@ -102,27 +102,53 @@ def total_bytes(w, ctx_lens, kv_kept, elem, scoring):
             + B * w.num_q_heads * w.head_dim * (elem + 4))
 
 
-def cpu_baseline(x, p, seconds):
-    """The float64 oracle on the host, single thread, over the step's sequences
-    in order (cycling) for about `seconds`; scaled to whole steps per second."""
+_BASE = None   # (inputs, params) of the CPU baseline, shared with forked workers
+
+
+def _oracle_worker(args):
+    """Sequence-steps of the oracle on sequences start, start + stride, ...
+    for about `seconds` (one thread); returns how many ran and the time."""
+    start, stride, seconds = args
+    x, p = _BASE
     from threadpoolctl import threadpool_limits
 
     from oracle import step as St
     B = x.workload.batch
-    done = 0
+    done, s = 0, start
     t0 = time.perf_counter()
     with threadpool_limits(limits=1):
         while done == 0 or time.perf_counter() - t0 < seconds:
-            St.sequence_step(done % B, k_pool=x.k_pool, v_pool=x.v_pool, tables=x.block_tables,
+            St.sequence_step(s % B, k_pool=x.k_pool, v_pool=x.v_pool, tables=x.block_tables,
                              ctx_lens=x.ctx_lens, q=x.q[0], logits=x.logits[0], h_prev=x.h_prev,
                              tau=x.tau, temp=x.temp, uniforms=x.uniforms[0], params=p,
                              block_size=16)
             done += 1
-    el = time.perf_counter() - t0
-    return {"value": (done / B) / el, "unit": "steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"float64 oracle, all stages, {done} sequence-steps cycling over the {B} "
-                      f"sequences of one {x.workload.name} step ({el:.1f} s, one thread); "
-                      f"scaled to whole steps"}
+            s += stride
+    return done, time.perf_counter() - t0
+
+
+def cpu_baseline(x, p, seconds):
+    """The float64 oracle on the host, cycling over the step's sequences: one
+    process per core of the host (sequences split between them, one thread
+    each) for about `seconds`, then one thread alone for half of that; both
+    scaled to whole steps per second.  Runs before the GPU is initialised,
+    so the worker processes hold no device state."""
+    import multiprocessing as mp
+    global _BASE
+    _BASE = (x, p)         # inherited by the forked workers, not pickled
+    B = x.workload.batch
+    n = max(1, min(len(os.sched_getaffinity(0)), 16))
+    with mp.get_context("fork").Pool(n) as pool:
+        res = pool.map(_oracle_worker, [(i, n, seconds) for i in range(n)])
+    el = max(r[1] for r in res)
+    done = sum(r[0] for r in res)
+    one, el1 = _oracle_worker((0, 1, seconds / 2))
+    return {"value": (done / B) / el, "unit": "steps/s", "cores": n, "kind": "oracle",
+            "value_1core": (one / B) / el1,
+            "sample": f"float64 oracle, all stages: {done} sequence-steps of one "
+                      f"{x.workload.name} step in {el:.1f} s over {n} processes (one thread "
+                      f"each, sequences split between them), and {one} in {el1:.1f} s on one "
+                      f"thread (value_1core); scaled to whole steps"}
 
 
 def traffic_from_counters():
@@ -189,6 +215,11 @@ def closed_loop(args, w, p):
     x = generate(w)
     print(f"[bench] generated {w.name} ({w.steps} steps) in {time.perf_counter() - t0:.1f} s",
           file=sys.stderr, flush=True)
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(x, p, args.cpu_seconds)
+        print("[bench] cpu baseline done", file=sys.stderr, flush=True)
+    ent.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     d = upload(x, dev)
@@ -253,9 +284,6 @@ def closed_loop(args, w, p):
     ent.ent_destroy(ctx)
     metric_bytes = kv_kept / K + 4 * B * w.vocab
     gbps = metric_bytes / (ms_step * 1e-3) / 1e9
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(x, p, args.cpu_seconds)
     line = {
         "metric": METRIC, "value": round(1e3 / ms_step, 3), "unit": "steps/s", "n_gpus": 1,
         "steps": K, "warmup": W, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
@@ -293,7 +321,8 @@ def main():
     from synth import WORKLOADS, default_params, generate
     from synth.device import config_fields, upload
 
-    ent.load()
+    if not os.path.exists(ent.LIB_PATH):
+        ent.load()        # raises: the library has not been built (no fallback)
     w = WORKLOADS[args.workload]
     p = default_params(w)
     est = {"exact": 0, "topk": 1, "tail": 2}[args.estimator]
@@ -309,6 +338,11 @@ def main():
     x = generate(w)
     print(f"[bench] generated {w.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
           flush=True)
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(x, p, args.cpu_seconds)
+        print("[bench] cpu baseline done", file=sys.stderr, flush=True)
+    ent.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     copies = [upload(x, dev) for _ in range(max(1, args.copies))]
@@ -433,10 +467,6 @@ def main():
                  + 2 * 4 * int(n_kept.sum()) + 4 * B)
     achieved = dec_bytes / (dec_us * 1e-6) / 1e9
     ent.ent_destroy(ctx)
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(x, p, args.cpu_seconds)
 
     line = {
         "metric": METRIC, "value": round(steps_per_s, 3), "unit": "steps/s", "n_gpus": 1,
