@@ -188,7 +188,10 @@ __device__ __forceinline__ unsigned est_kth_largest(const Src& src, int n4, unsi
       const unsigned dmask = (1u << width) - 1u;
       for (int i = t; i < kEstBins; i += NT) sh.hist[i] = 0u;
       __syncthreads();
-#pragma unroll 4
+      // (The ballots of the tie-aware form are convergent: that loop cannot
+      // be unrolled over its run-time trip count.)
+      constexpr int kUnroll = kTies ? 1 : 4;
+#pragma unroll kUnroll
       for (int i = t; i < n4; i += NT) {
         const uint4 x = src.load4(i);
         const unsigned e[4] = {x.x, x.y, x.z, x.w};
