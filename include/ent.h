@@ -23,6 +23,9 @@
  *    ent_device_status reports.
  *  - A context is not thread-safe; calls that share a context must be ordered
  *    on one stream (the workspace is reused by every call).
+ *  - A context belongs to the HIP device current at ent_init; every call on it
+ *    must be made with that device current (else ENT_E_INVAL, nothing
+ *    launched).  ent_destroy accepts any current device.
  *  - Batch sizes: 0 <= B <= max_batch.  B == 0 launches nothing.
  *
  * Paged KV cache layout (block size 16 tokens, P = num_pool_blocks):

@@ -81,7 +81,18 @@ int hip_fail(ent_ctx* c, hipError_t e, const char* what) {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// Kernels of a context run on the device that was current at ent_init.
+int check_device(ent_ctx* c) {
+  int dev = -1;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(c, e, "hipGetDevice");
+  if (dev != c->device)
+    return fail(c, ENT_E_INVAL, "the current HIP device is not the context's (the one current at ent_init)");
+  return ENT_OK;
+}
+
 int check_batch(ent_ctx* c, int B) {
+  if (int r = check_device(c)) return r;
   if (B < 0 || B > c->cfg.max_batch)
     return fail(c, ENT_E_INVAL, "B must be in [0, max_batch]");
   return ENT_OK;
@@ -224,10 +235,16 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
 
 int ent_destroy(ent_ctx* c) {
   if (!c) return ENT_E_INVAL;
-  hipError_t e = hipDeviceSynchronize();
+  // The context's device is synchronised and freed on, whichever is current.
+  int cur = -1;
+  hipError_t e = hipGetDevice(&cur);
+  const bool other = e == hipSuccess && cur != c->device;
+  if (other) e = hipSetDevice(c->device);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
   const hipError_t e2 = hipFree(c->ws);
+  const hipError_t e3 = other ? hipSetDevice(cur) : hipSuccess;
   delete c;
-  return (e == hipSuccess && e2 == hipSuccess) ? ENT_OK : ENT_E_HIP;
+  return (e == hipSuccess && e2 == hipSuccess && e3 == hipSuccess) ? ENT_OK : ENT_E_HIP;
 }
 
 const char* ent_last_error(const ent_ctx* c) {
@@ -236,6 +253,7 @@ const char* ent_last_error(const ent_ctx* c) {
 
 int ent_device_status(ent_ctx* c, void* stream, unsigned* flags) {
   if (!c || !flags) return c ? fail(c, ENT_E_INVAL, "flags is NULL") : ENT_E_INVAL;
+  if (int r = check_device(c)) return r;
   hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(c, e, "stream synchronise");
   unsigned v = 0;
@@ -363,8 +381,10 @@ int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_st
     return fail(c, ENT_E_INVAL, "ent_decode_step: q, ksum, caches and out need 16-byte alignment");
   if (exact) {
     // The conservative scoring mode: the staged calls in order (every
-    // argument they check was checked above, so none fails part-way).
-    if (int r = ent_entropy_temperature(c, B, logits, ld, st, h_out, temp_used, row_stats, stream))
+    // argument they check was checked above, so none fails part-way).  The
+    // sampler reuses the entropy pass's row statistics.
+    float* stats = row_stats ? row_stats : c->stats_tmp;
+    if (int r = ent_entropy_temperature(c, B, logits, ld, st, h_out, temp_used, stats, stream))
       return r;
     if (int r = ent_block_select(c, B, q, ksum, k_cache, block_tables, ctx_lens, h_out, kept,
                                  n_kept, scores, theta, st.kappa, stream))
@@ -372,7 +392,7 @@ int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_st
     if (int r = ent_sparse_paged_decode(c, B, q, k_cache, v_cache, block_tables, ctx_lens, kept,
                                         n_kept, out, lse, stream))
       return r;
-    return ent_sample(c, B, logits, ld, row_stats, temp_used, uniforms, tokens, stream);
+    return ent_sample(c, B, logits, ld, stats, temp_used, uniforms, tokens, stream);
   }
   const hipError_t e = ent::launch_decode_step(c, B, logits, ld, st, q, k_cache, v_cache, ksum,
                                                block_tables, ctx_lens, uniforms, h_out,
@@ -403,6 +423,7 @@ int ent_schedule(ent_ctx* c, int N, const ent_sched_params* prm, const float* ta
                  const int* n_kept, const int* ctx_lens, float* tau_last, float* gain, int* age,
                  int b_sel, int* selected, int* n_selected, float* priority, void* stream) {
   if (!c) return ENT_E_INVAL;
+  if (int r = check_device(c)) return r;
   if (N < 0 || N > ENT_SCHED_MAX_POOL)
     return fail(c, ENT_E_INVAL, "ent_schedule: N must be in [0, ENT_SCHED_MAX_POOL]");
   if (!prm) return fail(c, ENT_E_INVAL, "ent_schedule: params is NULL");
