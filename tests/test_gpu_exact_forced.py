@@ -2,8 +2,9 @@
 (Section 3.2 block contributions from the exact attention weights; forced
 first and last blocks) through the C ABI, against the float64 oracle.
 Exact mode: bf16 (MFMA) and fp32 (VALU) caches, short and long block tables
-(one- and three-launch selections), ragged and one-token blocks, a closed
-loop with appends, and the staged calls against the one-call step.  Forced
+(one- and three-launch selections), ragged and one-token blocks, the full
+long-context batch on sampled sequences, a closed loop with appends, and the
+staged calls against the one-call step.  Forced
 keeps: mean-key and exact modes, forced sets that fill the budget, both
 selection forms.
 """
@@ -36,6 +37,18 @@ def test_exact_scoring(torch_cuda, w, fused):
     p = default_params(w).replace(scoring=1)
     reps, _ = _run(torch_cuda, x, p, fused=fused)
     _report(reps, w.name)
+    _assert_ok(reps)
+
+
+def test_exact_full_size_long_context_sampled(torch_cuda):
+    """The full long-context batch in exact mode (B=16, N up to 131072: up to
+    512 tiles of 16 blocks per sequence, every key of 2.5 GB of K read once),
+    parity on three sampled sequences."""
+    x = generate(LONG_CONTEXT)
+    seqs = sorted(np.random.default_rng(5).choice(LONG_CONTEXT.batch, size=3, replace=False).tolist())
+    print(f"[exact] full-size long_context, sampled sequences {seqs}", flush=True)
+    reps, _ = _run(torch_cuda, x, default_params(LONG_CONTEXT).replace(scoring=1), seqs=seqs)
+    _report(reps, "long_context full")
     _assert_ok(reps)
 
 
