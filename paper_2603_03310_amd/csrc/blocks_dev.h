@@ -78,8 +78,8 @@ __device__ __forceinline__ void chunk_lse(const float* zt, int nblk, int Hq, int
 }
 
 // One scoring item: a tile of kMfmaChunk = 16 blocks of sequence b (tile
-// ch) and one KV head g, by one wave: the summaries (16 blocks x d fp32) are
-// loaded with score_head_load and reduced with score_head_compute.
+// ch) and one KV head g, by one wave: the summaries (16 blocks x d fp32),
+// loaded by the prologue's score_job, are reduced with score_head_compute.
 constexpr int kScoreSlots = 8;          // float4 slots per lane (d <= 128)
 
 // Table entry of tile row r16 (lane & 15), read before the context length
@@ -102,20 +102,6 @@ __device__ __forceinline__ int score_tile_check(int p, int ch, int nb, int P, un
   return p;
 }
 
-
-// Lane (r16, gq) loads, for head g of block row r16, the float4 slots
-// j = 0 .. D/16 - 1 at dims 16 j + 4 gq .. +3 (the four lanes of a row read
-// 64 contiguous bytes per slot).
-template <int D>
-__device__ __forceinline__ void score_head_load(const float* __restrict__ ksum, int p, int Hkv,
-                                                int g, float4 (&buf)[kScoreSlots]) {
-  constexpr int NJ = D / 16;
-  static_assert(NJ <= kScoreSlots, "slots");
-  const int gq = (threadIdx.x & 63) >> 4;
-  const float* src = ksum + (static_cast<long long>(p) * Hkv + g) * D + gq * 4;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) buf[j] = *reinterpret_cast<const float4*>(src + 16 * j);
-}
 
 typedef float sf32x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 sbf16x2_t __attribute__((ext_vector_type(2)));
