@@ -191,7 +191,8 @@ __device__ __forceinline__ UnitMeta unit_meta(const DecodeArgs& a, int x, int u1
 // measured 8% faster on the decode than plain loads (the queries, read by
 // every wave of a segment, keep plain loads: 1 us better).  The same bit made
 // the exact scoring's K reads and the block-summary gather slower, and the
-// logit pass no faster, so it is used here only.
+// logit pass no faster, so it is used here only.  Whole-row K loads staged
+// through LDS measured 1-2% faster than loads straight into the MFMA layout.
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ bf16x8_t load_bf16x8(const uint16_t* p) {
@@ -214,6 +215,8 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   extern __shared__ __attribute__((aligned(16))) int s_mem[];
   __shared__ int s_red[kWaves];
   __shared__ int s_cseg[2 * kWaves];
+  // Each wave's K tile in the MFMA layout's source form, rows padded by 16 B.
+  __shared__ __attribute__((aligned(16))) uint16_t s_kst[kWaves * kBlock * (D + 8)];
   // Dynamic LDS: cut partials first (16-byte aligned), then the plan.
   float* s_cacc = reinterpret_cast<float*>(s_mem);
   float* s_cml = s_cacc + 2 * kWaves * a.G * D;
@@ -254,10 +257,10 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
     const int p = max(__shfl(win.p, i), 0);
     const int g = max(seg, 0) % a.Hkv;
     const long long tile = (static_cast<long long>(p) * a.Hkv + g) * kBlock * D;
-    // MFMA k-slot (gq, element e) of QK step ks holds dim ks*32 + gq*8 + e,
-    // for both operands.
+    // K: load ks covers the tile's bytes [ks, ks + 1) * 4 KB / KS whole (lane
+    // l its 16 bytes l), staged through LDS into the MFMA layout before use.
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kr[ks] = load_bf16x8_nt(kc + tile + r16 * D + ks * 32 + gq * 8);
+    for (int ks = 0; ks < KS; ++ks) kr[ks] = load_bf16x8_nt(kc + tile + ks * (kBlock * D / KS) + lane * 8);
 #pragma unroll
     for (int m = 0; m < MT; ++m) vr[m] = load_s16x4(vc + tile + (16 * m + r16) * kBlock + 4 * gq);
   };
@@ -347,10 +350,31 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
     const int p = __shfl(win.p, i);
     const int nv = __shfl(win.nv, i);
     if (p >= 0) {
+      // The K tile through the wave's LDS rows: written as loaded (whole
+      // rows per load), read back with lane (r16, gq) holding row r16, MFMA
+      // k-slot (gq, e) of step ks = dim 32 ks + 8 gq + e (the queries' slots
+      // too).  The rows are the wave's own, so wave-level barriers order the
+      // exchange (and the previous unit's reads before this unit's writes).
+      uint16_t* st = s_kst + wave * kBlock * (D + 8);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int e0 = ks * (kBlock * D / KS) + lane * 8;
+        *reinterpret_cast<bf16x8_t*>(st + (e0 / D) * (D + 8) + (e0 % D)) = kc[ks];
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      bf16x8_t kmf[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        kmf[ks] = *reinterpret_cast<const bf16x8_t*>(st + r16 * (D + 8) + ks * 32 + gq * 8);
       f32x4_t sacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc[ks], qreg[ks], sacc, 0, 0, 0);
+        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kmf[ks], qreg[ks], sacc, 0, 0, 0);
       float sc[4];
       bool up = false;
 #pragma unroll
