@@ -19,12 +19,15 @@
 //
 // bf16 path (MFMA, gfx950).  Per kept block of 16 tokens:
 //   S^T[16 tok x 16 heads] = K[16 x d] . Q^T[d x 16]   v_mfma_f32_16x16x32_bf16,
-//     A = K rows from the token-major K tile (16 B per lane per step),
+//     A = K rows from the token-major K tile (16 B per lane per step), the
+//         tile loaded 1 KB whole per instruction (non-temporal) and passed
+//         through the wave's LDS rows into this layout,
 //     B = the G query heads (zero-padded to 16 columns), held in registers;
 //   online softmax per head column (log2 domain, fp32); the cross-lane max is
 //   taken only when some score exceeds a head's running max;
 //   O^T[d x 16] += V^T[d x 16 tok] . P^T[16 tok x 16]   v_mfma_f32_16x16x16_bf16,
-//     A = rows of the dim-major V tile (8 B per lane per 16-dim tile),
+//     A = rows of the dim-major V tile (8 B per lane per 16-dim tile, each
+//         load instruction a whole 512 B span; non-temporal),
 //     B = P^T taken straight from the S^T accumulator registers, split into
 //         a bf16 high part and a bf16 remainder (two MFMAs), so P keeps
 //         about 16 bits.

@@ -34,6 +34,7 @@ constexpr int kExWaves = kExThreads / 64;
 constexpr int kExPerWave = kMfmaChunk / kExWaves;   // blocks per wave
 
 typedef __bf16 xbf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef unsigned u32x4nt_t __attribute__((ext_vector_type(4)));
 typedef float xf32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
 
 struct ExactArgs {
@@ -109,7 +110,9 @@ __global__ __launch_bounds__(kExThreads) void exact_score_bf16_kernel(ExactArgs 
   // = dim 32 ks + 8 gq + e) and the wave's K tiles, each load instruction
   // covering 1 KB of a tile whole (lane l its 16 bytes l): against loads
   // straight into the MFMA layout (64 B of each of the 16 token rows per
-  // instruction) the staged selection took 148 us against 153 us.
+  // instruction) the staged selection took 148 us against 153 us, and 135 us
+  // with the non-temporal bit on these loads (which made the same loads in
+  // the MFMA layout slower).
   xbf16x8_t qreg[KS];
   const long long qh = (static_cast<long long>(b) * Hq + g * G + r16) * D;
 #pragma unroll
@@ -124,7 +127,8 @@ __global__ __launch_bounds__(kExThreads) void exact_score_bf16_kernel(ExactArgs 
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       kr[i][ks] = __builtin_bit_cast(
-          xbf16x8_t, *reinterpret_cast<const uint4*>(kc + tile + ks * (kBlock * D / KS) + lane * 8));
+          xbf16x8_t, __builtin_nontemporal_load(
+                         reinterpret_cast<const u32x4nt_t*>(kc + tile + ks * (kBlock * D / KS) + lane * 8)));
   }
   uint16_t* st = s_kst + wave * kBlock * (D + 8);
   float run_m = -INFINITY, run_s = 0.f;
