@@ -193,7 +193,9 @@ int ent_entropy_temperature(ent_ctx* c, int B, const float* logits, long long ld
  * sequence b < B and logical block j < nb_b, with p = block_tables[b][j]:
  *   ksum[p, g, :] = (1/n_j) sum over the n_j valid slots of k_cache[p, g, slot, :]
  * ksum: float [P, H_kv, d], indexed by physical block.  Entries of blocks not
- * listed are left untouched.  ctx_lens: int [B]. */
+ * listed are left untouched.  ctx_lens: int [B].  k_cache: 16-byte aligned.
+ * Each mean sums the slots in slot order, as ent_kv_append's refresh does,
+ * so both give the same bits. */
 int ent_block_summary(ent_ctx* c, int B, const void* k_cache, const int* block_tables,
                       const int* ctx_lens, float* ksum, void* stream);
 

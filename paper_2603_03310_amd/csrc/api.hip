@@ -289,6 +289,8 @@ int ent_block_summary(ent_ctx* c, int B, const void* k_cache, const int* block_t
   if (B == 0) return ENT_OK;
   if (!k_cache || !block_tables || !ctx_lens || !ksum)
     return fail(c, ENT_E_INVAL, "ent_block_summary: NULL required pointer");
+  if (!aligned(k_cache, 16))
+    return fail(c, ENT_E_INVAL, "ent_block_summary: k_cache needs 16-byte alignment");
   const hipError_t e = ent::launch_block_summary(c, B, k_cache, block_tables, ctx_lens, ksum,
                                                  static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(c, e, "ent_block_summary launch");

@@ -30,8 +30,9 @@ namespace {
 constexpr int kThreads = 256;
 
 // Mean over slots [0, n) of element (g, dd) of physical block p's K tile, in
-// slot order.  Shared by the summary and append kernels so both produce the
-// same bits.  `last` (slot n-1) is passed in by the caller.
+// slot order (the append kernel's; the summary kernel sums in the same order,
+// so both produce the same bits).  `last` (slot n-1) is passed in by the
+// caller.
 template <typename T>
 __device__ __forceinline__ float block_mean(const T* __restrict__ kc, long long tile, int D, int dd,
                                             int n, float last) {
@@ -59,11 +60,33 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(
     return;
   }
   const int n = (j == nb - 1) ? N - kBlock * (nb - 1) : kBlock;
-  for (int e = threadIdx.x; e < Hkv * D; e += kThreads) {
-    const int g = e / D, dd = e % D;
+  // Each thread takes VE consecutive elements of one KV head's row: the 16
+  // slots' 16-byte loads are all issued at once (slots past n are read and
+  // not used: the tile always holds 16), then each element is summed in slot
+  // order, as block_mean does, so the bits match the append kernel's.
+  constexpr int VE = 16 / sizeof(T);
+  for (int v = threadIdx.x; v < Hkv * D / VE; v += kThreads) {
+    const int e0 = v * VE;
+    const int g = e0 / D, dd = e0 % D;
     const long long tile = (static_cast<long long>(p) * Hkv + g) * kBlock * D;
-    const float last = load_elem<T>(kc + tile + (n - 1) * D + dd);
-    ksum[(static_cast<long long>(p) * Hkv + g) * D + dd] = block_mean<T>(kc, tile, D, dd, n, last);
+    uint4 raw[kBlock];
+#pragma unroll
+    for (int slot = 0; slot < kBlock; ++slot)
+      raw[slot] = *reinterpret_cast<const uint4*>(kc + tile + slot * D + dd);
+    float sum[VE];
+#pragma unroll
+    for (int i = 0; i < VE; ++i) sum[i] = 0.f;
+#pragma unroll
+    for (int slot = 0; slot < kBlock; ++slot) {
+      const T* x = reinterpret_cast<const T*>(&raw[slot]);
+      if (slot < n) {
+#pragma unroll
+        for (int i = 0; i < VE; ++i) sum[i] += load_elem<T>(x + i);
+      }
+    }
+    float* out = ksum + (static_cast<long long>(p) * Hkv + g) * D + dd;
+#pragma unroll
+    for (int i = 0; i < VE; ++i) out[i] = __fdiv_rn(sum[i], static_cast<float>(n));
   }
 }
 

@@ -150,6 +150,28 @@ def test_closed_loop_with_appends(torch_cuda, fused):
     assert list(dev.ctx_lens.cpu().numpy()) == list(x.ctx_lens + 6)
 
 
+def test_append_refresh_matches_fresh_summary(torch_cuda):
+    """The mean keys that appends keep up to date equal, bit for bit, the
+    ones a fresh summary pass computes over the grown cache (both sum a
+    block's slots in slot order)."""
+    from paper_2603_03310_amd.runner import Decoder
+    w = small(LLAMA70B_LOOP, 4, ctx=("uniform", 100, 600), steps=6, suffix="refresh")
+    x = generate(w)
+    p = default_params(w)
+    reps, dev = _run(torch_cuda, x, p, steps=6)
+    _assert_ok(reps)
+    fresh = torch_cuda.zeros_like(dev.ksum)
+    with Decoder(**config_fields(w, p, x.num_pool_blocks)) as dec:
+        dec.summarize(w.batch, dev.k_pool, dev.block_tables, dev.ctx_lens, fresh)
+        torch_cuda.cuda.synchronize()
+        assert dec.device_status() == 0
+    a, b = dev.ksum.cpu().numpy(), fresh.cpu().numpy()
+    ctx = dev.ctx_lens.cpu().numpy()
+    for s in range(w.batch):
+        phys = np.asarray(x.block_tables[s][: -(-int(ctx[s]) // 16)], dtype=np.int64)
+        assert np.array_equal(a[phys], b[phys]), f"seq {s}"
+
+
 FUSED_CASES = [
     TINY,
     small(LLAMA3_8B, 5, ctx=("uniform", 100, 2500), suffix="fused"),
