@@ -278,7 +278,8 @@ int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_st
  * v_cache[p, g, :, N%16], recompute ksum[p, g, :] over the block's N%16 + 1
  * valid slots (bit-identical to ent_block_summary), and set ctx_lens[b] = N+1.
  * k_new, v_new: [B, H_kv, d] (kv_dtype).  ksum may be NULL in the exact
- * scoring mode, which does not read summaries (then none is maintained). */
+ * scoring mode, which does not read summaries (then none is maintained).
+ * Alignment: k_new, v_new and k_cache 16 bytes. */
 int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new,
                   const int* block_tables, int* ctx_lens, void* k_cache, void* v_cache,
                   float* ksum, void* stream);

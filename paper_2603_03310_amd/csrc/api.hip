@@ -414,6 +414,8 @@ int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new, const
   if (!k_new || !v_new || !block_tables || !ctx_lens || !k_cache || !v_cache ||
       (!ksum && c->cfg.scoring != ENT_SCORE_EXACT))
     return fail(c, ENT_E_INVAL, "ent_kv_append: NULL required pointer");
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16))
+    return fail(c, ENT_E_INVAL, "ent_kv_append: k_new, v_new and k_cache need 16-byte alignment");
   const hipError_t e = ent::launch_kv_append(c, B, k_new, v_new, block_tables, ctx_lens, k_cache,
                                              v_cache, ksum, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(c, e, "ent_kv_append launch");

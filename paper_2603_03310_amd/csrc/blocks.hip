@@ -29,18 +29,9 @@ namespace {
 
 constexpr int kThreads = 256;
 
-// Mean over slots [0, n) of element (g, dd) of physical block p's K tile, in
-// slot order (the append kernel's; the summary kernel sums in the same order,
-// so both produce the same bits).  `last` (slot n-1) is passed in by the
-// caller.
-template <typename T>
-__device__ __forceinline__ float block_mean(const T* __restrict__ kc, long long tile, int D, int dd,
-                                            int n, float last) {
-  float s = 0.f;
-  for (int slot = 0; slot < n - 1; ++slot) s += load_elem<T>(kc + tile + slot * D + dd);
-  s += last;
-  return __fdiv_rn(s, static_cast<float>(n));
-}
+// A block's mean key is the sum of its valid slots in slot order, divided by
+// their number (correctly rounded): the summary and append kernels both
+// evaluate it so, and give the same bits.
 
 template <typename T>
 __global__ __launch_bounds__(kThreads) void summary_kernel(
@@ -63,7 +54,7 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(
   // Each thread takes VE consecutive elements of one KV head's row: the 16
   // slots' 16-byte loads are all issued at once (slots past n are read and
   // not used: the tile always holds 16), then each element is summed in slot
-  // order, as block_mean does, so the bits match the append kernel's.
+  // order.
   constexpr int VE = 16 / sizeof(T);
   for (int v = threadIdx.x; v < Hkv * D / VE; v += kThreads) {
     const int e0 = v * VE;
@@ -107,16 +98,46 @@ __global__ __launch_bounds__(kThreads) void append_kernel(
     if (threadIdx.x == 0) raise_flag(flags, ENT_DEV_BAD_TABLE);
     return;
   }
-  for (int e = threadIdx.x; e < Hkv * D; e += kThreads) {
-    const int g = e / D, dd = e % D;
+  // Each thread takes VE consecutive elements of one KV head's row (16
+  // bytes): the new key and value, and (for the block's mean) the earlier
+  // slots' keys, all loaded at once (slots from `slot` on are read and not
+  // used: the tile always holds 16); each element is then summed in slot
+  // order, the new key last.
+  constexpr int VE = 16 / sizeof(T);
+  for (int v = threadIdx.x; v < Hkv * D / VE; v += kThreads) {
+    const int e0 = v * VE;
+    const int g = e0 / D, dd = e0 % D;
     const long long src = (static_cast<long long>(b) * Hkv + g) * D + dd;
     const long long tile = (static_cast<long long>(p) * Hkv + g) * kBlock * D;
-    const T kv = k_new[src];
-    kc[tile + slot * D + dd] = kv;
-    vc[tile + dd * kBlock + slot] = v_new[src];
-    if (ksum)
-      ksum[(static_cast<long long>(p) * Hkv + g) * D + dd] =
-          block_mean<T>(kc, tile, D, dd, slot + 1, load_elem<T>(&kv));
+    const uint4 kraw = *reinterpret_cast<const uint4*>(k_new + src);
+    const uint4 vraw = *reinterpret_cast<const uint4*>(v_new + src);
+    uint4 raw[kBlock - 1];
+    if (ksum) {
+#pragma unroll
+      for (int s2 = 0; s2 < kBlock - 1; ++s2)
+        raw[s2] = *reinterpret_cast<const uint4*>(kc + tile + s2 * D + dd);
+    }
+    *reinterpret_cast<uint4*>(kc + tile + slot * D + dd) = kraw;
+    const T* kx = reinterpret_cast<const T*>(&kraw);
+    const T* vx = reinterpret_cast<const T*>(&vraw);
+#pragma unroll
+    for (int i = 0; i < VE; ++i) vc[tile + (dd + i) * kBlock + slot] = vx[i];
+    if (ksum) {
+      float sum[VE];
+#pragma unroll
+      for (int i = 0; i < VE; ++i) sum[i] = 0.f;
+#pragma unroll
+      for (int s2 = 0; s2 < kBlock - 1; ++s2) {
+        const T* x = reinterpret_cast<const T*>(&raw[s2]);
+        if (s2 < slot) {
+#pragma unroll
+          for (int i = 0; i < VE; ++i) sum[i] += load_elem<T>(x + i);
+        }
+      }
+      float* out = ksum + (static_cast<long long>(p) * Hkv + g) * D + dd;
+#pragma unroll
+      for (int i = 0; i < VE; ++i) out[i] = __fdiv_rn(sum[i] + load_elem<T>(kx + i), static_cast<float>(slot + 1));
+    }
   }
   __syncthreads();
   if (threadIdx.x == 0) ctx_lens[b] = N + 1;
