@@ -5,7 +5,7 @@ the temperature law (Section 3.3), the clip bounds T_min/T_max, the
 estimator error bound epsilon_H (Section 3.3), and the guards H_min and
 B_min (Section 3.3, "Conservative pruning under uncertainty bounds";
 Section 5, "Robust control with uncertainty floors").  The defaults below are
-this build's readings.  Both the HIP library configuration and the oracle
+readings of those passages, chosen here.  Both the HIP library configuration and the oracle
 are driven from one `Params` object in tests and benchmarks.
 """
 from __future__ import annotations
