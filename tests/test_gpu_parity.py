@@ -150,12 +150,16 @@ def test_closed_loop_with_appends(torch_cuda, fused):
     assert list(dev.ctx_lens.cpu().numpy()) == list(x.ctx_lens + 6)
 
 
-def test_append_refresh_matches_fresh_summary(torch_cuda):
+@pytest.mark.parametrize("w", [small(LLAMA70B_LOOP, 4, ctx=("uniform", 100, 600), steps=6,
+                                     suffix="refresh"),
+                               small(TINY, TINY.batch, steps=6, suffix="refresh")],
+                         ids=lambda w: w.name)
+def test_append_refresh_matches_fresh_summary(torch_cuda, w):
     """The mean keys that appends keep up to date equal, bit for bit, the
     ones a fresh summary pass computes over the grown cache (both sum a
-    block's slots in slot order)."""
+    block's slots in slot order), for bf16 and fp32 caches; every step is
+    checked against the oracle on the way."""
     from paper_2603_03310_amd.runner import Decoder
-    w = small(LLAMA70B_LOOP, 4, ctx=("uniform", 100, 600), steps=6, suffix="refresh")
     x = generate(w)
     p = default_params(w)
     reps, dev = _run(torch_cuda, x, p, steps=6)
