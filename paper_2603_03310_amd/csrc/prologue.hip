@@ -12,7 +12,8 @@
 //
 // Both read HBM once (block summaries, logits) at a few flops per byte and
 // do not depend on each other; scoring jobs come first.  Every workgroup
-// keeps few registers, so many jobs' loads are in flight at once.  Two grid
+// keeps few registers and 33.8 KB of LDS (the scoring waves' staging rows, at
+// d = 128), so four workgroups per CU have their loads in flight at once.  Two grid
 // forms: dense (one workgroup per job slot; slots for tiles past a
 // sequence's end exit at once) and, when the block tables are much wider
 // than the sequences, compact (the grid is sized to the chip's resident
