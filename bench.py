@@ -1,24 +1,35 @@
-"""Benchmark of one entropic-time decode step on one MI355X.
+"""Benchmark of entropic-time decode steps on one MI355X.
 
-A step is the whole hot path over one batch, issued as one ent_decode_step
-call: entropy and controller, block scoring and selection, kept-block decode
-attention and sampling.  A second pass issues the same steps through the
-per-stage entry points (ent_entropy_temperature, ent_block_select,
-ent_sparse_paged_decode, ent_sample) with events between them for the
-per-stage times.  Inputs are seeded synthetic data of the named workload,
-resident in HBM before timing; two copies of every input rotate between
-steps so the 256 MB Infinity Cache cannot serve a step from the previous
-one, and every step starts from a fresh copy of the controller state, so all
-timed steps do identical work.
+A step is the whole hot path over one batch: entropy and controller, block
+scoring and selection, kept-block decode attention and sampling (one
+ent_decode_step call), and in a closed loop the append of the new token's
+K/V (ent_kv_append).  Inputs are seeded synthetic data of the named
+workload, resident in HBM before timing.
+
+Default workload: the 70B-shaped closed loop (batch 128, 64/8 heads, d 128,
+contexts U[4096, 16384], |V| 128256, 64 loop steps with fresh logits and one
+appended token per step, state on the device).  --warmup loop steps run
+untimed, then --steps consecutive loop steps are timed; the roofline is the
+decode entry point (attention and segment merge) replayed once per timed
+step, back to back between two HIP events on the launch stream, on that
+step's kept lists.
+
+Single-step workloads (--workload llama3_8b_decode, long_context,
+skewed_mixed, tiny): --steps fused steps timed back to back; --copies copies
+of every input rotate between steps so the 256 MB Infinity Cache cannot
+serve a step from the previous one, and every step starts from a fresh copy
+of the controller state, so all timed steps do identical work; a second
+pass issues the same steps through the per-stage entry points with events
+between them, and a third the decode entry point alone (the roofline).
 
 Prints one JSON line: decode steps/s, the achieved HBM rate on kept KV +
-logit bytes, the roofline of the dominant kernel (decode attention and its
-segment merge: K back-to-back calls of that entry point between two HIP
-events on the launch stream), and the float64 oracle timed on the host's
-cores on a bounded sample of the same workload.
+logit bytes and on every byte the step moves, the roofline of the dominant
+kernel, and the float64 oracle timed on the host's cores on a bounded sample
+of the same workload.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
                     [--estimator exact|topk|tail] [--est-k K] [--eps-h E]
+                    [--scoring meankey|exact] [--keep-first N] [--keep-last N]
 """
 from __future__ import annotations
 
@@ -29,12 +40,13 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 METRIC = "decode steps/sec and achieved HBM GB/s (kept KV + logits) vs peak, 1 MI355X"
-COUNTERS = os.path.join(ROOT, "profiles", "decode_counters.json")
 # Sources of the decode entry point's kernels (attention and segment merge).
 DECODE_SRCS = [os.path.join(ROOT, "paper_2603_03310_amd", "csrc", f)
                for f in ("decode.hip", "ent_internal.h")]
@@ -51,9 +63,9 @@ def decode_src_digest() -> str:
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=59)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="llama3_8b_decode")
+    ap.add_argument("--workload", default="llama70b_closed_loop")
     ap.add_argument("--copies", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -106,33 +118,53 @@ _BASE = None   # (inputs, params) of the CPU baseline, shared with forked worker
 
 
 def _oracle_worker(args):
-    """Sequence-steps of the oracle on sequences start, start + stride, ...
-    for about `seconds` (one thread); returns how many ran and the time."""
+    """Sequence-steps of the oracle for about `seconds` (one thread); returns
+    how many ran and the time.  Single-step workloads: sequences start,
+    start + stride, ... of the step.  Closed loops: the same sequences, each
+    run through consecutive loop steps from step 0 with the oracle's own
+    controller and kept-fraction state and its own appended tokens (on the
+    worker's copy-on-write view of the pools)."""
     start, stride, seconds = args
     x, p = _BASE
     from threadpoolctl import threadpool_limits
 
+    from oracle import append as OAp
     from oracle import step as St
-    B = x.workload.batch
-    done, s = 0, start
+    B, S = x.workload.batch, x.steps
+    loop = S > 1
+    h_prev, tau, temp = (a.astype(np.float64).copy() for a in (x.h_prev, x.tau, x.temp))
+    kappa = np.full(B, np.nan)
+    ctx = x.ctx_lens.copy()
+    done, s, t = 0, start % B, 0
     t0 = time.perf_counter()
     with threadpool_limits(limits=1):
         while done == 0 or time.perf_counter() - t0 < seconds:
-            St.sequence_step(s % B, k_pool=x.k_pool, v_pool=x.v_pool, tables=x.block_tables,
-                             ctx_lens=x.ctx_lens, q=x.q[0], logits=x.logits[0], h_prev=x.h_prev,
-                             tau=x.tau, temp=x.temp, uniforms=x.uniforms[0], params=p,
-                             block_size=16)
+            if loop and t == 0:       # the sequence starts the loop from its initial state
+                h_prev[s], tau[s], temp[s] = x.h_prev[s], x.tau[s], x.temp[s]
+                kappa[s], ctx[s] = np.nan, x.ctx_lens[s]
+            o = St.sequence_step(s, k_pool=x.k_pool, v_pool=x.v_pool, tables=x.block_tables,
+                                 ctx_lens=ctx, q=x.q[t], logits=x.logits[t], h_prev=h_prev,
+                                 tau=tau, temp=temp, uniforms=x.uniforms[t], params=p,
+                                 block_size=16, kappa=kappa)
             done += 1
-            s += stride
+            if loop:
+                h_prev[s], tau[s], temp[s], kappa[s] = o["h"], o["tau"], o["temp_next"], o["kappa"]
+                ctx[s] = OAp.append_token(x.k_pool, x.v_pool, x.block_tables[s], int(ctx[s]),
+                                          x.k_new[t, s], x.v_new[t, s], 16)
+                t += 1
+                if t < S:
+                    continue
+                t = 0
+            s = (s + stride) % B
     return done, time.perf_counter() - t0
 
 
 def cpu_baseline(x, p, seconds):
-    """The float64 oracle on the host, cycling over the step's sequences: one
-    process per core of the host (sequences split between them, one thread
-    each) for about `seconds`, then one thread alone for half of that; both
-    scaled to whole steps per second.  Runs before the GPU is initialised,
-    so the worker processes hold no device state."""
+    """The float64 oracle on the host (all stages; closed loops also the
+    append): one process per core of the host (sequences split between them,
+    one thread each) for about `seconds`, then one thread alone for half of
+    that; both scaled to whole steps per second.  Runs before the GPU is
+    initialised, so the worker processes hold no device state."""
     import multiprocessing as mp
     global _BASE
     _BASE = (x, p)         # inherited by the forked workers, not pickled
@@ -142,21 +174,35 @@ def cpu_baseline(x, p, seconds):
         res = pool.map(_oracle_worker, [(i, n, seconds) for i in range(n)])
     el = max(r[1] for r in res)
     done = sum(r[0] for r in res)
-    one, el1 = _oracle_worker((0, 1, seconds / 2))
+    # The one-thread figure also runs in a child: appends write the pools.
+    with mp.get_context("fork").Pool(1) as pool:
+        one, el1 = pool.map(_oracle_worker, [(0, 1, seconds / 2)])[0]
+    if x.steps > 1:
+        what = (f"{done} sequence-steps of the {x.workload.name} loop (each process runs its "
+                f"sequences through consecutive loop steps from step 0, carrying the oracle's own "
+                f"state and appends)")
+    else:
+        what = f"{done} sequence-steps of one {x.workload.name} step"
     return {"value": (done / B) / el, "unit": "steps/s", "cores": n, "kind": "oracle",
             "value_1core": (one / B) / el1,
-            "sample": f"float64 oracle, all stages: {done} sequence-steps of one "
-                      f"{x.workload.name} step in {el:.1f} s over {n} processes (one thread "
-                      f"each, sequences split between them), and {one} in {el1:.1f} s on one "
-                      f"thread (value_1core); scaled to whole steps"}
+            "sample": f"float64 oracle, all stages: {what} in {el:.1f} s over {n} processes "
+                      f"(one thread each, sequences split between them), and {one} in "
+                      f"{el1:.1f} s on one thread (value_1core); scaled to whole steps of "
+                      f"{B} sequences"}
 
 
-def traffic_from_counters():
-    """HBM bytes per decode launch from committed rocprofv3 counters, if they
-    were taken on the current decode kernel source (else None)."""
-    if not os.path.exists(COUNTERS):
+def counters_path(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"decode_counters_{workload}.json")
+
+
+def traffic_from_counters(workload: str):
+    """HBM bytes per decode launch of this workload from committed rocprofv3
+    counters, if they were taken on the current decode kernel source (else
+    None)."""
+    path = counters_path(workload)
+    if not os.path.exists(path):
         return None
-    with open(COUNTERS) as f:
+    with open(path) as f:
         c = json.load(f)
     if c.get("decode_src_sha256") != decode_src_digest():
         return None
@@ -197,14 +243,22 @@ def sched_time(ent, torch, ctx, sp, b_sel, K, W):
 
 
 def closed_loop(args, w, p):
-    """A closed-loop workload: every step is ent_decode_step then
+    """A closed-loop workload: every loop step is ent_decode_step then
     ent_kv_append (the new token's K/V), the controller state and the
-    kept-fraction state carried on the device.  The timed region is
-    min(--steps, the workload's steps) consecutive steps after --warmup
-    steps and a reset of the lengths and state; a second, untimed pass over
-    the same steps (the same results: the loop is deterministic) records the
-    kept lists for the byte count."""
-    import numpy as np
+    kept-fraction state carried on the device, fresh logits, queries and
+    uniforms per step.  --warmup loop steps run untimed, then --steps
+    consecutive loop steps are timed between two events (a pass past the
+    workload's last step starts the loop over from its initial state: lengths,
+    controller state, kept-fraction state and the appended blocks' summaries
+    restored by device copies).
+
+    A second, untimed pass replays the same steps from the initial state
+    (the loop is deterministic) and records each timed step's kept lists and
+    lengths, for the byte count and for the roofline pass: the decode entry
+    point (attention plus segment merge) issued once per timed step, back to
+    back between two events, on that step's queries, kept lists and lengths
+    (the pools then hold later appended tokens too, past those lengths,
+    which the decode never reads)."""
     import torch
 
     from paper_2603_03310_amd import ent
@@ -223,9 +277,8 @@ def closed_loop(args, w, p):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     d = upload(x, dev)
-    B = w.batch
-    K = min(args.steps, w.steps)
-    W = min(args.warmup, w.steps)
+    B, S = w.batch, w.steps
+    K, W = args.steps, args.warmup
     cfg = ent.ent_config()
     for k, v in config_fields(w, p, x.num_pool_blocks).items():
         setattr(cfg, k, v)
@@ -234,29 +287,39 @@ def closed_loop(args, w, p):
     ent.ent_block_summary(ctx, B, d.k_pool, d.block_tables, d.ctx_lens, d.ksum, sp)
     ld = x.logits.shape[2]
     init = [torch.from_numpy(a).to(dev) for a in (x.h_prev, x.tau, x.temp, x.ctx_lens)]
+    # Summaries of every block a pass of appends touches (the blocks holding
+    # positions ctx_len .. ctx_len + S - 1), saved to restore them.
+    touched = sorted({int(x.block_tables[s][j])
+                      for s in range(B)
+                      for j in range(int(x.ctx_lens[s]) // 16, (int(x.ctx_lens[s]) + S - 1) // 16 + 1)})
+    touched = torch.tensor(touched, dtype=torch.long, device=dev)
+    ksum_saved = d.ksum.index_select(0, touched)
 
     def reset():
         for dst, src in zip((d.h_prev, d.tau, d.temp, d.ctx_lens), init):
             dst.copy_(src)
         d.kappa.fill_(float("nan"))
+        d.ksum.index_copy_(0, touched, ksum_saved)
 
     def step(t):
-        ent.ent_decode_step(ctx, B, d.logits[t], ld, d.h_prev, d.tau, d.temp, d.q[t], d.k_pool,
-                            d.v_pool, d.ksum, d.block_tables, d.ctx_lens, d.uniforms[t], d.h,
+        if t % S == 0 and t > 0:
+            reset()
+        i = t % S
+        ent.ent_decode_step(ctx, B, d.logits[i], ld, d.h_prev, d.tau, d.temp, d.q[i], d.k_pool,
+                            d.v_pool, d.ksum, d.block_tables, d.ctx_lens, d.uniforms[i], d.h,
                             d.temp_used, d.kept, d.n_kept, d.out, d.tokens, d.row_stats, d.lse,
                             None, None, sp, d.kappa)
-        ent.ent_kv_append(ctx, B, d.k_new[t], d.v_new[t], d.block_tables, d.ctx_lens, d.k_pool,
+        ent.ent_kv_append(ctx, B, d.k_new[i], d.v_new[i], d.block_tables, d.ctx_lens, d.k_pool,
                           d.v_pool, d.ksum, sp)
 
+    # Pass A: W warm-up loop steps, then K timed consecutive loop steps.
     for t in range(W):
         step(t)
-    torch.cuda.synchronize()
-    reset()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_wall = time.perf_counter()
     e0.record()
-    for t in range(K):
+    for t in range(W, W + K):
         step(t)
     e1.record()
     torch.cuda.synchronize()
@@ -265,35 +328,76 @@ def closed_loop(args, w, p):
     flags = ent.ent_device_status(ctx, sp)
     if flags:
         raise SystemExit(f"device flags raised: {flags}")
-    # Untimed pass: the kept lists of every step (for the bytes moved).
+    print(f"[bench] timed {K} loop steps after {W} warm-up steps", file=sys.stderr, flush=True)
+
+    # Pass B (untimed): the same steps from the initial state; each timed
+    # step's kept lists, counts and lengths are kept on the device.
     reset()
-    elem = 2 if w.kv_dtype == "bf16" else 4
+    elem = w.elem_bytes
     kv_kept, blocks_kept, blocks_all, all_bytes = 0, 0, 0, 0
+    rec_kept = torch.empty((K,) + tuple(d.kept.shape), dtype=torch.int32, device=dev)
+    rec_nk = torch.empty((K, B), dtype=torch.int32, device=dev)
+    rec_ctx = torch.empty((K, B), dtype=torch.int32, device=dev)
+    dec_bytes = 0
+    Hq, hd = w.num_q_heads, w.head_dim
     xs = type("X", (), {})()
     xs.workload = w
-    for t in range(K):
+    for t in range(W + K):
+        if t >= W:
+            if t % S == 0 and t > 0:
+                reset()
+            rec_ctx[t - W].copy_(d.ctx_lens)
+            xs.ctx_lens = d.ctx_lens.cpu().numpy()
         step(t)
+        if t < W:
+            continue
         torch.cuda.synchronize()
-        xs.ctx_lens = x.ctx_lens + t
+        rec_kept[t - W].copy_(d.kept)
+        rec_nk[t - W].copy_(d.n_kept)
         nk, kp = d.n_kept.cpu().numpy(), d.kept.cpu().numpy()
         kv_step = kv_bytes_kept(xs, nk, kp, elem)
         kv_kept += kv_step
         all_bytes += total_bytes(w, xs.ctx_lens, kv_step, elem, p.scoring)
         blocks_kept += int(nk.sum())
         blocks_all += int(sum(-(-int(n) // 16) for n in xs.ctx_lens))
+        dec_bytes += (kv_step + B * Hq * hd * elem + B * Hq * hd * 4 + B * Hq * 4
+                      + 2 * 4 * int(nk.sum()) + 4 * B)
+
+    # Pass C: the roofline kernel's entry point, once per timed step (its
+    # queries, kept lists and lengths), back to back between two events on
+    # the launch stream; W warm-up calls first.
+    def decode_call(j):
+        i = (W + j) % S
+        ent.ent_sparse_paged_decode(ctx, B, d.q[i], d.k_pool, d.v_pool, d.block_tables,
+                                    rec_ctx[j], rec_kept[j], rec_nk[j], d.out, d.lse, sp)
+
+    for j in range(min(W, K)):
+        decode_call(j)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for j in range(K):
+        decode_call(j)
+    c1.record()
+    torch.cuda.synchronize()
+    dec_us = c0.elapsed_time(c1) / K * 1e3
+    flags = ent.ent_device_status(ctx, sp)
+    if flags:
+        raise SystemExit(f"device flags raised: {flags}")
     ent.ent_destroy(ctx)
+
     metric_bytes = kv_kept / K + 4 * B * w.vocab
     gbps = metric_bytes / (ms_step * 1e-3) / 1e9
+    dec_per_launch = dec_bytes / K
+    achieved = dec_per_launch / (dec_us * 1e-6) / 1e9
     line = {
         "metric": METRIC, "value": round(1e3 / ms_step, 3), "unit": "steps/s", "n_gpus": 1,
         "steps": K, "warmup": W, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "scaling": "weak", "vs_baseline": None, "dtype": w.kv_dtype,
         "data": "synthetic (seeded; shapes and value recipes of the workload)",
-        "config": {"workload": w.name, "batch": B, "q_heads": w.num_q_heads,
-                   "kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "block_size": 16,
-                   "ctx": list(w.ctx), "vocab": w.vocab, "kv_dtype": w.kv_dtype,
-                   "closed_loop_steps": K, "step": "ent_decode_step + ent_kv_append",
-                   "entropy": args.estimator},
+        "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": w.num_kv_heads,
+                   "head_dim": hd, "block_size": 16, "ctx": list(w.ctx), "vocab": w.vocab,
+                   "kv_dtype": w.kv_dtype, "loop_steps": S, "timed_loop_steps": [W, W + K],
+                   "step": "ent_decode_step + ent_kv_append", "entropy": args.estimator},
         "hbm_gbps_kept_kv_plus_logits": round(gbps, 1),
         "hbm_frac_kept_kv_plus_logits": round(gbps / HBM_PEAK_GBPS, 4),
         "metric_bytes_per_step": int(metric_bytes),
@@ -302,7 +406,11 @@ def closed_loop(args, w, p):
         "hbm_frac_total": round(all_bytes / K / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "kept_block_fraction": round(blocks_kept / max(1, blocks_all), 4),
         "wall_ms_per_step": round(wall_ms / K, 5),
-        "roofline": None,
+        "roofline": {"kernel": "sparse_paged_decode", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic_from_counters(w.name),
+                     "bytes_per_launch": int(dec_per_launch), "avg_launch_us": round(dec_us, 2)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
@@ -471,7 +579,7 @@ def main():
     line = {
         "metric": METRIC, "value": round(steps_per_s, 3), "unit": "steps/s", "n_gpus": 1,
         "steps": K, "warmup": W, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "scaling": "weak", "vs_baseline": None, "dtype": w.kv_dtype,
         "data": "synthetic (seeded; shapes and value recipes of the workload)",
         "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": w.num_kv_heads,
                    "head_dim": d, "block_size": 16, "ctx": list(w.ctx), "vocab": w.vocab,
@@ -494,7 +602,7 @@ def main():
         "roofline": {"kernel": "sparse_paged_decode", "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic_from_counters(),
+                     "traffic": traffic_from_counters(w.name),
                      "bytes_per_launch": int(dec_bytes), "avg_launch_us": round(dec_us, 2)},
         "cpu_baseline": cpu,
         "schedule": sched,

@@ -33,6 +33,9 @@ THETA_BAND = 1e-6
 ATT_ABS = 2e-3
 ATT_REL = 2e-3
 TOKEN_BAND = 1e-6
+# Block scores I_b: |delta| <= SCORE_ABS + SCORE_REL |I_b|.
+SCORE_ABS = 1e-6
+SCORE_REL = 1e-4
 
 
 @dataclass
@@ -61,6 +64,7 @@ class Report:
     max_att_err: float = 0.0
     max_h_err: float = 0.0
     max_score_err: float = 0.0
+    max_score_rel_err: float = 0.0
 
     def fail(self, msg):
         self.failures.append(msg)
@@ -138,7 +142,11 @@ def check_step(*, k_pool, v_pool, tables, ctx_lens, q, logits, uniforms, h_prev,
             I_g = gpu.scores[s][:nb].astype(np.float32)
             serr = np.abs(I_g.astype(np.float64) - I_o)
             rep.max_score_err = max(rep.max_score_err, float(serr.max(initial=0.0)))
-            if np.any(serr > 1e-6 + 1e-4 * np.abs(I_o)):
+            big = np.abs(I_o) > SCORE_ABS / SCORE_REL
+            if np.any(big):
+                rep.max_score_rel_err = max(rep.max_score_rel_err,
+                                            float((serr[big] / np.abs(I_o[big])).max()))
+            if np.any(serr > SCORE_ABS + SCORE_REL * np.abs(I_o)):
                 rep.fail(f"seq {s}: block scores differ by {serr.max():.3g}")
             forced = OB.forced_blocks(nb, getattr(params, "keep_first", 0),
                                       getattr(params, "keep_last", 0))

@@ -53,6 +53,9 @@ def _run(torch, x, p, steps=1, seqs=None, max_blocks=None, check_ksum=True, fuse
                              logits=x.logits[t], uniforms=x.uniforms[t], h_prev=state[0],
                              tau=state[1], temp=state[2], params=p, gpu=gpu, seqs=seqs,
                              check_ksum=check_ksum)
+            print(f"[parity] {w.name} step {t}: score err {rep.max_score_err:.2e} "
+                  f"(rel {rep.max_score_rel_err:.2e}), attention err {rep.max_att_err:.2e}, "
+                  f"entropy err {rep.max_h_err:.2e}", flush=True)
             reps.append(rep)
             if steps > 1:
                 dec.append(B, dev.k_new[t], dev.v_new[t], dev.block_tables, dev.ctx_lens,
