@@ -242,6 +242,17 @@ def sched_time(ent, torch, ctx, sp, b_sel, K, W):
     return {"pool": n, "b_sel": b_sel, "avg_launch_us": round(e0.elapsed_time(e1) / K * 1e3, 2)}
 
 
+def calibrate_copy(torch, dev):
+    """A plain 1 GiB device copy: profilers' byte counters for this kernel
+    calibrate those taken on the step's kernels."""
+    src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def closed_loop(args, w, p):
     """A closed-loop workload: every loop step is ent_decode_step then
     ent_kv_append (the new token's K/V), the controller state and the
@@ -312,6 +323,8 @@ def closed_loop(args, w, p):
         ent.ent_kv_append(ctx, B, d.k_new[i], d.v_new[i], d.block_tables, d.ctx_lens, d.k_pool,
                           d.v_pool, d.ksum, sp)
 
+    if args.calibrate_copy:
+        calibrate_copy(torch, dev)
     # Pass A: W warm-up loop steps, then K timed consecutive loop steps.
     for t in range(W):
         step(t)
@@ -496,14 +509,7 @@ def main():
         ev[4].record(stream)
 
     if args.calibrate_copy:
-        # A plain copy kernel of known size: profilers' byte counters for this
-        # kernel calibrate those taken on the step's kernels.
-        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        calibrate_copy(torch, dev)
 
     # Pass A: the timed steps (ent_decode_step), nothing between the launches.
     for i in range(W):
