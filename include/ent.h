@@ -189,6 +189,26 @@ int ent_entropy_temperature(ent_ctx* c, int B, const float* logits, long long ld
                             ent_state st, float* h_out, float* temp_used, float* row_stats,
                             void* stream);
 
+/* ent_entropy_temperature for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Needs no context and allocates nothing: the configuration
+ * is passed directly (host pointer, checked as by ent_init; only vocab,
+ * max_batch, the controller and estimator fields and head_dim matter), and
+ * the kernels' scratch (the chunk partials of the entropy pass, and with an
+ * estimator the chunk threads' logit maxima) is a static device array of
+ * ENT_NOALLOC_SCRATCH_BYTES that each GPU holds until the process ends.
+ * Arguments and results as in ent_entropy_temperature, bit-identical to it.
+ * Limit: 12 B ceil(vocab / 4096) bytes (+ 1024 B ceil(vocab / 4096) with an
+ * estimator) + 256, each term rounded up to 256, must fit the array, else
+ * ENT_E_UNSUPPORTED with nothing launched (e.g. B <= 4096 rows of 128256
+ * logits with the exact entropy, B <= 63 with an estimator).  Every call on
+ * a GPU shares that GPU's array: calls that overlap on one GPU (two streams,
+ * two threads) race and give undefined results.  Errors: ent_last_error(NULL). */
+#define ENT_NOALLOC_SCRATCH_BYTES (2u << 20)
+int ent_entropy_temperature_noalloc(const ent_config* cfg, int B, const float* logits,
+                                    long long ld, ent_state st, float* h_out, float* temp_used,
+                                    float* row_stats, void* stream);
+
 /* Per-block mean keys (the summaries block scoring reads).  For each
  * sequence b < B and logical block j < nb_b, with p = block_tables[b][j]:
  *   ksum[p, g, :] = (1/n_j) sum over the n_j valid slots of k_cache[p, g, slot, :]

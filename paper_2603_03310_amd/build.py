@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libent.so")
-SOURCES = ["api.hip", "entropy.hip", "blocks.hip", "decode.hip", "step.hip", "prologue.hip", "schedule.hip", "exact.hip"]
+SOURCES = ["api.hip", "entropy.hip", "blocks.hip", "decode.hip", "step.hip", "prologue.hip", "schedule.hip", "exact.hip", "noalloc.hip"]
 
 
 def hipcc() -> str:

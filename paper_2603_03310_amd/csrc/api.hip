@@ -102,6 +102,11 @@ size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 }  // namespace
 
+namespace ent {
+std::string config_error(const ent_config* cfg, int* code) { return check_config(cfg, code); }
+void set_free_error(const std::string& msg) { g_init_error = msg; }
+}  // namespace ent
+
 extern "C" {
 
 void ent_default_config(ent_config* out) {

@@ -175,6 +175,12 @@ hipError_t launch_schedule(int N, const ent_sched_params& p, const float* tau, c
                            const int* ctx_lens, float* tau_last, float* gain, int* age, int b_sel,
                            int* selected, int* n_selected, float* priority, hipStream_t s);
 
+// Configuration check of ent_init (message, ENT_OK / ENT_E_INVAL /
+// ENT_E_UNSUPPORTED in *code), and the message ent_last_error(NULL) returns
+// (calls without a context: ent_init, ent_entropy_temperature_noalloc).
+std::string config_error(const ent_config* cfg, int* code);
+void set_free_error(const std::string& msg);
+
 // Occupancy-derived persistent grid of the decode kernel, and the number of
 // partial slots its split segments may use (waves + segments).
 int decode_grid_size(const ent_ctx* c);

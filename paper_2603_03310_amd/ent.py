@@ -27,7 +27,8 @@ ENT_DEV_BAD_TABLE, ENT_DEV_BAD_CTXLEN, ENT_DEV_CACHE_FULL = 1, 2, 4
 EXPORTED = ("ent_default_config", "ent_check_config", "ent_row_stats_chunks", "ent_init",
             "ent_destroy", "ent_last_error", "ent_device_status", "ent_entropy_temperature",
             "ent_block_summary", "ent_block_select", "ent_sparse_paged_decode", "ent_sample",
-            "ent_kv_append", "ent_decode_step", "ent_schedule")
+            "ent_kv_append", "ent_decode_step", "ent_schedule", "ent_entropy_temperature_noalloc")
+ENT_NOALLOC_SCRATCH_BYTES = 2 << 20
 ENT_SCHED_MAX_POOL = 8192
 
 
@@ -74,6 +75,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python -m paper_2603_03310_amd.build`")
+    # torch first: its HIP runtime is then the one the library binds to (torch's
+    # libraries name the runtime without a version, so a runtime loaded first
+    # for the library would not be shared and the process would hold two).
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     vp, i, ll = ctypes.c_void_p, ctypes.c_int, ctypes.c_longlong
     cfgp = ctypes.POINTER(ent_config)
@@ -86,6 +91,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "ent_last_error": (ctypes.c_char_p, [vp]),
         "ent_device_status": (i, [vp, vp, ctypes.POINTER(ctypes.c_uint)]),
         "ent_entropy_temperature": (i, [vp, i, vp, ll, ent_state, vp, vp, vp, vp]),
+        "ent_entropy_temperature_noalloc": (i, [cfgp, i, vp, ll, ent_state, vp, vp, vp, vp]),
         "ent_block_summary": (i, [vp, i, vp, vp, vp, vp, vp]),
         "ent_block_select": (i, [vp, i] + [vp] * 12),
         "ent_sparse_paged_decode": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
@@ -169,6 +175,15 @@ def ent_entropy_temperature(ctx, B, logits, ld, h_prev, tau, temp, h_out, temp_u
     st = ent_state(ptr(h_prev), ptr(tau), ptr(temp), None)
     _check(ctx, load().ent_entropy_temperature(ctx, B, ptr(logits), ld, st, ptr(h_out),
                                                ptr(temp_used), ptr(row_stats), _stream(stream)))
+
+
+def ent_entropy_temperature_noalloc(cfg: ent_config, B, logits, ld, h_prev, tau, temp, h_out,
+                                    temp_used, row_stats=None, stream=None):
+    """ent_entropy_temperature without a context: no device allocation."""
+    st = ent_state(ptr(h_prev), ptr(tau), ptr(temp), None)
+    _check(None, load().ent_entropy_temperature_noalloc(ctypes.byref(cfg), B, ptr(logits), ld, st,
+                                                        ptr(h_out), ptr(temp_used),
+                                                        ptr(row_stats), _stream(stream)))
 
 
 def ent_block_summary(ctx, B, k_cache, block_tables, ctx_lens, ksum, stream=None):
