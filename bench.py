@@ -6,7 +6,8 @@ ent_decode_step call), and in a closed loop the append of the new token's
 K/V (ent_kv_append).  Inputs are seeded synthetic data of the named
 workload, resident in HBM before timing.
 
-Default workload: the 70B-shaped closed loop (batch 128, 64/8 heads, d 128,
+Default workload: the 70B-shaped closed loop (one ent_decode_step_append call
+per loop step) (batch 128, 64/8 heads, d 128,
 contexts U[4096, 16384], |V| 128256, 64 loop steps with fresh logits and one
 appended token per step, state on the device).  --warmup loop steps run
 untimed, then --steps consecutive loop steps are timed; the roofline is the
@@ -254,10 +255,10 @@ def calibrate_copy(torch, dev):
 
 
 def closed_loop(args, w, p):
-    """A closed-loop workload: every loop step is ent_decode_step then
-    ent_kv_append (the new token's K/V), the controller state and the
-    kept-fraction state carried on the device, fresh logits, queries and
-    uniforms per step.  --warmup loop steps run untimed, then --steps
+    """A closed-loop workload: every loop step is one ent_decode_step_append
+    call (the decode step, then the append of the new token's K/V), the
+    controller state and the kept-fraction state carried on the device, fresh
+    logits, queries and uniforms per step.  --warmup loop steps run untimed, then --steps
     consecutive loop steps are timed between two events (a pass past the
     workload's last step starts the loop over from its initial state: lengths,
     controller state, kept-fraction state and the appended blocks' summaries
@@ -316,12 +317,11 @@ def closed_loop(args, w, p):
         if t % S == 0 and t > 0:
             reset()
         i = t % S
-        ent.ent_decode_step(ctx, B, d.logits[i], ld, d.h_prev, d.tau, d.temp, d.q[i], d.k_pool,
-                            d.v_pool, d.ksum, d.block_tables, d.ctx_lens, d.uniforms[i], d.h,
-                            d.temp_used, d.kept, d.n_kept, d.out, d.tokens, d.row_stats, d.lse,
-                            None, None, sp, d.kappa)
-        ent.ent_kv_append(ctx, B, d.k_new[i], d.v_new[i], d.block_tables, d.ctx_lens, d.k_pool,
-                          d.v_pool, d.ksum, sp)
+        ent.ent_decode_step_append(ctx, B, d.logits[i], ld, d.h_prev, d.tau, d.temp, d.q[i],
+                                   d.k_pool, d.v_pool, d.ksum, d.block_tables, d.ctx_lens,
+                                   d.uniforms[i], d.k_new[i], d.v_new[i], d.h, d.temp_used, d.kept,
+                                   d.n_kept, d.out, d.tokens, d.row_stats, d.lse, None, None, sp,
+                                   d.kappa)
 
     if args.calibrate_copy:
         calibrate_copy(torch, dev)
@@ -410,7 +410,7 @@ def closed_loop(args, w, p):
         "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": w.num_kv_heads,
                    "head_dim": hd, "block_size": 16, "ctx": list(w.ctx), "vocab": w.vocab,
                    "kv_dtype": w.kv_dtype, "loop_steps": S, "timed_loop_steps": [W, W + K],
-                   "step": "ent_decode_step + ent_kv_append", "entropy": args.estimator},
+                   "step": "ent_decode_step_append", "entropy": args.estimator},
         "hbm_gbps_kept_kv_plus_logits": round(gbps, 1),
         "hbm_frac_kept_kv_plus_logits": round(gbps / HBM_PEAK_GBPS, 4),
         "metric_bytes_per_step": int(metric_bytes),

@@ -304,6 +304,22 @@ int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new,
                   const int* block_tables, int* ctx_lens, void* k_cache, void* v_cache,
                   float* ksum, void* stream);
 
+/* One step of the closed loop (Section 3.4: the step's outputs, then the
+ * state's memory grows by the new token): ent_decode_step followed by
+ * ent_kv_append of this step's new token, bit-identical to the two calls in
+ * that order.  k_new, v_new: [B, H_kv, d] (kv_dtype, 16-byte aligned).  The
+ * append runs on workgroups of its own inside the step's last launch, the
+ * merge of split attention segments, which reads nothing the append writes
+ * (in the exact scoring mode: the staged calls, then the append).
+ * Arguments as in the two calls: ctx_lens is incremented, k_cache, v_cache
+ * and ksum receive the new token. */
+int ent_decode_step_append(ent_ctx* c, int B, const float* logits, long long ld, ent_state st,
+                           const void* q, void* k_cache, void* v_cache, float* ksum,
+                           const int* block_tables, int* ctx_lens, const float* uniforms,
+                           const void* k_new, const void* v_new, float* h_out, float* temp_used,
+                           float* row_stats, int* kept, int* n_kept, float* out, float* lse,
+                           int* tokens, float* scores, float* theta, void* stream);
+
 /* Entropy-aware scheduling over a pool of N active sequences (Section 3.1:
  * the priority pi(s) = E[Delta H_s] / (alpha C_s + beta M_s + gamma L_s);
  * Section 7: nonnegative bounded terms, no starvation).  Readings: the

@@ -411,6 +411,52 @@ int ent_decode_step(ent_ctx* c, int B, const float* logits, long long ld, ent_st
   return ENT_OK;
 }
 
+int ent_decode_step_append(ent_ctx* c, int B, const float* logits, long long ld, ent_state st,
+                           const void* q, void* k_cache, void* v_cache, float* ksum,
+                           const int* block_tables, int* ctx_lens, const float* uniforms,
+                           const void* k_new, const void* v_new, float* h_out, float* temp_used,
+                           float* row_stats, int* kept, int* n_kept, float* out, float* lse,
+                           int* tokens, float* scores, float* theta, void* stream) {
+  if (!c) return ENT_E_INVAL;
+  if (int r = check_batch(c, B)) return r;
+  if (B == 0) return ENT_OK;
+  const bool exact = c->cfg.scoring == ENT_SCORE_EXACT;
+  if (!k_new || !v_new)
+    return fail(c, ENT_E_INVAL, "ent_decode_step_append: NULL required pointer");
+  if (!aligned(k_new, 16) || !aligned(v_new, 16))
+    return fail(c, ENT_E_INVAL, "ent_decode_step_append: k_new and v_new need 16-byte alignment");
+  if (exact) {
+    // The staged step, then the append.
+    if (int r = ent_decode_step(c, B, logits, ld, st, q, k_cache, v_cache, ksum, block_tables,
+                                ctx_lens, uniforms, h_out, temp_used, row_stats, kept, n_kept, out,
+                                lse, tokens, scores, theta, stream))
+      return r;
+    return ent_kv_append(c, B, k_new, v_new, block_tables, ctx_lens, k_cache, v_cache, ksum,
+                         stream);
+  }
+  if (!logits || !st.h_prev || !st.tau || !st.temp || !q || !k_cache || !v_cache || !ksum ||
+      !block_tables || !ctx_lens || !uniforms || !h_out || !temp_used || !kept || !n_kept || !out ||
+      !tokens)
+    return fail(c, ENT_E_INVAL, "ent_decode_step_append: NULL required pointer");
+  if (ld < c->cfg.vocab) return fail(c, ENT_E_INVAL, "ent_decode_step_append: ld < vocab");
+  if (h_out == st.h_prev) return fail(c, ENT_E_INVAL, "ent_decode_step_append: h_out aliases h_prev");
+  if (temp_used == st.temp)
+    return fail(c, ENT_E_INVAL, "ent_decode_step_append: temp_used aliases temp");
+  if (!aligned(q, 16) || !aligned(ksum, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
+      !aligned(out, 16))
+    return fail(c, ENT_E_INVAL,
+                "ent_decode_step_append: q, ksum, caches and out need 16-byte alignment");
+  const ent::AppendArgs ap =
+      ent::make_append_args(c, k_new, v_new, block_tables, ctx_lens, k_cache, v_cache, ksum);
+  const hipError_t e = ent::launch_decode_step(c, B, logits, ld, st, q, k_cache, v_cache, ksum,
+                                               block_tables, ctx_lens, uniforms, h_out, temp_used,
+                                               row_stats, kept, n_kept, out, lse, tokens, scores,
+                                               theta, static_cast<hipStream_t>(stream), &ap);
+  if (e != hipSuccess) return hip_fail(c, e, "ent_decode_step_append launch");
+  c->err.clear();
+  return ENT_OK;
+}
+
 int ent_kv_append(ent_ctx* c, int B, const void* k_new, const void* v_new, const int* block_tables,
                   int* ctx_lens, void* k_cache, void* v_cache, float* ksum, void* stream) {
   if (!c) return ENT_E_INVAL;

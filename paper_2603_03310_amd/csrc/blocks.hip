@@ -14,7 +14,7 @@
 //   summary_kernel   per-block mean keys (setup)
 //   (bf16 scoring runs in the persistent kernel of prologue.hip)
 //   score_valu_kernel   z for 16 blocks x all heads per workgroup (fp32, VALU)
-//   select_fused_kernel per sequence (short block tables): L_h, I_b, the
+//   select_fused_kernel per sequence (tables that fit its registers): L_h, I_b, the
 //                       budget, an 8-bit radix select of the k-th largest
 //                       score, ascending compaction with ballots
 //   lse_merge_kernel,   the same in three launches for long block tables:
@@ -82,65 +82,8 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(
 }
 
 template <typename T>
-__global__ __launch_bounds__(kThreads) void append_kernel(
-    const T* __restrict__ k_new, const T* __restrict__ v_new, const int* __restrict__ tables,
-    int* __restrict__ ctx_lens, T* __restrict__ kc, T* __restrict__ vc, float* __restrict__ ksum,
-    int Hkv, int D, int MAXB, int P, unsigned* flags) {
-  const int b = blockIdx.x;
-  const int N = ctx_lens[b];
-  if (N < 0 || N >= MAXB * kBlock) {
-    if (threadIdx.x == 0) raise_flag(flags, N < 0 ? ENT_DEV_BAD_CTXLEN : ENT_DEV_CACHE_FULL);
-    return;
-  }
-  const int j = N / kBlock, slot = N % kBlock;
-  const int p = tables[static_cast<long long>(b) * MAXB + j];
-  if (p < 0 || p >= P) {
-    if (threadIdx.x == 0) raise_flag(flags, ENT_DEV_BAD_TABLE);
-    return;
-  }
-  // Each thread takes VE consecutive elements of one KV head's row (16
-  // bytes): the new key and value, and (for the block's mean) the earlier
-  // slots' keys, all loaded at once (slots from `slot` on are read and not
-  // used: the tile always holds 16); each element is then summed in slot
-  // order, the new key last.
-  constexpr int VE = 16 / sizeof(T);
-  for (int v = threadIdx.x; v < Hkv * D / VE; v += kThreads) {
-    const int e0 = v * VE;
-    const int g = e0 / D, dd = e0 % D;
-    const long long src = (static_cast<long long>(b) * Hkv + g) * D + dd;
-    const long long tile = (static_cast<long long>(p) * Hkv + g) * kBlock * D;
-    const uint4 kraw = *reinterpret_cast<const uint4*>(k_new + src);
-    const uint4 vraw = *reinterpret_cast<const uint4*>(v_new + src);
-    uint4 raw[kBlock - 1];
-    if (ksum) {
-#pragma unroll
-      for (int s2 = 0; s2 < kBlock - 1; ++s2)
-        raw[s2] = *reinterpret_cast<const uint4*>(kc + tile + s2 * D + dd);
-    }
-    *reinterpret_cast<uint4*>(kc + tile + slot * D + dd) = kraw;
-    const T* kx = reinterpret_cast<const T*>(&kraw);
-    const T* vx = reinterpret_cast<const T*>(&vraw);
-#pragma unroll
-    for (int i = 0; i < VE; ++i) vc[tile + (dd + i) * kBlock + slot] = vx[i];
-    if (ksum) {
-      float sum[VE];
-#pragma unroll
-      for (int i = 0; i < VE; ++i) sum[i] = 0.f;
-#pragma unroll
-      for (int s2 = 0; s2 < kBlock - 1; ++s2) {
-        const T* x = reinterpret_cast<const T*>(&raw[s2]);
-        if (s2 < slot) {
-#pragma unroll
-          for (int i = 0; i < VE; ++i) sum[i] += load_elem<T>(x + i);
-        }
-      }
-      float* out = ksum + (static_cast<long long>(p) * Hkv + g) * D + dd;
-#pragma unroll
-      for (int i = 0; i < VE; ++i) out[i] = __fdiv_rn(sum[i] + load_elem<T>(kx + i), static_cast<float>(slot + 1));
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) ctx_lens[b] = N + 1;
+__global__ __launch_bounds__(kAppendThreads) void append_kernel(AppendArgs a) {
+  append_body<T>(a, blockIdx.x);
 }
 
 // Per-stage kernels over the shared bodies.
@@ -154,10 +97,10 @@ __global__ __launch_bounds__(kScoreThreads) void score_valu_kernel(
                         flags, blockIdx.x, blockIdx.y, smem);
 }
 
-__global__ __launch_bounds__(kRowThreads) void lse_merge_kernel(
+__global__ __launch_bounds__(kFoldThreads) void lse_merge_kernel(
     const float* __restrict__ lse_part, const int* __restrict__ ctx_lens, float* __restrict__ L,
     int Hq, int MAXB, int nch_max) {
-  __shared__ float s_pm[kRowThreads], s_ps[kRowThreads];
+  __shared__ float s_pm[kFoldThreads], s_ps[kFoldThreads];
   lse_merge_body(lse_part, ctx_lens, L + static_cast<long long>(blockIdx.x) * Hq, Hq, MAXB, nch_max,
                  blockIdx.x, s_pm, s_ps);
 }
@@ -182,19 +125,19 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 }
 
 // All three selection steps per sequence (short block tables).
-template <int HPL>
+template <int PASSES, int TILES>
 __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, const int* __restrict__ tables,
     const float* __restrict__ hvec, float* __restrict__ scores, float* __restrict__ theta_out,
     int* __restrict__ kept, int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P,
-    int nch_max, Budget bu, unsigned* flags) {
+    int nch_max, int Hq, Budget bu, unsigned* flags) {
   extern __shared__ unsigned keys[];        // [MAXB] keys, then [MAXB] encoded blocks
   __shared__ SelectShared sh;
   const int b = blockIdx.x;
-  select_fused_body<HPL>(zbuf, lse_part, ctx_lens, tables, hvec[b], scores, theta_out, kept,
-                         kphys, n_kept, MAXB, P, nch_max, bu, flags, b, keys,
-                         reinterpret_cast<int*>(keys + MAXB), sh);
+  select_fused_body<PASSES, TILES>(zbuf, lse_part, ctx_lens, tables, hvec[b], scores, theta_out,
+                                   kept, kphys, n_kept, MAXB, P, nch_max, Hq, bu, flags, b, keys,
+                                   reinterpret_cast<int*>(keys + MAXB), sh);
 }
 
 template <int D>
@@ -313,25 +256,17 @@ hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const in
   const ent_config& cf = c->cfg;
   const Budget bu = make_budget(cf, kappa);
   const size_t lds = static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-  const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
-  if (hpl) {
+  const int form = select_one_launch(cf.max_blocks_per_seq, cf.num_q_heads);
+  if (form) {
     const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-#define ENT_SEL_CASE(HH)                                                                       \
-  case HH:                                                                                     \
-    hipLaunchKernelGGL((select_fused_kernel<HH>), dim3(B), dim3(kSelThreads), lds, s, c->zbuf, \
-                       c->lse_part, ctx_lens, tables, h, scores, theta, kept, c->kept_phys,    \
-                       n_kept, cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, bu,   \
-                       c->dev_flags);                                                          \
-    break;
-    switch (hpl) {
-      ENT_SEL_CASE(1)
-      ENT_SEL_CASE(2)
-      ENT_SEL_CASE(4)
-      ENT_SEL_CASE(8)
-      default:
-        return hipErrorInvalidValue;
-    }
-#undef ENT_SEL_CASE
+#define ENT_SEL_LAUNCH(PP, TT)                                                                  \
+  hipLaunchKernelGGL((select_fused_kernel<PP, TT>), dim3(B), dim3(kSelThreads), lds, s, c->zbuf, \
+                     c->lse_part, ctx_lens, tables, h, scores, theta, kept, c->kept_phys,        \
+                     n_kept, cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks,           \
+                     cf.num_q_heads, bu, c->dev_flags)
+    if (form == 1) ENT_SEL_LAUNCH(8, 4);
+    else ENT_SEL_LAUNCH(16, 4);
+#undef ENT_SEL_LAUNCH
     return hipGetLastError();
   }
   hipError_t e = launch_lse_merge(c, B, ctx_lens, s);
@@ -344,7 +279,7 @@ hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const in
 
 hipError_t launch_lse_merge(const ent_ctx* c, int B, const int* ctx_lens, hipStream_t s) {
   const ent_config& cf = c->cfg;
-  hipLaunchKernelGGL(lse_merge_kernel, dim3(B), dim3(kRowThreads), 0, s, c->lse_part, ctx_lens,
+  hipLaunchKernelGGL(lse_merge_kernel, dim3(B), dim3(kFoldThreads), 0, s, c->lse_part, ctx_lens,
                      c->lrow, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks);
   return hipGetLastError();
 }
@@ -369,22 +304,35 @@ hipError_t launch_select_rows(const ent_ctx* c, int B, const int* tables, const 
   return hipGetLastError();
 }
 
+AppendArgs make_append_args(const ent_ctx* c, const void* k_new, const void* v_new,
+                            const int* tables, int* ctx_lens, void* k_cache, void* v_cache,
+                            float* ksum) {
+  const ent_config& cf = c->cfg;
+  AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.tables = tables;
+  a.ctx_lens = ctx_lens;
+  a.kc = k_cache;
+  a.vc = v_cache;
+  a.ksum = ksum;
+  a.Hkv = cf.num_kv_heads;
+  a.D = cf.head_dim;
+  a.MAXB = cf.max_blocks_per_seq;
+  a.P = cf.num_pool_blocks;
+  a.flags = c->dev_flags;
+  a.bf16 = cf.kv_dtype == ENT_BF16;
+  return a;
+}
+
 hipError_t launch_kv_append(const ent_ctx* c, int B, const void* k_new, const void* v_new,
                             const int* tables, int* ctx_lens, void* k_cache, void* v_cache,
                             float* ksum, hipStream_t s) {
-  const ent_config& cf = c->cfg;
-  if (cf.kv_dtype == ENT_BF16)
-    hipLaunchKernelGGL(append_kernel<uint16_t>, dim3(B), dim3(kThreads), 0, s,
-                       static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
-                       tables, ctx_lens, static_cast<uint16_t*>(k_cache),
-                       static_cast<uint16_t*>(v_cache), ksum, cf.num_kv_heads, cf.head_dim,
-                       cf.max_blocks_per_seq, cf.num_pool_blocks, c->dev_flags);
+  const AppendArgs a = make_append_args(c, k_new, v_new, tables, ctx_lens, k_cache, v_cache, ksum);
+  if (a.bf16)
+    hipLaunchKernelGGL(append_kernel<uint16_t>, dim3(B), dim3(kAppendThreads), 0, s, a);
   else
-    hipLaunchKernelGGL(append_kernel<float>, dim3(B), dim3(kThreads), 0, s,
-                       static_cast<const float*>(k_new), static_cast<const float*>(v_new), tables,
-                       ctx_lens, static_cast<float*>(k_cache), static_cast<float*>(v_cache), ksum,
-                       cf.num_kv_heads, cf.head_dim, cf.max_blocks_per_seq, cf.num_pool_blocks,
-                       c->dev_flags);
+    hipLaunchKernelGGL(append_kernel<float>, dim3(B), dim3(kAppendThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -331,24 +331,66 @@ __device__ __forceinline__ void budget_record(const Budget& bu, int b, float kap
 //  A. L_h = ln sum_b n_b e^{z_bh}, merged from the scoring pass's per-tile
 //     partials (one workgroup per sequence);
 //  B. I_b = (1/H_q) sum_h e^{z_bh + ln n_b - L_h} (L_h - z_bh) for every
-//     block, four lanes per block;
+//     block, H_q / 4 lanes per block (block_score_body);
 //  C. budget k from the entropy, the k-th largest score by an 8-bit radix
 //     select over the bits in which the scores differ, and ascending
 //     compaction of {b : I_b >= theta} with wave ballots.
-// When the block tables are short (kFusedSelectMaxBlocks), one workgroup per
-// sequence runs all three; otherwise B runs as its own chip-wide launch (one
+// When the block tables are short enough for the registers
+// (select_one_launch), one workgroup per sequence runs all three; otherwise
+// B runs as its own chip-wide launch (one
 // workgroup per 64 blocks) between two per-sequence launches, so long
 // sequences spread their exponentials over the chip.  Both forms perform the
 // same arithmetic in the same order, so their results are identical.
-constexpr int kRowThreads = 256;          // threads of the L merge
+constexpr int kRowThreads = 256;          // threads of the chip-wide block-score launch
 constexpr int kTileBlocks = 64;           // blocks per scoring workgroup of step B
 constexpr int kSelThreads = 512;          // step C (and the one-launch form)
 constexpr int kSelWaves = kSelThreads / 64;
-constexpr int kFusedSelectMaxBlocks = 1024;
+constexpr int kSelMaxBlocks = 2048;       // block-table width of the one-launch form, at most (LDS)
 
-// Step A for sequence b: the first kRowThreads threads fold, every thread of
-// the workgroup must call it.  Writes L_h to Lout[h] (-inf for an empty or
-// invalid sequence); Lout may be global or LDS memory.
+// Step A's fold of the per-tile partials (max, sum) of head h into L_h is
+// defined over kFoldThreads virtual threads, VPH = kFoldThreads / H_q per
+// head: virtual thread (h, v) folds tiles v, v + VPH, v + 2 VPH, ... (their
+// maximum first, then the rescaled sums: independent loads, no serial
+// rescaling chain), and the VPH partials of head h are then merged in v
+// order.  Launches of any size evaluate exactly this.
+constexpr int kFoldThreads = 512;
+
+// The fold of virtual thread vt (head vt % H_q) over the nch tiles.
+__device__ __forceinline__ void lse_fold_vthread(const float* __restrict__ lse_part, int Hq,
+                                                 int nch, int nch_max, int b, int vt, float& m,
+                                                 float& sum) {
+  const int vph = kFoldThreads / Hq;
+  m = -INFINITY;
+  sum = 0.f;
+  if (vt >= vph * Hq) return;
+  const int h = vt % Hq;
+  const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
+  for (int c = vt / Hq; c < nch; c += vph) m = fmaxf(m, lp[static_cast<long long>(c) * Hq * 2]);
+  if (m != -INFINITY)
+    for (int c = vt / Hq; c < nch; c += vph) {
+      const float mc = lp[static_cast<long long>(c) * Hq * 2];
+      sum += lp[static_cast<long long>(c) * Hq * 2 + 1] * expf(mc - m);
+    }
+}
+
+// The merge of head t's VPH partials (s_pm, s_ps indexed by virtual thread).
+__device__ __forceinline__ float lse_merge_head(const float* s_pm, const float* s_ps, int Hq, int t) {
+  const int vph = kFoldThreads / Hq;
+  float mm = -INFINITY, ss = 0.f;
+  for (int i = 0; i < vph; ++i) {
+    const float mc = s_pm[i * Hq + t], sc = s_ps[i * Hq + t];
+    if (mc == -INFINITY) continue;
+    const float mn = fmaxf(mm, mc);
+    ss = ss * expf(mm - mn) + sc * expf(mc - mn);
+    mm = mn;
+  }
+  return (mm == -INFINITY) ? -INFINITY : mm + logf(ss);
+}
+
+// Step A for sequence b (kFoldThreads threads: one virtual thread each):
+// writes L_h to Lout[h] (-inf for an empty or invalid sequence); every thread
+// of the workgroup must call it; Lout may be global or LDS memory; s_pm,
+// s_ps: LDS [kFoldThreads].
 __device__ __forceinline__ void lse_merge_body(const float* __restrict__ lse_part,
                                                const int* __restrict__ ctx_lens, float* Lout,
                                                int Hq, int MAXB, int nch_max, int b, float* s_pm,
@@ -357,60 +399,40 @@ __device__ __forceinline__ void lse_merge_body(const float* __restrict__ lse_par
   const int N = ctx_lens[b];
   const int nb = (N >= 0 && N <= MAXB * kBlock) ? (N + kBlock - 1) / kBlock : 0;
   const int nch = (nb + kMfmaChunk - 1) / kMfmaChunk;
-  const int per_head = kRowThreads / Hq;     // threads per head (Hq <= 128)
-  // Each thread folds a strided subset of the tiles of head t % Hq: first
-  // their maximum, then the rescaled sums (independent loads, no serial
-  // rescaling chain).
-  if (t < kRowThreads) {
-    float m = -INFINITY, sum = 0.f;
-    if (t < per_head * Hq) {
-      const int h = t % Hq;
-      const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
-      for (int c = t / Hq; c < nch; c += per_head) m = fmaxf(m, lp[static_cast<long long>(c) * Hq * 2]);
-      if (m != -INFINITY)
-        for (int c = t / Hq; c < nch; c += per_head) {
-          const float mc = lp[static_cast<long long>(c) * Hq * 2];
-          sum += lp[static_cast<long long>(c) * Hq * 2 + 1] * expf(mc - m);
-        }
-    }
-    s_pm[t] = m;
-    s_ps[t] = sum;
-  }
+  if (t < kFoldThreads) lse_fold_vthread(lse_part, Hq, nch, nch_max, b, t, s_pm[t], s_ps[t]);
   __syncthreads();
-  if (t < Hq) {
-    float mm = -INFINITY, ss = 0.f;
-    for (int i = 0; i < per_head; ++i) {
-      const float mc = s_pm[i * Hq + t], sc = s_ps[i * Hq + t];
-      if (mc == -INFINITY) continue;
-      const float mn = fmaxf(mm, mc);
-      ss = ss * expf(mm - mn) + sc * expf(mc - mn);
-      mm = mn;
-    }
-    Lout[t] = (mm == -INFINITY) ? -INFINITY : mm + logf(ss);
-  }
+  if (t < Hq) Lout[t] = lse_merge_head(s_pm, s_ps, Hq, t);
 }
 
-// Step B for block j of sequence b (context N, nb blocks) by the four lanes
-// qq = 0..3 of a lane quad (heads qq, qq + 4, ...); the score in every lane
-// of the quad.  sL: L_h in LDS.
-__device__ __forceinline__ float block_score_quad(const float* __restrict__ zbuf, const float* sL,
-                                                  int Hq, int MAXB, int b, int j, int N, int nb,
-                                                  int qq) {
-  float acc = 0.f;
-  if (j < nb) {
-    const float lnn = logf(static_cast<float>(j == nb - 1 ? N - kBlock * (nb - 1) : kBlock));
-    const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq;
-    for (int h = qq; h < Hq; h += 4) {
-      const float z = zr[h];
-      acc += expf(z + lnn - sL[h]) * (sL[h] - z);
-    }
-  }
-  acc += __shfl_xor(acc, 1);
-  acc += __shfl_xor(acc, 2);
-  return __fdiv_rn(acc, static_cast<float>(Hq));
+// Step B's sum over query heads.  A block's H_q heads are split between
+// LPB = H_q / HPLN lanes of HPLN consecutive heads each: HPLN = 4 when
+// H_q / 4 is a power of two (a lane's block logits are then one 16-byte
+// load, and a wave reads whole spans of the block-logit rows), otherwise one
+// lane takes all H_q heads.  A lane adds its heads' terms in head order, then
+// the LPB lanes add by an xor butterfly, which leaves the same float in each
+// of them; both selection forms use exactly this order.
+__host__ __device__ inline int heads_per_lane(int Hq) {
+  const int l = Hq / 4;
+  return (Hq % 4 == 0 && (l & (l - 1)) == 0) ? 4 : Hq;
 }
 
-// Step B as its own launch: blocks j0 .. j0 + 63 of sequence b by 256 threads.
+// Term of head h in I_b: e^{z + ln n_b - L_h} (L_h - z).
+__device__ __forceinline__ float score_term(float z, float lnn, float L) {
+  return expf(z + lnn - L) * (L - z);
+}
+
+__device__ __forceinline__ float lanes_sum(float acc, int LPB) {
+  for (int o = 1; o < LPB; o <<= 1) acc += __shfl_xor(acc, o);
+  return acc;
+}
+
+// ln n_b of block j (of nb; the last holds N - 16 (nb - 1) tokens).
+__device__ __forceinline__ float block_ln_count(int j, int N, int nb) {
+  return logf(static_cast<float>(j == nb - 1 ? N - kBlock * (nb - 1) : kBlock));
+}
+
+// Step B as its own launch: blocks j0 .. j0 + 63 of sequence b by 256
+// threads, in passes of 256 / LPB blocks.
 __device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
                                                  const float* __restrict__ L,
                                                  const int* __restrict__ ctx_lens,
@@ -423,9 +445,31 @@ __device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
   if (j0 >= nb) return;
   for (int h = t; h < Hq; h += kRowThreads) sL[h] = L[static_cast<long long>(b) * Hq + h];
   __syncthreads();
-  const int j = j0 + (t >> 2);
-  const float I = block_score_quad(zbuf, sL, Hq, MAXB, b, j, N, nb, t & 3);
-  if (j < nb && (t & 3) == 0) scores[static_cast<long long>(b) * MAXB + j] = I;
+  const int HPLN = heads_per_lane(Hq);
+  const int LPB = Hq / HPLN;
+  const int bpp = kRowThreads / LPB;
+  const int li = t % LPB;
+  for (int jp = j0; jp < j0 + kTileBlocks; jp += bpp) {
+    const int j = jp + t / LPB;
+    const bool ok = j < nb && j < j0 + kTileBlocks;
+    float acc = 0.f;
+    if (ok) {
+      const float lnn = block_ln_count(j, N, nb);
+      const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq + li * HPLN;
+      if (HPLN == 4) {
+        const float4 z4 = *reinterpret_cast<const float4*>(zr);
+        const int h = li * 4;
+        acc += score_term(z4.x, lnn, sL[h]);
+        acc += score_term(z4.y, lnn, sL[h + 1]);
+        acc += score_term(z4.z, lnn, sL[h + 2]);
+        acc += score_term(z4.w, lnn, sL[h + 3]);
+      } else {
+        for (int e = 0; e < HPLN; ++e) acc += score_term(zr[e], lnn, sL[li * HPLN + e]);
+      }
+    }
+    acc = lanes_sum(acc, LPB);
+    if (ok && li == 0) scores[static_cast<long long>(b) * MAXB + j] = __fdiv_rn(acc, static_cast<float>(Hq));
+  }
 }
 
 constexpr int kSelRankMax = 64;    // prefix groups this small are finished by counting ranks
@@ -433,7 +477,7 @@ constexpr int kSelRankMax = 64;    // prefix groups this small are finished by c
 struct SelectShared {
   unsigned hist[256];                // radix histogram, then the last candidates
   unsigned red[2 * kSelWaves];
-  float pm[kRowThreads], ps[kRowThreads], L[128];
+  float pm[kFoldThreads], ps[kFoldThreads], L[128];
   int digit, krem, ncand, wcnt[kSelWaves];
   unsigned rv;
 };
@@ -660,131 +704,141 @@ __device__ __forceinline__ void select_row_body(
   select_core(keys, tbl, nb, k, theta_out, kept, kphys, n_kept, MAXB, b, sh);
 }
 
-// Steps A, B and C in one workgroup (short block tables), in two parts so
-// that a caller can overlap other work with the loads: select_load issues
-// every global read of the sequence at once (its block logits, four lanes
-// per block and HPL = H_q / 4 heads per lane, and the per-tile log-sum-exp
-// partials of the L merge) into registers, for the whole block-table row,
-// so that no load waits for the context length (entries past the sequence's
-// blocks are read and never used); select_finish merges L, scores the blocks
-// and selects.  The arithmetic, and its order, is that of the
-// three-launch form (lse_merge_body, block_score_quad, select_core).
-constexpr int kFusedRegs = 32;            // logits per lane, at most
-constexpr int kFusedTiles = 8;            // L-merge tiles per thread, at most
+// Steps A, B and C in one workgroup (block tables up to kSelMaxBlocks wide,
+// H_q / 4 a power of two), in two parts so that a caller can overlap other
+// work with the loads: select_load issues every global read of the sequence
+// at once into registers, for the whole block-table row, so that no load
+// waits for the context length (entries past the sequence's blocks are read
+// and never used): the block logits (LPB = H_q / 4 lanes per block, one
+// 16-byte load of four heads per lane and pass), the table entries (thread
+// t takes entries t, t + 512, ...) and the per-tile log-sum-exp partials of
+// the L merge; select_finish merges L, scores the blocks and selects.  The
+// arithmetic, and its order, is that of the three-launch form
+// (lse_merge_body, block_score_body, select_core).  PASSES and TILES size the
+// registers: the passes of kSelThreads / LPB blocks and the L-merge tiles
+// per thread that the block-table width needs (two sizes, select_one_launch).
+constexpr int kSelTableRegs = kSelMaxBlocks / kSelThreads;
 
-template <int HPL>
+typedef float sel_f32x4 __attribute__((ext_vector_type(4)));
+
+template <int PASSES, int TILES>
 struct SelectRegs {
-  static constexpr int kPasses = kFusedRegs / HPL;   // 128 blocks per pass
-  float z[kFusedRegs];
-  float2 pr[kFusedTiles];
-  int tb[kPasses];                         // table entries (lanes qq == 0)
+  sel_f32x4 z[PASSES];
+  float2 pr[TILES];
+  int tb[kSelTableRegs];
 };
 
-// Whether the one-launch form applies (both the staged and the fused step
-// decide with this, so they take the same form).
-__host__ __device__ inline int select_one_launch_hpl(int MAXB, int Hq) {
-  if (MAXB > kFusedSelectMaxBlocks || (Hq != 4 && Hq != 8 && Hq != 16 && Hq != 32)) return 0;
-  const int hpl = Hq / 4;
+// Register sizes of the one-launch form: 1 (8 passes, 4 tiles), 2 (16
+// passes, 4 tiles), or 0 when the three-launch form applies.  Both the staged
+// and the fused step decide with this, so they take the same form.
+constexpr int kSelMaxTerms = 32768;      // H_q x block-table width of the one-launch form, at most
+
+__host__ __device__ inline int select_one_launch(int MAXB, int Hq) {
+  // One workgroup evaluates every head's term of every block of its
+  // sequence; beyond kSelMaxTerms the chip-wide block scores of the
+  // three-launch form are faster (64 heads x 1028 blocks: 37 us against 30 us).
+  if (Hq > 128 || heads_per_lane(Hq) != 4 || MAXB > kSelMaxBlocks) return 0;
+  if (static_cast<long long>(Hq) * MAXB > kSelMaxTerms) return 0;
+  const int bpp = kSelThreads / (Hq / 4);
+  const int passes = (MAXB + bpp - 1) / bpp;
   const int nch = (MAXB + kMfmaChunk - 1) / kMfmaChunk;
-  const int per_head = kRowThreads / Hq;
-  if (MAXB > (kFusedRegs / hpl) * (kSelThreads / 4)) return 0;
-  if ((nch + per_head - 1) / per_head > kFusedTiles) return 0;
-  return hpl;
+  const int vph = kFoldThreads / Hq;
+  const int tiles = (nch + vph - 1) / vph;
+  if (passes <= 8 && tiles <= 4) return 1;
+  if (passes <= 16 && tiles <= 4) return 2;
+  return 0;
 }
 
-template <int HPL>
+template <int PASSES, int TILES>
 __device__ __forceinline__ void select_load(const float* __restrict__ zbuf,
                                             const float* __restrict__ lse_part,
                                             const int* __restrict__ tables, int MAXB,
-                                            int nch_max, int b, SelectRegs<HPL>& R) {
-  constexpr int Hq = 4 * HPL;
-  const int t = threadIdx.x, qq = t & 3;
-  const int nb = MAXB;
+                                            int nch_max, int b, int Hq,
+                                            SelectRegs<PASSES, TILES>& R) {
+  const int t = threadIdx.x;
+  const int LPB = Hq / 4;
+  const int bpp = kSelThreads / LPB;
+  const int li = t % LPB;
 #pragma unroll
-  for (int p = 0; p < SelectRegs<HPL>::kPasses; ++p) {
-    const int j = p * (kSelThreads / 4) + (t >> 2);
-    if (j < nb) {
-      const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq;
-#pragma unroll
-      for (int i = 0; i < HPL; ++i) R.z[p * HPL + i] = zr[qq + 4 * i];
-      if (qq == 0) R.tb[p] = tables[static_cast<long long>(b) * MAXB + j];
-    }
+  for (int p = 0; p < PASSES; ++p) {
+    const int j = p * bpp + t / LPB;
+    if (j < MAXB)
+      R.z[p] = *reinterpret_cast<const sel_f32x4*>(zbuf + (static_cast<long long>(b) * MAXB + j) * Hq + 4 * li);
   }
-  const int nch = (nb + kMfmaChunk - 1) / kMfmaChunk;
-  constexpr int per_head = kRowThreads / Hq;
-  if (t < per_head * Hq) {
+#pragma unroll
+  for (int i = 0; i < kSelTableRegs; ++i) {
+    const int j = t + i * kSelThreads;
+    if (j < MAXB) R.tb[i] = tables[static_cast<long long>(b) * MAXB + j];
+  }
+  static_assert(kSelThreads == kFoldThreads, "one virtual fold thread per thread");
+  const int nch = (MAXB + kMfmaChunk - 1) / kMfmaChunk;
+  const int vph = kFoldThreads / Hq;
+  if (t < vph * Hq) {
     const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + t % Hq) * 2;
 #pragma unroll
-    for (int i = 0; i < kFusedTiles; ++i) {
-      const int c = t / Hq + i * per_head;
+    for (int i = 0; i < TILES; ++i) {
+      const int c = t / Hq + i * vph;
       if (c < nch) R.pr[i] = *reinterpret_cast<const float2*>(lp + static_cast<long long>(c) * Hq * 2);
     }
   }
 }
 
-template <int HPL>
+template <int PASSES, int TILES>
 __device__ __forceinline__ void select_finish(
-    const SelectRegs<HPL>& R, int N, int nb, float hval, float* __restrict__ scores_out,
+    const SelectRegs<PASSES, TILES>& R, int N, int nb, float hval, float* __restrict__ scores_out,
     float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ kphys,
-    int* __restrict__ n_kept, int MAXB, int P, const Budget& bu, float kprev, int b,
+    int* __restrict__ n_kept, int MAXB, int P, const Budget& bu, float kprev, int b, int Hq,
     unsigned* keys, int* tbl, SelectShared& sh) {
-  constexpr int Hq = 4 * HPL;
-  constexpr int per_head = kRowThreads / Hq;
+  const int vph = kFoldThreads / Hq;
   const int t = threadIdx.x;
-  // Step A (the fold of lse_merge_body, from the registers).
+  // Step A (lse_fold_vthread and lse_merge_head, from the registers).
   const int nch = (nb + kMfmaChunk - 1) / kMfmaChunk;
-  if (t < kRowThreads) {
+  {
     float m = -INFINITY, sum = 0.f;
-    if (t < per_head * Hq) {
+    if (t < vph * Hq) {
 #pragma unroll
-      for (int i = 0; i < kFusedTiles; ++i)
-        if (t / Hq + i * per_head < nch) m = fmaxf(m, R.pr[i].x);
+      for (int i = 0; i < TILES; ++i)
+        if (t / Hq + i * vph < nch) m = fmaxf(m, R.pr[i].x);
       if (m != -INFINITY) {
 #pragma unroll
-        for (int i = 0; i < kFusedTiles; ++i)
-          if (t / Hq + i * per_head < nch) sum += R.pr[i].y * expf(R.pr[i].x - m);
+        for (int i = 0; i < TILES; ++i)
+          if (t / Hq + i * vph < nch) sum += R.pr[i].y * expf(R.pr[i].x - m);
       }
     }
     sh.pm[t] = m;
     sh.ps[t] = sum;
   }
   __syncthreads();
-  if (t < Hq) {
-    float mm = -INFINITY, ss = 0.f;
-    for (int i = 0; i < per_head; ++i) {
-      const float mc = sh.pm[i * Hq + t], sc = sh.ps[i * Hq + t];
-      if (mc == -INFINITY) continue;
-      const float mn = fmaxf(mm, mc);
-      ss = ss * expf(mm - mn) + sc * expf(mc - mn);
-      mm = mn;
-    }
-    sh.L[t] = (mm == -INFINITY) ? -INFINITY : mm + logf(ss);
-  }
+  if (t < Hq) sh.L[t] = lse_merge_head(sh.pm, sh.ps, Hq, t);
   __syncthreads();
-  // Step B (block_score_quad on the registers).
-  const int qq = t & 3;
+  // Step B (block_score_body's head sum, on the registers).
+  const int LPB = Hq / 4;
+  const int bpp = kSelThreads / LPB;
+  const int li = t % LPB;
 #pragma unroll
-  for (int p = 0; p < SelectRegs<HPL>::kPasses; ++p) {
-    const int j = p * (kSelThreads / 4) + (t >> 2);
-    if (p * (kSelThreads / 4) >= nb) break;
+  for (int p = 0; p < PASSES; ++p) {
+    if (p * bpp >= nb) break;
+    const int j = p * bpp + t / LPB;
     float acc = 0.f;
     if (j < nb) {
-      const float lnn = logf(static_cast<float>(j == nb - 1 ? N - kBlock * (nb - 1) : kBlock));
-#pragma unroll
-      for (int i = 0; i < HPL; ++i) {
-        const int h = qq + 4 * i;
-        const float z = R.z[p * HPL + i];
-        acc += expf(z + lnn - sh.L[h]) * (sh.L[h] - z);
-      }
+      const float lnn = block_ln_count(j, N, nb);
+      const int h = li * 4;
+      acc += score_term(R.z[p].x, lnn, sh.L[h]);
+      acc += score_term(R.z[p].y, lnn, sh.L[h + 1]);
+      acc += score_term(R.z[p].z, lnn, sh.L[h + 2]);
+      acc += score_term(R.z[p].w, lnn, sh.L[h + 3]);
     }
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
+    acc = lanes_sum(acc, LPB);
     const float I = __fdiv_rn(acc, static_cast<float>(Hq));
-    if (j < nb && qq == 0) {
+    if (j < nb && li == 0) {
       keys[j] = select_key(I, j, nb, bu);
-      tbl[j] = encode_phys(R.tb[p], j, nb, P);
       if (scores_out) scores_out[static_cast<long long>(b) * MAXB + j] = I;
     }
+  }
+#pragma unroll
+  for (int i = 0; i < kSelTableRegs; ++i) {
+    const int j = t + i * kSelThreads;
+    if (j < nb) tbl[j] = encode_phys(R.tb[i], j, nb, P);
   }
   __syncthreads();
   float ku;
@@ -798,22 +852,97 @@ __device__ __forceinline__ void select_finish(
 }
 
 // The one-launch selection of sequence b with its entropy in hval.
-template <int HPL>
+template <int PASSES, int TILES>
 __device__ __forceinline__ void select_fused_body(
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, const int* __restrict__ tables, float hval,
     float* __restrict__ scores_out, float* __restrict__ theta_out, int* __restrict__ kept,
-    int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P, int nch_max,
+    int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P, int nch_max, int Hq,
     const Budget& bu, unsigned* flags, int b, unsigned* keys, int* tbl, SelectShared& sh) {
-  SelectRegs<HPL> R;
-  select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, R);
+  SelectRegs<PASSES, TILES> R;
+  select_load<PASSES, TILES>(zbuf, lse_part, tables, MAXB, nch_max, b, Hq, R);
   const int N = ctx_lens[b];
   const float kprev = budget_prev(bu, b);
   int nb, k;
   if (!select_prepare(N, hval, theta_out, n_kept, MAXB, bu, kprev, flags, b, nb, k))
     return;
-  select_finish<HPL>(R, N, nb, hval, scores_out, theta_out, kept, kphys, n_kept, MAXB, P, bu,
-                     kprev, b, keys, tbl, sh);
+  select_finish<PASSES, TILES>(R, N, nb, hval, scores_out, theta_out, kept, kphys, n_kept, MAXB,
+                               P, bu, kprev, b, Hq, keys, tbl, sh);
+}
+
+// Append of one token to sequence b's cache by one workgroup of
+// kAppendThreads threads (ent_kv_append): write its key and value at
+// position N = ctx_lens[b], refresh its block's mean key, set ctx_lens[b] =
+// N + 1.  The block's mean is the sum of its valid slots in slot order,
+// divided by their number (correctly rounded), as the summary pass computes
+// it, so both give the same bits.
+constexpr int kAppendThreads = 256;
+
+template <typename T>
+__device__ __forceinline__ void append_body(const AppendArgs& a, int b) {
+  const T* __restrict__ k_new = static_cast<const T*>(a.k_new);
+  const T* __restrict__ v_new = static_cast<const T*>(a.v_new);
+  const int* __restrict__ tables = a.tables;
+  int* __restrict__ ctx_lens = a.ctx_lens;
+  T* __restrict__ kc = static_cast<T*>(a.kc);
+  T* __restrict__ vc = static_cast<T*>(a.vc);
+  float* __restrict__ ksum = a.ksum;
+  const int Hkv = a.Hkv, D = a.D, MAXB = a.MAXB, P = a.P;
+  unsigned* flags = a.flags;
+  const int N = ctx_lens[b];
+  if (N < 0 || N >= MAXB * kBlock) {
+    if (threadIdx.x == 0) raise_flag(flags, N < 0 ? ENT_DEV_BAD_CTXLEN : ENT_DEV_CACHE_FULL);
+    return;
+  }
+  const int j = N / kBlock, slot = N % kBlock;
+  const int p = tables[static_cast<long long>(b) * MAXB + j];
+  if (p < 0 || p >= P) {
+    if (threadIdx.x == 0) raise_flag(flags, ENT_DEV_BAD_TABLE);
+    return;
+  }
+  // Each thread takes VE consecutive elements of one KV head's row (16
+  // bytes): the new key and value, and (for the block's mean) the earlier
+  // slots' keys, all loaded at once (slots from `slot` on are read and not
+  // used: the tile always holds 16); each element is then summed in slot
+  // order, the new key last.
+  constexpr int VE = 16 / sizeof(T);
+  for (int v = threadIdx.x; v < Hkv * D / VE; v += kAppendThreads) {
+    const int e0 = v * VE;
+    const int g = e0 / D, dd = e0 % D;
+    const long long src = (static_cast<long long>(b) * Hkv + g) * D + dd;
+    const long long tile = (static_cast<long long>(p) * Hkv + g) * kBlock * D;
+    const uint4 kraw = *reinterpret_cast<const uint4*>(k_new + src);
+    const uint4 vraw = *reinterpret_cast<const uint4*>(v_new + src);
+    uint4 raw[kBlock - 1];
+    if (ksum) {
+#pragma unroll
+      for (int s2 = 0; s2 < kBlock - 1; ++s2)
+        raw[s2] = *reinterpret_cast<const uint4*>(kc + tile + s2 * D + dd);
+    }
+    *reinterpret_cast<uint4*>(kc + tile + slot * D + dd) = kraw;
+    const T* kx = reinterpret_cast<const T*>(&kraw);
+    const T* vx = reinterpret_cast<const T*>(&vraw);
+#pragma unroll
+    for (int i = 0; i < VE; ++i) vc[tile + (dd + i) * kBlock + slot] = vx[i];
+    if (ksum) {
+      float sum[VE];
+#pragma unroll
+      for (int i = 0; i < VE; ++i) sum[i] = 0.f;
+#pragma unroll
+      for (int s2 = 0; s2 < kBlock - 1; ++s2) {
+        const T* x = reinterpret_cast<const T*>(&raw[s2]);
+        if (s2 < slot) {
+#pragma unroll
+          for (int i = 0; i < VE; ++i) sum[i] += load_elem<T>(x + i);
+        }
+      }
+      float* out = ksum + (static_cast<long long>(p) * Hkv + g) * D + dd;
+#pragma unroll
+      for (int i = 0; i < VE; ++i) out[i] = __fdiv_rn(sum[i] + load_elem<T>(kx + i), static_cast<float>(slot + 1));
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) ctx_lens[b] = N + 1;
 }
 
 }  // namespace

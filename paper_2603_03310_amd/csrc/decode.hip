@@ -33,7 +33,7 @@
 //         about 16 bits.
 // fp32 path (VALU): the same decomposition with scalar dot products.
 
-#include "ent_internal.h"
+#include "blocks_dev.h"
 
 #include <math.h>
 
@@ -689,6 +689,19 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
   combine_body<D>(a, blockIdx.x);
 }
 
+// The merge and, on workgroups of their own, the append of one token per
+// sequence (ent_decode_step_append): the merge reads only partials and
+// records and writes outputs, none of which the append touches, and the
+// kernels that read the lengths and the cache tiles have finished.
+template <int D, typename T>
+__global__ __launch_bounds__(kThreads) void combine_append_kernel(DecodeArgs a, AppendArgs ap) {
+  static_assert(kThreads == kAppendThreads, "append workgroup size");
+  // The appends' workgroups come first: their chains of dependent loads
+  // then overlap the merge instead of following it.
+  if (static_cast<int>(blockIdx.x) < a.B) append_body<T>(ap, blockIdx.x);
+  else combine_body<D>(a, blockIdx.x - a.B);
+}
+
 template <typename K>
 int occupancy_blocks(K kernel, size_t lds) {
   int n = 0;
@@ -729,7 +742,7 @@ long long decode_partial_slots(int decode_grid, int max_batch, int num_kv_heads)
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
-                         hipStream_t s, const int* kept_phys) {
+                         hipStream_t s, const int* kept_phys, const AppendArgs* ap) {
   const ent_config& cf = c->cfg;
   DecodeArgs a;
   a.q = q;
@@ -772,7 +785,22 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   if (e != hipSuccess) return e;
   // Slices per segment: one output per merge thread.
   a.nsl = std::max(1, c->group * cf.head_dim / kThreads);
-  const dim3 cgrid(a.R * a.nsl);
+  const int n_combine = a.R * a.nsl;
+  if (ap) {
+    const dim3 g2(n_combine + B);
+#define ENT_COMBINE_APPEND(DD)                                                                  \
+  do {                                                                                        \
+    if (ap->bf16)                                                                             \
+      hipLaunchKernelGGL((combine_append_kernel<DD, uint16_t>), g2, dim3(kThreads), 0, s, a, *ap); \
+    else                                                                                      \
+      hipLaunchKernelGGL((combine_append_kernel<DD, float>), g2, dim3(kThreads), 0, s, a, *ap);    \
+  } while (0)
+    if (cf.head_dim == 128) ENT_COMBINE_APPEND(128);
+    else ENT_COMBINE_APPEND(64);
+#undef ENT_COMBINE_APPEND
+    return hipGetLastError();
+  }
+  const dim3 cgrid(n_combine);
   if (cf.head_dim == 128)
     hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), 0, s, a);
   else

@@ -37,6 +37,21 @@ struct Budget {
   float* kappa;   // nullable [B]: previous kept fraction (NaN = none), updated in place
 };
 
+// Arguments of the append body (ent_kv_append), which also runs inside the
+// last launch of ent_decode_step_append.
+struct AppendArgs {
+  const void* k_new;
+  const void* v_new;
+  const int* tables;
+  int* ctx_lens;
+  void* kc;
+  void* vc;
+  float* ksum;
+  int Hkv, D, MAXB, P;
+  unsigned* flags;
+  bool bf16;
+};
+
 }  // namespace ent
 
 struct ent_ctx {
@@ -157,17 +172,23 @@ struct SampleArgs {
 
 // kept_phys (nullable): the selection's encoded physical blocks of the same
 // kept lists, read instead of kept + tables.
+// ap (nullable): an append of one token per sequence that shares the launch
+// merging the split attention segments (it reads nothing that launch writes).
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
-                         hipStream_t s, const int* kept_phys = nullptr);
+                         hipStream_t s, const int* kept_phys = nullptr,
+                         const AppendArgs* ap = nullptr);
 hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
                               ent_state st, const void* q, const void* k_cache,
                               const void* v_cache, const float* ksum, const int* tables,
                               const int* ctx_lens, const float* uniforms, float* h_out,
                               float* temp_used, float* row_stats, int* kept, int* n_kept,
                               float* out, float* lse, int* tokens, float* scores, float* theta,
-                              hipStream_t s);
+                              hipStream_t s, const AppendArgs* ap = nullptr);
+AppendArgs make_append_args(const ent_ctx* c, const void* k_new, const void* v_new,
+                            const int* tables, int* ctx_lens, void* k_cache, void* v_cache,
+                            float* ksum);
 hipError_t launch_kv_append(const ent_ctx* c, int B, const void* k_new, const void* v_new,
                             const int* tables, int* ctx_lens, void* k_cache, void* v_cache,
                             float* ksum, hipStream_t s);

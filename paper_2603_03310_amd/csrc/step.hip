@@ -15,7 +15,8 @@
 //      own, sampling at T_t (it needs only the row statistics of A, so it
 //      runs on the CUs the per-sequence selection leaves idle);
 //   C  kept-block decode attention;
-//   D  the merge of split decode segments.
+//   D  the merge of split decode segments (ent_decode_step_append: and, on
+//      workgroups of their own, the append of the new token's K/V).
 
 #include "blocks_dev.h"
 #include "estimate_dev.h"
@@ -36,14 +37,14 @@ __device__ __forceinline__ void step_sample(const SampleArgs& sa, int b, SampleS
 // update (first wave), and L_h for the selection (all threads); workgroups
 // B .. 2B-1 sample.
 template <bool VEC>
-__global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
+__global__ __launch_bounds__(kFoldThreads) void step_b0_kernel(
     int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
     float* h_out, Control ct, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, float* __restrict__ L, int Hq, int MAXB, int nch_max,
     SampleArgs sa, int est, int est_k, const float* __restrict__ tmax) {
-  static_assert(kRowThreads >= kSampleThreads && kRowThreads >= kEstThreads, "workgroup size");
+  static_assert(kFoldThreads >= kSampleThreads && kFoldThreads >= kEstThreads, "workgroup size");
   extern __shared__ __attribute__((aligned(16))) unsigned est_lds[];
-  __shared__ float s_pm[kRowThreads], s_ps[kRowThreads];
+  __shared__ float s_pm[kFoldThreads], s_ps[kFoldThreads];
   __shared__ SampleShared ssh;
   __shared__ EstShared esh;
   const int b = blockIdx.x;
@@ -64,17 +65,18 @@ __global__ __launch_bounds__(kRowThreads) void step_b0_kernel(
                  s_pm, s_ps);
 }
 
-// Per sequence, short block tables: the selection's loads are issued first,
-// then the first wave computes the row's entropy and the controller update
-// while they are in flight, then the whole kept-block selection; workgroups
-// B .. 2B-1 sample.
-template <int HPL, bool VEC>
+// Per sequence, block tables that fit the one-launch selection: the
+// selection's loads are issued first, then the first wave computes the row's
+// entropy and the controller update while they are in flight (with an
+// estimator, the estimate comes first), then the whole kept-block selection;
+// workgroups B .. 2B-1 sample.
+template <int PASSES, int TILES, bool VEC>
 __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
     float* h_out, Control ct, const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, const int* __restrict__ tables, float* __restrict__ scores,
     float* __restrict__ theta, int* __restrict__ kept, int* __restrict__ kphys,
-    int* __restrict__ n_kept, int MAXB, int P, int nch_max, Budget bu, unsigned* flags,
+    int* __restrict__ n_kept, int MAXB, int P, int nch_max, int Hq, Budget bu, unsigned* flags,
     SampleArgs sa, int est, int est_k, const float* __restrict__ tmax) {
   static_assert(kSelThreads >= kSampleThreads && kSelThreads >= kEstThreads, "workgroup size");
   extern __shared__ __attribute__((aligned(16))) unsigned keys[];   // [MAXB] keys, [MAXB] blocks, estimator
@@ -87,28 +89,32 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     step_sample<VEC>(sa, b - B, ssh);
     return;
   }
-  SelectRegs<HPL> R;
-  select_load<HPL>(zbuf, lse_part, tables, MAXB, nch_max, b, R);
-  const int N = ctx_lens[b];
-  const float kprev = budget_prev(bu, b);
-  const bool ok = N >= 0 && N <= MAXB * kBlock;
-  const int nb = ok ? (N + kBlock - 1) / kBlock : 0;
+  SelectRegs<PASSES, TILES> R;
   if (est != ENT_EST_EXACT) {
+    // The estimate needs most registers itself: the selection's loads follow it.
     const float T = temp[b];
     const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T * sa.t_cal, b,
                                  keys + est_lds_offset(2 * MAXB), esh);
     if (threadIdx.x == 0) s_H = controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, ct);
-  } else if (threadIdx.x < 64) {
-    const float H = row_entropy(part, C, b);
-    if (threadIdx.x == 0)
-      s_H = controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, ct);
+    select_load<PASSES, TILES>(zbuf, lse_part, tables, MAXB, nch_max, b, Hq, R);
+  } else {
+    select_load<PASSES, TILES>(zbuf, lse_part, tables, MAXB, nch_max, b, Hq, R);
+    if (threadIdx.x < 64) {
+      const float H = row_entropy(part, C, b);
+      if (threadIdx.x == 0)
+        s_H = controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, ct);
+    }
   }
+  const int N = ctx_lens[b];
+  const float kprev = budget_prev(bu, b);
+  const bool ok = N >= 0 && N <= MAXB * kBlock;
+  const int nb = ok ? (N + kBlock - 1) / kBlock : 0;
   __syncthreads();
   const float H = s_H;
   int nb2, k;
   if (!select_prepare(N, H, theta, n_kept, MAXB, bu, kprev, flags, b, nb2, k)) return;
-  select_finish<HPL>(R, N, nb, H, scores, theta, kept, kphys, n_kept, MAXB, P, bu, kprev, b, keys,
-                     reinterpret_cast<int*>(keys + MAXB), sh);
+  select_finish<PASSES, TILES>(R, N, nb, H, scores, theta, kept, kphys, n_kept, MAXB, P, bu, kprev,
+                               b, Hq, keys, reinterpret_cast<int*>(keys + MAXB), sh);
 }
 }  // namespace
 
@@ -118,7 +124,7 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
                               const int* ctx_lens, const float* uniforms, float* h_out,
                               float* temp_used, float* row_stats, int* kept, int* n_kept,
                               float* out, float* lse, int* tokens, float* scores, float* theta,
-                              hipStream_t s) {
+                              hipStream_t s, const AppendArgs* ap) {
   const ent_config& cf = c->cfg;
   float* stats = row_stats ? row_stats : c->stats_tmp;
   const bool bf16 = cf.kv_dtype == ENT_BF16;
@@ -172,36 +178,27 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   const Control ct = make_control(cf);
   const Budget bu = make_budget(cf, st.kappa);
   const bool vec = row_vec_ok(logits, ld);
-  const int hpl = select_one_launch_hpl(cf.max_blocks_per_seq, cf.num_q_heads);
-  if (hpl) {
+  const int form = select_one_launch(cf.max_blocks_per_seq, cf.num_q_heads);
+  if (form) {
     const size_t lds =
         static_cast<size_t>(est_lds_offset(2 * cf.max_blocks_per_seq)) * sizeof(unsigned) + est_lds;
-#define ENT_STEPB_CASE(HH, VV)                                                                 \
-  hipLaunchKernelGGL((step_b_kernel<HH, VV>), dim3(2 * B), dim3(kSelThreads), lds, s, B,       \
-                     c->ent_part, c->chunks, st.temp, st.h_prev, st.tau, h_out, ct, c->zbuf,   \
-                     c->lse_part, ctx_lens, tables, scores, theta, kept, c->kept_phys, n_kept, \
-                     cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, bu,             \
-                     c->dev_flags, sa, est_mode, cf.est_k, c->tmax)
-#define ENT_STEPB_HPL(HH)                   \
-  case HH:                                  \
-    if (vec) ENT_STEPB_CASE(HH, true);      \
-    else ENT_STEPB_CASE(HH, false);         \
-    break;
-    switch (hpl) {
-      ENT_STEPB_HPL(1)
-      ENT_STEPB_HPL(2)
-      ENT_STEPB_HPL(4)
-      ENT_STEPB_HPL(8)
-      default:
-        return hipErrorInvalidValue;
+#define ENT_STEPB_CASE(PP, TT, VV)                                                               \
+  hipLaunchKernelGGL((step_b_kernel<PP, TT, VV>), dim3(2 * B), dim3(kSelThreads), lds, s, B,    \
+                     c->ent_part, c->chunks, st.temp, st.h_prev, st.tau, h_out, ct, c->zbuf,     \
+                     c->lse_part, ctx_lens, tables, scores, theta, kept, c->kept_phys, n_kept,   \
+                     cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, cf.num_q_heads,  \
+                     bu, c->dev_flags, sa, est_mode, cf.est_k, c->tmax)
+    if (form == 1) {
+      if (vec) ENT_STEPB_CASE(8, 4, true); else ENT_STEPB_CASE(8, 4, false);
+    } else {
+      if (vec) ENT_STEPB_CASE(16, 4, true); else ENT_STEPB_CASE(16, 4, false);
     }
-#undef ENT_STEPB_HPL
 #undef ENT_STEPB_CASE
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   } else {
     auto k0 = vec ? step_b0_kernel<true> : step_b0_kernel<false>;
-    hipLaunchKernelGGL(k0, dim3(2 * B), dim3(kRowThreads), est_lds, s, B, c->ent_part, c->chunks,
+    hipLaunchKernelGGL(k0, dim3(2 * B), dim3(kFoldThreads), est_lds, s, B, c->ent_part, c->chunks,
                        st.temp, st.h_prev, st.tau, h_out, ct, c->lse_part, ctx_lens, c->lrow,
                        cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks, sa, est_mode,
                        cf.est_k, c->tmax);
@@ -214,7 +211,7 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
     if (e != hipSuccess) return e;
   }
   return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s,
-                       c->kept_phys);
+                       c->kept_phys, ap);
 }
 
 }  // namespace ent

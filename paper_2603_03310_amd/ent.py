@@ -27,7 +27,8 @@ ENT_DEV_BAD_TABLE, ENT_DEV_BAD_CTXLEN, ENT_DEV_CACHE_FULL = 1, 2, 4
 EXPORTED = ("ent_default_config", "ent_check_config", "ent_row_stats_chunks", "ent_init",
             "ent_destroy", "ent_last_error", "ent_device_status", "ent_entropy_temperature",
             "ent_block_summary", "ent_block_select", "ent_sparse_paged_decode", "ent_sample",
-            "ent_kv_append", "ent_decode_step", "ent_schedule", "ent_entropy_temperature_noalloc")
+            "ent_kv_append", "ent_decode_step", "ent_schedule", "ent_entropy_temperature_noalloc",
+            "ent_decode_step_append")
 ENT_NOALLOC_SCRATCH_BYTES = 2 << 20
 ENT_SCHED_MAX_POOL = 8192
 
@@ -98,6 +99,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "ent_sample": (i, [vp, i, vp, ll, vp, vp, vp, vp, vp]),
         "ent_kv_append": (i, [vp, i, vp, vp, vp, vp, vp, vp, vp, vp]),
         "ent_decode_step": (i, [vp, i, vp, ll, ent_state] + [vp] * 18),
+        "ent_decode_step_append": (i, [vp, i, vp, ll, ent_state] + [vp] * 20),
         "ent_schedule": (i, [vp, i, ctypes.POINTER(ent_sched_params)] + [vp] * 6
                          + [i] + [vp] * 4),
     }
@@ -228,6 +230,18 @@ def ent_decode_step(ctx, B, logits, ld, h_prev, tau, temp, q, k_cache, v_cache, 
                                        ptr(uniforms), ptr(h_out), ptr(temp_used), ptr(row_stats),
                                        ptr(kept), ptr(n_kept), ptr(out), ptr(lse), ptr(tokens),
                                        ptr(scores), ptr(theta), _stream(stream)))
+
+
+def ent_decode_step_append(ctx, B, logits, ld, h_prev, tau, temp, q, k_cache, v_cache, ksum,
+                           block_tables, ctx_lens, uniforms, k_new, v_new, h_out, temp_used, kept,
+                           n_kept, out, tokens, row_stats=None, lse=None, scores=None, theta=None,
+                           stream=None, kappa=None):
+    st = ent_state(ptr(h_prev), ptr(tau), ptr(temp), ptr(kappa))
+    _check(ctx, load().ent_decode_step_append(
+        ctx, B, ptr(logits), ld, st, ptr(q), ptr(k_cache), ptr(v_cache), ptr(ksum),
+        ptr(block_tables), ptr(ctx_lens), ptr(uniforms), ptr(k_new), ptr(v_new), ptr(h_out),
+        ptr(temp_used), ptr(row_stats), ptr(kept), ptr(n_kept), ptr(out), ptr(lse), ptr(tokens),
+        ptr(scores), ptr(theta), _stream(stream)))
 
 
 def ent_schedule(ctx, N, prm: ent_sched_params, tau, n_kept, ctx_lens, tau_last, gain, age,

@@ -16,3 +16,12 @@ def pytest_configure(config):
 def gpu_available():
     import torch
     return torch.cuda.is_available()
+
+
+def pytest_terminal_summary(terminalreporter):
+    """The largest GPU-vs-oracle errors seen by check_step in this run."""
+    import sys
+    mod = sys.modules.get("tests.parity")
+    if mod is not None and any(mod.SEEN.values()):
+        terminalreporter.write_line(
+            "parity: largest errors seen: " + ", ".join(f"{k} {v:.3g}" for k, v in mod.SEEN.items()))

@@ -1,9 +1,9 @@
 """The 70B-shaped closed loop at full size and full length, against the oracle.
 
 Batch 128, 64/8 heads, d = 128, contexts U[4096, 16384], |V| = 128256: all
-64 steps run on the device as the benchmark runs them (ent_decode_step then
-ent_kv_append, the controller and kept-fraction state carried in device
-memory, each step appending its token's K/V).  At steps 0, 15, 31, 47 and 63
+64 steps run on the device as the benchmark runs them (ent_decode_step_append:
+the decode step, then the append of its token's K/V, the controller and
+kept-fraction state carried in device memory).  At steps 0, 15, 31, 47 and 63
 the step is checked against the oracle on sampled sequences, teacher-forced
 (tests/parity.py): the oracle reads the state the step started from, and
 host copies of the pools that receive the same appended tokens.  The late
@@ -16,7 +16,7 @@ import pytest
 from oracle import append as OAp
 from synth import LLAMA70B_LOOP, default_params, generate
 from synth.device import config_fields, upload
-from tests.parity import check_step, collect, run_step
+from tests.parity import check_step, collect
 from tests.test_gpu_parity import _sampled, torch_cuda  # noqa: F401
 
 pytestmark = pytest.mark.gpu
@@ -25,6 +25,7 @@ CHECK_STEPS = (0, 15, 31, 47, 63)
 
 
 def test_full_size_70b_loop_all_steps(torch_cuda):
+    from paper_2603_03310_amd import ent
     from paper_2603_03310_amd.runner import Decoder
     torch = torch_cuda
     w = LLAMA70B_LOOP
@@ -45,10 +46,19 @@ def test_full_size_70b_loop_all_steps(torch_cuda):
             if check:
                 torch.cuda.synchronize()
                 state = [a.cpu().numpy().copy() for a in (dev.h_prev, dev.tau, dev.temp, dev.kappa)]
-            run_step(dec, dev, t, kappa=True)
+                # The summaries the step scores with (the step's append then
+                # refreshes the last block's).
+                ksum_pre = dev.ksum.cpu().numpy().copy()
+            ent.ent_decode_step_append(dec.ctx, B, dev.logits[t], dev.logits.shape[2], dev.h_prev,
+                                       dev.tau, dev.temp, dev.q[t], dev.k_pool, dev.v_pool,
+                                       dev.ksum, dev.block_tables, dev.ctx_lens, dev.uniforms[t],
+                                       dev.k_new[t], dev.v_new[t], dev.h, dev.temp_used, dev.kept,
+                                       dev.n_kept, dev.out, dev.tokens, dev.row_stats, dev.lse,
+                                       dev.scores, dev.theta, None, dev.kappa)
             if check:
                 torch.cuda.synchronize()
                 gpu = collect(dev, with_kappa=True)
+                gpu.ksum = ksum_pre
                 nb_all = sum(-(-int(n) // 16) for n in ctx)
                 fractions[t] = float(gpu.n_kept.sum()) / nb_all
                 rep = check_step(k_pool=kp, v_pool=vp, tables=x.block_tables, ctx_lens=ctx,
@@ -60,8 +70,6 @@ def test_full_size_70b_loop_all_steps(torch_cuda):
                       f"{rep.max_score_err:.2e} (rel {rep.max_score_rel_err:.2e}), attention err "
                       f"{rep.max_att_err:.2e}, band {rep.band_exempt}", flush=True)
                 failures += [f"step {t}: {m}" for m in rep.failures]
-            dec.append(B, dev.k_new[t], dev.v_new[t], dev.block_tables, dev.ctx_lens, dev.k_pool,
-                       dev.v_pool, dev.ksum)
             # Only the sampled sequences' blocks are read on the host.
             for s in seqs:
                 ctx[s] = OAp.append_token(kp, vp, x.block_tables[s], int(ctx[s]), x.k_new[t, s],
