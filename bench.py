@@ -67,7 +67,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=59)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama70b_closed_loop")
-    ap.add_argument("--copies", type=int, default=2)
+    ap.add_argument("--copies", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--estimator", choices=["exact", "topk", "tail"], default="exact",
@@ -79,6 +79,8 @@ def parse():
                     help="block scores from mean keys, or from exact token-level weights")
     ap.add_argument("--keep-first", type=int, default=0, help="leading blocks always kept")
     ap.add_argument("--keep-last", type=int, default=0, help="trailing blocks always kept")
+    ap.add_argument("--q-heads", type=int, default=None,
+                    help="query heads (the GQA group is q-heads / the workload's KV heads)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -445,6 +447,8 @@ def main():
     if not os.path.exists(ent.LIB_PATH):
         ent.load()        # raises: the library has not been built (no fallback)
     w = WORKLOADS[args.workload]
+    if args.q_heads:
+        w = w.replace(num_q_heads=args.q_heads, name=f"{w.name}_q{args.q_heads}")
     p = default_params(w)
     est = {"exact": 0, "topk": 1, "tail": 2}[args.estimator]
     if est:

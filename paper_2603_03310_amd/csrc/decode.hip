@@ -192,10 +192,12 @@ __device__ __forceinline__ UnitMeta unit_meta(const DecodeArgs& a, int x, int u1
 
 // K and V tiles are read once per step: non-temporal loads (the nt bit)
 // measured 8% faster on the decode than plain loads (the queries, read by
-// every wave of a segment, keep plain loads: 1 us better).  The same bit made
-// the exact scoring's K reads and the block-summary gather slower, and the
-// logit pass no faster, so it is used here only.  Whole-row K loads staged
-// through LDS measured 1-2% faster than loads straight into the MFMA layout.
+// every wave of a segment, keep plain loads: 1 us better).  The exact
+// scoring mode's whole-row K loads (staged through LDS) use the bit too; it
+// made loads straight into the MFMA layout and the block-summary gather
+// slower, and the logit pass no faster, so those keep plain loads.
+// Whole-row K loads staged through LDS measured 1-2% faster than loads
+// straight into the MFMA layout.
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ bf16x8_t load_bf16x8(const uint16_t* p) {
