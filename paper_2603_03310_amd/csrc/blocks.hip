@@ -125,7 +125,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 }
 
 // All three selection steps per sequence (short block tables).
-template <int PASSES, int TILES>
+template <int F4>
 __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, const int* __restrict__ tables,
@@ -135,9 +135,9 @@ __global__ __launch_bounds__(kSelThreads) void select_fused_kernel(
   extern __shared__ unsigned keys[];        // [MAXB] keys, then [MAXB] encoded blocks
   __shared__ SelectShared sh;
   const int b = blockIdx.x;
-  select_fused_body<PASSES, TILES>(zbuf, lse_part, ctx_lens, tables, hvec[b], scores, theta_out,
-                                   kept, kphys, n_kept, MAXB, P, nch_max, Hq, bu, flags, b, keys,
-                                   reinterpret_cast<int*>(keys + MAXB), sh);
+  select_fused_body<F4>(zbuf, lse_part, ctx_lens, tables, hvec[b], scores, theta_out, kept, kphys,
+                        n_kept, MAXB, P, nch_max, Hq, bu, flags, b, keys,
+                        reinterpret_cast<int*>(keys + MAXB), sh);
 }
 
 template <int D>
@@ -259,13 +259,18 @@ hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const in
   const int form = select_one_launch(cf.max_blocks_per_seq, cf.num_q_heads);
   if (form) {
     const size_t lds = 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned);
-#define ENT_SEL_LAUNCH(PP, TT)                                                                  \
-  hipLaunchKernelGGL((select_fused_kernel<PP, TT>), dim3(B), dim3(kSelThreads), lds, s, c->zbuf, \
+#define ENT_SEL_LAUNCH(FF)                                                                      \
+  hipLaunchKernelGGL((select_fused_kernel<FF>), dim3(B), dim3(kSelThreads), lds, s, c->zbuf,     \
                      c->lse_part, ctx_lens, tables, h, scores, theta, kept, c->kept_phys,        \
                      n_kept, cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks,           \
                      cf.num_q_heads, bu, c->dev_flags)
-    if (form == 1) ENT_SEL_LAUNCH(8, 4);
-    else ENT_SEL_LAUNCH(16, 4);
+    switch (form) {
+      case 1: ENT_SEL_LAUNCH(1); break;
+      case 2: ENT_SEL_LAUNCH(2); break;
+      case 4: ENT_SEL_LAUNCH(4); break;
+      case 8: ENT_SEL_LAUNCH(8); break;
+      default: return hipErrorInvalidValue;
+    }
 #undef ENT_SEL_LAUNCH
     return hipGetLastError();
   }

@@ -351,8 +351,8 @@ constexpr int kSelMaxBlocks = 2048;       // block-table width of the one-launch
 // defined over kFoldThreads virtual threads, VPH = kFoldThreads / H_q per
 // head: virtual thread (h, v) folds tiles v, v + VPH, v + 2 VPH, ... (their
 // maximum first, then the rescaled sums: independent loads, no serial
-// rescaling chain), and the VPH partials of head h are then merged in v
-// order.  Launches of any size evaluate exactly this.
+// rescaling chain), and the VPH partials of head h are then merged by a
+// fixed pairwise tree.  Launches of any size evaluate exactly this.
 constexpr int kFoldThreads = 512;
 
 // The fold of virtual thread vt (head vt % H_q) over the nch tiles.
@@ -373,18 +373,33 @@ __device__ __forceinline__ void lse_fold_vthread(const float* __restrict__ lse_p
     }
 }
 
-// The merge of head t's VPH partials (s_pm, s_ps indexed by virtual thread).
-__device__ __forceinline__ float lse_merge_head(const float* s_pm, const float* s_ps, int Hq, int t) {
+// The merge of each head's VPH partials (s_pm, s_ps indexed by virtual
+// thread v H_q + h), as a fixed pairwise tree: at each level partial v takes
+// in partial v + st (st = VPH / 2, VPH / 4, ..., 1), in place.  Every thread
+// of the workgroup must call it (it holds the barriers); afterwards L_h =
+// s_pm[h] + ln s_ps[h] (lse_merged).
+__device__ __forceinline__ void lse_merge_tree(float* s_pm, float* s_ps, int Hq) {
   const int vph = kFoldThreads / Hq;
-  float mm = -INFINITY, ss = 0.f;
-  for (int i = 0; i < vph; ++i) {
-    const float mc = s_pm[i * Hq + t], sc = s_ps[i * Hq + t];
-    if (mc == -INFINITY) continue;
-    const float mn = fmaxf(mm, mc);
-    ss = ss * expf(mm - mn) + sc * expf(mc - mn);
-    mm = mn;
+  for (int st = vph >> 1; st >= 1; st >>= 1) {
+    for (int i = threadIdx.x; i < st * Hq; i += blockDim.x) {
+      const float m1 = s_pm[i], s1 = s_ps[i];
+      const float m2 = s_pm[i + st * Hq], s2 = s_ps[i + st * Hq];
+      if (m2 == -INFINITY) continue;
+      if (m1 == -INFINITY) {
+        s_pm[i] = m2;
+        s_ps[i] = s2;
+        continue;
+      }
+      const float mn = fmaxf(m1, m2);
+      s_pm[i] = mn;
+      s_ps[i] = s1 * expf(m1 - mn) + s2 * expf(m2 - mn);
+    }
+    __syncthreads();
   }
-  return (mm == -INFINITY) ? -INFINITY : mm + logf(ss);
+}
+
+__device__ __forceinline__ float lse_merged(const float* s_pm, const float* s_ps, int h) {
+  return s_pm[h] == -INFINITY ? -INFINITY : s_pm[h] + logf(s_ps[h]);
 }
 
 // Step A for sequence b (kFoldThreads threads: one virtual thread each):
@@ -401,19 +416,21 @@ __device__ __forceinline__ void lse_merge_body(const float* __restrict__ lse_par
   const int nch = (nb + kMfmaChunk - 1) / kMfmaChunk;
   if (t < kFoldThreads) lse_fold_vthread(lse_part, Hq, nch, nch_max, b, t, s_pm[t], s_ps[t]);
   __syncthreads();
-  if (t < Hq) Lout[t] = lse_merge_head(s_pm, s_ps, Hq, t);
+  lse_merge_tree(s_pm, s_ps, Hq);
+  if (t < Hq) Lout[t] = lse_merged(s_pm, s_ps, t);
 }
 
 // Step B's sum over query heads.  A block's H_q heads are split between
-// LPB = H_q / HPLN lanes of HPLN consecutive heads each: HPLN = 4 when
-// H_q / 4 is a power of two (a lane's block logits are then one 16-byte
-// load, and a wave reads whole spans of the block-logit rows), otherwise one
-// lane takes all H_q heads.  A lane adds its heads' terms in head order, then
-// the LPB lanes add by an xor butterfly, which leaves the same float in each
-// of them; both selection forms use exactly this order.
-__host__ __device__ inline int heads_per_lane(int Hq) {
+// LPB lanes of HPLN = H_q / LPB consecutive heads each: when H_q / 4 is a
+// power of two, LPB = min(4, H_q / 4) and a lane's block logits are HPLN / 4
+// 16-byte loads (a wave reads whole spans of the block-logit rows);
+// otherwise one lane takes all H_q heads.  A lane adds its heads' terms in
+// head order, then the LPB lanes add by an xor butterfly, which leaves the
+// same float in each of them; both selection forms use exactly this order.
+__host__ __device__ inline int lanes_per_block(int Hq) {
   const int l = Hq / 4;
-  return (Hq % 4 == 0 && (l & (l - 1)) == 0) ? 4 : Hq;
+  if (Hq % 4 != 0 || (l & (l - 1)) != 0) return 1;
+  return l < 4 ? l : 4;
 }
 
 // Term of head h in I_b: e^{z + ln n_b - L_h} (L_h - z).
@@ -421,8 +438,11 @@ __device__ __forceinline__ float score_term(float z, float lnn, float L) {
   return expf(z + lnn - L) * (L - z);
 }
 
+// LPB is 1, 2 or 4: constant offsets (cheap cross-lane moves), the levels
+// past LPB skipped uniformly.
 __device__ __forceinline__ float lanes_sum(float acc, int LPB) {
-  for (int o = 1; o < LPB; o <<= 1) acc += __shfl_xor(acc, o);
+  if (LPB > 1) acc += __shfl_xor(acc, 1);
+  if (LPB > 2) acc += __shfl_xor(acc, 2);
   return acc;
 }
 
@@ -445,8 +465,8 @@ __device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
   if (j0 >= nb) return;
   for (int h = t; h < Hq; h += kRowThreads) sL[h] = L[static_cast<long long>(b) * Hq + h];
   __syncthreads();
-  const int HPLN = heads_per_lane(Hq);
-  const int LPB = Hq / HPLN;
+  const int LPB = lanes_per_block(Hq);
+  const int HPLN = Hq / LPB;
   const int bpp = kRowThreads / LPB;
   const int li = t % LPB;
   for (int jp = j0; jp < j0 + kTileBlocks; jp += bpp) {
@@ -456,13 +476,15 @@ __device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
     if (ok) {
       const float lnn = block_ln_count(j, N, nb);
       const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq + li * HPLN;
-      if (HPLN == 4) {
-        const float4 z4 = *reinterpret_cast<const float4*>(zr);
-        const int h = li * 4;
-        acc += score_term(z4.x, lnn, sL[h]);
-        acc += score_term(z4.y, lnn, sL[h + 1]);
-        acc += score_term(z4.z, lnn, sL[h + 2]);
-        acc += score_term(z4.w, lnn, sL[h + 3]);
+      if (HPLN % 4 == 0) {
+        for (int f = 0; f < HPLN / 4; ++f) {
+          const float4 z4 = *reinterpret_cast<const float4*>(zr + 4 * f);
+          const int h = li * HPLN + 4 * f;
+          acc += score_term(z4.x, lnn, sL[h]);
+          acc += score_term(z4.y, lnn, sL[h + 1]);
+          acc += score_term(z4.z, lnn, sL[h + 2]);
+          acc += score_term(z4.w, lnn, sL[h + 3]);
+        }
       } else {
         for (int e = 0; e < HPLN; ++e) acc += score_term(zr[e], lnn, sL[li * HPLN + e]);
       }
@@ -704,66 +726,73 @@ __device__ __forceinline__ void select_row_body(
   select_core(keys, tbl, nb, k, theta_out, kept, kphys, n_kept, MAXB, b, sh);
 }
 
-// Steps A, B and C in one workgroup (block tables up to kSelMaxBlocks wide,
-// H_q / 4 a power of two), in two parts so that a caller can overlap other
-// work with the loads: select_load issues every global read of the sequence
-// at once into registers, for the whole block-table row, so that no load
-// waits for the context length (entries past the sequence's blocks are read
-// and never used): the block logits (LPB = H_q / 4 lanes per block, one
-// 16-byte load of four heads per lane and pass), the table entries (thread
-// t takes entries t, t + 512, ...) and the per-tile log-sum-exp partials of
-// the L merge; select_finish merges L, scores the blocks and selects.  The
-// arithmetic, and its order, is that of the three-launch form
-// (lse_merge_body, block_score_body, select_core).  PASSES and TILES size the
-// registers: the passes of kSelThreads / LPB blocks and the L-merge tiles
-// per thread that the block-table width needs (two sizes, select_one_launch).
+// Steps A, B and C in one workgroup (block tables up to kSelMaxBlocks wide
+// and H_q x width up to kSelMaxTerms, H_q / 4 a power of two), in two parts
+// so that a caller can overlap other work with the loads: select_load
+// issues every global read of the sequence at once into registers, for the
+// whole block-table row, so that no load waits for the context length
+// (entries past the sequence's blocks are read and never used): the block
+// logits (LPB lanes per block, F4 = H_q / (4 LPB) 16-byte loads of four
+// heads per lane and pass), the table entries (thread t takes entries t,
+// t + 512, ...) and the per-tile log-sum-exp partials of the L merge;
+// select_finish merges L, scores the blocks and selects.  The arithmetic,
+// and its order, is that of the three-launch form (lse_merge_body,
+// block_score_body, select_core).  The block logits take kSelZRegs float4
+// registers: 16 / F4 passes of kSelThreads / LPB blocks.
 constexpr int kSelTableRegs = kSelMaxBlocks / kSelThreads;
+constexpr int kSelZRegs = 16;
+constexpr int kSelTiles = 4;              // L-merge tiles per thread, at most
+constexpr int kSelMaxTerms = 32768;       // H_q x block-table width, at most
 
 typedef float sel_f32x4 __attribute__((ext_vector_type(4)));
 
-template <int PASSES, int TILES>
+template <int F4>
 struct SelectRegs {
-  sel_f32x4 z[PASSES];
-  float2 pr[TILES];
+  static constexpr int kPasses = kSelZRegs / F4;
+  sel_f32x4 z[kSelZRegs];
+  float2 pr[kSelTiles];
   int tb[kSelTableRegs];
 };
 
-// Register sizes of the one-launch form: 1 (8 passes, 4 tiles), 2 (16
-// passes, 4 tiles), or 0 when the three-launch form applies.  Both the staged
-// and the fused step decide with this, so they take the same form.
-constexpr int kSelMaxTerms = 32768;      // H_q x block-table width of the one-launch form, at most
-
+// F4 of the one-launch form (1, 2, 4 or 8), or 0 when the three-launch form
+// applies.  Both the staged and the fused step decide with this, so they
+// take the same form.  One workgroup evaluates every head's term of every
+// block of its sequence: beyond kSelMaxTerms the chip-wide block scores of
+// the three-launch form are faster (64 heads x 1028 blocks: 37 us against
+// 28 us).
 __host__ __device__ inline int select_one_launch(int MAXB, int Hq) {
-  // One workgroup evaluates every head's term of every block of its
-  // sequence; beyond kSelMaxTerms the chip-wide block scores of the
-  // three-launch form are faster (64 heads x 1028 blocks: 37 us against 30 us).
-  if (Hq > 128 || heads_per_lane(Hq) != 4 || MAXB > kSelMaxBlocks) return 0;
+  if (Hq > 128 || Hq % 4 != 0 || MAXB > kSelMaxBlocks) return 0;
+  const int lpb = lanes_per_block(Hq);
+  if (lpb * 4 > Hq || ((Hq / 4) & (Hq / 4 - 1)) != 0) return 0;
   if (static_cast<long long>(Hq) * MAXB > kSelMaxTerms) return 0;
-  const int bpp = kSelThreads / (Hq / 4);
+  const int f4 = Hq / (4 * lpb);
+  const int bpp = kSelThreads / lpb;
   const int passes = (MAXB + bpp - 1) / bpp;
   const int nch = (MAXB + kMfmaChunk - 1) / kMfmaChunk;
   const int vph = kFoldThreads / Hq;
   const int tiles = (nch + vph - 1) / vph;
-  if (passes <= 8 && tiles <= 4) return 1;
-  if (passes <= 16 && tiles <= 4) return 2;
-  return 0;
+  if (passes * f4 > kSelZRegs || tiles > kSelTiles) return 0;
+  return f4;
 }
 
-template <int PASSES, int TILES>
+template <int F4>
 __device__ __forceinline__ void select_load(const float* __restrict__ zbuf,
                                             const float* __restrict__ lse_part,
                                             const int* __restrict__ tables, int MAXB,
-                                            int nch_max, int b, int Hq,
-                                            SelectRegs<PASSES, TILES>& R) {
+                                            int nch_max, int b, int Hq, SelectRegs<F4>& R) {
   const int t = threadIdx.x;
-  const int LPB = Hq / 4;
-  const int bpp = kSelThreads / LPB;
-  const int li = t % LPB;
+  const int LPB = lanes_per_block(Hq);
+  const int lg = LPB == 4 ? 2 : LPB - 1;      // log2 LPB
+  const int bpp = kSelThreads >> lg;
+  const int li = t & (LPB - 1);
 #pragma unroll
-  for (int p = 0; p < PASSES; ++p) {
-    const int j = p * bpp + t / LPB;
-    if (j < MAXB)
-      R.z[p] = *reinterpret_cast<const sel_f32x4*>(zbuf + (static_cast<long long>(b) * MAXB + j) * Hq + 4 * li);
+  for (int p = 0; p < SelectRegs<F4>::kPasses; ++p) {
+    const int j = p * bpp + (t >> lg);
+    if (j < MAXB) {
+      const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq + li * (4 * F4);
+#pragma unroll
+      for (int f = 0; f < F4; ++f) R.z[p * F4 + f] = *reinterpret_cast<const sel_f32x4*>(zr + 4 * f);
+    }
   }
 #pragma unroll
   for (int i = 0; i < kSelTableRegs; ++i) {
@@ -776,32 +805,32 @@ __device__ __forceinline__ void select_load(const float* __restrict__ zbuf,
   if (t < vph * Hq) {
     const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + t % Hq) * 2;
 #pragma unroll
-    for (int i = 0; i < TILES; ++i) {
+    for (int i = 0; i < kSelTiles; ++i) {
       const int c = t / Hq + i * vph;
       if (c < nch) R.pr[i] = *reinterpret_cast<const float2*>(lp + static_cast<long long>(c) * Hq * 2);
     }
   }
 }
 
-template <int PASSES, int TILES>
+template <int F4>
 __device__ __forceinline__ void select_finish(
-    const SelectRegs<PASSES, TILES>& R, int N, int nb, float hval, float* __restrict__ scores_out,
+    const SelectRegs<F4>& R, int N, int nb, float hval, float* __restrict__ scores_out,
     float* __restrict__ theta_out, int* __restrict__ kept, int* __restrict__ kphys,
     int* __restrict__ n_kept, int MAXB, int P, const Budget& bu, float kprev, int b, int Hq,
     unsigned* keys, int* tbl, SelectShared& sh) {
   const int vph = kFoldThreads / Hq;
   const int t = threadIdx.x;
-  // Step A (lse_fold_vthread and lse_merge_head, from the registers).
+  // Step A (lse_fold_vthread and lse_merge_tree, from the registers).
   const int nch = (nb + kMfmaChunk - 1) / kMfmaChunk;
   {
     float m = -INFINITY, sum = 0.f;
     if (t < vph * Hq) {
 #pragma unroll
-      for (int i = 0; i < TILES; ++i)
+      for (int i = 0; i < kSelTiles; ++i)
         if (t / Hq + i * vph < nch) m = fmaxf(m, R.pr[i].x);
       if (m != -INFINITY) {
 #pragma unroll
-        for (int i = 0; i < TILES; ++i)
+        for (int i = 0; i < kSelTiles; ++i)
           if (t / Hq + i * vph < nch) sum += R.pr[i].y * expf(R.pr[i].x - m);
       }
     }
@@ -809,24 +838,30 @@ __device__ __forceinline__ void select_finish(
     sh.ps[t] = sum;
   }
   __syncthreads();
-  if (t < Hq) sh.L[t] = lse_merge_head(sh.pm, sh.ps, Hq, t);
+  lse_merge_tree(sh.pm, sh.ps, Hq);
+  if (t < Hq) sh.L[t] = lse_merged(sh.pm, sh.ps, t);
   __syncthreads();
   // Step B (block_score_body's head sum, on the registers).
-  const int LPB = Hq / 4;
-  const int bpp = kSelThreads / LPB;
-  const int li = t % LPB;
+  const int LPB = lanes_per_block(Hq);
+  const int lg = LPB == 4 ? 2 : LPB - 1;
+  const int bpp = kSelThreads >> lg;
+  const int li = t & (LPB - 1);
 #pragma unroll
-  for (int p = 0; p < PASSES; ++p) {
+  for (int p = 0; p < SelectRegs<F4>::kPasses; ++p) {
     if (p * bpp >= nb) break;
-    const int j = p * bpp + t / LPB;
+    const int j = p * bpp + (t >> lg);
     float acc = 0.f;
     if (j < nb) {
       const float lnn = block_ln_count(j, N, nb);
-      const int h = li * 4;
-      acc += score_term(R.z[p].x, lnn, sh.L[h]);
-      acc += score_term(R.z[p].y, lnn, sh.L[h + 1]);
-      acc += score_term(R.z[p].z, lnn, sh.L[h + 2]);
-      acc += score_term(R.z[p].w, lnn, sh.L[h + 3]);
+#pragma unroll
+      for (int f = 0; f < F4; ++f) {
+        const int h = li * (4 * F4) + 4 * f;
+        const sel_f32x4 z = R.z[p * F4 + f];
+        acc += score_term(z.x, lnn, sh.L[h]);
+        acc += score_term(z.y, lnn, sh.L[h + 1]);
+        acc += score_term(z.z, lnn, sh.L[h + 2]);
+        acc += score_term(z.w, lnn, sh.L[h + 3]);
+      }
     }
     acc = lanes_sum(acc, LPB);
     const float I = __fdiv_rn(acc, static_cast<float>(Hq));
@@ -852,22 +887,22 @@ __device__ __forceinline__ void select_finish(
 }
 
 // The one-launch selection of sequence b with its entropy in hval.
-template <int PASSES, int TILES>
+template <int F4>
 __device__ __forceinline__ void select_fused_body(
     const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, const int* __restrict__ tables, float hval,
     float* __restrict__ scores_out, float* __restrict__ theta_out, int* __restrict__ kept,
     int* __restrict__ kphys, int* __restrict__ n_kept, int MAXB, int P, int nch_max, int Hq,
     const Budget& bu, unsigned* flags, int b, unsigned* keys, int* tbl, SelectShared& sh) {
-  SelectRegs<PASSES, TILES> R;
-  select_load<PASSES, TILES>(zbuf, lse_part, tables, MAXB, nch_max, b, Hq, R);
+  SelectRegs<F4> R;
+  select_load<F4>(zbuf, lse_part, tables, MAXB, nch_max, b, Hq, R);
   const int N = ctx_lens[b];
   const float kprev = budget_prev(bu, b);
   int nb, k;
   if (!select_prepare(N, hval, theta_out, n_kept, MAXB, bu, kprev, flags, b, nb, k))
     return;
-  select_finish<PASSES, TILES>(R, N, nb, hval, scores_out, theta_out, kept, kphys, n_kept, MAXB,
-                               P, bu, kprev, b, Hq, keys, tbl, sh);
+  select_finish<F4>(R, N, nb, hval, scores_out, theta_out, kept, kphys, n_kept, MAXB, P, bu, kprev,
+                    b, Hq, keys, tbl, sh);
 }
 
 // Append of one token to sequence b's cache by one workgroup of

@@ -70,7 +70,7 @@ __global__ __launch_bounds__(kFoldThreads) void step_b0_kernel(
 // entropy and the controller update while they are in flight (with an
 // estimator, the estimate comes first), then the whole kept-block selection;
 // workgroups B .. 2B-1 sample.
-template <int PASSES, int TILES, bool VEC>
+template <int F4, bool VEC>
 __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
     float* h_out, Control ct, const float* __restrict__ zbuf, const float* __restrict__ lse_part,
@@ -89,16 +89,16 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
     step_sample<VEC>(sa, b - B, ssh);
     return;
   }
-  SelectRegs<PASSES, TILES> R;
+  SelectRegs<F4> R;
   if (est != ENT_EST_EXACT) {
     // The estimate needs most registers itself: the selection's loads follow it.
     const float T = temp[b];
     const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T * sa.t_cal, b,
                                  keys + est_lds_offset(2 * MAXB), esh);
     if (threadIdx.x == 0) s_H = controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, ct);
-    select_load<PASSES, TILES>(zbuf, lse_part, tables, MAXB, nch_max, b, Hq, R);
+    select_load<F4>(zbuf, lse_part, tables, MAXB, nch_max, b, Hq, R);
   } else {
-    select_load<PASSES, TILES>(zbuf, lse_part, tables, MAXB, nch_max, b, Hq, R);
+    select_load<F4>(zbuf, lse_part, tables, MAXB, nch_max, b, Hq, R);
     if (threadIdx.x < 64) {
       const float H = row_entropy(part, C, b);
       if (threadIdx.x == 0)
@@ -113,8 +113,8 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
   const float H = s_H;
   int nb2, k;
   if (!select_prepare(N, H, theta, n_kept, MAXB, bu, kprev, flags, b, nb2, k)) return;
-  select_finish<PASSES, TILES>(R, N, nb, H, scores, theta, kept, kphys, n_kept, MAXB, P, bu, kprev,
-                               b, Hq, keys, reinterpret_cast<int*>(keys + MAXB), sh);
+  select_finish<F4>(R, N, nb, H, scores, theta, kept, kphys, n_kept, MAXB, P, bu, kprev, b, Hq,
+                    keys, reinterpret_cast<int*>(keys + MAXB), sh);
 }
 }  // namespace
 
@@ -182,17 +182,26 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   if (form) {
     const size_t lds =
         static_cast<size_t>(est_lds_offset(2 * cf.max_blocks_per_seq)) * sizeof(unsigned) + est_lds;
-#define ENT_STEPB_CASE(PP, TT, VV)                                                               \
-  hipLaunchKernelGGL((step_b_kernel<PP, TT, VV>), dim3(2 * B), dim3(kSelThreads), lds, s, B,    \
+#define ENT_STEPB_CASE(FF, VV)                                                                   \
+  hipLaunchKernelGGL((step_b_kernel<FF, VV>), dim3(2 * B), dim3(kSelThreads), lds, s, B,        \
                      c->ent_part, c->chunks, st.temp, st.h_prev, st.tau, h_out, ct, c->zbuf,     \
                      c->lse_part, ctx_lens, tables, scores, theta, kept, c->kept_phys, n_kept,   \
                      cf.max_blocks_per_seq, cf.num_pool_blocks, c->lse_chunks, cf.num_q_heads,  \
                      bu, c->dev_flags, sa, est_mode, cf.est_k, c->tmax)
-    if (form == 1) {
-      if (vec) ENT_STEPB_CASE(8, 4, true); else ENT_STEPB_CASE(8, 4, false);
-    } else {
-      if (vec) ENT_STEPB_CASE(16, 4, true); else ENT_STEPB_CASE(16, 4, false);
+#define ENT_STEPB_F4(FF)                               \
+  case FF:                                             \
+    if (vec) ENT_STEPB_CASE(FF, true);                 \
+    else ENT_STEPB_CASE(FF, false);                    \
+    break;
+    switch (form) {
+      ENT_STEPB_F4(1)
+      ENT_STEPB_F4(2)
+      ENT_STEPB_F4(4)
+      ENT_STEPB_F4(8)
+      default:
+        return hipErrorInvalidValue;
     }
+#undef ENT_STEPB_F4
 #undef ENT_STEPB_CASE
     e = hipGetLastError();
     if (e != hipSuccess) return e;
