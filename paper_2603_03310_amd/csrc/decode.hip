@@ -440,20 +440,53 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   // Workgroup merge: consecutive slots of one segment (in unit order) are one
   // group; a group whose segment lies inside the workgroup's range is final,
   // else it becomes the workgroup's partial of that segment (slot wg + seg).
+  // First, per (slot, head), the slot's weight 2^(m - M) in its group and the
+  // group's (M, L), all slots' loads issued at once; then every output is one
+  // weighted sum over its group's slots, in slot order.
+  constexpr int kSlots = 2 * kWaves;
+  static_assert(kSlots * kMaxGroup <= kThreads, "one thread per (slot, head)");
+  static_assert(3 * kSlots * kMaxGroup * sizeof(float) <= sizeof(s_kst), "merge weights in the K rows");
+  // The K staging rows are dead once every wave has left its loop.
+  float* s_wf = reinterpret_cast<float*>(s_kst);
+  float* s_wm = s_wf + kSlots * kMaxGroup;
+  float* s_wl = s_wm + kSlots * kMaxGroup;
+  __syncthreads();
+  if (threadIdx.x < kSlots * kMaxGroup) {
+    const int k = threadIdx.x / kMaxGroup, r = threadIdx.x % kMaxGroup;
+    const int seg = s_cseg[k];
+    float f = 0.f, M = -INFINITY, L = 0.f;
+    if (seg >= 0 && r < G) {
+#pragma unroll
+      for (int kk = 0; kk < kSlots; ++kk)
+        if (s_cseg[kk] == seg && s_cml[(kk * kMaxGroup + r) * 2 + 1] > 0.f)
+          M = fmaxf(M, s_cml[(kk * kMaxGroup + r) * 2]);
+#pragma unroll
+      for (int kk = 0; kk < kSlots; ++kk) {
+        const float l = s_cml[(kk * kMaxGroup + r) * 2 + 1];
+        if (s_cseg[kk] != seg || !(l > 0.f)) continue;
+        const float fk = exp2f(s_cml[(kk * kMaxGroup + r) * 2] - M);
+        L += l * fk;
+        if (kk == k) f = fk;
+      }
+    }
+    s_wf[threadIdx.x] = f;
+    s_wm[threadIdx.x] = M;
+    s_wl[threadIdx.x] = L;
+  }
   __syncthreads();
   const int wg = blockIdx.x;
   const int g0 = range_begin(wg * kWaves, U, a.W), g1 = range_begin(wg * kWaves + kWaves, U, a.W);
   int owner = -1, owner_last = 0;            // cut segment that begins in this range
   int i = 0;
-  while (i < 2 * kWaves) {
+  while (i < kSlots) {
     const int seg = s_cseg[i];
     if (seg < 0) {
       ++i;
       continue;
     }
     int j = i + 1;
-    while (j < 2 * kWaves && (s_cseg[j] == seg || s_cseg[j] < 0)) ++j;
-    // Slots i .. j-1 with s_cseg == seg form the group.
+    while (j < kSlots && (s_cseg[j] == seg || s_cseg[j] < 0)) ++j;
+    // Slots i .. j-1 with s_cseg == seg form the group (the others weigh 0).
     const int b = seg / a.Hkv, g = seg % a.Hkv;
     const int seg_start = s_pref[b] + g * s_nk[b];
     const int seg_end = seg_start + s_nk[b];
@@ -465,19 +498,14 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
     }
     for (int o = threadIdx.x; o < G * D; o += kThreads) {
       const int r = o / D, d = o - r * D;
-      float M = -INFINITY;
-      for (int k = i; k < j; ++k)
-        if (s_cseg[k] == seg && s_cml[(k * kMaxGroup + r) * 2 + 1] > 0.f)
-          M = fmaxf(M, s_cml[(k * kMaxGroup + r) * 2]);
-      float L = 0.f, acc = 0.f;
-      for (int k = i; k < j; ++k) {
-        if (s_cseg[k] != seg) continue;
-        const float l = s_cml[(k * kMaxGroup + r) * 2 + 1];
-        if (!(l > 0.f)) continue;
-        const float f = exp2f(s_cml[(k * kMaxGroup + r) * 2] - M);
-        L += l * f;
-        acc += f * s_cacc[(static_cast<long long>(k) * G + r) * D + d];
+      float acc = 0.f;
+#pragma unroll
+      for (int k = 0; k < kSlots; ++k) {
+        const float f = s_wf[k * kMaxGroup + r];
+        const float v = s_cacc[(k * G + r) * D + d];
+        if (k >= i && k < j && f != 0.f) acc += f * v;
       }
+      const float M = s_wm[i * kMaxGroup + r], L = s_wl[i * kMaxGroup + r];
       if (whole) {
         const long long oh = static_cast<long long>(b) * Hq + g * G + r;
         a.out[oh * D + d] = L > 0.f ? acc / L : 0.f;
