@@ -355,7 +355,10 @@ constexpr int kSelMaxBlocks = 2048;       // block-table width of the one-launch
 // fixed pairwise tree.  Launches of any size evaluate exactly this.
 constexpr int kFoldThreads = 512;
 
-// The fold of virtual thread vt (head vt % H_q) over the nch tiles.
+// The fold of virtual thread vt (head vt % H_q) over the nch tiles.  Up to
+// kFoldRegs tiles per virtual thread are loaded at once into registers; past
+// that the two passes stream them (same arithmetic).
+constexpr int kFoldRegs = 16;
 __device__ __forceinline__ void lse_fold_vthread(const float* __restrict__ lse_part, int Hq,
                                                  int nch, int nch_max, int b, int vt, float& m,
                                                  float& sum) {
@@ -365,9 +368,25 @@ __device__ __forceinline__ void lse_fold_vthread(const float* __restrict__ lse_p
   if (vt >= vph * Hq) return;
   const int h = vt % Hq;
   const float* lp = lse_part + (static_cast<long long>(b) * nch_max * Hq + h) * 2;
-  for (int c = vt / Hq; c < nch; c += vph) m = fmaxf(m, lp[static_cast<long long>(c) * Hq * 2]);
+  const int c0 = vt / Hq;
+  const int n = c0 < nch ? (nch - c0 + vph - 1) / vph : 0;     // tiles of this virtual thread
+  if (n <= kFoldRegs) {
+    float2 x[kFoldRegs];
+#pragma unroll
+    for (int u = 0; u < kFoldRegs; ++u)
+      x[u] = u < n ? *reinterpret_cast<const float2*>(lp + static_cast<long long>(c0 + u * vph) * Hq * 2)
+                   : make_float2(-INFINITY, 0.f);
+#pragma unroll
+    for (int u = 0; u < kFoldRegs; ++u) m = fmaxf(m, x[u].x);
+    if (m != -INFINITY)
+#pragma unroll
+      for (int u = 0; u < kFoldRegs; ++u)
+        if (u < n) sum += x[u].y * expf(x[u].x - m);
+    return;
+  }
+  for (int c = c0; c < nch; c += vph) m = fmaxf(m, lp[static_cast<long long>(c) * Hq * 2]);
   if (m != -INFINITY)
-    for (int c = vt / Hq; c < nch; c += vph) {
+    for (int c = c0; c < nch; c += vph) {
       const float mc = lp[static_cast<long long>(c) * Hq * 2];
       sum += lp[static_cast<long long>(c) * Hq * 2 + 1] * expf(mc - m);
     }
@@ -451,39 +470,40 @@ __device__ __forceinline__ float block_ln_count(int j, int N, int nb) {
   return logf(static_cast<float>(j == nb - 1 ? N - kBlock * (nb - 1) : kBlock));
 }
 
-// Step B as its own launch: blocks j0 .. j0 + 63 of sequence b by 256
-// threads, in passes of 256 / LPB blocks.
-__device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
-                                                 const float* __restrict__ L,
-                                                 const int* __restrict__ ctx_lens,
+// Step B for blocks j0 .. j0 + TB - 1 of sequence b (context length N, nb
+// blocks) by NT threads, in passes of NT / LPB blocks, L_h in LDS (sL).  A
+// block's terms and their order do not depend on NT or TB.
+template <int NT, int TB>
+__device__ __forceinline__ void block_score_tile(const float* __restrict__ zbuf, const float* sL,
                                                  float* __restrict__ scores, int Hq, int MAXB,
-                                                 int b, int j0, float* sL) {
+                                                 int b, int N, int nb, int j0) {
   const int t = threadIdx.x;
-  const int N = ctx_lens[b];
-  if (N < 0 || N > MAXB * kBlock) return;    // flagged in step C
-  const int nb = (N + kBlock - 1) / kBlock;
-  if (j0 >= nb) return;
-  for (int h = t; h < Hq; h += kRowThreads) sL[h] = L[static_cast<long long>(b) * Hq + h];
-  __syncthreads();
   const int LPB = lanes_per_block(Hq);
   const int HPLN = Hq / LPB;
-  const int bpp = kRowThreads / LPB;
+  const int bpp = NT / LPB;
   const int li = t % LPB;
-  for (int jp = j0; jp < j0 + kTileBlocks; jp += bpp) {
+  for (int jp = j0; jp < j0 + TB; jp += bpp) {
     const int j = jp + t / LPB;
-    const bool ok = j < nb && j < j0 + kTileBlocks;
+    const bool ok = j < nb && j < j0 + TB;
     float acc = 0.f;
     if (ok) {
       const float lnn = block_ln_count(j, N, nb);
       const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq + li * HPLN;
       if (HPLN % 4 == 0) {
-        for (int f = 0; f < HPLN / 4; ++f) {
-          const float4 z4 = *reinterpret_cast<const float4*>(zr + 4 * f);
+        // All of the lane's loads first (at most 32 heads: H_q <= 128).
+        constexpr int kMaxF4 = 8;
+        float4 z4[kMaxF4];
+#pragma unroll
+        for (int f = 0; f < kMaxF4; ++f)
+          if (f < HPLN / 4) z4[f] = *reinterpret_cast<const float4*>(zr + 4 * f);
+#pragma unroll
+        for (int f = 0; f < kMaxF4; ++f) {
+          if (f >= HPLN / 4) break;
           const int h = li * HPLN + 4 * f;
-          acc += score_term(z4.x, lnn, sL[h]);
-          acc += score_term(z4.y, lnn, sL[h + 1]);
-          acc += score_term(z4.z, lnn, sL[h + 2]);
-          acc += score_term(z4.w, lnn, sL[h + 3]);
+          acc += score_term(z4[f].x, lnn, sL[h]);
+          acc += score_term(z4[f].y, lnn, sL[h + 1]);
+          acc += score_term(z4[f].z, lnn, sL[h + 2]);
+          acc += score_term(z4[f].w, lnn, sL[h + 3]);
         }
       } else {
         for (int e = 0; e < HPLN; ++e) acc += score_term(zr[e], lnn, sL[li * HPLN + e]);
@@ -492,6 +512,42 @@ __device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
     acc = lanes_sum(acc, LPB);
     if (ok && li == 0) scores[static_cast<long long>(b) * MAXB + j] = __fdiv_rn(acc, static_cast<float>(Hq));
   }
+}
+
+// Step B as its own launch: blocks j0 .. j0 + 63 of sequence b by 256
+// threads, L_h from the per-sequence launch of step A.
+__device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
+                                                 const float* __restrict__ L,
+                                                 const int* __restrict__ ctx_lens,
+                                                 float* __restrict__ scores, int Hq, int MAXB,
+                                                 int b, int j0, float* sL) {
+  const int N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) return;    // flagged in step C
+  const int nb = (N + kBlock - 1) / kBlock;
+  if (j0 >= nb) return;
+  for (int h = threadIdx.x; h < Hq; h += kRowThreads) sL[h] = L[static_cast<long long>(b) * Hq + h];
+  __syncthreads();
+  block_score_tile<kRowThreads, kTileBlocks>(zbuf, sL, scores, Hq, MAXB, b, N, nb, j0);
+}
+
+// Steps A and B together for blocks j0 .. j0 + kStepTileBlocks - 1 of
+// sequence b, by kFoldThreads threads (the fused step's long-table form):
+// L_h merged in LDS exactly as step A's own launch merges it, then the
+// tile's scores.  Every thread must call it.
+constexpr int kStepTileBlocks = 256;
+__device__ __forceinline__ void lse_block_score_body(const float* __restrict__ zbuf,
+                                                     const float* __restrict__ lse_part,
+                                                     const int* __restrict__ ctx_lens,
+                                                     float* __restrict__ scores, int Hq, int MAXB,
+                                                     int nch_max, int b, int j0, float* s_pm,
+                                                     float* s_ps, float* sL) {
+  const int N = ctx_lens[b];
+  if (N < 0 || N > MAXB * kBlock) return;    // flagged in step C
+  const int nb = (N + kBlock - 1) / kBlock;
+  if (j0 >= nb) return;
+  lse_merge_body(lse_part, ctx_lens, sL, Hq, MAXB, nch_max, b, s_pm, s_ps);
+  __syncthreads();
+  block_score_tile<kFoldThreads, kStepTileBlocks>(zbuf, sL, scores, Hq, MAXB, b, N, nb, j0);
 }
 
 constexpr int kSelRankMax = 64;    // prefix groups this small are finished by counting ranks

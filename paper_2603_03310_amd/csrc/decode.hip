@@ -34,6 +34,7 @@
 // fp32 path (VALU): the same decomposition with scalar dot products.
 
 #include "blocks_dev.h"
+#include "entropy_dev.h"
 
 #include <math.h>
 
@@ -193,8 +194,8 @@ __device__ __forceinline__ UnitMeta unit_meta(const DecodeArgs& a, int x, int u1
 // K and V tiles are read once per step: non-temporal loads (the nt bit)
 // measured 8% faster on the decode than plain loads (the queries, read by
 // every wave of a segment, keep plain loads: 1 us better).  The exact
-// scoring mode's whole-row K loads (staged through LDS) use the bit too; it
-// made loads straight into the MFMA layout and the block-summary gather
+// scoring mode's whole-row K loads and the block-summary gather (both staged
+// through LDS) use the bit too; it made loads straight into the MFMA layout
 // slower, and the logit pass no faster, so those keep plain loads.
 // Whole-row K loads staged through LDS measured 1-2% faster than loads
 // straight into the MFMA layout.
@@ -719,17 +720,33 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(DecodeArgs a) {
   combine_body<D>(a, blockIdx.x);
 }
 
-// The merge and, on workgroups of their own, the append of one token per
-// sequence (ent_decode_step_append): the merge reads only partials and
-// records and writes outputs, none of which the append touches, and the
-// kernels that read the lengths and the cache tiles have finished.
-template <int D, typename T>
-__global__ __launch_bounds__(kThreads) void combine_append_kernel(DecodeArgs a, AppendArgs ap) {
-  static_assert(kThreads == kAppendThreads, "append workgroup size");
-  // The appends' workgroups come first: their chains of dependent loads
-  // then overlap the merge instead of following it.
-  if (static_cast<int>(blockIdx.x) < a.B) append_body<T>(ap, blockIdx.x);
-  else combine_body<D>(a, blockIdx.x - a.B);
+// The merge and, on workgroups of their own placed first (their chains of
+// dependent loads then overlap the merge instead of following it), the
+// append of one token per sequence (APP: ent_decode_step_append) and the
+// sampling of every row (nS = B; the decode step with long block tables).
+// The merge reads only partials and records and writes outputs; the appends
+// write the caches, the summaries and the lengths; sampling reads the logits
+// and their row statistics: none of them reads what another writes.
+template <int D, typename T, bool APP, bool VEC>
+__global__ __launch_bounds__(kThreads) void merge_kernel(DecodeArgs a, AppendArgs ap, SampleArgs sp,
+                                                         int nS) {
+  static_assert(kThreads == kAppendThreads && kThreads == kSampleThreads, "workgroup size");
+  __shared__ SampleShared ssh;
+  int id = blockIdx.x;
+  if (APP) {
+    if (id < a.B) {
+      append_body<T>(ap, id);
+      return;
+    }
+    id -= a.B;
+  }
+  if (id < nS) {
+    const int tok = sample_body<VEC>(sp.logits, sp.ld, sp.V, sp.C, sp.stats,
+                                     sp.temp_used[id] * sp.t_cal, sp.uniforms[id], id, ssh);
+    if (threadIdx.x == 0) sp.tokens[id] = tok;
+    return;
+  }
+  combine_body<D>(a, id - nS);
 }
 
 template <typename K>
@@ -772,7 +789,8 @@ long long decode_partial_slots(int decode_grid, int max_batch, int num_kv_heads)
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
-                         hipStream_t s, const int* kept_phys, const AppendArgs* ap) {
+                         hipStream_t s, const int* kept_phys, const AppendArgs* ap,
+                         const SampleArgs* sp) {
   const ent_config& cf = c->cfg;
   DecodeArgs a;
   a.q = q;
@@ -816,18 +834,31 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   // Slices per segment: one output per merge thread.
   a.nsl = std::max(1, c->group * cf.head_dim / kThreads);
   const int n_combine = a.R * a.nsl;
-  if (ap) {
-    const dim3 g2(n_combine + B);
-#define ENT_COMBINE_APPEND(DD)                                                                  \
-  do {                                                                                        \
-    if (ap->bf16)                                                                             \
-      hipLaunchKernelGGL((combine_append_kernel<DD, uint16_t>), g2, dim3(kThreads), 0, s, a, *ap); \
-    else                                                                                      \
-      hipLaunchKernelGGL((combine_append_kernel<DD, float>), g2, dim3(kThreads), 0, s, a, *ap);    \
+  if (ap || sp) {
+    const int nS = sp ? B : 0;
+    const dim3 g2(n_combine + (ap ? B : 0) + nS);
+    const bool vec = !sp || row_vec_ok(sp->logits, sp->ld);
+    const AppendArgs an{};
+    const SampleArgs sn{};
+    const AppendArgs& aa = ap ? *ap : an;
+    const SampleArgs& ss = sp ? *sp : sn;
+#define ENT_MERGE(DD, TT, AP)                                                                  \
+  do {                                                                                         \
+    if (vec)                                                                                   \
+      hipLaunchKernelGGL((merge_kernel<DD, TT, AP, true>), g2, dim3(kThreads), 0, s, a, aa, ss, nS); \
+    else                                                                                       \
+      hipLaunchKernelGGL((merge_kernel<DD, TT, AP, false>), g2, dim3(kThreads), 0, s, a, aa, ss, nS); \
   } while (0)
-    if (cf.head_dim == 128) ENT_COMBINE_APPEND(128);
-    else ENT_COMBINE_APPEND(64);
-#undef ENT_COMBINE_APPEND
+#define ENT_MERGE_D(DD)                                      \
+  do {                                                       \
+    if (!ap) ENT_MERGE(DD, uint16_t, false);                 \
+    else if (ap->bf16) ENT_MERGE(DD, uint16_t, true);        \
+    else ENT_MERGE(DD, float, true);                         \
+  } while (0)
+    if (cf.head_dim == 128) ENT_MERGE_D(128);
+    else ENT_MERGE_D(64);
+#undef ENT_MERGE_D
+#undef ENT_MERGE
     return hipGetLastError();
   }
   const dim3 cgrid(n_combine);

@@ -172,13 +172,14 @@ struct SampleArgs {
 
 // kept_phys (nullable): the selection's encoded physical blocks of the same
 // kept lists, read instead of kept + tables.
-// ap (nullable): an append of one token per sequence that shares the launch
-// merging the split attention segments (it reads nothing that launch writes).
+// ap (nullable): an append of one token per sequence, and sp (nullable) the
+// sampling of every row, that share the launch merging the split attention
+// segments (none of the three reads what another writes).
 hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_cache,
                          const void* v_cache, const int* tables, const int* ctx_lens,
                          const int* kept, const int* n_kept, float* out, float* lse,
                          hipStream_t s, const int* kept_phys = nullptr,
-                         const AppendArgs* ap = nullptr);
+                         const AppendArgs* ap = nullptr, const SampleArgs* sp = nullptr);
 hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
                               ent_state st, const void* q, const void* k_cache,
                               const void* v_cache, const float* ksum, const int* tables,

@@ -31,6 +31,7 @@ namespace ent {
 namespace {
 
 constexpr int kProThreads = 256;
+typedef float nt_f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kProWaves = kProThreads / 64;
 
 __host__ __device__ inline int head_groups(int Hkv) { return (Hkv + kProWaves - 1) / kProWaves; }
@@ -80,7 +81,9 @@ __device__ void tile_plan(const int* __restrict__ ctx_lens, int B, int MAXB, int
 // l*LPB .. l*LPB + LPB - 1 read one block's d floats), staged in the wave's
 // LDS rows and read back in the MFMA layout: against loads straight into the
 // MFMA layout (64 B of each of 16 blocks per instruction) the scoring pass
-// got 4.7 us faster on the 8B shape and 7.6 us on the 70B-shaped loop.
+// got 4.7 us faster on the 8B shape and 7.6 us on the 70B-shaped loop.  The
+// summaries are read once per step: non-temporal loads (the nt bit), 2 us
+// faster on the 70B-shaped loop's prologue and 1 us on the 8B shape's.
 template <int D>
 __device__ __forceinline__ void score_job(const PrologueArgs& a, int b, int ch, int hg, int N,
                                           int entry, float* s_stage) {
@@ -99,8 +102,9 @@ __device__ __forceinline__ void score_job(const PrologueArgs& a, int b, int ch, 
   for (int k = 0; k < NI; ++k) {
     const int blk = k * BPI + lane / LPB;
     const int pb = __shfl(p, blk);
-    buf[k] = *reinterpret_cast<const float4*>(a.ksum + (static_cast<long long>(pb) * a.Hkv + g) * D +
-                                              (lane % LPB) * 4);
+    const nt_f32x4_t x = __builtin_nontemporal_load(reinterpret_cast<const nt_f32x4_t*>(
+        a.ksum + (static_cast<long long>(pb) * a.Hkv + g) * D + (lane % LPB) * 4));
+    buf[k] = make_float4(x.x, x.y, x.z, x.w);
   }
   uint2 qv[D / 16];
   score_q_load<D>(a.q, b, g, a.Hkv, a.G, qv);

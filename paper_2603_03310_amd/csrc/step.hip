@@ -9,14 +9,16 @@
 //      launch, on the VALU); each row's T_t is recorded in temp_used;
 //   B  one workgroup per sequence: the row's entropy from the chunk triples,
 //      the controller update and the kept-block selection under the
-//      entropy-driven budget (for long block tables: entropy, controller and
-//      L_h per sequence, the block scores over the whole chip, then the
-//      selection per sequence); in the same launch, on workgroups of their
+//      entropy-driven budget; in the same launch, on workgroups of their
 //      own, sampling at T_t (it needs only the row statistics of A, so it
-//      runs on the CUs the per-sequence selection leaves idle);
+//      runs on the CUs the per-sequence selection leaves idle).  For long
+//      block tables: entropy and controller per sequence and, on workgroups
+//      of their own, L_h and the block scores per tile of 256 blocks, then
+//      the selection per sequence in a second launch; sampling moves to D;
 //   C  kept-block decode attention;
-//   D  the merge of split decode segments (ent_decode_step_append: and, on
-//      workgroups of their own, the append of the new token's K/V).
+//   D  the merge of split decode segments (and, on workgroups of their own,
+//      ent_decode_step_append's append of the new token's K/V and, for long
+//      block tables, the sampling).
 
 #include "blocks_dev.h"
 #include "estimate_dev.h"
@@ -33,23 +35,27 @@ __device__ __forceinline__ void step_sample(const SampleArgs& sa, int b, SampleS
   if (threadIdx.x == 0) sa.tokens[b] = tok;
 }
 
-// Per sequence: the row's entropy from the chunk triples and the controller
-// update (first wave), and L_h for the selection (all threads); workgroups
-// B .. 2B-1 sample.
+// Block tables too wide for the one-launch selection: workgroups 0 .. B-1
+// take a row's entropy from the chunk triples and the controller update (with
+// an estimator, the estimate first), and the rest one (sequence, tile of
+// kStepTileBlocks blocks) each: the sequence's L_h, merged as the per-stage
+// launch merges it, then the tile's block scores.  Tiles past a sequence's
+// blocks exit at once.  (Sampling runs in the merge launch of this form.)
 template <bool VEC>
-__global__ __launch_bounds__(kFoldThreads) void step_b0_kernel(
+__global__ __launch_bounds__(kFoldThreads) void step_b1_kernel(
     int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
-    float* h_out, Control ct, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, float* __restrict__ L, int Hq, int MAXB, int nch_max,
-    SampleArgs sa, int est, int est_k, const float* __restrict__ tmax) {
-  static_assert(kFoldThreads >= kSampleThreads && kFoldThreads >= kEstThreads, "workgroup size");
+    float* h_out, Control ct, const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, float* __restrict__ scores, int Hq, int MAXB, int nch_max,
+    int ntile, SampleArgs sa, int est, int est_k, const float* __restrict__ tmax) {
+  static_assert(kFoldThreads >= kEstThreads, "workgroup size");
   extern __shared__ __attribute__((aligned(16))) unsigned est_lds[];
-  __shared__ float s_pm[kFoldThreads], s_ps[kFoldThreads];
-  __shared__ SampleShared ssh;
+  __shared__ float s_pm[kFoldThreads], s_ps[kFoldThreads], sL[128];
   __shared__ EstShared esh;
   const int b = blockIdx.x;
   if (b >= B) {
-    step_sample<VEC>(sa, b - B, ssh);
+    const int r = b - B, seq = r / ntile;
+    lse_block_score_body(zbuf, lse_part, ctx_lens, scores, Hq, MAXB, nch_max, seq,
+                         (r - seq * ntile) * kStepTileBlocks, s_pm, s_ps, sL);
     return;
   }
   if (est != ENT_EST_EXACT) {
@@ -61,8 +67,6 @@ __global__ __launch_bounds__(kFoldThreads) void step_b0_kernel(
     const float H = row_entropy(part, C, b);
     if (threadIdx.x == 0) controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, ct);
   }
-  lse_merge_body(lse_part, ctx_lens, L + static_cast<long long>(b) * Hq, Hq, MAXB, nch_max, b,
-                 s_pm, s_ps);
 }
 
 // Per sequence, block tables that fit the one-launch selection: the
@@ -206,18 +210,19 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   } else {
-    auto k0 = vec ? step_b0_kernel<true> : step_b0_kernel<false>;
-    hipLaunchKernelGGL(k0, dim3(2 * B), dim3(kFoldThreads), est_lds, s, B, c->ent_part, c->chunks,
-                       st.temp, st.h_prev, st.tau, h_out, ct, c->lse_part, ctx_lens, c->lrow,
-                       cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks, sa, est_mode,
-                       cf.est_k, c->tmax);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
     float* sc = scores ? scores : c->iscores;
-    e = launch_block_scores(c, B, ctx_lens, sc, s);
+    const int ntile = (cf.max_blocks_per_seq + kStepTileBlocks - 1) / kStepTileBlocks;
+    auto k1 = vec ? step_b1_kernel<true> : step_b1_kernel<false>;
+    hipLaunchKernelGGL(k1, dim3(B + B * ntile), dim3(kFoldThreads), est_lds, s, B, c->ent_part,
+                       c->chunks, st.temp, st.h_prev, st.tau, h_out, ct, c->zbuf, c->lse_part,
+                       ctx_lens, sc, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks, ntile, sa,
+                       est_mode, cf.est_k, c->tmax);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     e = launch_select_rows(c, B, tables, ctx_lens, h_out, sc, theta, kept, n_kept, st.kappa, s);
     if (e != hipSuccess) return e;
+    return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s,
+                         c->kept_phys, ap, &sa);
   }
   return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s,
                        c->kept_phys, ap);
