@@ -664,12 +664,14 @@ __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
 // Merge of the partials of every segment that the decode ranges cut.  One
 // workgroup per (decode range, slice of the G x d outputs); the range's
 // record names the cut segment that begins in it, if any, and the last range
-// holding a piece of it; a.nsl slices of at most 256 outputs per segment.
-// Each thread merges one output on its own, in
-// range order, with a running (max, sum, output) rescaled as the maximum
-// grows; the loads of eight partials are issued together, so one memory
-// round trip follows the record for segments cut into at most eight pieces.
-// Ranges with no units (fewer units than ranges) wrote no partial.
+// holding a piece of it; a.nsl slices of at most 256 groups of four outputs
+// per segment.  Each thread merges four consecutive outputs of one head row
+// on its own (a partial's max and sum loaded once, its four sums as one
+// 16-byte load), in range order, with a running (max, sum, output) rescaled
+// as the maximum grows; the loads of eight partials are issued together, so
+// one memory round trip follows the record for segments cut into at most
+// eight pieces.  Ranges with no units (fewer units than ranges) wrote no
+// partial.
 constexpr int kCombinePrefetch = 8;        // partials whose loads are issued together
 
 template <int D>
@@ -683,14 +685,15 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int item) {
   const int G = a.G;
   const int b = seg / a.Hkv, g = seg % a.Hkv;
   const int Hq = a.Hkv * G;
-  const int span = G * D / a.nsl;            // outputs of this workgroup, <= kThreads
-  const int o = slice * span + static_cast<int>(threadIdx.x);
-  if (static_cast<int>(threadIdx.x) >= span) return;
-  const int r = o / D, d = o - r * D;
+  const int q4 = slice * kThreads + static_cast<int>(threadIdx.x);   // group of four outputs
+  if (q4 >= G * D / 4) return;
+  const int r = (4 * q4) / D, d = 4 * q4 - r * D;
   const long long ob = static_cast<long long>(b) * Hq + g * G;   // first output head row
-  float M = -INFINITY, L = 0.f, acc = 0.f;
+  float M = -INFINITY, L = 0.f;
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
   for (int c0 = w0; c0 <= w1; c0 += kCombinePrefetch) {
-    float m[kCombinePrefetch], l[kCombinePrefetch], v[kCombinePrefetch];
+    float m[kCombinePrefetch], l[kCombinePrefetch];
+    f32x4_t v[kCombinePrefetch];
 #pragma unroll
     for (int k = 0; k < kCombinePrefetch; ++k) {
       const int wi = c0 + k;
@@ -698,7 +701,8 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int item) {
       const long long slot = static_cast<long long>(wi) + seg;
       m[k] = ok ? a.part_ml[(slot * G + r) * 2 + 0] : -INFINITY;
       l[k] = ok ? a.part_ml[(slot * G + r) * 2 + 1] : 0.f;
-      v[k] = ok ? a.part_acc[(slot * G + r) * D + d] : 0.f;
+      v[k] = ok ? *reinterpret_cast<const f32x4_t*>(a.part_acc + (slot * G + r) * D + d)
+                : f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
     for (int k = 0; k < kCombinePrefetch; ++k) {
@@ -711,7 +715,8 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int item) {
       M = Mn;
     }
   }
-  a.out[(ob + r) * D + d] = L > 0.f ? acc / L : 0.f;
+  const f32x4_t res = L > 0.f ? acc / L : f32x4_t{0.f, 0.f, 0.f, 0.f};
+  *reinterpret_cast<f32x4_t*>(a.out + (ob + r) * D + d) = res;
   if (d == 0 && a.lse) a.lse[ob + r] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
 }
 
@@ -831,8 +836,8 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // Slices per segment: one output per merge thread.
-  a.nsl = std::max(1, c->group * cf.head_dim / kThreads);
+  // Slices per segment: four outputs per merge thread.
+  a.nsl = (c->group * cf.head_dim / 4 + kThreads - 1) / kThreads;
   const int n_combine = a.R * a.nsl;
   if (ap || sp) {
     const int nS = sp ? B : 0;
