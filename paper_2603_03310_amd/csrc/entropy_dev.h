@@ -217,63 +217,103 @@ __device__ __forceinline__ double block_excl_scan_d(double v, double* wsum) {
 }
 
 struct SampleShared {
-  double w[kMaxChunks];
   double wsum[kSampleThreads / 64];
-  float red[16];
   int chunk, idx, lastpos;
+  float M;
   double before, target;
 };
 
 // Inverse-CDF sample of row b at temperature T and uniform u.  Every thread
 // of the workgroup calls it; the first kSampleThreads threads do the work.
-// Returns the token (meaningful in thread 0).
+// Returns the token (meaningful in thread 0).  The first wave picks the
+// chunk: lane l holds chunks 4 l .. 4 l + 3 (kMaxChunks = 256), their masses
+// 2^(M_c - M) S_c in double, a wave scan of the lanes' sums, the lane where
+// the running mass first exceeds u times the total by a ballot, then the
+// chunk within that lane by a sequential walk.
 template <bool VEC>
 __device__ __forceinline__ int sample_body(const float* __restrict__ logits, long long ld, int V,
                                            int C, const float* __restrict__ stats, float T,
                                            float u, int b, SampleShared& sh) {
+  static_assert(kMaxChunks == 4 * 64, "four chunks per lane of one wave");
   const int t = threadIdx.x;
   const bool worker = t < kSampleThreads;
   const float c2 = __fdiv_rn(kLog2e, T);
   const float* row = logits + static_cast<long long>(b) * ld;
   const float* st = stats + static_cast<long long>(b) * C * 2;
-  const float mc = (worker && t < C) ? st[2 * t] : -INFINITY;
-  const float sc = (worker && t < C) ? st[2 * t + 1] : 0.f;
-  const float M = block_max<kSampleThreads>(mc, sh.red);
-  if (worker)
-    sh.w[t] = (t < C && sc > 0.f)
-                  ? static_cast<double>(sc) * exp2(static_cast<double>(mc) - static_cast<double>(M))
+  if (t < 64) {
+    constexpr int PER = kMaxChunks / 64;
+    float mc[PER], sc[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = PER * t + k;
+      mc[k] = i < C ? st[2 * i] : -INFINITY;
+      sc[k] = i < C ? st[2 * i + 1] : 0.f;
+    }
+    float ml = mc[0];
+#pragma unroll
+    for (int k = 1; k < PER; ++k) ml = fmaxf(ml, mc[k]);
+    const float M = wave_max(ml);
+    double wl[PER];
+    int lastk = -1;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      wl[k] = (PER * t + k < C && sc[k] > 0.f)
+                  ? static_cast<double>(sc[k]) * exp2(static_cast<double>(mc[k]) - static_cast<double>(M))
                   : 0.0;
-  if (t == 0) {
-    sh.idx = 0x7fffffff;
-    sh.lastpos = -1;
-  }
-  __syncthreads();
-  if (t == 0) {
-    double tot = 0.0;
-    for (int i = 0; i < C; ++i) tot += sh.w[i];
+      if (wl[k] > 0.0) lastk = k;
+    }
+    double loc = 0.0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) loc += wl[k];
+    double incl = loc;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const double n = __shfl_up(incl, o);
+      if (t >= o) incl += n;
+    }
+    const double tot = __shfl(incl, 63);
     const double target = static_cast<double>(u) * tot;
-    double cum = 0.0;
-    int chunk = -1, lastpos = 0;
-    double before = 0.0;
-    for (int i = 0; i < C; ++i) {
-      if (sh.w[i] > 0.0) lastpos = i;
-      if (chunk < 0 && cum + sh.w[i] > target) {
-        chunk = i;
-        before = cum;
+    // The lane's running mass, stepped chunk by chunk from its exclusive prefix.
+    double cum = incl - loc, run = cum;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) run += wl[k];
+    const unsigned long long hit = __ballot(run > target);
+    if (hit != 0ull) {
+      if (t == __ffsll(static_cast<long long>(hit)) - 1) {
+        int chunk = PER * t + PER - 1;
+        double before = cum;
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+          if (cum + wl[k] > target) {
+            chunk = PER * t + k;
+            before = cum;
+            break;
+          }
+          cum += wl[k];
+        }
+        sh.chunk = chunk;
+        sh.before = before;
+        sh.target = target;
       }
-      cum += sh.w[i];
+    } else {
+      // Rounding put the target at the very top: the last chunk of positive
+      // mass (chunk 0 when there is none), its last token of positive mass.
+      const unsigned long long pos = __ballot(lastk >= 0);
+      const int L = pos ? 63 - __clzll(static_cast<long long>(pos)) : 0;
+      if (t == L) {
+        sh.chunk = pos ? PER * t + lastk : 0;
+        sh.before = 0.0;
+        sh.target = HUGE_VAL;
+      }
     }
-    double tgt = target;
-    if (chunk < 0) {            // rounding put the target at the very top:
-      chunk = lastpos;          // take the last token of positive mass
-      before = 0.0;
-      tgt = HUGE_VAL;
+    if (t == 0) {
+      sh.M = M;
+      sh.idx = 0x7fffffff;
+      sh.lastpos = -1;
     }
-    sh.chunk = chunk;
-    sh.before = before;
-    sh.target = tgt;
   }
   __syncthreads();
+  const float M = sh.M;
   const int base = sh.chunk * kRowChunk + t * kPerThread;
   float e[kPerThread];
   if (!worker) {
