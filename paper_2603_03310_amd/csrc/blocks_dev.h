@@ -393,14 +393,15 @@ __device__ __forceinline__ void lse_fold_vthread(const float* __restrict__ lse_p
 }
 
 // The merge of each head's VPH partials (s_pm, s_ps indexed by virtual
-// thread v H_q + h), as a fixed pairwise tree: at each level partial v takes
-// in partial v + st (st = VPH / 2, VPH / 4, ..., 1), in place.  Every thread
-// of the workgroup must call it (it holds the barriers); afterwards L_h =
-// s_pm[h] + ln s_ps[h] (lse_merged).
+// thread v H_q + h), as a fixed pairwise tree: while n > 1 partials remain
+// (n = VPH at first), partial v < n - h takes in partial v + h, in place,
+// with h = ceil(n / 2), and n becomes h (for a power of two, the strides
+// VPH / 2, VPH / 4, ..., 1).  Every thread of the workgroup must call it (it
+// holds the barriers); afterwards L_h = s_pm[h] + ln s_ps[h] (lse_merged).
 __device__ __forceinline__ void lse_merge_tree(float* s_pm, float* s_ps, int Hq) {
-  const int vph = kFoldThreads / Hq;
-  for (int st = vph >> 1; st >= 1; st >>= 1) {
-    for (int i = threadIdx.x; i < st * Hq; i += blockDim.x) {
+  for (int n = kFoldThreads / Hq; n > 1;) {
+    const int st = (n + 1) >> 1;
+    for (int i = threadIdx.x; i < (n - st) * Hq; i += blockDim.x) {
       const float m1 = s_pm[i], s1 = s_ps[i];
       const float m2 = s_pm[i + st * Hq], s2 = s_ps[i + st * Hq];
       if (m2 == -INFINITY) continue;
@@ -414,6 +415,7 @@ __device__ __forceinline__ void lse_merge_tree(float* s_pm, float* s_ps, int Hq)
       s_ps[i] = s1 * expf(m1 - mn) + s2 * expf(m2 - mn);
     }
     __syncthreads();
+    n = st;
   }
 }
 
@@ -490,20 +492,24 @@ __device__ __forceinline__ void block_score_tile(const float* __restrict__ zbuf,
       const float lnn = block_ln_count(j, N, nb);
       const float* zr = zbuf + (static_cast<long long>(b) * MAXB + j) * Hq + li * HPLN;
       if (HPLN % 4 == 0) {
-        // All of the lane's loads first (at most 32 heads: H_q <= 128).
-        constexpr int kMaxF4 = 8;
-        float4 z4[kMaxF4];
+        // The lane's loads in batches of eight issued together (one batch
+        // for four lanes per block; up to four when one lane takes all of
+        // H_q <= 128 heads), the terms in head order.
+        constexpr int kBatchF4 = 8;
+        for (int f0 = 0; f0 < HPLN / 4; f0 += kBatchF4) {
+          float4 z4[kBatchF4];
 #pragma unroll
-        for (int f = 0; f < kMaxF4; ++f)
-          if (f < HPLN / 4) z4[f] = *reinterpret_cast<const float4*>(zr + 4 * f);
+          for (int f = 0; f < kBatchF4; ++f)
+            if (f0 + f < HPLN / 4) z4[f] = *reinterpret_cast<const float4*>(zr + 4 * (f0 + f));
 #pragma unroll
-        for (int f = 0; f < kMaxF4; ++f) {
-          if (f >= HPLN / 4) break;
-          const int h = li * HPLN + 4 * f;
-          acc += score_term(z4[f].x, lnn, sL[h]);
-          acc += score_term(z4[f].y, lnn, sL[h + 1]);
-          acc += score_term(z4[f].z, lnn, sL[h + 2]);
-          acc += score_term(z4[f].w, lnn, sL[h + 3]);
+          for (int f = 0; f < kBatchF4; ++f) {
+            if (f0 + f >= HPLN / 4) break;
+            const int h = li * HPLN + 4 * (f0 + f);
+            acc += score_term(z4[f].x, lnn, sL[h]);
+            acc += score_term(z4[f].y, lnn, sL[h + 1]);
+            acc += score_term(z4[f].z, lnn, sL[h + 2]);
+            acc += score_term(z4[f].w, lnn, sL[h + 3]);
+          }
         }
       } else {
         for (int e = 0; e < HPLN; ++e) acc += score_term(zr[e], lnn, sL[li * HPLN + e]);

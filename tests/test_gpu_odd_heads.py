@@ -1,0 +1,42 @@
+"""Head layouts off the common shapes, against the oracle (Section 3.2 scoring
+and selection, Section 3.4 decode).
+
+Query-head counts whose H_q / 4 is not a power of two (the block scores
+then give one lane all of a block's heads), odd KV-head counts, and a
+GQA group of 16, each with block tables short enough for the one-launch
+selection and too wide for it (the tile launch that merges L_h per tile of
+256 blocks): 2500 blocks exceed the one-launch table width, and
+H_q x blocks above 32768 its register budget.  With H_q = 12 and 48 the
+merge of L_h runs over 42 and 10 partials per head (512 virtual threads),
+not a power of two, and the sequences have more tiles than that.  Fused
+step and staged calls.
+"""
+import pytest
+
+from synth import LLAMA3_8B, default_params, generate, small
+from tests.test_gpu_parity import _assert_ok, _run, torch_cuda  # noqa: F401
+
+pytestmark = pytest.mark.gpu
+
+# (name, KV heads, group, context lengths)
+CASES = [
+    ("hq12_short", 3, 4, [1, 17, 300, 900]),
+    ("hq12_mid", 3, 4, [1, 17, 300, 20000]),
+    ("hq12_long", 3, 4, [1, 17, 300, 40000]),
+    ("hq48_short", 6, 8, [5, 64, 700, 2000]),
+    ("hq48_long", 6, 8, [5, 64, 700, 12000]),
+    ("hq96_long", 6, 16, [33, 1000, 6000]),
+]
+
+
+@pytest.mark.parametrize("fused", [True, False], ids=["step", "staged"])
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_odd_head_layouts(torch_cuda, case, fused):
+    name, hkv, group, ctx = case
+    w = small(LLAMA3_8B.replace(num_q_heads=hkv * group, num_kv_heads=hkv), len(ctx),
+              ctx=("fixed", ctx), vocab=20000, suffix=name)
+    print(f"[heads] {name}: H_q={hkv * group}, H_kv={hkv}, blocks up to {w.max_blocks_per_seq}",
+          flush=True)
+    x = generate(w)
+    reps, dev = _run(torch_cuda, x, default_params(w), fused=fused)
+    _assert_ok(reps)
