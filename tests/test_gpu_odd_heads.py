@@ -13,7 +13,7 @@ step and staged calls.
 """
 import pytest
 
-from synth import LLAMA3_8B, default_params, generate, small
+from synth import LLAMA3_8B, TINY, default_params, generate, small
 from tests.test_gpu_parity import _assert_ok, _run, torch_cuda  # noqa: F401
 
 pytestmark = pytest.mark.gpu
@@ -38,5 +38,17 @@ def test_odd_head_layouts(torch_cuda, case, fused):
     print(f"[heads] {name}: H_q={hkv * group}, H_kv={hkv}, blocks up to {w.max_blocks_per_seq}",
           flush=True)
     x = generate(w)
+    reps, dev = _run(torch_cuda, x, default_params(w), fused=fused)
+    _assert_ok(reps)
+
+
+@pytest.mark.parametrize("fused", [True, False], ids=["step", "staged"])
+def test_fp32_wide_tables(torch_cuda, fused):
+    """fp32 caches (block scores on the VALU) with a table too wide for the
+    one-launch selection (2500 blocks): the tile launch and the merge
+    launch's sampling on that path."""
+    w = small(TINY, 3, ctx=("fixed", [7, 300, 40000]), suffix="f32_wide")
+    x = generate(w)
+    print(f"[heads] fp32 wide: blocks up to {w.max_blocks_per_seq}", flush=True)
     reps, dev = _run(torch_cuda, x, default_params(w), fused=fused)
     _assert_ok(reps)

@@ -2,10 +2,12 @@
 append of the step's new token, the append sharing the step's last launch)
 against ent_decode_step followed by ent_kv_append, through the C ABI: every
 output, the controller and kept-fraction state, the caches, the block
-summaries and the lengths agree bit for bit over a 6-step loop; bf16
+summaries and the lengths agree bit for bit over a multi-step loop; bf16
 batches in both selection forms (one launch per sequence, and the
-three-launch form of wide block tables) and the fp32 (VALU) path.  Parity of
-the loop itself against the oracle: tests/test_gpu_full_loop.py."""
+long-table form: the tile launch, the selection, sampling in the last
+launch beside the appends) and the fp32 (VALU) path with short and wide
+tables.  Parity of the loop itself against the oracle:
+tests/test_gpu_full_loop.py."""
 import numpy as np
 import pytest
 
@@ -19,6 +21,7 @@ CASES = [
     small(LLAMA70B_LOOP, 4, ctx=("uniform", 100, 600), steps=6, suffix="sa_one"),
     small(LLAMA70B_LOOP, 3, ctx=("uniform", 6000, 9000), steps=6, suffix="sa_three"),
     small(TINY, TINY.batch, steps=6, suffix="sa_f32"),
+    small(TINY, 2, ctx=("fixed", [300, 40000]), steps=4, suffix="sa_f32_wide"),
 ]
 FIELDS = ("h", "tau", "temp", "temp_used", "row_stats", "kept", "n_kept", "scores", "theta", "out",
           "lse", "tokens", "kappa", "ctx_lens", "k_pool", "v_pool", "ksum")
