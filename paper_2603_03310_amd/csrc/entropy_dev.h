@@ -353,8 +353,15 @@ __device__ __forceinline__ int sample_body(const float* __restrict__ logits, lon
         break;
       }
     }
-    if (found != 0x7fffffff) atomicMin(&sh.idx, found);
-    if (lastpos >= 0) atomicMax(&sh.lastpos, lastpos);
+  }
+  // The smallest index found and the largest of positive mass: per wave by
+  // shuffles, then one shared-memory atomic per wave (one per thread made
+  // the threads' atomics on one address serialise: 4 us per row).
+  const unsigned fmin = wave_min_u(static_cast<unsigned>(found));
+  const unsigned lmax = wave_max_u(static_cast<unsigned>(lastpos + 1));
+  if (worker && (t & 63) == 0) {
+    if (fmin != 0x7fffffffu) atomicMin(&sh.idx, static_cast<int>(fmin));
+    if (lmax != 0u) atomicMax(&sh.lastpos, static_cast<int>(lmax) - 1);
   }
   __syncthreads();
   return (sh.idx != 0x7fffffff) ? sh.idx : sh.lastpos;
