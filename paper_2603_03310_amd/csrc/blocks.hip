@@ -17,9 +17,11 @@
 //   select_fused_kernel per sequence (tables that fit its registers): L_h, I_b, the
 //                       budget, an 8-bit radix select of the k-th largest
 //                       score, ascending compaction with ballots
-//   lse_merge_kernel,   the same in three launches for long block tables:
-//   block_score_kernel, per sequence L_h; per 64 blocks I_b; per sequence
-//   select_kernel       the selection
+//   lse_merge_kernel,   the same in three launches for long block tables
+//   block_score_kernel, (the per-stage entry point): per sequence L_h; per 64
+//   select_kernel       blocks I_b; per sequence the selection (the fused step
+//                       runs L_h and I_b per 256-block tile in one launch,
+//                       step.hip, then select_kernel)
 //   append_kernel    writes one token and refreshes its block's mean key
 
 #include "blocks_dev.h"

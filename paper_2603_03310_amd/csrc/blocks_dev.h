@@ -337,10 +337,12 @@ __device__ __forceinline__ void budget_record(const Budget& bu, int b, float kap
 //     compaction of {b : I_b >= theta} with wave ballots.
 // When the block tables are short enough for the registers
 // (select_one_launch), one workgroup per sequence runs all three; otherwise
-// B runs as its own chip-wide launch (one
-// workgroup per 64 blocks) between two per-sequence launches, so long
-// sequences spread their exponentials over the chip.  Both forms perform the
-// same arithmetic in the same order, so their results are identical.
+// (the long-table forms) B runs over the whole chip, so long sequences
+// spread their exponentials: the per-stage entry point in three launches
+// (per-sequence A, B per 64 blocks, per-sequence C), the fused step in two
+// (A and B together per tile of 256 blocks, lse_block_score_body, then C).
+// All forms perform the same arithmetic in the same order, so their results
+// are identical.
 constexpr int kRowThreads = 256;          // threads of the chip-wide block-score launch
 constexpr int kTileBlocks = 64;           // blocks per scoring workgroup of step B
 constexpr int kSelThreads = 512;          // step C (and the one-launch form)
@@ -798,8 +800,8 @@ __device__ __forceinline__ void select_row_body(
 // heads per lane and pass), the table entries (thread t takes entries t,
 // t + 512, ...) and the per-tile log-sum-exp partials of the L merge;
 // select_finish merges L, scores the blocks and selects.  The arithmetic,
-// and its order, is that of the three-launch form (lse_merge_body,
-// block_score_body, select_core).  The block logits take kSelZRegs float4
+// and its order, is that of the long-table forms (lse_merge_body,
+// block_score_tile, select_core).  The block logits take kSelZRegs float4
 // registers: 16 / F4 passes of kSelThreads / LPB blocks.
 constexpr int kSelTableRegs = kSelMaxBlocks / kSelThreads;
 constexpr int kSelZRegs = 16;
@@ -816,12 +818,12 @@ struct SelectRegs {
   int tb[kSelTableRegs];
 };
 
-// F4 of the one-launch form (1, 2, 4 or 8), or 0 when the three-launch form
-// applies.  Both the staged and the fused step decide with this, so they
-// take the same form.  One workgroup evaluates every head's term of every
-// block of its sequence: beyond kSelMaxTerms the chip-wide block scores of
-// the three-launch form are faster (64 heads x 1028 blocks: 37 us against
-// 28 us).
+// F4 of the one-launch form (1, 2, 4 or 8), or 0 when the long-table forms
+// apply.  Both the staged and the fused step decide with this, so they take
+// the same selection arithmetic.  One workgroup evaluates every head's term
+// of every block of its sequence: beyond kSelMaxTerms the chip-wide block
+// scores of the long-table forms are faster (64 heads x 1028 blocks: 37 us
+// against 28 us for the three launches and 20 us for the fused step's two).
 __host__ __device__ inline int select_one_launch(int MAXB, int Hq) {
   if (Hq > 128 || Hq % 4 != 0 || MAXB > kSelMaxBlocks) return 0;
   const int lpb = lanes_per_block(Hq);

@@ -5,7 +5,7 @@ through the C ABI, against the float64 oracle.
 Cases: the 8B-shaped batch (thread maxima staged in LDS), a vocabulary above
 131072 (thread maxima read from memory), rows with ties at every level,
 uniform, one-hot and partly masked rows, k >= |V| (the exact entropy), k = 1,
-the selection in three launches (block tables over 1024 blocks), and a
+the long-table selection (block tables over 1024 blocks), and a
 closed loop with a positive estimator error bound in the budget.  The fused
 step must give exactly the outputs of the four per-stage calls.
 """

@@ -2,7 +2,7 @@
 (Section 3.2 block contributions from the exact attention weights; forced
 first and last blocks) through the C ABI, against the float64 oracle.
 Exact mode: bf16 (MFMA) and fp32 (VALU) caches, short and long block tables
-(one- and three-launch selections), ragged and one-token blocks, the full
+(one-launch and long-table selections), ragged and one-token blocks, the full
 long-context batch on sampled sequences, a closed loop with appends, and the
 staged calls against the one-call step.  Forced
 keeps: mean-key and exact modes, forced sets that fill the budget, both

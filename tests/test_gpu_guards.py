@@ -129,7 +129,7 @@ def test_entropy_bias(torch_cuda, bias):
 
 @pytest.mark.parametrize("w", [
     small(LLAMA70B_LOOP, 3, ctx=("uniform", 100, 600), steps=3, suffix="guards_fused"),
-    # block tables over 1024 blocks: the selection in three launches
+    # block tables over 1024 blocks: the long-table selection
     small(LONG_CONTEXT, 2, ctx=("uniform", 9000, 17000), steps=1, suffix="guards_long"),
 ], ids=lambda w: w.name)
 def test_fused_equals_staged_with_every_guard(torch_cuda, w):

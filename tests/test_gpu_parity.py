@@ -182,7 +182,7 @@ def test_append_refresh_matches_fresh_summary(torch_cuda, w):
 FUSED_CASES = [
     TINY,
     small(LLAMA3_8B, 5, ctx=("uniform", 100, 2500), suffix="fused"),
-    # more than 1024 blocks per table row: selection in three launches
+    # more than 1024 blocks per table row: the long-table selection
     small(LONG_CONTEXT, 3, ctx=("uniform", 9000, 20000), suffix="fused_long"),
     small(SKEWED, 10, ctx=("fixed", [0, 1, 15, 16, 17, 33, 64, 65, 100, 1000]), vocab=5000,
           suffix="fused_edge"),
