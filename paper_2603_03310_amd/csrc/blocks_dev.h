@@ -999,45 +999,123 @@ __device__ __forceinline__ void append_body(const AppendArgs& a, int b) {
     if (threadIdx.x == 0) raise_flag(flags, ENT_DEV_BAD_TABLE);
     return;
   }
-  // Each thread takes VE consecutive elements of one KV head's row (16
-  // bytes): the new key and value, and (for the block's mean) the earlier
-  // slots' keys, all loaded at once (slots from `slot` on are read and not
-  // used: the tile always holds 16); each element is then summed in slot
-  // order, the new key last.
+  // A 16-byte piece of one KV head's row (VE elements) at a time: the new
+  // key and value, and (for the block's mean) the earlier slots' keys, all
+  // loaded at once (slots from `slot` on are read and not used: the tile
+  // always holds 16); each element is then summed in slot order, the new key
+  // last.  When the workgroup has two threads per piece, the first loads and
+  // sums slots 0..7 and hands its sums through LDS to the second, which
+  // continues with slots 8..14 (the same additions in the same order, half
+  // the registers each).
   constexpr int VE = 16 / sizeof(T);
-  for (int v = threadIdx.x; v < Hkv * D / VE; v += kAppendThreads) {
+  constexpr int kHalf = kBlock / 2;           // slots of the first thread of a pair
+  __shared__ float s_part[kAppendThreads / 2 * VE];
+  const int items = Hkv * D / VE;
+  if (2 * items <= kAppendThreads) {
+    const int half = threadIdx.x / items, v = threadIdx.x - half * items;
+    const bool act = half < 2;
     const int e0 = v * VE;
     const int g = e0 / D, dd = e0 % D;
     const long long src = (static_cast<long long>(b) * Hkv + g) * D + dd;
     const long long tile = (static_cast<long long>(p) * Hkv + g) * kBlock * D;
-    const uint4 kraw = *reinterpret_cast<const uint4*>(k_new + src);
-    const uint4 vraw = *reinterpret_cast<const uint4*>(v_new + src);
-    uint4 raw[kBlock - 1];
-    if (ksum) {
+    uint4 kraw = make_uint4(0u, 0u, 0u, 0u), vraw = kraw;
+    uint4 raw[kHalf];
+    if (act) {
+      kraw = *reinterpret_cast<const uint4*>(k_new + src);
+      if (half == 0) vraw = *reinterpret_cast<const uint4*>(v_new + src);
+      if (ksum) {
 #pragma unroll
-      for (int s2 = 0; s2 < kBlock - 1; ++s2)
-        raw[s2] = *reinterpret_cast<const uint4*>(kc + tile + s2 * D + dd);
+        for (int i = 0; i < kHalf; ++i)
+          if (half == 0 || i < kHalf - 1)
+            raw[i] = *reinterpret_cast<const uint4*>(kc + tile + (half * kHalf + i) * D + dd);
+      }
     }
-    *reinterpret_cast<uint4*>(kc + tile + slot * D + dd) = kraw;
-    const T* kx = reinterpret_cast<const T*>(&kraw);
-    const T* vx = reinterpret_cast<const T*>(&vraw);
+    float sum[VE];
 #pragma unroll
-    for (int i = 0; i < VE; ++i) vc[tile + (dd + i) * kBlock + slot] = vx[i];
-    if (ksum) {
-      float sum[VE];
+    for (int i = 0; i < VE; ++i) sum[i] = 0.f;
+    if (act && half == 0) {
+      *reinterpret_cast<uint4*>(kc + tile + slot * D + dd) = kraw;
+      const T* vx = reinterpret_cast<const T*>(&vraw);
 #pragma unroll
-      for (int i = 0; i < VE; ++i) sum[i] = 0.f;
+      for (int i = 0; i < VE; ++i) vc[tile + (dd + i) * kBlock + slot] = vx[i];
+      if (ksum) {
 #pragma unroll
-      for (int s2 = 0; s2 < kBlock - 1; ++s2) {
-        const T* x = reinterpret_cast<const T*>(&raw[s2]);
+        for (int s2 = 0; s2 < kHalf; ++s2) {
+          const T* x = reinterpret_cast<const T*>(&raw[s2]);
+          if (s2 < slot) {
+#pragma unroll
+            for (int i = 0; i < VE; ++i) sum[i] += load_elem<T>(x + i);
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < VE; ++i) s_part[v * VE + i] = sum[i];
+      }
+    }
+    __syncthreads();
+    if (act && half == 1 && ksum) {
+#pragma unroll
+      for (int i = 0; i < VE; ++i) sum[i] = s_part[v * VE + i];
+#pragma unroll
+      for (int s2 = kHalf; s2 < kBlock - 1; ++s2) {
+        const T* x = reinterpret_cast<const T*>(&raw[s2 - kHalf]);
         if (s2 < slot) {
 #pragma unroll
           for (int i = 0; i < VE; ++i) sum[i] += load_elem<T>(x + i);
         }
       }
+      const T* kx = reinterpret_cast<const T*>(&kraw);
       float* out = ksum + (static_cast<long long>(p) * Hkv + g) * D + dd;
 #pragma unroll
       for (int i = 0; i < VE; ++i) out[i] = __fdiv_rn(sum[i] + load_elem<T>(kx + i), static_cast<float>(slot + 1));
+    }
+  } else {
+    for (int v = threadIdx.x; v < items; v += kAppendThreads) {
+      const int e0 = v * VE;
+      const int g = e0 / D, dd = e0 % D;
+      const long long src = (static_cast<long long>(b) * Hkv + g) * D + dd;
+      const long long tile = (static_cast<long long>(p) * Hkv + g) * kBlock * D;
+      const uint4 kraw = *reinterpret_cast<const uint4*>(k_new + src);
+      const uint4 vraw = *reinterpret_cast<const uint4*>(v_new + src);
+      // The earlier slots in two halves of kHalf rows through one array.
+      uint4 raw[kHalf];
+      if (ksum) {
+#pragma unroll
+        for (int i = 0; i < kHalf; ++i) raw[i] = *reinterpret_cast<const uint4*>(kc + tile + i * D + dd);
+      }
+      *reinterpret_cast<uint4*>(kc + tile + slot * D + dd) = kraw;
+      const T* kx = reinterpret_cast<const T*>(&kraw);
+      const T* vx = reinterpret_cast<const T*>(&vraw);
+#pragma unroll
+      for (int i = 0; i < VE; ++i) vc[tile + (dd + i) * kBlock + slot] = vx[i];
+      if (ksum) {
+        float sum[VE];
+#pragma unroll
+        for (int i = 0; i < VE; ++i) sum[i] = 0.f;
+#pragma unroll
+        for (int s2 = 0; s2 < kHalf; ++s2) {
+          const T* x = reinterpret_cast<const T*>(&raw[s2]);
+          if (s2 < slot) {
+#pragma unroll
+            for (int i = 0; i < VE; ++i) sum[i] += load_elem<T>(x + i);
+          }
+        }
+        if (slot > kHalf) {
+#pragma unroll
+          for (int i = 0; i < kHalf - 1; ++i)
+            raw[i] = *reinterpret_cast<const uint4*>(kc + tile + (kHalf + i) * D + dd);
+#pragma unroll
+          for (int s2 = kHalf; s2 < kBlock - 1; ++s2) {
+            const T* x = reinterpret_cast<const T*>(&raw[s2 - kHalf]);
+            if (s2 < slot) {
+#pragma unroll
+              for (int i = 0; i < VE; ++i) sum[i] += load_elem<T>(x + i);
+            }
+          }
+        }
+        float* out = ksum + (static_cast<long long>(p) * Hkv + g) * D + dd;
+#pragma unroll
+        for (int i = 0; i < VE; ++i) out[i] = __fdiv_rn(sum[i] + load_elem<T>(kx + i), static_cast<float>(slot + 1));
+      }
     }
   }
   __syncthreads();
