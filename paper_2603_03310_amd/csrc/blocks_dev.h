@@ -154,11 +154,15 @@ __device__ __forceinline__ void score_q_load(const uint16_t* __restrict__ q, int
   }
 }
 
+// With store false (G <= 8 only) the block logits are not written: they are
+// returned packed two per lane for store_held_z to write later (lanes r16 < 8
+// keep blocks 4 gq, 4 gq + 1 of head r16; lanes r16 >= 8 take blocks
+// 4 gq + 2, 4 gq + 3 of head r16 - 8, from the padding columns' lanes).
 template <int D>
-__device__ __forceinline__ void score_head_compute(
+__device__ __forceinline__ sf32x2_t score_head_compute(
     const uint2 (&qv)[D / 16], const float4 (&buf)[kScoreSlots],
     float* __restrict__ zbuf, float* __restrict__ lse_part, int b, int ch, int g, int N, int nb,
-    int Hkv, int G, int MAXB, int nch_max, float scale) {
+    int Hkv, int G, int MAXB, int nch_max, float scale, bool store) {
   constexpr int KS = D / 32;
   const int Hq = Hkv * G;
   const int lane = threadIdx.x & 63;
@@ -180,14 +184,15 @@ __device__ __forceinline__ void score_head_compute(
   const float ln_last = logf(static_cast<float>(N - kBlock * (nb - 1)));
   const float ln_full = logf(static_cast<float>(kBlock));
   float* zrow = zbuf + (static_cast<long long>(b) * MAXB + jt) * Hq;
-  float l[4];
+  float l[4], zv[4];
   float m = -INFINITY;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int j = jt + 4 * gq + e;
     const float z = acc[e] * scale;
+    zv[e] = z;
     const bool ok = j < nb;
-    if (ok && r16 < G) zrow[(4 * gq + e) * Hq + g * G + r16] = z;
+    if (store && ok && r16 < G) zrow[(4 * gq + e) * Hq + g * G + r16] = z;
     l[e] = ok ? z + ((j == nb - 1) ? ln_last : ln_full) : -INFINITY;
     m = fmaxf(m, l[e]);
   }
@@ -203,6 +208,25 @@ __device__ __forceinline__ void score_head_compute(
     lp[0] = m;
     lp[1] = sum;
   }
+  if (store) return sf32x2_t{0.f, 0.f};
+  const int src = r16 >= 8 ? lane - 8 : lane;
+  const float z2 = __shfl(zv[2], src), z3 = __shfl(zv[3], src);
+  return r16 < 8 ? sf32x2_t{zv[0], zv[1]} : sf32x2_t{z2, z3};
+}
+
+// Writes the block logits that score_head_compute returned packed (tile ch
+// of sequence b with nb blocks, KV head g; G <= 8).
+__device__ __forceinline__ void store_held_z(sf32x2_t v, float* __restrict__ zbuf, int b, int ch,
+                                             int g, int nb, int Hkv, int G, int MAXB) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, gq = lane >> 4;
+  const int h = r16 & 7, e0 = 4 * gq + (r16 < 8 ? 0 : 2);
+  if (h >= G) return;
+  const int Hq = Hkv * G;
+  const int jt = ch * kMfmaChunk;
+  float* zrow = zbuf + (static_cast<long long>(b) * MAXB + jt) * Hq + g * G + h;
+  if (jt + e0 < nb) zrow[e0 * Hq] = v.x;
+  if (jt + e0 + 1 < nb) zrow[(e0 + 1) * Hq] = v.y;
 }
 
 template <int G, int L>
