@@ -202,9 +202,10 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   const size_t sz_ex = f.scoring == ENT_SCORE_EXACT
                            ? align_up(Bm * f.max_blocks_per_seq * f.num_q_heads * 2 * sizeof(float))
                            : 0;
+  const size_t sz_tick = align_up(Bm * sizeof(unsigned));
   const size_t sz_flags = align_up(sizeof(unsigned));
   c->ws_bytes = sz_ent_part + sz_stats + sz_z + sz_lse + sz_lrow + sz_isc + sz_kphys + sz_acc + sz_ml +
-                sz_rec + sz_tmax + sz_ex + sz_flags;
+                sz_rec + sz_tmax + sz_ex + sz_tick + sz_flags;
   e = hipMalloc(&c->ws, c->ws_bytes);
   if (e != hipSuccess) {
     g_init_error = std::string("workspace allocation failed: ") + hipGetErrorString(e);
@@ -233,6 +234,7 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->dec_rec = reinterpret_cast<int4*>(take(sz_rec));
   c->tmax = sz_tmax ? reinterpret_cast<float*>(take(sz_tmax)) : nullptr;
   c->exbuf = sz_ex ? reinterpret_cast<float2*>(take(sz_ex)) : nullptr;
+  c->tickets = reinterpret_cast<unsigned*>(take(sz_tick));
   c->dev_flags = reinterpret_cast<unsigned*>(take(sz_flags));
   *out = c;
   return ENT_OK;

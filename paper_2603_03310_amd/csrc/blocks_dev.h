@@ -363,8 +363,9 @@ __device__ __forceinline__ void budget_record(const Budget& bu, int b, float kap
 // (select_one_launch), one workgroup per sequence runs all three; otherwise
 // (the long-table forms) B runs over the whole chip, so long sequences
 // spread their exponentials: the per-stage entry point in three launches
-// (per-sequence A, B per 64 blocks, per-sequence C), the fused step in two
-// (A and B together per tile of 256 blocks, lse_block_score_body, then C).
+// (per-sequence A, B per 64 blocks, per-sequence C), the fused step in one
+// (A and B together per tile of 256 blocks, lse_block_score_body, and C on
+// the last of a sequence's workgroups to finish).
 // All forms perform the same arithmetic in the same order, so their results
 // are identical.
 constexpr int kRowThreads = 256;          // threads of the chip-wide block-score launch
@@ -501,7 +502,9 @@ __device__ __forceinline__ float block_ln_count(int j, int N, int nb) {
 // Step B for blocks j0 .. j0 + TB - 1 of sequence b (context length N, nb
 // blocks) by NT threads, in passes of NT / LPB blocks, L_h in LDS (sL).  A
 // block's terms and their order do not depend on NT or TB.
-template <int NT, int TB>
+// COH: the scores are stored at device scope (read by another workgroup of
+// the same launch).
+template <int NT, int TB, bool COH = false>
 __device__ __forceinline__ void block_score_tile(const float* __restrict__ zbuf, const float* sL,
                                                  float* __restrict__ scores, int Hq, int MAXB,
                                                  int b, int N, int nb, int j0) {
@@ -542,7 +545,12 @@ __device__ __forceinline__ void block_score_tile(const float* __restrict__ zbuf,
       }
     }
     acc = lanes_sum(acc, LPB);
-    if (ok && li == 0) scores[static_cast<long long>(b) * MAXB + j] = __fdiv_rn(acc, static_cast<float>(Hq));
+    if (ok && li == 0) {
+      float* dst = scores + static_cast<long long>(b) * MAXB + j;
+      const float I = __fdiv_rn(acc, static_cast<float>(Hq));
+      if (COH) __hip_atomic_store(dst, I, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      else *dst = I;
+    }
   }
 }
 
@@ -567,6 +575,7 @@ __device__ __forceinline__ void block_score_body(const float* __restrict__ zbuf,
 // L_h merged in LDS exactly as step A's own launch merges it, then the
 // tile's scores.  Every thread must call it.
 constexpr int kStepTileBlocks = 256;
+template <bool COH = false>
 __device__ __forceinline__ void lse_block_score_body(const float* __restrict__ zbuf,
                                                      const float* __restrict__ lse_part,
                                                      const int* __restrict__ ctx_lens,
@@ -579,7 +588,7 @@ __device__ __forceinline__ void lse_block_score_body(const float* __restrict__ z
   if (j0 >= nb) return;
   lse_merge_body(lse_part, ctx_lens, sL, Hq, MAXB, nch_max, b, s_pm, s_ps);
   __syncthreads();
-  block_score_tile<kFoldThreads, kStepTileBlocks>(zbuf, sL, scores, Hq, MAXB, b, N, nb, j0);
+  block_score_tile<kFoldThreads, kStepTileBlocks, COH>(zbuf, sL, scores, Hq, MAXB, b, N, nb, j0);
 }
 
 constexpr int kSelRankMax = 64;    // prefix groups this small are finished by counting ranks
@@ -782,7 +791,9 @@ __device__ __forceinline__ bool select_prepare(int N, float hval, float* __restr
   return true;
 }
 
-// Step C as its own launch: keys from step B's scores.
+// Step C as its own launch: keys from step B's scores (COH: read at device
+// scope, written by other workgroups of the same launch).
+template <bool COH = false>
 __device__ __forceinline__ void select_row_body(
     const float* __restrict__ scores, const int* __restrict__ ctx_lens,
     const int* __restrict__ tables, float hval, float* __restrict__ theta_out,
@@ -807,7 +818,8 @@ __device__ __forceinline__ void select_row_body(
   const float* sr = scores + static_cast<long long>(b) * MAXB;
   const int* tr = tables + static_cast<long long>(b) * MAXB;
   for (int i = threadIdx.x; i < nb; i += kSelThreads) {
-    keys[i] = select_key(sr[i], i, nb, bu);
+    const float I = COH ? __hip_atomic_load(sr + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : sr[i];
+    keys[i] = select_key(I, i, nb, bu);
     tbl[i] = encode_phys(tr[i], i, nb, P);
   }
   __syncthreads();

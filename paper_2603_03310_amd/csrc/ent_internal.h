@@ -78,6 +78,7 @@ struct ent_ctx {
   int4* dec_rec = nullptr;        // [decode waves]  cut-segment records of the decode ranges
   float* tmax = nullptr;          // [max_batch, chunks, 256]  per-thread logit maxima (estimators)
   float2* exbuf = nullptr;        // [max_batch, MAXB, H_q]  exact mode: (log mass, mean logit) per block
+  unsigned* tickets = nullptr;    // [max_batch]  per-sequence counters of the fused step (zero between launches)
   unsigned* dev_flags = nullptr;  // [1]
 
   std::string err;

@@ -13,8 +13,9 @@
 //      own, sampling at T_t (it needs only the row statistics of A, so it
 //      runs on the CUs the per-sequence selection leaves idle).  For long
 //      block tables: entropy and controller per sequence and, on workgroups
-//      of their own, L_h and the block scores per tile of 256 blocks, then
-//      the selection per sequence in a second launch; sampling moves to D;
+//      of their own, L_h and the block scores per tile of 256 blocks, each
+//      sequence's selection on the last of its workgroups to finish (a
+//      ticket per sequence); sampling moves to D;
 //   C  kept-block decode attention;
 //   D  the merge of split decode segments (and, on workgroups of their own,
 //      ent_decode_step_append's append of the new token's K/V and, for long
@@ -22,6 +23,8 @@
 
 #include "blocks_dev.h"
 #include "estimate_dev.h"
+
+#include <algorithm>
 
 namespace ent {
 namespace {
@@ -40,33 +43,68 @@ __device__ __forceinline__ void step_sample(const SampleArgs& sa, int b, SampleS
 // an estimator, the estimate first), and the rest one (sequence, tile of
 // kStepTileBlocks blocks) each: the sequence's L_h, merged as the per-stage
 // launch merges it, then the tile's block scores.  Tiles past a sequence's
-// blocks exit at once.  (Sampling runs in the merge launch of this form.)
+// blocks exit at once.  Each sequence's selection runs on whichever of its
+// workgroups (the entropy one and those of its tiles with blocks) finishes
+// last: each stores what the selection reads (the entropy, the scores) at
+// device scope, waits for those stores, then takes a ticket from the
+// sequence's device-scope counter; the one that takes the last ticket
+// resets the counter and selects, as the per-stage selection launch does.
+// Nothing waits for another workgroup.  (Sampling runs in the merge launch
+// of this form.)
 template <bool VEC>
 __global__ __launch_bounds__(kFoldThreads) void step_b1_kernel(
     int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
     float* h_out, Control ct, const float* __restrict__ zbuf, const float* __restrict__ lse_part,
     const int* __restrict__ ctx_lens, float* __restrict__ scores, int Hq, int MAXB, int nch_max,
-    int ntile, SampleArgs sa, int est, int est_k, const float* __restrict__ tmax) {
-  static_assert(kFoldThreads >= kEstThreads, "workgroup size");
-  extern __shared__ __attribute__((aligned(16))) unsigned est_lds[];
+    int ntile, SampleArgs sa, int est, int est_k, const float* __restrict__ tmax,
+    const int* __restrict__ tables, float* __restrict__ theta, int* __restrict__ kept,
+    int* __restrict__ kphys, int* __restrict__ n_kept, int P, Budget bu, unsigned* flags,
+    unsigned* tickets) {
+  static_assert(kFoldThreads >= kEstThreads && kFoldThreads == kSelThreads, "workgroup size");
+  // Estimator LDS, then (the selecting workgroup) the keys and encoded blocks.
+  extern __shared__ __attribute__((aligned(16))) unsigned dyn_lds[];
   __shared__ float s_pm[kFoldThreads], s_ps[kFoldThreads], sL[128];
   __shared__ EstShared esh;
-  const int b = blockIdx.x;
-  if (b >= B) {
-    const int r = b - B, seq = r / ntile;
-    lse_block_score_body(zbuf, lse_part, ctx_lens, scores, Hq, MAXB, nch_max, seq,
-                         (r - seq * ntile) * kStepTileBlocks, s_pm, s_ps, sL);
-    return;
+  __shared__ SelectShared ssel;
+  __shared__ int s_last;
+  int seq;
+  if (blockIdx.x >= B) {
+    const int r = blockIdx.x - B;
+    seq = r / ntile;
+    const int j0 = (r - seq * ntile) * kStepTileBlocks;
+    const int N = ctx_lens[seq];
+    if (N < 0 || N > MAXB * kBlock || j0 >= (N + kBlock - 1) / kBlock) return;   // no blocks
+    lse_block_score_body<true>(zbuf, lse_part, ctx_lens, scores, Hq, MAXB, nch_max, seq, j0, s_pm,
+                               s_ps, sL);
+  } else {
+    seq = blockIdx.x;
+    if (est != ENT_EST_EXACT) {
+      const float T = temp[seq];
+      const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T * sa.t_cal,
+                                   seq, dyn_lds, esh);
+      if (threadIdx.x == 0) controller_update(seq, H, T, h_prev, tau, temp, h_out, nullptr, ct);
+    } else if (threadIdx.x < 64) {
+      const float H = row_entropy(part, C, seq);
+      if (threadIdx.x == 0) controller_update(seq, H, temp[seq], h_prev, tau, temp, h_out, nullptr, ct);
+    }
+    if (threadIdx.x == 0)
+      __hip_atomic_store(h_out + seq, h_out[seq], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  if (est != ENT_EST_EXACT) {
-    const float T = temp[b];
-    const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T * sa.t_cal, b,
-                                 est_lds, esh);
-    if (threadIdx.x == 0) controller_update(b, H, T, h_prev, tau, temp, h_out, nullptr, ct);
-  } else if (threadIdx.x < 64) {
-    const float H = row_entropy(part, C, b);
-    if (threadIdx.x == 0) controller_update(b, H, temp[b], h_prev, tau, temp, h_out, nullptr, ct);
-  }
+  const int N = ctx_lens[seq];
+  const bool ok = N >= 0 && N <= MAXB * kBlock;
+  const int nb = ok ? (N + kBlock - 1) / kBlock : 0;
+  const unsigned parts = static_cast<unsigned>((nb + kStepTileBlocks - 1) / kStepTileBlocks) + 1u;
+  __builtin_amdgcn_s_waitcnt(0);           // this wave's device-scope stores have completed
+  __syncthreads();
+  if (threadIdx.x == 0)
+    s_last = __hip_atomic_fetch_add(tickets + seq, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+             parts - 1;
+  __syncthreads();
+  if (!s_last) return;
+  if (threadIdx.x == 0) tickets[seq] = 0u;
+  const float hval = __hip_atomic_load(h_out + seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  select_row_body<true>(scores, ctx_lens, tables, hval, theta, kept, kphys, n_kept, MAXB, P, bu,
+                        flags, seq, dyn_lds, reinterpret_cast<int*>(dyn_lds + MAXB), ssel);
 }
 
 // Per sequence, block tables that fit the one-launch selection: the
@@ -212,14 +250,15 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   } else {
     float* sc = scores ? scores : c->iscores;
     const int ntile = (cf.max_blocks_per_seq + kStepTileBlocks - 1) / kStepTileBlocks;
+    const size_t lds =
+        std::max(est_lds, 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned));
     auto k1 = vec ? step_b1_kernel<true> : step_b1_kernel<false>;
-    hipLaunchKernelGGL(k1, dim3(B + B * ntile), dim3(kFoldThreads), est_lds, s, B, c->ent_part,
+    hipLaunchKernelGGL(k1, dim3(B + B * ntile), dim3(kFoldThreads), lds, s, B, c->ent_part,
                        c->chunks, st.temp, st.h_prev, st.tau, h_out, ct, c->zbuf, c->lse_part,
                        ctx_lens, sc, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks, ntile, sa,
-                       est_mode, cf.est_k, c->tmax);
+                       est_mode, cf.est_k, c->tmax, tables, theta, kept, c->kept_phys, n_kept,
+                       cf.num_pool_blocks, bu, c->dev_flags, c->tickets);
     e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    e = launch_select_rows(c, B, tables, ctx_lens, h_out, sc, theta, kept, n_kept, st.kappa, s);
     if (e != hipSuccess) return e;
     return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s,
                          c->kept_phys, ap, &sa);
