@@ -4,9 +4,9 @@ against ent_decode_step followed by ent_kv_append, through the C ABI: every
 output, the controller and kept-fraction state, the caches, the block
 summaries and the lengths agree bit for bit over a multi-step loop; bf16
 batches in both selection forms (one launch per sequence, and the
-long-table form: the tile launch, the selection, sampling in the last
-launch beside the appends) and the fp32 (VALU) path with short and wide
-tables.  Parity of the loop itself against the oracle:
+long-table form: the tile launch with each sequence's selection on its last
+workgroup, sampling in the last launch beside the appends) and the fp32
+(VALU) path with short and wide tables.  Parity of the loop itself against the oracle:
 tests/test_gpu_full_loop.py."""
 import numpy as np
 import pytest
