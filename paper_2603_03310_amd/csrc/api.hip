@@ -182,6 +182,7 @@ int ent_init(const ent_config* cfg, ent_ctx** out) {
   c->lse_chunks = (f.max_blocks_per_seq + ent::kMinScoreChunk - 1) / ent::kMinScoreChunk;
   c->decode_grid = ent::decode_grid_size(c);
   c->prologue_grid = ent::prologue_grid_size(c);
+  ent::step_occupancy(c);
 
   const size_t Bm = static_cast<size_t>(f.max_batch);
   const size_t sz_ent_part = align_up(Bm * c->chunks * 3 * sizeof(float));

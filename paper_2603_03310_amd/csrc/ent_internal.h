@@ -63,6 +63,8 @@ struct ent_ctx {
   int lse_chunks = 0;       // log-sum-exp partials per sequence (finest chunking)
   int decode_grid = 0;      // persistent decode workgroups
   int prologue_grid = 0;    // resident entropy / scoring workgroups
+  int b1_occ_plain = 0;     // resident tile-launch workgroups per CU, without the selection inside
+  int b1_occ_ticket = 0;    // ... and with it
 
   void* ws = nullptr;       // one workspace allocation
   size_t ws_bytes = 0;
@@ -144,6 +146,9 @@ struct PrologueArgs {
 };
 hipError_t launch_prologue(const ent_ctx* c, const PrologueArgs& a, hipStream_t s);
 int prologue_grid_size(const ent_ctx* c);
+// Residency of the fused step's tile launch with and without the selection
+// inside (ent_ctx::b1_occ_*).
+void step_occupancy(ent_ctx* c);
 // The kept-block selection after scoring (L merge, block scores, radix
 // select), given each sequence's entropy h.
 hipError_t launch_selection(const ent_ctx* c, int B, const int* tables, const int* ctx_lens,

@@ -38,58 +38,15 @@ __device__ __forceinline__ void step_sample(const SampleArgs& sa, int b, SampleS
   if (threadIdx.x == 0) sa.tokens[b] = tok;
 }
 
-// Block tables too wide for the one-launch selection: workgroups 0 .. B-1
-// take a row's entropy from the chunk triples and the controller update (with
-// an estimator, the estimate first), and the rest one (sequence, tile of
-// kStepTileBlocks blocks) each: the sequence's L_h, merged as the per-stage
-// launch merges it, then the tile's block scores.  Tiles past a sequence's
-// blocks exit at once.  Each sequence's selection runs on whichever of its
-// workgroups (the entropy one and those of its tiles with blocks) finishes
-// last: each stores what the selection reads (the entropy, the scores) at
-// device scope, waits for those stores, then takes a ticket from the
-// sequence's device-scope counter; the one that takes the last ticket
-// resets the counter and selects, as the per-stage selection launch does.
-// Nothing waits for another workgroup.  (Sampling runs in the merge launch
-// of this form.)
-template <bool VEC>
-__global__ __launch_bounds__(kFoldThreads) void step_b1_kernel(
-    int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
-    float* h_out, Control ct, const float* __restrict__ zbuf, const float* __restrict__ lse_part,
-    const int* __restrict__ ctx_lens, float* __restrict__ scores, int Hq, int MAXB, int nch_max,
-    int ntile, SampleArgs sa, int est, int est_k, const float* __restrict__ tmax,
-    const int* __restrict__ tables, float* __restrict__ theta, int* __restrict__ kept,
-    int* __restrict__ kphys, int* __restrict__ n_kept, int P, Budget bu, unsigned* flags,
-    unsigned* tickets) {
-  static_assert(kFoldThreads >= kEstThreads && kFoldThreads == kSelThreads, "workgroup size");
-  // Estimator LDS, then (the selecting workgroup) the keys and encoded blocks.
-  extern __shared__ __attribute__((aligned(16))) unsigned dyn_lds[];
-  __shared__ float s_pm[kFoldThreads], s_ps[kFoldThreads], sL[128];
-  __shared__ EstShared esh;
+// The ticket and, on the last workgroup of sequence seq, its selection.
+__device__ __forceinline__ void step_b1_select(int seq, const int* __restrict__ ctx_lens,
+                                            const float* h_out, const float* scores,
+                                            const int* __restrict__ tables, float* theta,
+                                            int* kept, int* kphys, int* n_kept, int MAXB, int P,
+                                            Budget bu, unsigned* flags, unsigned* tickets,
+                                            unsigned* dyn_lds) {
   __shared__ SelectShared ssel;
   __shared__ int s_last;
-  int seq;
-  if (blockIdx.x >= B) {
-    const int r = blockIdx.x - B;
-    seq = r / ntile;
-    const int j0 = (r - seq * ntile) * kStepTileBlocks;
-    const int N = ctx_lens[seq];
-    if (N < 0 || N > MAXB * kBlock || j0 >= (N + kBlock - 1) / kBlock) return;   // no blocks
-    lse_block_score_body<true>(zbuf, lse_part, ctx_lens, scores, Hq, MAXB, nch_max, seq, j0, s_pm,
-                               s_ps, sL);
-  } else {
-    seq = blockIdx.x;
-    if (est != ENT_EST_EXACT) {
-      const float T = temp[seq];
-      const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T * sa.t_cal,
-                                   seq, dyn_lds, esh);
-      if (threadIdx.x == 0) controller_update(seq, H, T, h_prev, tau, temp, h_out, nullptr, ct);
-    } else if (threadIdx.x < 64) {
-      const float H = row_entropy(part, C, seq);
-      if (threadIdx.x == 0) controller_update(seq, H, temp[seq], h_prev, tau, temp, h_out, nullptr, ct);
-    }
-    if (threadIdx.x == 0)
-      __hip_atomic_store(h_out + seq, h_out[seq], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
   const int N = ctx_lens[seq];
   const bool ok = N >= 0 && N <= MAXB * kBlock;
   const int nb = ok ? (N + kBlock - 1) / kBlock : 0;
@@ -105,6 +62,62 @@ __global__ __launch_bounds__(kFoldThreads) void step_b1_kernel(
   const float hval = __hip_atomic_load(h_out + seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   select_row_body<true>(scores, ctx_lens, tables, hval, theta, kept, kphys, n_kept, MAXB, P, bu,
                         flags, seq, dyn_lds, reinterpret_cast<int*>(dyn_lds + MAXB), ssel);
+}
+
+// Block tables too wide for the one-launch selection: workgroups 0 .. B-1
+// take a row's entropy from the chunk triples and the controller update (with
+// an estimator, the estimate first), and the rest one (sequence, tile of
+// kStepTileBlocks blocks) each: the sequence's L_h, merged as the per-stage
+// launch merges it, then the tile's block scores.  Tiles past a sequence's
+// blocks exit at once.  With TICK, each sequence's selection
+// runs on whichever of its workgroups (the entropy one and those of its
+// tiles with blocks) finishes last: each stores what the selection reads
+// (the entropy, the scores) at device scope, waits for those stores, then
+// takes a ticket from the sequence's device-scope counter; the one that
+// takes the last ticket resets the counter and selects, as the per-stage
+// selection launch does.  Nothing waits for another workgroup.  Without,
+// the selection launch follows.  (Sampling runs in the merge launch of this
+// form.)
+template <bool VEC, bool TICK>
+__global__ __launch_bounds__(kFoldThreads) void step_b1_kernel(
+    int B, const float* __restrict__ part, int C, float* temp, float* h_prev, float* tau,
+    float* h_out, Control ct, const float* __restrict__ zbuf, const float* __restrict__ lse_part,
+    const int* __restrict__ ctx_lens, float* __restrict__ scores, int Hq, int MAXB, int nch_max,
+    int ntile, SampleArgs sa, int est, int est_k, const float* __restrict__ tmax,
+    const int* __restrict__ tables, float* __restrict__ theta, int* __restrict__ kept,
+    int* __restrict__ kphys, int* __restrict__ n_kept, int P, Budget bu, unsigned* flags,
+    unsigned* tickets) {
+  static_assert(kFoldThreads >= kEstThreads && kFoldThreads == kSelThreads, "workgroup size");
+  // Estimator LDS, then (the selecting workgroup) the keys and encoded blocks.
+  extern __shared__ __attribute__((aligned(16))) unsigned dyn_lds[];
+  __shared__ float s_pm[kFoldThreads], s_ps[kFoldThreads], sL[128];
+  __shared__ EstShared esh;
+  int seq;
+  if (blockIdx.x >= B) {
+    const int r = blockIdx.x - B;
+    seq = r / ntile;
+    const int j0 = (r - seq * ntile) * kStepTileBlocks;
+    const int N = ctx_lens[seq];
+    if (N < 0 || N > MAXB * kBlock || j0 >= (N + kBlock - 1) / kBlock) return;   // no blocks
+    lse_block_score_body<TICK>(zbuf, lse_part, ctx_lens, scores, Hq, MAXB, nch_max, seq, j0, s_pm,
+                               s_ps, sL);
+  } else {
+    seq = blockIdx.x;
+    if (est != ENT_EST_EXACT) {
+      const float T = temp[seq];
+      const float H = row_estimate(est, est_k, part, tmax, sa.logits, sa.ld, sa.V, C, T * sa.t_cal,
+                                   seq, dyn_lds, esh);
+      if (threadIdx.x == 0) controller_update(seq, H, T, h_prev, tau, temp, h_out, nullptr, ct);
+    } else if (threadIdx.x < 64) {
+      const float H = row_entropy(part, C, seq);
+      if (threadIdx.x == 0) controller_update(seq, H, temp[seq], h_prev, tau, temp, h_out, nullptr, ct);
+    }
+    if constexpr (TICK)
+      if (threadIdx.x == 0) __hip_atomic_store(h_out + seq, h_out[seq], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  if constexpr (TICK)
+    step_b1_select(seq, ctx_lens, h_out, scores, tables, theta, kept, kphys, n_kept, MAXB, P, bu,
+                   flags, tickets, dyn_lds);
 }
 
 // Per sequence, block tables that fit the one-launch selection: the
@@ -159,6 +172,26 @@ __global__ __launch_bounds__(kSelThreads) void step_b_kernel(
                     keys, reinterpret_cast<int*>(keys + MAXB), sh);
 }
 }  // namespace
+
+// Dynamic LDS of the tile launch: the estimator's, and with the selection
+// inside, at least the keys and encoded blocks of a table row.
+static size_t step_b1_lds(const ent_ctx* c, bool tickets) {
+  const ent_config& cf = c->cfg;
+  const size_t est = uses_estimate(cf) ? est_lds_bytes(c->chunks, cf.est_k) : 0;
+  return tickets ? std::max(est, 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned))
+                 : est;
+}
+
+void step_occupancy(ent_ctx* c) {
+  c->b1_occ_plain = 0;
+  c->b1_occ_ticket = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&c->b1_occ_plain, step_b1_kernel<true, false>,
+                                                   kFoldThreads, step_b1_lds(c, false)) != hipSuccess)
+    c->b1_occ_plain = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&c->b1_occ_ticket, step_b1_kernel<true, true>,
+                                                   kFoldThreads, step_b1_lds(c, true)) != hipSuccess)
+    c->b1_occ_ticket = 0;
+}
 
 hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long long ld,
                               ent_state st, const void* q, const void* k_cache,
@@ -250,16 +283,28 @@ hipError_t launch_decode_step(const ent_ctx* c, int B, const float* logits, long
   } else {
     float* sc = scores ? scores : c->iscores;
     const int ntile = (cf.max_blocks_per_seq + kStepTileBlocks - 1) / kStepTileBlocks;
-    const size_t lds =
-        std::max(est_lds, 2 * static_cast<size_t>(cf.max_blocks_per_seq) * sizeof(unsigned));
-    auto k1 = vec ? step_b1_kernel<true> : step_b1_kernel<false>;
-    hipLaunchKernelGGL(k1, dim3(B + B * ntile), dim3(kFoldThreads), lds, s, B, c->ent_part,
+    const int grid = B + B * ntile;
+    // The selection inside the tile launch pays when its keys leave the
+    // launch's residency as it is and the grid takes at most two rounds of
+    // it (else the selecting workgroups hold slots that tiles wait for): on
+    // the 70B-shaped loop 2 us faster, at 8192-block tables (one workgroup
+    // per CU less) and a 2304-workgroup grid 18 and 10 us slower.
+    const bool tick = c->b1_occ_ticket >= c->b1_occ_plain &&
+                      grid <= 2 * c->num_cu * c->b1_occ_plain;
+    const size_t lds = tick ? step_b1_lds(c, true) : step_b1_lds(c, false);
+    auto k1 = tick ? (vec ? step_b1_kernel<true, true> : step_b1_kernel<false, true>)
+                   : (vec ? step_b1_kernel<true, false> : step_b1_kernel<false, false>);
+    hipLaunchKernelGGL(k1, dim3(grid), dim3(kFoldThreads), lds, s, B, c->ent_part,
                        c->chunks, st.temp, st.h_prev, st.tau, h_out, ct, c->zbuf, c->lse_part,
                        ctx_lens, sc, cf.num_q_heads, cf.max_blocks_per_seq, c->lse_chunks, ntile, sa,
                        est_mode, cf.est_k, c->tmax, tables, theta, kept, c->kept_phys, n_kept,
-                       cf.num_pool_blocks, bu, c->dev_flags, c->tickets);
+                       cf.num_pool_blocks, bu, c->dev_flags, tick ? c->tickets : nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (!tick) {
+      e = launch_select_rows(c, B, tables, ctx_lens, h_out, sc, theta, kept, n_kept, st.kappa, s);
+      if (e != hipSuccess) return e;
+    }
     return launch_decode(c, B, q, k_cache, v_cache, tables, ctx_lens, kept, n_kept, out, lse, s,
                          c->kept_phys, ap, &sa);
   }
