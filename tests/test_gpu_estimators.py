@@ -105,8 +105,11 @@ def test_ties_uniform_onehot_masked_rows(torch_cuda, est):
 
 
 def test_three_launch_selection(torch_cuda):
-    """Block tables over 1024 blocks: entropy estimate, controller and L_h per
-    sequence in the first of three selection launches."""
+    """Block tables over 1024 blocks: the entropy estimate and the controller
+    in the fused step's tile launch (whose selecting workgroup, when it is
+    the entropy one, reuses the estimator's LDS for its keys) and in the
+    first of the staged form's three selection launches; both forms equal
+    bit for bit."""
     w = small(LONG_CONTEXT, 3, ctx=("uniform", 9000, 20000), suffix="est_long")
     p = default_params(w).replace(estimator=TAIL, est_k=256)
     _both(torch_cuda, w, p)
