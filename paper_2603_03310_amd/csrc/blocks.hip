@@ -21,7 +21,8 @@
 //   block_score_kernel, (the per-stage entry point): per sequence L_h; per 64
 //   select_kernel       blocks I_b; per sequence the selection (the fused step
 //                       runs L_h and I_b per 256-block tile in one launch,
-//                       step.hip, then select_kernel)
+//                       step.hip, with the selection on each sequence's last
+//                       workgroup or in select_kernel after it)
 //   append_kernel    writes one token and refreshes its block's mean key
 
 #include "blocks_dev.h"

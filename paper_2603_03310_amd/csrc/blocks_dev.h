@@ -364,8 +364,10 @@ __device__ __forceinline__ void budget_record(const Budget& bu, int b, float kap
 // (the long-table forms) B runs over the whole chip, so long sequences
 // spread their exponentials: the per-stage entry point in three launches
 // (per-sequence A, B per 64 blocks, per-sequence C), the fused step in one
-// (A and B together per tile of 256 blocks, lse_block_score_body, and C on
-// the last of a sequence's workgroups to finish).
+// or two (A and B together per tile of 256 blocks, lse_block_score_body,
+// and C on the last of a sequence's workgroups to finish, or in a launch of
+// its own when that would lower the tile launch's residency or its grid is
+// many rounds of it).
 // All forms perform the same arithmetic in the same order, so their results
 // are identical.
 constexpr int kRowThreads = 256;          // threads of the chip-wide block-score launch
