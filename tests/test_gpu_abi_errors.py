@@ -1,7 +1,8 @@
 """Argument checks of the entry points on a real context (they need a
 device for ent_init): a bad argument returns ENT_E_INVAL with nothing
-launched (the outputs keep their sentinel values) and a message; the exact
-scoring mode runs without block summaries, in the step and in append.
+launched (the outputs keep their sentinel values) and a message; an empty
+batch (B = 0) launches nothing in every entry point that takes a batch; the
+exact scoring mode runs without block summaries, in the step and in append.
 """
 import numpy as np
 import pytest
@@ -100,3 +101,87 @@ def test_exact_step_and_append_without_summaries(torch_cuda):
                                           x.v_new[t, s], 16)
         assert dec.device_status() == 0
     assert list(dev.ctx_lens.cpu().numpy()) == list(ctx)
+
+
+# Every buffer an entry point could write, compared byte for byte.
+MUTABLE = ("ctx_lens", "k_pool", "v_pool", "h_prev", "tau", "temp", "ksum", "h", "temp_used",
+           "row_stats", "kept", "n_kept", "scores", "theta", "out", "lse", "tokens", "kappa")
+
+
+def _batch_calls(ent, dec, d):
+    """Every entry point that takes a batch, as f(B, nul), with step 0's
+    inputs; nul passes NULL for every pointer."""
+    ld = d.logits[0].stride(0)
+
+    def p(v, nul):
+        return None if nul else v
+
+    return {
+        "ent_entropy_temperature": lambda B, n: ent.ent_entropy_temperature(
+            dec.ctx, B, p(d.logits[0], n), ld, p(d.h_prev, n), p(d.tau, n), p(d.temp, n),
+            p(d.h, n), p(d.temp_used, n), p(d.row_stats, n)),
+        "ent_entropy_temperature_noalloc": lambda B, n: ent.ent_entropy_temperature_noalloc(
+            dec.cfg, B, p(d.logits[0], n), ld, p(d.h_prev, n), p(d.tau, n), p(d.temp, n),
+            p(d.h, n), p(d.temp_used, n), p(d.row_stats, n)),
+        "ent_block_summary": lambda B, n: ent.ent_block_summary(
+            dec.ctx, B, p(d.k_pool, n), p(d.block_tables, n), p(d.ctx_lens, n), p(d.ksum, n)),
+        "ent_block_select": lambda B, n: ent.ent_block_select(
+            dec.ctx, B, p(d.q[0], n), p(d.ksum, n), p(d.block_tables, n), p(d.ctx_lens, n),
+            p(d.h, n), p(d.kept, n), p(d.n_kept, n), p(d.scores, n), p(d.theta, n), None,
+            p(d.kappa, n), p(d.k_pool, n)),
+        "ent_sparse_paged_decode": lambda B, n: ent.ent_sparse_paged_decode(
+            dec.ctx, B, p(d.q[0], n), p(d.k_pool, n), p(d.v_pool, n), p(d.block_tables, n),
+            p(d.ctx_lens, n), p(d.kept, n), p(d.n_kept, n), p(d.out, n), p(d.lse, n)),
+        "ent_sample": lambda B, n: ent.ent_sample(
+            dec.ctx, B, p(d.logits[0], n), ld, p(d.row_stats, n), p(d.temp_used, n),
+            p(d.uniforms[0], n), p(d.tokens, n)),
+        "ent_kv_append": lambda B, n: ent.ent_kv_append(
+            dec.ctx, B, p(d.k_new[0], n), p(d.v_new[0], n), p(d.block_tables, n),
+            p(d.ctx_lens, n), p(d.k_pool, n), p(d.v_pool, n), p(d.ksum, n)),
+        "ent_decode_step": lambda B, n: ent.ent_decode_step(
+            dec.ctx, B, p(d.logits[0], n), ld, p(d.h_prev, n), p(d.tau, n), p(d.temp, n),
+            p(d.q[0], n), p(d.k_pool, n), p(d.v_pool, n), p(d.ksum, n), p(d.block_tables, n),
+            p(d.ctx_lens, n), p(d.uniforms[0], n), p(d.h, n), p(d.temp_used, n), p(d.kept, n),
+            p(d.n_kept, n), p(d.out, n), p(d.tokens, n), p(d.row_stats, n), p(d.lse, n),
+            p(d.scores, n), p(d.theta, n), None, p(d.kappa, n)),
+        "ent_decode_step_append": lambda B, n: ent.ent_decode_step_append(
+            dec.ctx, B, p(d.logits[0], n), ld, p(d.h_prev, n), p(d.tau, n), p(d.temp, n),
+            p(d.q[0], n), p(d.k_pool, n), p(d.v_pool, n), p(d.ksum, n), p(d.block_tables, n),
+            p(d.ctx_lens, n), p(d.uniforms[0], n), p(d.k_new[0], n), p(d.v_new[0], n), p(d.h, n),
+            p(d.temp_used, n), p(d.kept, n), p(d.n_kept, n), p(d.out, n), p(d.tokens, n),
+            p(d.row_stats, n), p(d.lse, n), p(d.scores, n), p(d.theta, n), None, p(d.kappa, n)),
+    }
+
+
+def test_empty_batch_and_batch_bounds(torch_cuda):
+    """B = 0 returns ENT_OK and launches nothing, with NULL pointers or with
+    real buffers; B = -1 and B = max_batch + 1 return ENT_E_INVAL with the
+    batch range in the message and nothing launched.  Every entry point that
+    takes a batch; no buffer changes by a single byte."""
+    from paper_2603_03310_amd import ent
+    torch = torch_cuda
+    w = small(LLAMA3_8B, 2, ctx=("uniform", 100, 300), steps=2, suffix="bounds")
+    x = generate(w)
+    d = upload(x)
+    with _dec(x, default_params(w)) as dec:
+        dec.summarize(w.batch, d.k_pool, d.block_tables, d.ctx_lens, d.ksum)
+        for f in ("h", "temp_used", "row_stats", "scores", "theta", "out", "lse"):
+            getattr(d, f).fill_(-5.0)
+        for f in ("kept", "n_kept", "tokens"):
+            getattr(d, f).fill_(-5)
+        torch.cuda.synchronize()
+        before = {f: getattr(d, f).clone() for f in MUTABLE}
+        for name, call in _batch_calls(ent, dec, d).items():
+            print(f"[bounds] {name}", flush=True)
+            call(0, True)
+            call(0, False)
+            for B in (-1, w.batch + 1):
+                with pytest.raises(ent.EntError) as e:
+                    call(B, False)
+                assert e.value.code == ent.ENT_E_INVAL, (name, B)
+                assert "B must be in [0, max_batch]" in str(e.value), (name, B)
+        torch.cuda.synchronize()
+        for f in MUTABLE:
+            a, b = getattr(d, f), before[f]
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), f
+        assert dec.device_status() == 0
