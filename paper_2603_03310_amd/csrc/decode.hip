@@ -443,7 +443,10 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   // else it becomes the workgroup's partial of that segment (slot wg + seg).
   // First, per (slot, head), the slot's weight 2^(m - M) in its group and the
   // group's (M, L), all slots' loads issued at once; then every output is one
-  // weighted sum over its group's slots, in slot order.
+  // weighted sum over its group's slots, in slot order, four consecutive
+  // outputs per thread (16-byte LDS reads and stores: with one float each the
+  // stores, issued while the other workgroups' loads fill the CU's memory
+  // pipeline, made this loop the longest part of a workgroup's end).
   constexpr int kSlots = 2 * kWaves;
   static_assert(kSlots * kMaxGroup <= kThreads, "one thread per (slot, head)");
   static_assert(3 * kSlots * kMaxGroup * sizeof(float) <= sizeof(s_kst), "merge weights in the K rows");
@@ -497,22 +500,29 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
       owner = seg;
       owner_last = wave_of(seg_end - 1, U, a.R);
     }
-    for (int o = threadIdx.x; o < G * D; o += kThreads) {
-      const int r = o / D, d = o - r * D;
-      float acc = 0.f;
+    for (int o = threadIdx.x; o < G * D / 4; o += kThreads) {
+      const int r = (4 * o) / D, d = 4 * o - r * D;
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
       for (int k = 0; k < kSlots; ++k) {
         const float f = s_wf[k * kMaxGroup + r];
-        const float v = s_cacc[(k * G + r) * D + d];
-        if (k >= i && k < j && f != 0.f) acc += f * v;
+        const float4 v = *reinterpret_cast<const float4*>(s_cacc + (k * G + r) * D + d);
+        if (k >= i && k < j && f != 0.f) {
+          acc.x += f * v.x;
+          acc.y += f * v.y;
+          acc.z += f * v.z;
+          acc.w += f * v.w;
+        }
       }
       const float M = s_wm[i * kMaxGroup + r], L = s_wl[i * kMaxGroup + r];
       if (whole) {
         const long long oh = static_cast<long long>(b) * Hq + g * G + r;
-        a.out[oh * D + d] = L > 0.f ? acc / L : 0.f;
+        const float4 res = L > 0.f ? make_float4(acc.x / L, acc.y / L, acc.z / L, acc.w / L)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+        *reinterpret_cast<float4*>(a.out + oh * D + d) = res;
         if (d == 0 && a.lse) a.lse[oh] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
       } else {
-        a.part_acc[(slot * G + r) * D + d] = acc;
+        *reinterpret_cast<float4*>(a.part_acc + (slot * G + r) * D + d) = acc;
         if (d == 0) {
           a.part_ml[(slot * G + r) * 2 + 0] = M;
           a.part_ml[(slot * G + r) * 2 + 1] = L;
