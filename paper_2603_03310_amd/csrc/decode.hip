@@ -131,9 +131,10 @@ __device__ __forceinline__ void zero_empty(const DecodeArgs& a, const int* s_nk)
 __device__ __forceinline__ int range_begin(int w, int U, int W) {
   return static_cast<int>(static_cast<long long>(w) * U / W);
 }
-// The wave whose range holds unit x (U > 0).
+// The wave whose range holds unit x (U > 0); the product in 64 bits, since
+// (x + 1) W passes 2^31 once the kept units do 2^31 / W.
 __device__ __forceinline__ int wave_of(int x, int U, int W) {
-  return static_cast<int>(((x + 1) * W - 1) / U);
+  return static_cast<int>((static_cast<long long>(x + 1) * W - 1) / U);
 }
 
 // Sequence holding unit x: the largest b with s_pref[b] <= x.
