@@ -222,6 +222,8 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   extern __shared__ __attribute__((aligned(16))) int s_mem[];
   __shared__ int s_red[kWaves];
   __shared__ int s_cseg[2 * kWaves];
+  __shared__ int4 s_gd[2 * kWaves];         // merge groups: slots, segment, its record
+  __shared__ int s_ng;
   // Each wave's K tile in the MFMA layout's source form, rows padded by 16 B.
   __shared__ __attribute__((aligned(16))) uint16_t s_kst[kWaves * kBlock * (D + 8)];
   // Dynamic LDS: cut partials first (16-byte aligned), then the plan.
@@ -449,7 +451,7 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   // stores, issued while the other workgroups' loads fill the CU's memory
   // pipeline, made this loop the longest part of a workgroup's end).
   constexpr int kSlots = 2 * kWaves;
-  static_assert(kSlots * kMaxGroup <= kThreads, "one thread per (slot, head)");
+  static_assert(kSlots * kMaxGroup + kSlots <= kThreads, "one thread per (slot, head), then per slot");
   static_assert(3 * kSlots * kMaxGroup * sizeof(float) <= sizeof(s_kst), "merge weights in the K rows");
   // The K staging rows are dead once every wave has left its loop.
   float* s_wf = reinterpret_cast<float*>(s_kst);
@@ -477,29 +479,66 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
     s_wf[threadIdx.x] = f;
     s_wm[threadIdx.x] = M;
     s_wl[threadIdx.x] = L;
+  } else if (threadIdx.x < kSlots * kMaxGroup + kSlots) {
+    // Meanwhile, one thread per slot: a slot heads a group when it holds a
+    // segment other than that of the nearest earlier slot holding one; the
+    // group runs to the next slot holding another segment (the empty slots
+    // between weigh 0).  The heads, in slot order, get the group's slots,
+    // whether the segment lies inside this workgroup's range, and the record
+    // of a cut segment that begins in it.
+    const int k = threadIdx.x - kSlots * kMaxGroup;
+    int cs[kSlots];
+#pragma unroll
+    for (int kk = 0; kk < kSlots; ++kk) cs[kk] = s_cseg[kk];
+    bool hd[kSlots];
+    int prev = -1;
+#pragma unroll
+    for (int kk = 0; kk < kSlots; ++kk) {
+      hd[kk] = cs[kk] >= 0 && cs[kk] != prev;
+      if (cs[kk] >= 0) prev = cs[kk];
+    }
+    int seg = -1, rank = 0, ng = 0;
+    bool head = false;
+#pragma unroll
+    for (int kk = 0; kk < kSlots; ++kk) {
+      if (kk == k) {
+        seg = cs[kk];
+        head = hd[kk];
+      }
+      if (kk < k && hd[kk]) ++rank;
+      if (hd[kk]) ++ng;
+    }
+    int j = kSlots;
+#pragma unroll
+    for (int kk = kSlots - 1; kk >= 0; --kk)
+      if (kk > k && cs[kk] >= 0 && cs[kk] != seg) j = kk;
+    if (head) {
+      const int b = seg / a.Hkv, g = seg % a.Hkv;
+      const int seg_start = s_pref[b] + g * s_nk[b];
+      const int seg_end = seg_start + s_nk[b];
+      const int wg = blockIdx.x;
+      const int g0 = range_begin(wg * kWaves, U, a.W), g1 = range_begin(wg * kWaves + kWaves, U, a.W);
+      const bool whole = seg_start >= g0 && seg_end <= g1;
+      const bool own = !whole && seg_start >= g0;
+      s_gd[rank] = make_int4(k | (j << 8) | (whole ? 1 << 16 : 0) | (own ? 1 << 17 : 0), seg,
+                             own ? wave_of(seg_end - 1, U, a.R) : 0, 0);
+    }
+    if (k == 0) s_ng = ng;
   }
   __syncthreads();
   const int wg = blockIdx.x;
-  const int g0 = range_begin(wg * kWaves, U, a.W), g1 = range_begin(wg * kWaves + kWaves, U, a.W);
   int owner = -1, owner_last = 0;            // cut segment that begins in this range
-  int i = 0;
-  while (i < kSlots) {
-    const int seg = s_cseg[i];
-    if (seg < 0) {
-      ++i;
-      continue;
-    }
-    int j = i + 1;
-    while (j < kSlots && (s_cseg[j] == seg || s_cseg[j] < 0)) ++j;
+  const int ng = s_ng;
+  for (int gi = 0; gi < ng; ++gi) {
+    const int4 gd = s_gd[gi];
     // Slots i .. j-1 with s_cseg == seg form the group (the others weigh 0).
-    const int b = seg / a.Hkv, g = seg % a.Hkv;
-    const int seg_start = s_pref[b] + g * s_nk[b];
-    const int seg_end = seg_start + s_nk[b];
-    const bool whole = seg_start >= g0 && seg_end <= g1;
+    const int i = gd.x & 255, j = (gd.x >> 8) & 255;
+    const bool whole = (gd.x >> 16) & 1;
+    const int seg = gd.y;
     const long long slot = static_cast<long long>(wg) + seg;
-    if (!whole && seg_start >= g0) {
+    if ((gd.x >> 17) & 1) {
       owner = seg;
-      owner_last = wave_of(seg_end - 1, U, a.R);
+      owner_last = gd.z;
     }
     for (int o = threadIdx.x; o < G * D / 4; o += kThreads) {
       const int r = (4 * o) / D, d = 4 * o - r * D;
@@ -517,7 +556,7 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
       }
       const float M = s_wm[i * kMaxGroup + r], L = s_wl[i * kMaxGroup + r];
       if (whole) {
-        const long long oh = static_cast<long long>(b) * Hq + g * G + r;
+        const long long oh = static_cast<long long>(seg) * G + r;    // b H_q + g G + r
         const float4 res = L > 0.f ? make_float4(acc.x / L, acc.y / L, acc.z / L, acc.w / L)
                                    : make_float4(0.f, 0.f, 0.f, 0.f);
         *reinterpret_cast<float4*>(a.out + oh * D + d) = res;
@@ -530,7 +569,6 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
         }
       }
     }
-    i = j;
   }
   if (threadIdx.x == 0) a.rec[wg] = make_int4(owner, owner_last, U, 0);
 }
