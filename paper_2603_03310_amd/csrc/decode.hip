@@ -4,9 +4,10 @@
 // Work decomposition (stream-K).  A unit is one kept block of one sequence
 // for one KV head (its G query heads together).  Units are laid end to end,
 // sequence-major, then KV head, then kept-list order; the (sequence, KV head)
-// runs are "segments".  Every wave of the persistent grid takes an equal
-// contiguous range of units, so all waves do the same amount of work and the
-// pipeline never drains between work items.  A wave walks its range with a
+// runs are "segments".  Every wave of the persistent grid takes one
+// contiguous range of units (of equal length, or for bf16 weighted by the
+// XCD its workgroup runs on), so the waves finish together and the pipeline
+// never drains between work items.  A wave walks its range with a
 // 64-unit metadata window (kept id and physical block per lane, gathered in
 // parallel) and a one-block-ahead register prefetch of the K and V tiles.
 // Where its range covers a whole segment it writes the output directly;
@@ -71,6 +72,7 @@ struct DecodeArgs {
   int B, Hkv, G, MAXB, P;
   int W;              // waves of the decode grid
   int R;              // ranges that write partials (workgroups for bf16, waves for fp32)
+  int xw;             // 1: ranges weighted by XCD (bf16, wv_begin / wg_begin), 0: equal wave ranges
   int nsl;            // merge workgroups per segment
   float scale_log2;   // softmax scale times log2(e)
 };
@@ -135,6 +137,34 @@ __device__ __forceinline__ int range_begin(int w, int U, int W) {
 // (x + 1) W passes 2^31 once the kept units do 2^31 / W.
 __device__ __forceinline__ int wave_of(int x, int U, int W) {
   return static_cast<int>((static_cast<long long>(x + 1) * W - 1) / U);
+}
+
+// The bf16 decode's ranges, weighted by XCD: workgroups are dealt to the
+// eight XCDs in turn (workgroup x on XCD x mod 8), and waves on the odd XCDs
+// were measured streaming their units 10-15% slower than those on the even
+// ones (per-wave timestamps, the same in every range); an odd workgroup
+// therefore takes kOddW / kEvenW of an even one's units, its four waves
+// alike (10:9 measured best against 20:19, 7:6 and 5:4).  Each workgroup's
+// range is the union of its waves' ranges.
+constexpr int kEvenW = 10, kOddW = 9;
+__device__ __forceinline__ long long wg_weight(int x) {
+  return static_cast<long long>(x >> 1) * (kEvenW + kOddW) + ((x & 1) ? kEvenW : 0);
+}
+__device__ __forceinline__ int wg_begin(int x, int U, int R) {
+  return static_cast<int>(wg_weight(x) * U / wg_weight(R));
+}
+__device__ __forceinline__ int wv_begin(int w, int U, int R) {
+  const int x = w / kWaves, i = w - x * kWaves;
+  const long long c = kWaves * wg_weight(x) + static_cast<long long>(i) * ((x & 1) ? kOddW : kEvenW);
+  return static_cast<int>(c * U / (kWaves * wg_weight(R)));
+}
+// The workgroup whose range holds unit u (U > 0).
+__device__ __forceinline__ int wg_of(int u, int U, int R) {
+  int x = static_cast<int>(static_cast<long long>(u) * R / U);
+  x = x < 0 ? 0 : (x >= R ? R - 1 : x);
+  while (x > 0 && wg_begin(x, U, R) > u) --x;
+  while (x + 1 < R && wg_begin(x + 1, U, R) <= u) ++x;
+  return x;
 }
 
 // Sequence holding unit x: the largest b with s_pref[b] <= x.
@@ -247,7 +277,7 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
   // slot 2 i (wave i's first segment, begun before its range) and 2 i + 1
   // (its last, continuing after it): G x D sums and (max, sum) per head.
   if (lane < 2) s_cseg[2 * wave + lane] = -1;
-  const int u0 = range_begin(w, U, a.W), u1 = range_begin(w + 1, U, a.W);
+  const int u0 = wv_begin(w, U, a.R), u1 = wv_begin(w + 1, U, a.R);
   const int r16 = lane & 15, gq = lane >> 4;
   const int Hq = a.Hkv * G;
   const bool head_ok = r16 < G;
@@ -517,11 +547,11 @@ __global__ __launch_bounds__(kThreads, 3) void decode_bf16_kernel(DecodeArgs a) 
       const int seg_start = s_pref[b] + g * s_nk[b];
       const int seg_end = seg_start + s_nk[b];
       const int wg = blockIdx.x;
-      const int g0 = range_begin(wg * kWaves, U, a.W), g1 = range_begin(wg * kWaves + kWaves, U, a.W);
+      const int g0 = wg_begin(wg, U, a.R), g1 = wg_begin(wg + 1, U, a.R);
       const bool whole = seg_start >= g0 && seg_end <= g1;
       const bool own = !whole && seg_start >= g0;
       s_gd[rank] = make_int4(k | (j << 8) | (whole ? 1 << 16 : 0) | (own ? 1 << 17 : 0), seg,
-                             own ? wave_of(seg_end - 1, U, a.R) : 0, 0);
+                             own ? wg_of(seg_end - 1, U, a.R) : 0, 0);
     }
     if (k == 0) s_ng = ng;
   }
@@ -746,7 +776,8 @@ __device__ __forceinline__ void combine_body(const DecodeArgs& a, int item) {
 #pragma unroll
     for (int k = 0; k < kCombinePrefetch; ++k) {
       const int wi = c0 + k;
-      const bool ok = wi <= w1 && range_begin(wi + 1, U, a.R) > range_begin(wi, U, a.R);
+      const bool ok = wi <= w1 && (a.xw ? wg_begin(wi + 1, U, a.R) > wg_begin(wi, U, a.R)
+                                        : range_begin(wi + 1, U, a.R) > range_begin(wi, U, a.R));
       const long long slot = static_cast<long long>(wi) + seg;
       m[k] = ok ? a.part_ml[(slot * G + r) * 2 + 0] : -INFINITY;
       l[k] = ok ? a.part_ml[(slot * G + r) * 2 + 1] : 0.f;
@@ -874,6 +905,7 @@ hipError_t launch_decode(const ent_ctx* c, int B, const void* q, const void* k_c
   a.P = cf.num_pool_blocks;
   a.W = c->decode_grid * kWaves;
   a.R = cf.kv_dtype == ENT_BF16 ? c->decode_grid : a.W;
+  a.xw = cf.kv_dtype == ENT_BF16 ? 1 : 0;
   a.scale_log2 = cf.scale * kLog2e;
   const size_t lds = plan_lds_bytes(B);
   const dim3 grid(c->decode_grid);
